@@ -1,0 +1,300 @@
+"""CPU oracle for SANTA++ decode attention.
+
+TEST INFRASTRUCTURE ONLY: the fp64 statement of what the decode path computes,
+written from the paper.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import it; the GPU library never
+does, and this package imports nothing from the GPU library.
+
+The arithmetic lives in ``santapp_oracle.c`` (plain C, fp64, compiled with
+``-ffp-contract=off``); this module marshals numpy arrays into it and adds the
+bookkeeping of the paper's logical KV-access counter (eq. qwen-logical-access).
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import math
+import os
+import subprocess
+from typing import List, Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "santapp_oracle.c")
+_SO = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+_d = ctypes.POINTER(ctypes.c_double)
+_i = ctypes.POINTER(ctypes.c_int)
+_u64 = ctypes.POINTER(ctypes.c_uint64)
+
+
+def build() -> str:
+    """Compile the oracle into ``oracle/liboracle.so`` (always recompiles)."""
+    tmp = _SO + ".tmp"
+    cmd = ["gcc", "-O2", "-std=gnu11", "-fPIC", "-shared", "-ffp-contract=off",
+           "-fno-fast-math", "-Wall", "-o", tmp, _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, _SO)
+    return _SO
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_SO):
+            build()
+        L = ctypes.CDLL(_SO)
+        L.philox4x64_10.argtypes = [_u64, _u64, _u64]
+        L.philox4x64_10.restype = None
+        L.oracle_gumbel.argtypes = [ctypes.c_uint64]
+        L.oracle_gumbel.restype = ctypes.c_double
+        L.oracle_team_gumbel.argtypes = [ctypes.c_uint64] * 5
+        L.oracle_team_gumbel.restype = ctypes.c_double
+        L.oracle_build_teams.argtypes = [_d, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                         ctypes.c_int, _i, _i, _i]
+        L.oracle_build_teams.restype = ctypes.c_int
+        L.oracle_decode_head.argtypes = (
+            [_d, ctypes.c_int, _d, _d, ctypes.c_int, _i, _i, _i, ctypes.c_int,
+             _d, _d, ctypes.c_int, ctypes.c_int, ctypes.c_uint64, ctypes.c_uint64,
+             ctypes.c_uint64, ctypes.c_uint64, ctypes.c_double, ctypes.c_double,
+             _d, _d, _d, _d, _d, _d, _i, _d, _d])
+        L.oracle_decode_head.restype = ctypes.c_int
+        L.oracle_dense_head.argtypes = [_d, ctypes.c_int, _d, _d, ctypes.c_int, _d, _d,
+                                        ctypes.c_int, ctypes.c_double, _d, _d, _d, _d]
+        L.oracle_dense_head.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _pd(a: np.ndarray):
+    return a.ctypes.data_as(_d)
+
+
+def _pi(a: np.ndarray):
+    return a.ctypes.data_as(_i)
+
+
+def _f64(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+# --------------------------------------------------------------------------
+# Counter-based generator and Gumbel noise
+# --------------------------------------------------------------------------
+def philox(counter, key) -> np.ndarray:
+    """Philox4x64-10 of one 4x64-bit counter under a 2x64-bit key."""
+    c = (ctypes.c_uint64 * 4)(*[int(x) & (2**64 - 1) for x in counter])
+    k = (ctypes.c_uint64 * 2)(*[int(x) & (2**64 - 1) for x in key])
+    o = (ctypes.c_uint64 * 4)()
+    lib().philox4x64_10(c, k, o)
+    return np.array(list(o), dtype=np.uint64)
+
+
+def gumbel(word: int) -> float:
+    return lib().oracle_gumbel(int(word))
+
+
+def team_gumbel(seed: int, step: int, b: int, h: int, g: int) -> float:
+    return lib().oracle_team_gumbel(seed, step, b, h, g)
+
+
+# --------------------------------------------------------------------------
+# Team construction (contiguous parents, actual-key representatives)
+# --------------------------------------------------------------------------
+@dataclasses.dataclass
+class Teams:
+    """Team records of one (sequence, KV head), in team order.
+
+    ``members`` lists the token indices of team 0 (ascending), then team 1,
+    ...; ``team_ptr`` holds the CSR offsets; ``rep_token[g]`` is the token
+    whose key represents team g.
+    """
+    members: np.ndarray
+    team_ptr: np.ndarray
+    rep_token: np.ndarray
+
+    @property
+    def M(self) -> int:
+        return len(self.rep_token)
+
+    @property
+    def sizes(self) -> np.ndarray:
+        return np.diff(self.team_ptr)
+
+
+def build_teams(K: np.ndarray, P: int, R: int) -> Teams:
+    """Contiguous parents of P tokens, then up to R representatives each.
+
+    ``K`` is one KV head's prompt keys ``[N, d]`` (exact values).
+    """
+    K = _f64(K)
+    N, d = K.shape
+    members = np.empty(N, np.int32)
+    team_ptr = np.empty(N + 1, np.int32)
+    rep_token = np.empty(N, np.int32)
+    M = lib().oracle_build_teams(_pd(K), N, d, P, R, _pi(members), _pi(team_ptr), _pi(rep_token))
+    if M < 0:
+        raise ValueError("oracle_build_teams rejected its arguments")
+    return Teams(members, team_ptr[:M + 1].copy(), rep_token[:M].copy())
+
+
+def build_all(K: np.ndarray, P: int, R: int) -> List[List[Teams]]:
+    """``K`` is ``[B, Hkv, N, d]``; returns teams[b][kv]."""
+    return [[build_teams(K[b, kv], P, R) for kv in range(K.shape[1])] for b in range(K.shape[0])]
+
+
+# --------------------------------------------------------------------------
+# Decode: one query head, or a whole [B, Hq] step
+# --------------------------------------------------------------------------
+@dataclasses.dataclass
+class HeadResult:
+    out: np.ndarray        # [d] attention output o^ = U^ / Z^
+    U: np.ndarray          # [d] U^ in the shifted scale
+    Z: float               # Z^ in the shifted scale
+    shift: float           # U^ e^shift and Z^ e^shift are the unshifted sums
+    phi: np.ndarray        # [M] routing logits (NaN when every team is taken)
+    Y: np.ndarray          # [M] perturbed routing scores (NaN likewise)
+    sel: np.ndarray        # selected team ids, ascending
+    c: np.ndarray          # their conditional inclusion corrections
+    tau: float             # (K'+1)-th largest perturbed score, -inf if K' = M
+
+
+def decode_head(q, K, V, teams: Teams, sK, sV, Kbudget: int, seed: int, step: int,
+                b: int, h: int, scale: float, ref_shift: float = float("nan")) -> HeadResult:
+    q = _f64(q)
+    K = _f64(K)
+    V = _f64(V)
+    d = q.shape[0]
+    sK = _f64(sK).reshape(-1, d)
+    sV = _f64(sV).reshape(-1, d)
+    T = sK.shape[0]
+    M = teams.M
+    out = np.empty(d)
+    U = np.empty(d)
+    Z = np.empty(1)
+    sh = np.empty(1)
+    phi = np.empty(M)
+    Y = np.empty(M)
+    sel = np.empty(M, np.int32)
+    c = np.empty(M)
+    tau = np.empty(1)
+    members = np.ascontiguousarray(teams.members, np.int32)
+    tptr = np.ascontiguousarray(teams.team_ptr, np.int32)
+    reps = np.ascontiguousarray(teams.rep_token, np.int32)
+    ns = lib().oracle_decode_head(
+        _pd(q), d, _pd(K), _pd(V), K.shape[0], _pi(members), _pi(tptr), _pi(reps), M,
+        _pd(sK), _pd(sV), T, int(Kbudget), seed, step, b, h, float(scale), float(ref_shift),
+        _pd(out), _pd(U), _pd(Z), _pd(sh), _pd(phi), _pd(Y), _pi(sel), _pd(c), _pd(tau))
+    if ns < 0:
+        raise ValueError("oracle_decode_head rejected its arguments")
+    return HeadResult(out, U, float(Z[0]), float(sh[0]), phi, Y, sel[:ns].copy(), c[:ns].copy(),
+                      float(tau[0]))
+
+
+def dense_head(q, K, V, sK, sV, scale: float):
+    q = _f64(q)
+    d = q.shape[0]
+    K = _f64(K).reshape(-1, d)
+    V = _f64(V).reshape(-1, d)
+    sK = _f64(sK).reshape(-1, d)
+    sV = _f64(sV).reshape(-1, d)
+    out = np.empty(d)
+    U = np.empty(d)
+    Z = np.empty(1)
+    sh = np.empty(1)
+    rc = lib().oracle_dense_head(_pd(q), d, _pd(K), _pd(V), K.shape[0], _pd(sK), _pd(sV),
+                                 sK.shape[0], float(scale), _pd(out), _pd(U), _pd(Z), _pd(sh))
+    if rc != 0:
+        raise ValueError("oracle_dense_head rejected its arguments")
+    return out, U, float(Z[0]), float(sh[0])
+
+
+@dataclasses.dataclass
+class StepResult:
+    out: np.ndarray                 # [B, Hq, d]
+    heads: List[List[HeadResult]]   # [b][h]
+
+
+def decode(q, K, V, sK, sV, teams, Kbudget: int, seed: int, step: int, scale: float,
+           heads: Optional[List[tuple]] = None) -> StepResult:
+    """Alg. 1 for every (b, h) (or only the listed ``heads`` pairs).
+
+    ``q [B,Hq,d]``, ``K,V [B,Hkv,N,d]``, ``sK,sV [B,Hkv,T,d]`` hold exact
+    values (any float dtype); ``teams[b][kv]`` from :func:`build_all`.
+    Query head h reads KV head ``h // (Hq // Hkv)``.
+    """
+    B, Hq, d = q.shape
+    Hkv = K.shape[1]
+    G = Hq // Hkv
+    out = np.full((B, Hq, d), np.nan)
+    res = [[None] * Hq for _ in range(B)]
+    pairs = heads if heads is not None else [(b, h) for b in range(B) for h in range(Hq)]
+    cache = {}
+    for (b, h) in pairs:
+        kv = h // G
+        if (b, kv) not in cache:
+            cache = {(b, kv): (_f64(K[b, kv]), _f64(V[b, kv]), _f64(sK[b, kv]), _f64(sV[b, kv]))}
+        Kb, Vb, sKb, sVb = cache[(b, kv)]
+        r = decode_head(q[b, h], Kb, Vb, teams[b][kv], sKb, sVb, Kbudget, seed, step, b, h, scale)
+        out[b, h] = r.out
+        res[b][h] = r
+    return StepResult(out, res)
+
+
+def dense(q, K, V, sK, sV, scale: float, heads: Optional[List[tuple]] = None) -> np.ndarray:
+    B, Hq, d = q.shape
+    Hkv = K.shape[1]
+    G = Hq // Hkv
+    out = np.full((B, Hq, d), np.nan)
+    pairs = heads if heads is not None else [(b, h) for b in range(B) for h in range(Hq)]
+    for (b, h) in pairs:
+        kv = h // G
+        out[b, h] = dense_head(q[b, h], K[b, kv], V[b, kv], sK[b, kv], sV[b, kv], scale)[0]
+    return out
+
+
+# --------------------------------------------------------------------------
+# Logical KV-access counter (eq. qwen-logical-access)
+# --------------------------------------------------------------------------
+def union_rows(teams: Teams, selections) -> int:
+    """Prompt rows read for one KV head: the union of the selected teams of
+    the query heads sharing it (teams are disjoint, so sizes add)."""
+    u = set()
+    for s in selections:
+        u.update(int(g) for g in s)
+    sizes = teams.sizes
+    return int(sum(int(sizes[g]) for g in u))
+
+
+def access_counts(step: StepResult, teams, Hkv: int, T: int, Kbudget: int):
+    """Per (b, kv): (m, u, e, N) of the counter; m = 0 when every team is
+    taken (no routing pass is needed then)."""
+    B = len(step.heads)
+    Hq = len(step.heads[0])
+    G = Hq // Hkv
+    rows = []
+    for b in range(B):
+        for kv in range(Hkv):
+            tm = teams[b][kv]
+            sels = [step.heads[b][h].sel for h in range(kv * G, (kv + 1) * G)]
+            m = tm.M if min(Kbudget, tm.M) < tm.M else 0
+            rows.append((m, union_rows(tm, sels), T, int(tm.team_ptr[-1]) + T))
+    return rows
+
+
+def kv_access_fraction(counts) -> float:
+    num = sum(m + 2 * (u + e) for (m, u, e, _) in counts)
+    den = sum(2 * n for (_, _, _, n) in counts)
+    return num / den
+
+
+def rel_l2(a, b) -> float:
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
+
+
+def scale_for(d: int) -> float:
+    return 1.0 / math.sqrt(d)
