@@ -1,0 +1,239 @@
+#!/usr/bin/env python3
+"""Benchmark: SANTA++ decode attention on one MI355X.
+
+One step = one ``santapp_decode`` call: routing, sampling, GQA read plan,
+split-K attention over the sampled teams and the exact suffix, and the split
+merge, for every query head of one Qwen2.5-7B-shaped layer (28 Q / 4 KV heads,
+d = 128, bf16 K/V) at a 32768-token prompt, 32 sampled teams per head, 128
+suffix rows, batch 1.  The step index advances every step, so every step
+draws fresh Gumbel noise and reads a different set of teams.
+
+Timing: the inputs are resident in HBM; before every step a 1 GiB buffer is
+rewritten (outside the timed interval) so that the 256 MB last-level cache
+holds none of the step's data; each step is bracketed by HIP events on the
+stream the library launches on.  ``value`` is the mean step time in
+microseconds.  The dense flash-decode baseline over all 32768 + 128 rows is
+timed the same way.  The CPU oracle is timed on a bounded sample of the same
+steps on the host (single thread).
+
+Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, GB/s
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--workload", default="qwen32k")
+    p.add_argument("--K", type=int, default=None, help="teams per query head (default: workload's)")
+    p.add_argument("--B", type=int, default=None)
+    p.add_argument("--no-evict", action="store_true", help="keep the last-level cache warm")
+    p.add_argument("--cpu-seconds", type=float, default=12.0,
+                   help="budget of the oracle CPU-baseline sample (0 disables it)")
+    p.add_argument("--no-dense", action="store_true")
+    return p.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: this build has no multi-GPU path "
+              f"(--gpus {args.gpus} requested)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import datagen
+    import paper_2609_35629_amd as sp
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    sp._lib.load()  # raises when the HIP library is not built
+
+    wl = datagen.WORKLOADS[args.workload]
+    if args.K is not None:
+        wl = wl.with_(K=args.K)
+    if args.B is not None:
+        wl = wl.with_(B=args.B, data_seeds=tuple(range(100, 100 + args.B)))
+    print(f"[bench] workload={wl.name} B={wl.B} N={wl.N} K={wl.K} T={wl.T}", file=sys.stderr, flush=True)
+    batch = datagen.generate(wl)
+    db = upload(batch)
+    teams = sp.build_teams(db["K"], db["V"], wl.P, wl.R)
+    M = teams.M
+    ws = sp.decode_workspace(teams, wl.Hq, wl.T, wl.K)
+    out = torch.empty((wl.B, wl.Hq, wl.d), dtype=torch.float32, device="cuda")
+    evict = torch.empty(1 << 28, dtype=torch.float32, device="cuda")  # 1 GiB
+
+    def run_sparse(step, dbg=None):
+        sp.decode(teams, db["q"], db["sK"], db["sV"], wl.K, seed=wl.seed, step=step, scale=wl.scale,
+                  out=out, workspace=ws, debug=dbg)
+
+    dense_ws = sp.dense_workspace(wl.B, wl.Hq, wl.Hkv, wl.N, wl.T, wl.d)
+    dense_out = torch.empty_like(out)
+
+    def run_dense(step, dbg=None):
+        sp.dense_decode(db["q"], db["K"], db["V"], db["sK"], db["sV"], scale=wl.scale, out=dense_out,
+                        workspace=dense_ws)
+
+    def timed(fn, n, warm, with_stages):
+        for i in range(warm):
+            fn(i)
+        torch.cuda.synchronize()
+        ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+        ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+        stages = []
+        dbgs = [sp.DebugOut(wl.B, wl.Hq, wl.Hkv, M, wl.K, arrays=False, events=True)
+                for _ in range(n)] if with_stages else [None] * n
+        torch.cuda.synchronize()
+        for i in range(n):
+            if not args.no_evict:
+                evict.add_(1.0)
+            ev0[i].record()
+            fn(warm + i, dbgs[i])
+            ev1[i].record()
+        torch.cuda.synchronize()
+        times = np.array([a.elapsed_time(b) * 1e3 for a, b in zip(ev0, ev1)])  # us
+        if with_stages:
+            stages = np.array([[x * 1e3 for x in d.stage_ms()] for d in dbgs])
+        return times, stages
+
+    torch.cuda.synchronize()
+    t_wall0 = time.perf_counter()
+    sparse_us, stages_us = timed(run_sparse, args.steps, args.warmup, True)
+    t_wall1 = time.perf_counter()
+    dense_us = None
+    if not args.no_dense:
+        dense_us, _ = timed(run_dense, args.steps, args.warmup, False)
+
+    # bytes each timed step read: the union rows of every (b, kv) (replayed
+    # with the diagnostics on; same seed and step give the same selection)
+    row_bytes = 2 * wl.d * 2
+    union_rows = np.zeros(args.steps)
+    for i in range(args.steps):
+        dbg = sp.DebugOut(wl.B, wl.Hq, wl.Hkv, M, wl.K)
+        run_sparse(args.warmup + i, dbg)
+        torch.cuda.synchronize()
+        union_rows[i] = dbg.union_rows.sum().item()
+    sampled = wl.K < M
+    BH = wl.B * wl.Hkv
+    rep_bytes = BH * M * wl.d * 2 if sampled else 0
+    suffix_bytes = BH * wl.T * row_bytes
+    small_bytes = wl.B * wl.Hq * wl.d * 4 * 2  # q in, out
+    if not sampled:
+        union_rows[:] = BH * wl.N
+    attend_bytes = union_rows * row_bytes + suffix_bytes
+    step_bytes = rep_bytes + attend_bytes + small_bytes
+    dense_bytes = BH * (wl.N + wl.T) * row_bytes + small_bytes
+
+    attend_us = stages_us[:, 1]
+    achieved = float(np.mean(attend_bytes) / np.mean(attend_us) / 1e3)  # GB/s
+    value = float(np.mean(sparse_us))
+    # eq. qwen-logical-access: one key per representative, key + value per row read
+    read_fraction = float(np.mean(rep_bytes + attend_bytes) / (BH * (wl.N + wl.T) * row_bytes))
+
+    cpu = None
+    if args.cpu_seconds > 0:
+        cpu = cpu_baseline(wl, batch, args.cpu_seconds)
+
+    res = {
+        "metric": "SANTA++ decode-attn us/step/layer + achieved HBM GB/s, 32K ctx, 32 teams",
+        "value": round(value, 3),
+        "unit": "us/step/layer",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(value / 1e3, 6),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.dtype == datagen.BF16 else "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name}: Qwen2.5-7B-shaped layer, {wl.N}-token prompt, B={wl.B}",
+                   "B": wl.B, "Hq": wl.Hq, "Hkv": wl.Hkv, "d": wl.d, "N": wl.N, "T": wl.T,
+                   "P": wl.P, "R": wl.R, "M": M, "K": wl.K, "evict_1GiB": not args.no_evict},
+        "roofline": {"bound": "hbm", "kernel": "k_attend", "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": None},
+        "step_gbs": round(float(np.mean(step_bytes) / value / 1e3), 1),
+        "step_hbm_frac": round(float(np.mean(step_bytes) / value / 1e3) / HBM_PEAK_GBS, 4),
+        "step_bytes_mean": int(np.mean(step_bytes)),
+        "union_rows_mean": float(np.mean(union_rows)),
+        "read_fraction": round(read_fraction, 4),
+        "median_us": round(float(np.median(sparse_us)), 3),
+        "stage_us_mean": {"route_select": round(float(np.mean(stages_us[:, 0])), 3),
+                          "attend": round(float(np.mean(stages_us[:, 1])), 3),
+                          "merge": round(float(np.mean(stages_us[:, 2])), 3)},
+        "wall_s_sparse_loop": round(t_wall1 - t_wall0, 3),
+    }
+    if dense_us is not None:
+        d = float(np.mean(dense_us))
+        res["dense_us"] = round(d, 3)
+        res["dense_gbs"] = round(dense_bytes / d / 1e3, 1)
+        res["speedup_vs_dense"] = round(d / value, 3)
+    if cpu is not None:
+        res["cpu_baseline"] = cpu
+    print(json.dumps(res), flush=True)
+
+
+def upload(batch):
+    """Copy a datagen batch to the GPU (bf16 bit patterns become bfloat16)."""
+    import numpy as np
+    import torch
+
+    import datagen
+
+    def dev(a):
+        if batch.wl.dtype == datagen.BF16:
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+
+    T = batch.wl.T
+    return {"q": torch.from_numpy(batch.q).cuda(), "K": dev(batch.K), "V": dev(batch.V),
+            "sK": dev(batch.sK) if T else None, "sV": dev(batch.sV) if T else None}
+
+
+def cpu_baseline(wl, batch, budget_s):
+    """The oracle (test infrastructure) on the host: whole decode steps (all
+    query heads), as many as fit in the time budget; team construction is
+    excluded, as for the GPU."""
+    import numpy as np
+
+    import oracle
+    Kf = batch.f32(batch.K)
+    teams = oracle.build_all(Kf, wl.P, wl.R)
+    Vf = batch.f32(batch.V)
+    sKf = batch.f32(batch.sK)
+    sVf = batch.f32(batch.sV)
+    steps = 0
+    t0 = time.perf_counter()
+    while True:
+        oracle.decode(batch.q, Kf, Vf, sKf, sVf, teams, wl.K, wl.seed, steps, wl.scale)
+        steps += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    el = time.perf_counter() - t0
+    return {"value": round(el / steps * 1e6, 1), "unit": "us/step/layer", "cores": 1,
+            "kind": "oracle",
+            "sample": f"{steps} full decode steps ({wl.B}x{wl.Hq} heads each) of the same workload, "
+                      f"fp64 C oracle, one thread, team build excluded"}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,185 @@
+/*
+ * santapp -- SANTA++ decode-time attention on AMD Instinct MI355X (gfx950).
+ *
+ * C ABI of libsantapp.so.  The operations follow the paper "SANTA++: Sampling
+ * Attention through Representative Keys":
+ *
+ *   santapp_build_teams   section "Preparing parent groups and teams",
+ *                         Alg. "Contiguous parent partition" and
+ *                         Alg. "Build actual-key teams from a parent
+ *                         partition", plus the team-contiguous packed copy of
+ *                         the prompt K/V described for the GPU implementation
+ *                         (appendix "Triton decode kernels", first paragraph).
+ *   santapp_decode        Alg. "SANTA++ attention for one query head" for every
+ *                         query head of one decode step: eq. method-routing,
+ *                         the Gumbel-top-K sampler, eq. method-inclusion,
+ *                         eq. method-estimate, GQA sharing of the reads.
+ *   santapp_dense_decode  eq. method-attention over the whole current cache
+ *                         (the dense baseline).
+ *
+ * Conventions
+ *   - Every tensor argument is a DEVICE pointer owned by the caller unless
+ *     stated otherwise; layouts are dense row-major.
+ *   - K/V element type is bf16 (raw 16-bit patterns) or fp32, chosen by
+ *     santapp_dtype; queries are fp32; outputs are fp32.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Every call only enqueues work on that stream; none synchronises except
+ *     santapp_build_teams, which waits for its own kernels before returning.
+ *   - Every call returns a santapp_status.  On failure nothing is enqueued
+ *     after the failing step and santapp_last_error() returns a message for
+ *     the calling thread.  No call aborts the process.
+ *   - santapp_decode and santapp_dense_decode never allocate: the caller
+ *     provides a workspace of the queried size.
+ */
+#ifndef SANTAPP_H
+#define SANTAPP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    SANTAPP_OK = 0,
+    SANTAPP_EINVAL = 1,     /* invalid argument (size, budget, null pointer, scale) */
+    SANTAPP_EDTYPE = 2,     /* unsupported element type                             */
+    SANTAPP_ENOMEM = 3,     /* device allocation failed (santapp_build_teams only)  */
+    SANTAPP_EHIP = 4,       /* a HIP runtime call or kernel launch failed           */
+    SANTAPP_EWORKSPACE = 5, /* workspace missing or smaller than required           */
+    SANTAPP_ELIMIT = 6      /* valid but beyond this library's supported sizes      */
+} santapp_status;
+
+typedef enum { SANTAPP_BF16 = 0, SANTAPP_FP32 = 1 } santapp_dtype;
+
+/* Opaque team table of one layer: owns its device buffers. */
+typedef struct santapp_teams santapp_teams;
+
+/* Read-only view of a team table.  All pointers are device pointers owned by
+ * the table; every per-(b,kv) array is laid out [B][Hkv][...]. */
+typedef struct {
+    int B, Hkv, N, d;
+    santapp_dtype dtype;
+    int parent_size, reps_per_parent;
+    int M;                   /* teams per (b, kv); identical for all (b, kv) */
+    const void* packed_K;    /* [B,Hkv,N,d] prompt keys in team order        */
+    const void* packed_V;    /* [B,Hkv,N,d] prompt values in team order      */
+    const void* reps;        /* [B,Hkv,M,d] representative key of each team  */
+    const int* team_begin;   /* [B,Hkv,M] first packed row of each team      */
+    const int* team_size;    /* [B,Hkv,M] n_g                                */
+    const int* rep_token;    /* [B,Hkv,M] original token index of l_g        */
+    const int* perm;         /* [B,Hkv,N] packed row -> original token index */
+} santapp_teams_desc;
+
+/*
+ * Build the team table of one layer (done once after prefill).
+ *
+ * K, V:      [B,Hkv,N,d] post-RoPE prompt keys / values (device, caller-owned,
+ *            not modified; they may be freed after the call returns).
+ * parent_size (P >= 1):     contiguous parents [uP, min((u+1)P, N)).
+ * reps_per_parent (R >= 1): representatives per parent, r = min(R, |C|).
+ * Per parent: the first representative is the member nearest the parent
+ * mean; each later one is the member farthest from its nearest chosen
+ * representative (ties: lowest token index); every member joins its nearest
+ * representative (ties: earliest chosen); representatives own themselves.
+ * Distances are squared Euclidean in fp64 on the exact input values.
+ * Teams are numbered parent by parent in representative order; members of a
+ * team are stored contiguously in ascending token order.
+ *
+ * Limits: d in {64, 128}; R <= 1024 (else SANTAPP_ELIMIT).  Sampled decoding
+ * (K < M) supports M <= 8192 teams per (b, kv).
+ * On success *out receives a new table (free with santapp_teams_destroy).
+ * Allocates device memory; synchronises `stream` before returning.
+ */
+santapp_status santapp_build_teams(const void* K, const void* V, int B, int Hkv, int N, int d,
+                                   santapp_dtype dtype, int parent_size, int reps_per_parent,
+                                   void* stream, santapp_teams** out);
+
+/* Fill *desc with the table's sizes and device pointers. */
+santapp_status santapp_teams_info(const santapp_teams* teams, santapp_teams_desc* desc);
+
+/* Free a table and its device buffers (NULL is ignored).  The caller must
+ * make sure no enqueued decode still reads it. */
+void santapp_teams_destroy(santapp_teams* teams);
+
+/*
+ * eq. method-budget: K = min(M, S / (P / R)) for a nominal row budget S.
+ * Requires P % R == 0 and S % (P / R) == 0 (else SANTAPP_EINVAL).  Host-only.
+ */
+santapp_status santapp_budget_to_K(int S, int P, int R, int M, int* K);
+
+/* Optional diagnostic outputs of santapp_decode (device pointers; each may be
+ * NULL).  The arrays are written only when the step samples (K < M).
+ * events[0..3], when non-NULL, are hipEvent_t handles created by the caller;
+ * the call records them on `stream` before the routing/sampling kernels,
+ * before the attention kernel, before the merge kernel and after it, so that
+ * hipEventElapsedTime gives the time of each stage. */
+typedef struct {
+    double* phi;      /* [B,Hq,M] routing logits log n_g + scale q.l_g          */
+    double* Y;        /* [B,Hq,M] perturbed routing scores phi_g + G_g          */
+    int* sel;         /* [B,Hq,K] selected team ids per head, ascending         */
+    float* logc;      /* [B,Hq,K] log c_g of those teams                        */
+    double* tau;      /* [B,Hq]   (K+1)-th largest perturbed score              */
+    int* union_teams; /* [B,Hkv]  teams read for the kv head (union over heads) */
+    int* union_rows;  /* [B,Hkv]  prompt rows read for the kv head              */
+    void* events[4];  /* hipEvent_t stage markers (each may be NULL)            */
+} santapp_decode_debug;
+
+/*
+ * Workspace for santapp_decode with these sizes (bytes, host-only query).
+ * The workspace must be zero-filled before its first use (for instance with
+ * santapp_workspace_zero); the library keeps that state between calls.
+ */
+santapp_status santapp_decode_workspace_bytes(const santapp_teams* teams, int Hq, int T, int K,
+                                              size_t* bytes);
+
+/* Zero `bytes` bytes of device memory at `ws` on `stream` (a fill kernel,
+ * safe inside HIP graph capture). */
+santapp_status santapp_workspace_zero(void* ws, size_t bytes, void* stream);
+
+/*
+ * One SANTA++ decode step for every sequence b < B and query head h < Hq of
+ * one layer (query head h reads KV head h / (Hq / Hkv)).
+ *
+ * q:        [B,Hq,d] fp32 post-RoPE queries.
+ * suffix_K, suffix_V: [B,Hkv,T,d] generated rows attended exactly (same dtype
+ *           as the table; may be NULL when T == 0).
+ * K:        teams to sample per query head (>= 1).  K >= M selects every team
+ *           with correction 1 (dense attention over the cache).
+ * seed, step: Gumbel noise of team g for head h of sequence b is word g % 4 of
+ *           Philox4x64-10(key = {seed, 0}, counter = {g / 4, h, b, step});
+ *           U = ((w >> 12) + 1/2) 2^-52, G = -log(-log U).
+ * scale:    softmax scale; 0 means 1/sqrt(d).  Used for routing too.
+ * out:      [B,Hq,d] fp32 estimate U^ / Z^.
+ * Routing logits, the perturbed scores, the selection and tau are computed in
+ * fp64; attention scores and the online softmax in fp32.
+ * Never allocates and never synchronises.
+ */
+santapp_status santapp_decode(const santapp_teams* teams, const float* q, const void* suffix_K,
+                              const void* suffix_V, int T, int Hq, int K, uint64_t seed,
+                              uint64_t step, double scale, float* out, void* workspace,
+                              size_t ws_bytes, const santapp_decode_debug* dbg, void* stream);
+
+/* Workspace for santapp_dense_decode (bytes, host-only query). */
+santapp_status santapp_dense_workspace_bytes(int B, int Hq, int Hkv, int N, int T, int d,
+                                             size_t* bytes);
+
+/*
+ * Dense softmax attention over K, V [B,Hkv,N,d] followed by the suffix rows
+ * [B,Hkv,T,d] (eq. method-attention), with the same GQA mapping, dtypes and
+ * scale convention as santapp_decode.  Never allocates or synchronises.
+ */
+santapp_status santapp_dense_decode(const float* q, const void* K, const void* V, int B, int Hkv,
+                                    int N, int d, santapp_dtype dtype, const void* suffix_K,
+                                    const void* suffix_V, int T, int Hq, double scale, float* out,
+                                    void* workspace, size_t ws_bytes, void* stream);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* santapp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SANTAPP_H */

@@ -1,0 +1,416 @@
+// C ABI of libsantapp: argument checks, buffer ownership, workspace layout and
+// launch sequencing.  All arithmetic runs in the kernels.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <algorithm>
+#include <string>
+
+#include "internal.h"
+
+struct santapp_teams {
+    int B, Hkv, N, d;
+    santapp_dtype dtype;
+    int P, R, M;
+    void* packed_K;
+    void* packed_V;
+    void* reps;
+    int* team_begin;
+    int* team_size;
+    int* rep_token;
+    int* perm;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+santapp_status fail(santapp_status st, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return st;
+}
+
+santapp_status ok() {
+    g_err.clear();
+    return SANTAPP_OK;
+}
+
+santapp_status hip_fail(hipError_t e, const char* what) {
+    return fail(SANTAPP_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+size_t elem_size(santapp_dtype dt) { return dt == SANTAPP_BF16 ? 2 : 4; }
+
+bool dtype_ok(santapp_dtype dt) { return dt == SANTAPP_BF16 || dt == SANTAPP_FP32; }
+
+size_t align_up(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+// Teams per (b, kv) for contiguous parents: every parent but the last has P
+// members and min(R, P) teams.
+long long team_count(int N, int P, int R) {
+    const long long np = (static_cast<long long>(N) + P - 1) / P;
+    const long long last = N - (np - 1) * static_cast<long long>(P);
+    return (np - 1) * std::min<long long>(R, P) + std::min<long long>(R, last);
+}
+
+// Row splits per KV head: enough workgroups to cover the GPU about twice,
+// at least `min_rows` rows per split at the largest possible row count.
+int choose_split(int BH, int max_rows, int target_wg, int min_rows) {
+    int n = (target_wg + BH - 1) / BH;
+    const int cap = std::max(1, (max_rows + min_rows - 1) / min_rows);
+    return std::max(1, std::min(n, cap));
+}
+
+void free_teams(santapp_teams* t) {
+    if (!t) return;
+    hipFree(t->packed_K);
+    hipFree(t->packed_V);
+    hipFree(t->reps);
+    hipFree(t->team_begin);
+    hipFree(t->team_size);
+    hipFree(t->rep_token);
+    hipFree(t->perm);
+    delete t;
+}
+
+}  // namespace
+
+namespace santapp {
+
+DecodeLayout decode_layout(int B, int Hq, int Hkv, int N, int T, int d, int M) {
+    DecodeLayout L;
+    const size_t BH = static_cast<size_t>(B) * Hkv, BQ = static_cast<size_t>(B) * Hq;
+    L.n_split = choose_split(static_cast<int>(BH), N + T, 512, 16);
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = off;
+        off = align_up(off + bytes);
+        return at;
+    };
+    L.phi = take(BQ * M * sizeof(double));
+    L.Y = take(BQ * M * sizeof(double));
+    L.lc = take(BQ * M * sizeof(float));
+    L.hdr = take(BH * 4 * sizeof(int));
+    L.ubeg = take(BH * M * sizeof(int));
+    L.urs = take(BH * (M + 1) * sizeof(int));
+    L.ulogc = take(BH * M * kLogcStride * sizeof(float));
+    L.split = take(BH * L.n_split * sizeof(int));
+    L.po = take(BQ * L.n_split * d * sizeof(float));
+    L.pml = take(BQ * L.n_split * 2 * sizeof(float));
+    L.total = off;
+    return L;
+}
+
+DecodeLayout dense_layout(int B, int Hq, int Hkv, int N, int T, int d) {
+    DecodeLayout L;
+    const size_t BH = static_cast<size_t>(B) * Hkv, BQ = static_cast<size_t>(B) * Hq;
+    L.n_split = choose_split(static_cast<int>(BH), N + T, 1024, 64);
+    size_t off = 0;
+    L.po = off;
+    off = align_up(off + BQ * L.n_split * d * sizeof(float));
+    L.pml = off;
+    off = align_up(off + BQ * L.n_split * 2 * sizeof(float));
+    L.total = off;
+    return L;
+}
+
+}  // namespace santapp
+
+using namespace santapp;
+
+extern "C" {
+
+const char* santapp_last_error(void) { return g_err.c_str(); }
+
+santapp_status santapp_budget_to_K(int S, int P, int R, int M, int* K) {
+    if (!K) return fail(SANTAPP_EINVAL, "K is NULL");
+    if (S < 1 || P < 1 || R < 1 || M < 1)
+        return fail(SANTAPP_EINVAL, "S, P, R and M must be positive (got %d, %d, %d, %d)", S, P, R, M);
+    if (P % R != 0) return fail(SANTAPP_EINVAL, "P (%d) must be divisible by R (%d)", P, R);
+    const int per = P / R;
+    if (S % per != 0) return fail(SANTAPP_EINVAL, "S (%d) must be divisible by P/R (%d)", S, per);
+    *K = std::min(M, S / per);
+    return ok();
+}
+
+santapp_status santapp_build_teams(const void* K, const void* V, int B, int Hkv, int N, int d,
+                                   santapp_dtype dtype, int parent_size, int reps_per_parent,
+                                   void* stream, santapp_teams** out) {
+    if (!out) return fail(SANTAPP_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (!K || !V) return fail(SANTAPP_EINVAL, "K and V must be device pointers");
+    if (B < 1 || Hkv < 1 || N < 1) return fail(SANTAPP_EINVAL, "B, Hkv, N must be >= 1");
+    if (parent_size < 1) return fail(SANTAPP_EINVAL, "parent_size must be >= 1");
+    if (reps_per_parent < 1) return fail(SANTAPP_EINVAL, "reps_per_parent must be >= 1");
+    if (!dtype_ok(dtype)) return fail(SANTAPP_EDTYPE, "unsupported dtype %d", static_cast<int>(dtype));
+    if (d != 64 && d != 128) return fail(SANTAPP_ELIMIT, "head dim %d not supported (64 or 128)", d);
+    if (reps_per_parent > kMaxReps)
+        return fail(SANTAPP_ELIMIT, "reps_per_parent %d exceeds %d", reps_per_parent, kMaxReps);
+    const long long M = team_count(N, parent_size, reps_per_parent);
+    const size_t BH = static_cast<size_t>(B) * Hkv;
+    if (BH * static_cast<size_t>(N) > static_cast<size_t>(0x7fffffff))
+        return fail(SANTAPP_ELIMIT, "B*Hkv*N exceeds 2^31");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const size_t esz = elem_size(dtype);
+    const size_t row = static_cast<size_t>(d) * esz;
+
+    santapp_teams* t = new santapp_teams();
+    t->B = B;
+    t->Hkv = Hkv;
+    t->N = N;
+    t->d = d;
+    t->dtype = dtype;
+    t->P = parent_size;
+    t->R = reps_per_parent;
+    t->M = static_cast<int>(M);
+    double* mind = nullptr;
+    int* owner = nullptr;
+    hipError_t e = hipSuccess;
+    auto alloc = [&](void** p, size_t bytes) {
+        if (e == hipSuccess) e = hipMalloc(p, bytes);
+    };
+    alloc(&t->packed_K, BH * N * row);
+    alloc(&t->packed_V, BH * N * row);
+    alloc(&t->reps, BH * M * row);
+    alloc(reinterpret_cast<void**>(&t->team_begin), BH * M * sizeof(int));
+    alloc(reinterpret_cast<void**>(&t->team_size), BH * M * sizeof(int));
+    alloc(reinterpret_cast<void**>(&t->rep_token), BH * M * sizeof(int));
+    alloc(reinterpret_cast<void**>(&t->perm), BH * N * sizeof(int));
+    alloc(reinterpret_cast<void**>(&mind), BH * N * sizeof(double));
+    alloc(reinterpret_cast<void**>(&owner), BH * N * sizeof(int));
+    if (e != hipSuccess) {
+        hipFree(mind);
+        hipFree(owner);
+        free_teams(t);
+        (void)hipGetLastError();
+        return fail(SANTAPP_ENOMEM, "device allocation failed: %s", hipGetErrorString(e));
+    }
+    const char* what = "team build";
+    e = launch_build_parents(K, dtype, static_cast<int>(BH), N, d, parent_size, reps_per_parent,
+                             t->M, mind, owner, t->team_begin, t->team_size, t->rep_token, t->perm,
+                             s);
+    if (e == hipSuccess) {
+        what = "packing K";
+        e = launch_gather_rows(K, t->packed_K, t->perm, static_cast<int>(BH), N, N, row, s);
+    }
+    if (e == hipSuccess) {
+        what = "packing V";
+        e = launch_gather_rows(V, t->packed_V, t->perm, static_cast<int>(BH), N, N, row, s);
+    }
+    if (e == hipSuccess) {
+        what = "gathering representatives";
+        e = launch_gather_rows(K, t->reps, t->rep_token, static_cast<int>(BH), t->M, N, row, s);
+    }
+    if (e == hipSuccess) {
+        what = "team build sync";
+        e = hipStreamSynchronize(s);
+    }
+    hipFree(mind);
+    hipFree(owner);
+    if (e != hipSuccess) {
+        free_teams(t);
+        return hip_fail(e, what);
+    }
+    *out = t;
+    return ok();
+}
+
+santapp_status santapp_teams_info(const santapp_teams* t, santapp_teams_desc* d) {
+    if (!t || !d) return fail(SANTAPP_EINVAL, "NULL argument");
+    d->B = t->B;
+    d->Hkv = t->Hkv;
+    d->N = t->N;
+    d->d = t->d;
+    d->dtype = t->dtype;
+    d->parent_size = t->P;
+    d->reps_per_parent = t->R;
+    d->M = t->M;
+    d->packed_K = t->packed_K;
+    d->packed_V = t->packed_V;
+    d->reps = t->reps;
+    d->team_begin = t->team_begin;
+    d->team_size = t->team_size;
+    d->rep_token = t->rep_token;
+    d->perm = t->perm;
+    return ok();
+}
+
+void santapp_teams_destroy(santapp_teams* t) { free_teams(t); }
+
+santapp_status santapp_workspace_zero(void* ws, size_t bytes, void* stream) {
+    if (bytes == 0) return ok();
+    if (!ws) return fail(SANTAPP_EINVAL, "workspace is NULL");
+    const hipError_t e = launch_zero(ws, bytes, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? ok() : hip_fail(e, "workspace zero");
+}
+
+santapp_status santapp_decode_workspace_bytes(const santapp_teams* t, int Hq, int T, int K,
+                                              size_t* bytes) {
+    if (!t || !bytes) return fail(SANTAPP_EINVAL, "NULL argument");
+    if (Hq < 1 || Hq % t->Hkv != 0) return fail(SANTAPP_EINVAL, "Hq must be a positive multiple of Hkv");
+    if (T < 0 || K < 1) return fail(SANTAPP_EINVAL, "T must be >= 0 and K >= 1");
+    *bytes = decode_layout(t->B, Hq, t->Hkv, t->N, T, t->d, t->M).total;
+    return ok();
+}
+
+santapp_status santapp_dense_workspace_bytes(int B, int Hq, int Hkv, int N, int T, int d,
+                                             size_t* bytes) {
+    if (!bytes) return fail(SANTAPP_EINVAL, "NULL argument");
+    if (B < 1 || Hkv < 1 || Hq < 1 || Hq % Hkv != 0 || N < 0 || T < 0 || N + T < 1 || d < 1)
+        return fail(SANTAPP_EINVAL, "invalid sizes");
+    *bytes = dense_layout(B, Hq, Hkv, N, T, d).total;
+    return ok();
+}
+
+santapp_status santapp_decode(const santapp_teams* t, const float* q, const void* suffix_K,
+                              const void* suffix_V, int T, int Hq, int K, uint64_t seed,
+                              uint64_t step, double scale, float* out, void* workspace,
+                              size_t ws_bytes, const santapp_decode_debug* dbg, void* stream) {
+    if (!t) return fail(SANTAPP_EINVAL, "teams is NULL");
+    if (!q || !out) return fail(SANTAPP_EINVAL, "q and out must be device pointers");
+    if (Hq < 1 || Hq % t->Hkv != 0) return fail(SANTAPP_EINVAL, "Hq (%d) must be a positive multiple of Hkv (%d)", Hq, t->Hkv);
+    const int G = Hq / t->Hkv;
+    if (G > kMaxGroup) return fail(SANTAPP_ELIMIT, "%d query heads per KV head exceed %d", G, kMaxGroup);
+    if (T < 0) return fail(SANTAPP_EINVAL, "T must be >= 0");
+    if (T > 0 && (!suffix_K || !suffix_V)) return fail(SANTAPP_EINVAL, "suffix K/V are NULL with T > 0");
+    if (K < 1) return fail(SANTAPP_EINVAL, "K must be >= 1 (got %d)", K);
+    if (!(scale >= 0.0) || !isfinite(scale)) return fail(SANTAPP_EINVAL, "scale must be finite and >= 0");
+    if (scale == 0.0) scale = 1.0 / sqrt(static_cast<double>(t->d));
+    const DecodeLayout L = decode_layout(t->B, Hq, t->Hkv, t->N, T, t->d, t->M);
+    if (!workspace || ws_bytes < L.total)
+        return fail(SANTAPP_EWORKSPACE, "workspace of %zu bytes needed (got %zu)", L.total, ws_bytes);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    char* ws = static_cast<char*>(workspace);
+    const int Kp = std::min(K, t->M);
+
+    AttendArgs A{};
+    A.K = t->packed_K;
+    A.V = t->packed_V;
+    A.sK = suffix_K;
+    A.sV = suffix_V;
+    A.q = q;
+    A.B = t->B;
+    A.Hkv = t->Hkv;
+    A.Hq = Hq;
+    A.G = G;
+    A.d = t->d;
+    A.N = t->N;
+    A.T = T;
+    A.M = t->M;
+    A.n_split = L.n_split;
+    A.dtype = t->dtype;
+    A.scale = static_cast<float>(scale);
+    A.ws = ws;
+    A.lay = &L;
+    A.part_o = reinterpret_cast<float*>(ws + L.po);
+    A.part_ml = reinterpret_cast<float*>(ws + L.pml);
+    A.out = out;
+
+    hipError_t e;
+    auto mark = [&](int i) -> hipError_t {
+        if (dbg && dbg->events[i]) return hipEventRecord(static_cast<hipEvent_t>(dbg->events[i]), s);
+        return hipSuccess;
+    };
+    if ((e = mark(0)) != hipSuccess) return hip_fail(e, "event record");
+    if (Kp == t->M) {
+        // every team selected with correction 1: dense attention over the cache
+        A.dense = true;
+    } else {
+        if (t->M > kMaxTeams)
+            return fail(SANTAPP_ELIMIT, "%d teams per KV head exceed %d", t->M, kMaxTeams);
+        RouteArgs R{};
+        R.reps = t->reps;
+        R.team_size = t->team_size;
+        R.team_begin = t->team_begin;
+        R.q = q;
+        R.B = t->B;
+        R.Hkv = t->Hkv;
+        R.Hq = Hq;
+        R.G = G;
+        R.d = t->d;
+        R.M = t->M;
+        R.Kp = Kp;
+        R.T = T;
+        R.dtype = t->dtype;
+        R.scale = scale;
+        R.seed = seed;
+        R.step = step;
+        R.lay = &L;
+        R.ws = ws;
+        R.dbg = dbg;
+        if ((e = launch_route(R, s)) != hipSuccess) return hip_fail(e, "routing kernel");
+        if ((e = launch_select(R, s)) != hipSuccess) return hip_fail(e, "sampling kernel");
+        if (dbg && dbg->phi &&
+            (e = hipMemcpyAsync(dbg->phi, ws + L.phi, sizeof(double) * t->B * Hq * t->M,
+                                hipMemcpyDeviceToDevice, s)) != hipSuccess)
+            return hip_fail(e, "debug copy");
+        if (dbg && dbg->Y &&
+            (e = hipMemcpyAsync(dbg->Y, ws + L.Y, sizeof(double) * t->B * Hq * t->M,
+                                hipMemcpyDeviceToDevice, s)) != hipSuccess)
+            return hip_fail(e, "debug copy");
+        A.dense = false;
+    }
+    if ((e = mark(1)) != hipSuccess) return hip_fail(e, "event record");
+    if ((e = launch_attend(A, s)) != hipSuccess) return hip_fail(e, "attention kernel");
+    if ((e = mark(2)) != hipSuccess) return hip_fail(e, "event record");
+    if ((e = launch_merge(A, s)) != hipSuccess) return hip_fail(e, "merge kernel");
+    if ((e = mark(3)) != hipSuccess) return hip_fail(e, "event record");
+    return ok();
+}
+
+santapp_status santapp_dense_decode(const float* q, const void* K, const void* V, int B, int Hkv,
+                                    int N, int d, santapp_dtype dtype, const void* suffix_K,
+                                    const void* suffix_V, int T, int Hq, double scale, float* out,
+                                    void* workspace, size_t ws_bytes, void* stream) {
+    if (!q || !out) return fail(SANTAPP_EINVAL, "q and out must be device pointers");
+    if (B < 1 || Hkv < 1 || N < 0 || T < 0 || N + T < 1)
+        return fail(SANTAPP_EINVAL, "invalid sizes");
+    if (N > 0 && (!K || !V)) return fail(SANTAPP_EINVAL, "K and V are NULL with N > 0");
+    if (T > 0 && (!suffix_K || !suffix_V)) return fail(SANTAPP_EINVAL, "suffix K/V are NULL with T > 0");
+    if (Hq < 1 || Hq % Hkv != 0) return fail(SANTAPP_EINVAL, "Hq must be a positive multiple of Hkv");
+    if (Hq / Hkv > kMaxGroup) return fail(SANTAPP_ELIMIT, "more than %d query heads per KV head", kMaxGroup);
+    if (!dtype_ok(dtype)) return fail(SANTAPP_EDTYPE, "unsupported dtype %d", static_cast<int>(dtype));
+    if (d != 64 && d != 128) return fail(SANTAPP_ELIMIT, "head dim %d not supported (64 or 128)", d);
+    if (!(scale >= 0.0) || !isfinite(scale)) return fail(SANTAPP_EINVAL, "scale must be finite and >= 0");
+    if (scale == 0.0) scale = 1.0 / sqrt(static_cast<double>(d));
+    const DecodeLayout L = dense_layout(B, Hq, Hkv, N, T, d);
+    if (!workspace || ws_bytes < L.total)
+        return fail(SANTAPP_EWORKSPACE, "workspace of %zu bytes needed (got %zu)", L.total, ws_bytes);
+    char* ws = static_cast<char*>(workspace);
+    AttendArgs A{};
+    A.K = K;
+    A.V = V;
+    A.sK = suffix_K;
+    A.sV = suffix_V;
+    A.q = q;
+    A.B = B;
+    A.Hkv = Hkv;
+    A.Hq = Hq;
+    A.G = Hq / Hkv;
+    A.d = d;
+    A.N = N;
+    A.T = T;
+    A.M = 0;
+    A.n_split = L.n_split;
+    A.dtype = dtype;
+    A.scale = static_cast<float>(scale);
+    A.dense = true;
+    A.ws = ws;
+    A.lay = &L;
+    A.part_o = reinterpret_cast<float*>(ws + L.po);
+    A.part_ml = reinterpret_cast<float*>(ws + L.pml);
+    A.out = out;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e;
+    if ((e = launch_attend(A, s)) != hipSuccess) return hip_fail(e, "attention kernel");
+    if ((e = launch_merge(A, s)) != hipSuccess) return hip_fail(e, "merge kernel");
+    return ok();
+}
+
+}  // extern "C"

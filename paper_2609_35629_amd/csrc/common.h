@@ -1,0 +1,103 @@
+// Device helpers shared by the santapp kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace santapp {
+
+constexpr int kWave = 64;
+
+// Element types of K/V rows.
+struct bf16_t {
+    uint16_t bits;
+};
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+    return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// Low / high bf16 of a packed 32-bit word, widened exactly to fp32.
+__device__ __forceinline__ float bf16lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+template <typename T>
+__device__ __forceinline__ float load_elem(const T* p, size_t i);
+
+template <>
+__device__ __forceinline__ float load_elem<bf16_t>(const bf16_t* p, size_t i) {
+    return bf16_to_f32(p[i].bits);
+}
+
+template <>
+__device__ __forceinline__ float load_elem<float>(const float* p, size_t i) {
+    return p[i];
+}
+
+// ---------------------------------------------------------------------------
+// Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11).  One round maps
+// (x0,x1,x2,x3) to (hi(M1 x2)^x1^k0, lo(M1 x2), hi(M0 x0)^x3^k1, lo(M0 x0));
+// the key advances by the Weyl increments between rounds.
+// ---------------------------------------------------------------------------
+struct u64x4 {
+    uint64_t v[4];
+};
+
+__device__ __forceinline__ u64x4 philox4x64_10(uint64_t c0, uint64_t c1, uint64_t c2, uint64_t c3,
+                                               uint64_t k0, uint64_t k1) {
+    const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
+    const uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        if (r) {
+            k0 += W0;
+            k1 += W1;
+        }
+        const uint64_t lo0 = M0 * c0, hi0 = __umul64hi(M0, c0);
+        const uint64_t lo1 = M1 * c2, hi1 = __umul64hi(M1, c2);
+        const uint64_t n0 = hi1 ^ c1 ^ k0;
+        const uint64_t n2 = hi0 ^ c3 ^ k1;
+        c0 = n0;
+        c1 = lo1;
+        c2 = n2;
+        c3 = lo0;
+    }
+    u64x4 o;
+    o.v[0] = c0;
+    o.v[1] = c1;
+    o.v[2] = c2;
+    o.v[3] = c3;
+    return o;
+}
+
+// Standard Gumbel variate of team g for (seed, step, b, h): word g % 4 of the
+// block at counter (g / 4, h, b, step), key (seed, 0); U = ((w >> 12) + 1/2)
+// 2^-52 is exact and inside (0, 1); G = -log(-log U).
+__device__ __forceinline__ double team_gumbel(uint64_t seed, uint64_t step, uint64_t b, uint64_t h,
+                                              uint64_t g) {
+    const u64x4 r = philox4x64_10(g >> 2, h, b, step, seed, 0);
+    const uint64_t w = r.v[g & 3];
+    const double u = (static_cast<double>(w >> 12) + 0.5) * 0x1.0p-52;
+    return -log(-log(u));
+}
+
+// Order-preserving map of a double onto uint64 (larger value -> larger key).
+__device__ __forceinline__ uint64_t order_key(double y) {
+    const uint64_t b = static_cast<uint64_t>(__double_as_longlong(y));
+    return (b >> 63) ? ~b : (b | 0x8000000000000000ull);
+}
+
+__device__ __forceinline__ double key_value(uint64_t k) {
+    const uint64_t b = (k >> 63) ? (k & 0x7fffffffffffffffull) : ~k;
+    return __longlong_as_double(static_cast<long long>(b));
+}
+
+__device__ __forceinline__ uint64_t lanemask_lt() {
+    const int lane = threadIdx.x & (kWave - 1);
+    return (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+}
+
+__device__ __forceinline__ int wave_id() { return threadIdx.x / kWave; }
+__device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
+
+}  // namespace santapp
