@@ -59,14 +59,6 @@ long long team_count(int N, int P, int R) {
     return (np - 1) * std::min<long long>(R, P) + std::min<long long>(R, last);
 }
 
-// Row splits per KV head: enough workgroups to cover the GPU about twice,
-// at least `min_rows` rows per split at the largest possible row count.
-int choose_split(int BH, int max_rows, int target_wg, int min_rows) {
-    int n = (target_wg + BH - 1) / BH;
-    const int cap = std::max(1, (max_rows + min_rows - 1) / min_rows);
-    return std::max(1, std::min(n, cap));
-}
-
 void free_teams(santapp_teams* t) {
     if (!t) return;
     hipFree(t->packed_K);
@@ -86,7 +78,7 @@ namespace santapp {
 DecodeLayout decode_layout(int B, int Hq, int Hkv, int N, int T, int d, int M) {
     DecodeLayout L;
     const size_t BH = static_cast<size_t>(B) * Hkv, BQ = static_cast<size_t>(B) * Hq;
-    L.n_split = choose_split(static_cast<int>(BH), N + T, 512, 16);
+    L.max_split = (N + T + kSplitRows - 1) / kSplitRows;
     size_t off = 0;
     auto take = [&](size_t bytes) {
         const size_t at = off;
@@ -97,25 +89,24 @@ DecodeLayout decode_layout(int B, int Hq, int Hkv, int N, int T, int d, int M) {
     L.Y = take(BQ * M * sizeof(double));
     L.lc = take(BQ * M * sizeof(float));
     L.hdr = take(BH * 4 * sizeof(int));
-    L.ubeg = take(BH * M * sizeof(int));
-    L.urs = take(BH * (M + 1) * sizeof(int));
     L.ulogc = take(BH * M * kLogcStride * sizeof(float));
-    L.split = take(BH * L.n_split * sizeof(int));
-    L.po = take(BQ * L.n_split * d * sizeof(float));
-    L.pml = take(BQ * L.n_split * 2 * sizeof(float));
+    L.rowmap = take(BH * N * 2 * sizeof(int));
+    L.po = take(BQ * L.max_split * d * sizeof(float));
+    L.pml = take(BQ * L.max_split * 2 * sizeof(float));
     L.total = off;
     return L;
 }
 
 DecodeLayout dense_layout(int B, int Hq, int Hkv, int N, int T, int d) {
     DecodeLayout L;
-    const size_t BH = static_cast<size_t>(B) * Hkv, BQ = static_cast<size_t>(B) * Hq;
-    L.n_split = choose_split(static_cast<int>(BH), N + T, 1024, 64);
+    const size_t BQ = static_cast<size_t>(B) * Hq;
+    (void)Hkv;
+    L.max_split = (N + T + kSplitRows - 1) / kSplitRows;
     size_t off = 0;
     L.po = off;
-    off = align_up(off + BQ * L.n_split * d * sizeof(float));
+    off = align_up(off + BQ * L.max_split * d * sizeof(float));
     L.pml = off;
-    off = align_up(off + BQ * L.n_split * 2 * sizeof(float));
+    off = align_up(off + BQ * L.max_split * 2 * sizeof(float));
     L.total = off;
     return L;
 }
@@ -303,7 +294,7 @@ santapp_status santapp_decode(const santapp_teams* t, const float* q, const void
     A.N = t->N;
     A.T = T;
     A.M = t->M;
-    A.n_split = L.n_split;
+    A.max_split = L.max_split;
     A.dtype = t->dtype;
     A.scale = static_cast<float>(scale);
     A.ws = ws;
@@ -334,6 +325,7 @@ santapp_status santapp_decode(const santapp_teams* t, const float* q, const void
         R.Hq = Hq;
         R.G = G;
         R.d = t->d;
+        R.N = t->N;
         R.M = t->M;
         R.Kp = Kp;
         R.T = T;
@@ -397,7 +389,7 @@ santapp_status santapp_dense_decode(const float* q, const void* K, const void* V
     A.N = N;
     A.T = T;
     A.M = 0;
-    A.n_split = L.n_split;
+    A.max_split = L.max_split;
     A.dtype = dtype;
     A.scale = static_cast<float>(scale);
     A.dense = true;

@@ -2,19 +2,27 @@
 //
 // k_attend  eq. method-estimate in log space: every row read gets the logit
 //           w_{h,i} = scale q_h.k_i - log c_{g(i),h} for each query head h of
-//           the KV head (-inf when h did not select the team; no correction
-//           for suffix rows and on the dense path), and an online softmax
-//           accumulates (m, l, acc) per head.  The rows of one KV head are
-//           split into n_split equal ranges over [union rows ; suffix rows];
-//           each workgroup owns one range and writes one partial per head.
-//           The query heads sharing the KV head share every K/V row load.
+//           the KV head (no weight when h did not select the team; no
+//           correction for suffix rows and on the dense path), and an online
+//           softmax accumulates (m, l, acc) per head.  The rows of one KV head,
+//           [union rows ; suffix rows], are cut into ranges of kSplitRows
+//           rows; one workgroup owns one range and writes one partial per
+//           head.  The query heads sharing the KV head share every K/V load.
 // k_merge   rescales the partials of a head to a common maximum and divides
 //           the weighted value sum by the mass.
 //
-// Inside a workgroup: 16 lanes per K/V row, each lane owns d/16 consecutive
-// dimensions (one 16-byte load per row and lane for bf16 at d = 128); the 16
-// row groups of the workgroup take rows round-robin.  Exponentials are base 2
-// with log2(e) folded into the query and the corrections.
+// Scores on the matrix cores: for a tile of 16 rows, S[head][row] = Q K^T
+// with the query heads of the KV head (padded to 16) as the M dimension.
+// bf16 keys use v_mfma_f32_16x16x32_bf16 with the fp32 query split into
+// three bf16 terms (exact to fp32 precision), fp32 keys v_mfma_f32_16x16x4_f32.
+// The softmax runs on the 16x16 accumulator (lanes = rows, registers =
+// heads); the value sum runs on the vector ALUs with every lane owning d/64
+// dimensions of all heads and the probabilities broadcast through LDS.
+// Exponentials are base 2 with log2(e) folded into the query and the
+// corrections.  "No weight" is the finite logit kNeg, so differences of
+// logits never form inf - inf; a state that only ever saw kNeg logits gets
+// weight exp2(kNeg - m) = 0 as soon as it meets a real logit, and every head
+// has at least one real logit.
 #include <math.h>
 
 #include "common.h"
@@ -24,273 +32,399 @@ namespace santapp {
 
 namespace {
 
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
 constexpr int kAttThreads = 256;
 constexpr int kAttWaves = kAttThreads / kWave;
-constexpr int kAttGroups = kAttThreads / 16;
-constexpr int kTileRows = kAttThreads;  // rows described per staging pass
-constexpr int kTileTeams = kTileRows + 1;
+constexpr int kWaveRows = kSplitRows / kAttWaves;  // 32 rows per wave
+constexpr int kTiles = kWaveRows / 16;             // two 16-row MFMA tiles
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kSlotSuffix = -2;
-constexpr int kSlotPlain = -1;
+constexpr float kNeg = -1.0e30f;   // logit of a row that carries no weight
+constexpr float kSkip = 1.0e30f;   // correction of a head that did not select the team
+constexpr int kMergeThreads = 256;
+constexpr int kMergeDims = 32;  // output dimensions per merge workgroup
 
-template <typename T, int DPL>
-struct RowChunk;
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Scale factor of a state with maximum m when rebased to mn.
+__device__ __forceinline__ float rebase(float m, float mn) { return fast_exp2(m - mn); }
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_max_step(float v) {
+    return fmaxf(v, dpp_f32<CTRL>(v));
+}
+
+__device__ __forceinline__ float row16_max(float v) {
+    v = dpp_max_step<0x128>(v);
+    v = dpp_max_step<0x124>(v);
+    v = dpp_max_step<0x122>(v);
+    v = dpp_max_step<0x121>(v);
+    return v;
+}
+
+// Scores of one 16-row tile.  Lane l = 16 c + j feeds row j of the tile and
+// holds head 4 c + r of row j in accumulator register r.
+template <typename T, int D>
+struct QK;
+
+template <int D>
+struct QK<bf16_t, D> {
+    // block kb, lane group c: 16-byte chunk 4 kb + c of the row (dims
+    // 8 (4 kb + c) .. + 8); the same dims of the query head l % 16
+    static constexpr int KB = D / 32;
+    using frag = uint4;
+    bf16x8 qa[KB][3];
+
+    __device__ __forceinline__ void load_q(const float* qrow, float scale, int c) {
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) {
+            const float4* p = reinterpret_cast<const float4*>(qrow + 8 * (4 * kb + c));
+            const float4 u = p[0], v = p[1];
+            const float x[8] = {u.x, u.y, u.z, u.w, v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float f = x[e] * scale;
+                const __bf16 a = static_cast<__bf16>(f);
+                const float r1 = f - static_cast<float>(a);
+                const __bf16 b = static_cast<__bf16>(r1);
+                const float r2 = r1 - static_cast<float>(b);
+                qa[kb][0][e] = a;
+                qa[kb][1][e] = b;
+                qa[kb][2][e] = static_cast<__bf16>(r2);
+            }
+        }
+    }
+    __device__ __forceinline__ void load_k(const bf16_t* row, int c, frag* f) const {
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) f[kb] = *reinterpret_cast<const uint4*>(row + 8 * (4 * kb + c));
+    }
+    __device__ __forceinline__ f32x4 scores(const frag* f) const {
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) {
+            const bf16x8 k = __builtin_bit_cast(bf16x8, f[kb]);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[kb][2], k, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[kb][1], k, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[kb][0], k, acc, 0, 0, 0);
+        }
+        return acc;
+    }
+};
+
+template <int D>
+struct QK<float, D> {
+    // block kb, lane group c: dim (D / 4) c + kb
+    static constexpr int KB = D / 4;
+    using frag = float4;
+    float qa[KB];
+
+    __device__ __forceinline__ void load_q(const float* qrow, float scale, int c) {
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) qa[kb] = qrow[(D / 4) * c + kb] * scale;
+    }
+    __device__ __forceinline__ void load_k(const float* row, int c, frag* f) const {
+#pragma unroll
+        for (int i = 0; i < KB / 4; ++i) f[i] = *reinterpret_cast<const float4*>(row + (D / 4) * c + 4 * i);
+    }
+    __device__ __forceinline__ f32x4 scores(const frag* f) const {
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int i = 0; i < KB / 4; ++i) {
+            const float k[4] = {f[i].x, f[i].y, f[i].z, f[i].w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[4 * i + e], k[e], acc, 0, 0, 0);
+        }
+        return acc;
+    }
+};
+
+template <typename T, int D>
+constexpr int frag_count() {
+    return sizeof(T) == 2 ? D / 32 : D / 16;
+}
+
+// d / 64 value dimensions per lane: dims DPV l .. DPV l + DPV - 1 of a row.
+template <typename T, int DPV>
+struct VPart;
 
 template <>
-struct RowChunk<bf16_t, 8> {  // d = 128: 8 bf16 = 16 bytes per lane
-    static __device__ __forceinline__ void load(const bf16_t* p, float* x) {
-        const uint4 u = *reinterpret_cast<const uint4*>(p);
-        x[0] = bf16lo(u.x); x[1] = bf16hi(u.x); x[2] = bf16lo(u.y); x[3] = bf16hi(u.y);
-        x[4] = bf16lo(u.z); x[5] = bf16hi(u.z); x[6] = bf16lo(u.w); x[7] = bf16hi(u.w);
+struct VPart<bf16_t, 2> {
+    using raw = uint32_t;
+    static __device__ __forceinline__ raw load(const bf16_t* row, int lane) {
+        return reinterpret_cast<const uint32_t*>(row)[lane];
+    }
+    static __device__ __forceinline__ void unpack(raw r, float* x) {
+        x[0] = bf16lo(r);
+        x[1] = bf16hi(r);
     }
 };
 
 template <>
-struct RowChunk<bf16_t, 4> {  // d = 64
-    static __device__ __forceinline__ void load(const bf16_t* p, float* x) {
-        const uint2 u = *reinterpret_cast<const uint2*>(p);
-        x[0] = bf16lo(u.x); x[1] = bf16hi(u.x); x[2] = bf16lo(u.y); x[3] = bf16hi(u.y);
+struct VPart<bf16_t, 1> {
+    using raw = uint16_t;
+    static __device__ __forceinline__ raw load(const bf16_t* row, int lane) { return row[lane].bits; }
+    static __device__ __forceinline__ void unpack(raw r, float* x) { x[0] = bf16_to_f32(r); }
+};
+
+template <>
+struct VPart<float, 2> {
+    using raw = float2;
+    static __device__ __forceinline__ raw load(const float* row, int lane) {
+        return reinterpret_cast<const float2*>(row)[lane];
+    }
+    static __device__ __forceinline__ void unpack(raw r, float* x) {
+        x[0] = r.x;
+        x[1] = r.y;
     }
 };
 
 template <>
-struct RowChunk<float, 8> {
-    static __device__ __forceinline__ void load(const float* p, float* x) {
-        const float4 a = *reinterpret_cast<const float4*>(p);
-        const float4 c = *reinterpret_cast<const float4*>(p + 4);
-        x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
-        x[4] = c.x; x[5] = c.y; x[6] = c.z; x[7] = c.w;
-    }
+struct VPart<float, 1> {
+    using raw = float;
+    static __device__ __forceinline__ raw load(const float* row, int lane) { return row[lane]; }
+    static __device__ __forceinline__ void unpack(raw r, float* x) { x[0] = r; }
 };
 
-template <>
-struct RowChunk<float, 4> {
-    static __device__ __forceinline__ void load(const float* p, float* x) {
-        const float4 a = *reinterpret_cast<const float4*>(p);
-        x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
-    }
-};
-
-// Scale factor of a state with maximum m when rebased to mn (-inf = empty).
-__device__ __forceinline__ float rebase(float m, float mn) {
-    return (m == -INFINITY) ? 0.f : exp2f(m - mn);
+// Rows of one KV head are [prompt rows ; suffix rows]; the prompt part holds
+// rows_u rows (the union rows of the plan, or all N rows on the dense path).
+__device__ __forceinline__ int split_count(int rows_u, int T_suf) {
+    return (rows_u + T_suf + kSplitRows - 1) / kSplitRows;
 }
 
 template <typename T, int D, int G, bool DENSE>
 __global__ __launch_bounds__(kAttThreads) void k_attend(
     const T* __restrict__ K, const T* __restrict__ V, const T* __restrict__ sK,
     const T* __restrict__ sV, const float* __restrict__ q, int N, int T_suf, int M, int Hkv,
-    int Hq, int Greal, float scale_log2, int n_split, const int* __restrict__ hdr,
-    const int* __restrict__ ubeg, const int* __restrict__ urs, const float* __restrict__ ulogc,
-    const int* __restrict__ split_team, float* __restrict__ part_o, float* __restrict__ part_ml) {
-    constexpr int DPL = D / 16;
-    __shared__ int s_src[kTileRows];
-    __shared__ int s_slot[kTileRows];
-    __shared__ int s_trs[kTileTeams + 1];
-    __shared__ int s_tbeg[kTileTeams];
-    __shared__ float s_tlc[kTileTeams][G];
-    __shared__ float s_m[kAttWaves][G];
-    __shared__ float s_l[kAttWaves][G];
+    int Hq, int Greal, float scale_log2, int max_split, const int* __restrict__ hdr,
+    const int2* __restrict__ rowmap, const float* __restrict__ ulogc,
+    float* __restrict__ part_o, float* __restrict__ part_ml) {
+    constexpr int DPV = D / 64;
+    constexpr int NF = frag_count<T, D>();
+    using QKT = QK<T, D>;
+    using VP = VPart<T, DPV>;
+    __shared__ int s_src[kSplitRows];  // prompt row, or -(suffix row) - 1
+    __shared__ float4 s_lc[kSplitRows][2];  // log2 corrections of heads 0..7
+    __shared__ float4 s_p[kAttWaves][16][2];  // probabilities of one tile
+    __shared__ float4 s_a[kAttWaves][2];      // rescale factors of one tile
+    __shared__ float s_m[kAttWaves][8];
+    __shared__ float s_l[kAttWaves][8];
     __shared__ float s_o[kAttWaves][G][D];
 
-    const int s = blockIdx.x;
-    const int bh = blockIdx.y;
+    const int bh = blockIdx.x;  // KV heads vary fastest: active ranges dispatch first
+    const int s = blockIdx.y;
     const int b = bh / Hkv, kv = bh - b * Hkv;
-    const int tid = threadIdx.x, grp = tid >> 4, sub = tid & 15;
-    const int lane = lane_id(), w = wave_id();
+    const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
+    const int c = lane >> 4, j16 = lane & 15;
 
-    int rows_u, U = 0;
-    if (DENSE) {
-        rows_u = N;
-    } else {
-        U = hdr[bh * 4 + 0];
-        rows_u = hdr[bh * 4 + 1];
+    // query fragments: head l % 16 of this KV head (zero for padding heads)
+    QKT qk;
+    {
+        const int h = j16;
+        const int hq = kv * Greal + (h < Greal ? h : 0);
+        qk.load_q(q + (static_cast<size_t>(b) * Hq + hq) * D, h < Greal ? scale_log2 : 0.f, c);
     }
+
+    const int rows_u = DENSE ? N : hdr[bh * 4 + 1];
     const int total = rows_u + T_suf;
-    const int L = (total + n_split - 1) / n_split;
-    const int r0 = min(s * L, total), r1 = min(r0 + L, total);
+    if (s >= split_count(rows_u, T_suf)) return;  // uniform: nothing to read here
+    const int r0 = s * kSplitRows;
+    const int nrows = min(kSplitRows, total - r0);
 
-    // the G query heads of this KV head, this lane's dimensions, in log2 units
-    float qr[G][DPL];
+    if (tid < kSplitRows) {
+        // rows past the range repeat the last row with no weight for any head
+        const int r = r0 + min(tid, nrows - 1);
+        float lcv[8];
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-        const int hq = kv * Greal + h;
+        for (int h = 0; h < 8; ++h) lcv[h] = (h < Greal && tid < nrows) ? 0.f : kSkip;
+        int src;
+        if (r < rows_u) {
+            if (DENSE) {
+                src = r;
+            } else {
+                const int2 e = rowmap[static_cast<size_t>(bh) * N + r];
+                src = e.x;
+                const float4* L = reinterpret_cast<const float4*>(
+                    ulogc + (static_cast<size_t>(bh) * M + e.y) * kLogcStride);
+                const float4 u = L[0], v = L[1];
+                const float x[8] = {u.x, u.y, u.z, u.w, v.x, v.y, v.z, v.w};
 #pragma unroll
-        for (int e = 0; e < DPL; ++e)
-            qr[h][e] = (h < Greal)
-                           ? q[(static_cast<size_t>(b) * Hq + hq) * D + sub * DPL + e] * scale_log2
-                           : 0.f;
+                for (int h = 0; h < 8; ++h)
+                    if (h < Greal && tid < nrows) lcv[h] = x[h] * kLog2e;
+            }
+        } else {
+            src = -(r - rows_u) - 1;
+        }
+        s_src[tid] = src;
+        s_lc[tid][0] = make_float4(lcv[0], lcv[1], lcv[2], lcv[3]);
+        s_lc[tid][1] = make_float4(lcv[4], lcv[5], lcv[6], lcv[7]);
     }
-    float m[G], l[G], o[G][DPL];
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-        m[h] = -INFINITY;
-        l[h] = 0.f;
-#pragma unroll
-        for (int e = 0; e < DPL; ++e) o[h][e] = 0.f;
-    }
+    __syncthreads();
 
     const T* Kb = K + static_cast<size_t>(bh) * N * D;
     const T* Vb = V + static_cast<size_t>(bh) * N * D;
     const T* sKb = sK + static_cast<size_t>(bh) * T_suf * D;
     const T* sVb = sV + static_cast<size_t>(bh) * T_suf * D;
-    const int* ursb = urs + static_cast<size_t>(bh) * (M + 1);
-    const int* ubegb = ubeg + static_cast<size_t>(bh) * M;
-    const float* ulcb = ulogc + static_cast<size_t>(bh) * M * kLogcStride;
-    int t0 = DENSE ? 0 : split_team[static_cast<size_t>(bh) * n_split + s];
+    const int wrow = w * kWaveRows;
 
-    for (int tile = r0; tile < r1; tile += kTileRows) {
-        const int nrows = min(kTileRows, r1 - tile);
-        const bool has_union = !DENSE && tile < rows_u;
-        if (has_union) {
-            // teams t0 .. t0 + kTileRows hold every union row of this tile
-            for (int j = tid; j <= kTileTeams; j += kAttThreads) {
-                const int t = t0 + j;
-                s_trs[j] = (t <= U) ? ursb[t] : 0x7fffffff;
-            }
-            for (int j = tid; j < kTileTeams; j += kAttThreads) {
-                const int t = t0 + j;
-                if (t < U) {
-                    s_tbeg[j] = ubegb[t];
+    // every K and V load of the wave's 32 rows is issued before any math
+    typename QKT::frag kf[kTiles][NF];
+    typename VP::raw vr[kWaveRows];
 #pragma unroll
-                    for (int h = 0; h < G; ++h) s_tlc[j][h] = ulcb[t * kLogcStride + h] * kLog2e;
-                }
-            }
-            __syncthreads();
-        }
-        if (tid < nrows) {
-            const int r = tile + tid;
-            int src, slot;
-            if (r < rows_u) {
-                if (DENSE) {
-                    src = r;
-                    slot = kSlotPlain;
-                } else {
-                    int lo = 0, hi = min(kTileTeams, U - t0) - 1;  // largest j: s_trs[j] <= r
-                    while (lo < hi) {
-                        const int mid = (lo + hi + 1) >> 1;
-                        if (s_trs[mid] <= r)
-                            lo = mid;
-                        else
-                            hi = mid - 1;
-                    }
-                    src = s_tbeg[lo] + (r - s_trs[lo]);
-                    slot = lo;
-                }
-            } else {
-                src = r - rows_u;
-                slot = kSlotSuffix;
-            }
-            s_src[tid] = src;
-            s_slot[tid] = slot;
-        }
-        __syncthreads();
-
-        for (int i = grp; i < nrows; i += kAttGroups) {
-            const int src = s_src[i], slot = s_slot[i];
-            const T* kp = (slot == kSlotSuffix) ? sKb : Kb;
-            const T* vp = (slot == kSlotSuffix) ? sVb : Vb;
-            float kx[DPL], vx[DPL];
-            RowChunk<T, DPL>::load(kp + static_cast<size_t>(src) * D + sub * DPL, kx);
-            RowChunk<T, DPL>::load(vp + static_cast<size_t>(src) * D + sub * DPL, vx);
-            float sc[G];
+    for (int t = 0; t < kTiles; ++t) {
+        const int src = s_src[wrow + 16 * t + j16];
+        const T* row = (src >= 0) ? Kb + static_cast<size_t>(src) * D
+                                  : sKb + static_cast<size_t>(-src - 1) * D;
+        qk.load_k(row, c, kf[t]);
+    }
 #pragma unroll
-            for (int h = 0; h < G; ++h) {
-                float a = 0.f;
-#pragma unroll
-                for (int e = 0; e < DPL; ++e) a = fmaf(qr[h][e], kx[e], a);
-                sc[h] = a;
-            }
-#pragma unroll
-            for (int h = 0; h < G; ++h) {
-#pragma unroll
-                for (int off = 8; off > 0; off >>= 1) sc[h] += __shfl_xor(sc[h], off, 16);
-            }
-#pragma unroll
-            for (int h = 0; h < G; ++h) {
-                const float wv = (slot >= 0) ? sc[h] - s_tlc[slot][h] : sc[h];
-                const float mn = fmaxf(m[h], wv);
-                if (mn == -INFINITY) continue;  // nothing accumulated and nothing to add
-                const float a = rebase(m[h], mn);
-                const float p = exp2f(wv - mn);  // 0 for a masked head
-                l[h] = l[h] * a + p;
-#pragma unroll
-                for (int e = 0; e < DPL; ++e) o[h][e] = fmaf(p, vx[e], o[h][e] * a);
-                m[h] = mn;
-            }
-        }
-        __syncthreads();
-        if (has_union && nrows == kTileRows) {
-            const int last = s_slot[kTileRows - 1];
-            if (last >= 0) t0 += last;  // team of the tile's last row
-        }
+    for (int i = 0; i < kWaveRows; ++i) {
+        const int src = s_src[wrow + i];
+        const T* row = (src >= 0) ? Vb + static_cast<size_t>(src) * D
+                                  : sVb + static_cast<size_t>(-src - 1) * D;
+        vr[i] = VP::load(row, lane);
     }
 
-    // merge the four row groups of each wave, then the waves
+    float m[4], l[4], acc[G][DPV];
 #pragma unroll
-    for (int off = 16; off < kWave; off <<= 1) {
+    for (int r = 0; r < 4; ++r) {
+        m[r] = kNeg;
+        l[r] = 0.f;
+    }
 #pragma unroll
-        for (int h = 0; h < G; ++h) {
-            const float m2 = __shfl_xor(m[h], off);
-            const float l2 = __shfl_xor(l[h], off);
-            float o2[DPL];
+    for (int h = 0; h < G; ++h)
 #pragma unroll
-            for (int e = 0; e < DPL; ++e) o2[e] = __shfl_xor(o[h][e], off);
-            const float mn = fmaxf(m[h], m2);
-            const float a = rebase(m[h], mn), c = rebase(m2, mn);
-            l[h] = l[h] * a + l2 * c;
+        for (int e = 0; e < DPV; ++e) acc[h][e] = 0.f;
+
 #pragma unroll
-            for (int e = 0; e < DPL; ++e) o[h][e] = o[h][e] * a + o2[e] * c;
-            m[h] = mn;
+    for (int t = 0; t < kTiles; ++t) {
+        const f32x4 sc = qk.scores(kf[t]);
+        // lane (c, j16): row j16 of the tile, heads 4 c .. 4 c + 3
+        const float4 lc = s_lc[wrow + 16 * t + j16][c & 1];
+        const float lcr[4] = {lc.x, lc.y, lc.z, lc.w};
+        float a[4], p[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const float x = (c < 2) ? sc[r] - lcr[r] : kNeg;
+            const float mn = fmaxf(m[r], row16_max(x));
+            a[r] = rebase(m[r], mn);
+            p[r] = fast_exp2(x - mn);
+            l[r] = l[r] * a[r] + row16_sum(p[r]);
+            m[r] = mn;
+        }
+        if (c < 2) {
+            s_p[w][j16][c] = make_float4(p[0], p[1], p[2], p[3]);
+            if (j16 == 0) s_a[w][c] = make_float4(a[0], a[1], a[2], a[3]);
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        {
+            const float4 a0 = s_a[w][0], a1 = s_a[w][1];
+            const float av[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+#pragma unroll
+            for (int h = 0; h < G; ++h)
+#pragma unroll
+                for (int e = 0; e < DPV; ++e) acc[h][e] *= av[h];
+        }
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            float v[DPV];
+            VP::unpack(vr[16 * t + j], v);
+            const float4 p0 = s_p[w][j][0], p1 = s_p[w][j][1];
+            const float pv[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+#pragma unroll
+            for (int h = 0; h < G; ++h)
+#pragma unroll
+                for (int e = 0; e < DPV; ++e) acc[h][e] = fmaf(pv[h], v[e], acc[h][e]);
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+
+    // per-wave state of each head, then the four waves combined
+    if (c < 2 && j16 == 0) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            s_m[w][4 * c + r] = m[r];
+            s_l[w][4 * c + r] = l[r];
         }
     }
-    if (lane < 16) {
 #pragma unroll
-        for (int h = 0; h < G; ++h) {
+    for (int h = 0; h < G; ++h)
 #pragma unroll
-            for (int e = 0; e < DPL; ++e) s_o[w][h][sub * DPL + e] = o[h][e];
-            if (lane == 0) {
-                s_m[w][h] = m[h];
-                s_l[w][h] = l[h];
-            }
-        }
-    }
+        for (int e = 0; e < DPV; ++e) s_o[w][h][DPV * lane + e] = acc[h][e];
     __syncthreads();
     for (int idx = tid; idx < Greal * D; idx += kAttThreads) {
-        const int h = idx / D, j = idx - h * D;
-        float mx = -INFINITY;
+        const int h = idx / D, jd = idx - h * D;
+        float mx = s_m[0][h];
 #pragma unroll
-        for (int v = 0; v < kAttWaves; ++v) mx = fmaxf(mx, s_m[v][h]);
+        for (int v = 1; v < kAttWaves; ++v) mx = fmaxf(mx, s_m[v][h]);
         float lsum = 0.f, osum = 0.f;
 #pragma unroll
         for (int v = 0; v < kAttWaves; ++v) {
             const float a = rebase(s_m[v][h], mx);
             lsum += s_l[v][h] * a;
-            osum += s_o[v][h][j] * a;
+            osum += s_o[v][h][jd] * a;
         }
-        const size_t pidx = (static_cast<size_t>(b) * Hq + kv * Greal + h) * n_split + s;
-        part_o[pidx * D + j] = osum;
-        if (j == 0) {
+        const size_t pidx = (static_cast<size_t>(b) * Hq + kv * Greal + h) * max_split + s;
+        part_o[pidx * D + jd] = osum;
+        if (jd == 0) {
             part_ml[pidx * 2 + 0] = mx;
             part_ml[pidx * 2 + 1] = lsum;
         }
     }
 }
 
-__global__ void k_merge(const float* __restrict__ part_o, const float* __restrict__ part_ml,
-                        int n_split, int D, float* __restrict__ out) {
-    const size_t bhq = blockIdx.x;
-    const int j = threadIdx.x;
-    const float* ml = part_ml + bhq * n_split * 2;
+// One workgroup per (sequence, query head, 32 output dimensions).
+__global__ __launch_bounds__(kMergeThreads) void k_merge(
+    const float* __restrict__ part_o, const float* __restrict__ part_ml,
+    const int* __restrict__ hdr, int N, int T_suf, int Hq, int Hkv, int max_split, int D,
+    float* __restrict__ out) {
+    __shared__ float s_red[kMergeThreads / kWave];
+    __shared__ float s_acc[kMergeThreads / kMergeDims][kMergeDims];
+    const int bhq = blockIdx.x;
+    const int b = bhq / Hq, h = bhq - b * Hq;
+    const int bh = b * Hkv + h / (Hq / Hkv);
+    const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
+    const int rows_u = hdr ? hdr[bh * 4 + 1] : N;
+    const int n = split_count(rows_u, T_suf);
+    const float* ml = part_ml + static_cast<size_t>(bhq) * max_split * 2;
+    const float* po = part_o + static_cast<size_t>(bhq) * max_split * D;
+
     float mx = -INFINITY;
-    for (int s = 0; s < n_split; ++s) mx = fmaxf(mx, ml[2 * s]);
-    float lsum = 0.f, osum = 0.f;
-    for (int s = 0; s < n_split; ++s) {
-        const float a = rebase(ml[2 * s], mx);
-        lsum += ml[2 * s + 1] * a;
-        osum += part_o[(bhq * n_split + s) * D + j] * a;
+    for (int s = tid; s < n; s += kMergeThreads) mx = fmaxf(mx, ml[2 * s]);
+    for (int off = kWave / 2; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+    if (lane == 0) s_red[w] = mx;
+    __syncthreads();
+    mx = s_red[0];
+    for (int v = 1; v < kMergeThreads / kWave; ++v) mx = fmaxf(mx, s_red[v]);
+    __syncthreads();
+
+    float lsum = 0.f;
+    for (int s = tid; s < n; s += kMergeThreads) lsum += ml[2 * s + 1] * rebase(ml[2 * s], mx);
+    for (int off = kWave / 2; off > 0; off >>= 1) lsum += __shfl_xor(lsum, off);
+    if (lane == 0) s_red[w] = lsum;
+    __syncthreads();
+    lsum = 0.f;
+    for (int v = 0; v < kMergeThreads / kWave; ++v) lsum += s_red[v];
+
+    const int j = blockIdx.y * kMergeDims + (tid % kMergeDims);
+    const int sl = tid / kMergeDims;
+    constexpr int kLanes = kMergeThreads / kMergeDims;
+    float acc = 0.f;
+#pragma unroll 4
+    for (int s = sl; s < n; s += kLanes) acc += po[static_cast<size_t>(s) * D + j] * rebase(ml[2 * s], mx);
+    s_acc[sl][tid % kMergeDims] = acc;
+    __syncthreads();
+    if (tid < kMergeDims) {
+        float t = 0.f;
+#pragma unroll
+        for (int v = 0; v < kLanes; ++v) t += s_acc[v][tid];
+        out[static_cast<size_t>(bhq) * D + blockIdx.y * kMergeDims + tid] = t / lsum;
     }
-    out[bhq * D + j] = osum / lsum;
 }
 
 __global__ void k_zero(uint4* __restrict__ p, size_t n16, unsigned char* __restrict__ tail,
@@ -303,7 +437,7 @@ __global__ void k_zero(uint4* __restrict__ p, size_t n16, unsigned char* __restr
 
 template <typename T, int D, int G>
 hipError_t attend_g(const AttendArgs& a, hipStream_t s) {
-    const dim3 grid(a.n_split, a.B * a.Hkv);
+    const dim3 grid(a.B * a.Hkv, a.max_split);
     const float sl2 = a.scale * kLog2e;
     const T* K = static_cast<const T*>(a.K);
     const T* V = static_cast<const T*>(a.V);
@@ -311,16 +445,14 @@ hipError_t attend_g(const AttendArgs& a, hipStream_t s) {
     const T* sV = static_cast<const T*>(a.sV);
     if (a.dense) {
         k_attend<T, D, G, true><<<grid, kAttThreads, 0, s>>>(
-            K, V, sK, sV, a.q, a.N, a.T, 0, a.Hkv, a.Hq, a.G, sl2, a.n_split, nullptr, nullptr,
-            nullptr, nullptr, nullptr, a.part_o, a.part_ml);
+            K, V, sK, sV, a.q, a.N, a.T, 0, a.Hkv, a.Hq, a.G, sl2, a.max_split, nullptr, nullptr,
+            nullptr, a.part_o, a.part_ml);
     } else {
         const DecodeLayout& L = *a.lay;
         k_attend<T, D, G, false><<<grid, kAttThreads, 0, s>>>(
-            K, V, sK, sV, a.q, a.N, a.T, a.M, a.Hkv, a.Hq, a.G, sl2, a.n_split,
-            reinterpret_cast<const int*>(a.ws + L.hdr), reinterpret_cast<const int*>(a.ws + L.ubeg),
-            reinterpret_cast<const int*>(a.ws + L.urs),
-            reinterpret_cast<const float*>(a.ws + L.ulogc),
-            reinterpret_cast<const int*>(a.ws + L.split), a.part_o, a.part_ml);
+            K, V, sK, sV, a.q, a.N, a.T, a.M, a.Hkv, a.Hq, a.G, sl2, a.max_split,
+            reinterpret_cast<const int*>(a.ws + L.hdr), reinterpret_cast<const int2*>(a.ws + L.rowmap),
+            reinterpret_cast<const float*>(a.ws + L.ulogc), a.part_o, a.part_ml);
     }
     return hipGetLastError();
 }
@@ -356,7 +488,10 @@ hipError_t launch_attend(const AttendArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_merge(const AttendArgs& a, hipStream_t s) {
-    k_merge<<<a.B * a.Hq, a.d, 0, s>>>(a.part_o, a.part_ml, a.n_split, a.d, a.out);
+    const int* hdr = a.dense ? nullptr : reinterpret_cast<const int*>(a.ws + a.lay->hdr);
+    const dim3 grid(a.B * a.Hq, a.d / kMergeDims);
+    k_merge<<<grid, kMergeThreads, 0, s>>>(a.part_o, a.part_ml, hdr, a.N, a.T, a.Hq, a.Hkv,
+                                           a.max_split, a.d, a.out);
     return hipGetLastError();
 }
 

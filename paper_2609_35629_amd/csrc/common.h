@@ -100,4 +100,37 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
 __device__ __forceinline__ int wave_id() { return threadIdx.x / kWave; }
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
 
+// DPP row rotations (within each 16-lane row of the wave): row_ror:n is
+// control word 0x120 + n.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v) {
+    const long long b = __double_as_longlong(v);
+    const int lo = __builtin_amdgcn_update_dpp(0, static_cast<int>(b & 0xffffffff), CTRL, 0xF, 0xF, false);
+    const int hi = __builtin_amdgcn_update_dpp(0, static_cast<int>(b >> 32), CTRL, 0xF, 0xF, false);
+    return __longlong_as_double((static_cast<long long>(hi) << 32) |
+                                static_cast<long long>(static_cast<unsigned>(lo)));
+}
+
+// Sum over the 16 lanes of a DPP row; every lane of the row receives it.
+__device__ __forceinline__ float row16_sum(float v) {
+    v += dpp_f32<0x128>(v);
+    v += dpp_f32<0x124>(v);
+    v += dpp_f32<0x122>(v);
+    v += dpp_f32<0x121>(v);
+    return v;
+}
+
+__device__ __forceinline__ double row16_sum(double v) {
+    v += dpp_f64<0x128>(v);
+    v += dpp_f64<0x124>(v);
+    v += dpp_f64<0x122>(v);
+    v += dpp_f64<0x121>(v);
+    return v;
+}
+
 }  // namespace santapp

@@ -16,11 +16,15 @@ constexpr int kMaxGroup = 8;       // query heads per KV head (8-bit head masks)
 constexpr int kLogcStride = 8;     // floats per union team in the read plan
 
 // Workspace layout of santapp_decode; byte offsets into the caller's buffer.
+// Rows of one KV head are [union rows ; suffix rows]; the attention kernel
+// splits them into ranges of at most kSplitRows rows, so the number of
+// partials per head is at most max_split = ceil((N + T) / kSplitRows).
 struct DecodeLayout {
-    int n_split = 0;
-    size_t phi = 0, Y = 0, lc = 0, hdr = 0, ubeg = 0, urs = 0, ulogc = 0, split = 0, po = 0,
-           pml = 0, total = 0;
+    int max_split = 0;
+    size_t phi = 0, Y = 0, lc = 0, hdr = 0, ulogc = 0, rowmap = 0, po = 0, pml = 0, total = 0;
 };
+
+constexpr int kSplitRows = 128;  // rows per attention workgroup (16 groups x 8 rows)
 
 DecodeLayout decode_layout(int B, int Hq, int Hkv, int N, int T, int d, int M);
 DecodeLayout dense_layout(int B, int Hq, int Hkv, int N, int T, int d);
@@ -37,7 +41,7 @@ struct RouteArgs {
     const int* team_size;   // [BH, M]
     const int* team_begin;  // [BH, M]
     const float* q;         // [B, Hq, d]
-    int B, Hkv, Hq, G, d, M, Kp, T;
+    int B, Hkv, Hq, G, d, N, M, Kp, T;
     santapp_dtype dtype;
     double scale;
     uint64_t seed, step;
@@ -55,14 +59,14 @@ struct AttendArgs {
     const void* sK;   // [BH, T, d]
     const void* sV;
     const float* q;   // [B, Hq, d]
-    int B, Hkv, Hq, G, d, N, T, M, n_split;
+    int B, Hkv, Hq, G, d, N, T, M, max_split;
     santapp_dtype dtype;
     float scale;
     bool dense;                 // every row, every head, correction 1
     const char* ws;             // plan (sampled path)
     const DecodeLayout* lay;    // plan offsets (sampled path)
-    float* part_o;              // [B, Hq, n_split, d]
-    float* part_ml;             // [B, Hq, n_split, 2]
+    float* part_o;              // [B, Hq, max_split, d]
+    float* part_ml;             // [B, Hq, max_split, 2]
     float* out;                 // [B, Hq, d]
 };
 
