@@ -21,6 +21,7 @@ Prints one JSON line.
 from __future__ import annotations
 
 import argparse
+import ctypes
 import json
 import math
 import os
@@ -92,27 +93,33 @@ def main():
         sp.dense_decode(db["q"], db["K"], db["V"], db["sK"], db["sV"], scale=wl.scale, out=dense_out,
                         workspace=dense_ws)
 
+    hev = HipEvents(sp._lib.load())
+
     def timed(fn, n, warm, with_stages):
         for i in range(warm):
             fn(i)
         warm = max(warm, args.warmup)
-        torch.cuda.synchronize()
-        ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
-        ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
-        stages = []
-        dbgs = [sp.DebugOut(wl.B, wl.Hq, wl.Hkv, M, wl.K, arrays=False, events=True)
-                for _ in range(n)] if with_stages else [None] * n
+        stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        ev0 = [hev.make() for _ in range(n)]
+        ev1 = [hev.make() for _ in range(n)]
+        marks = [[hev.make() for _ in range(4)] for _ in range(n)] if with_stages else None
+        dbgs = [None] * n
+        if with_stages:
+            dbgs = [sp.DebugOut(wl.B, wl.Hq, wl.Hkv, M, wl.K, arrays=False) for _ in range(n)]
+            for d, mk in zip(dbgs, marks):
+                d.raw_events = mk
         torch.cuda.synchronize()
         for i in range(n):
             if not args.no_evict:
                 evict.add_(1.0)
-            ev0[i].record()
+            hev.record(ev0[i], stream)
             fn(warm + i, dbgs[i])
-            ev1[i].record()
+            hev.record(ev1[i], stream)
         torch.cuda.synchronize()
-        times = np.array([a.elapsed_time(b) * 1e3 for a, b in zip(ev0, ev1)])  # us
+        times = np.array([hev.us(a, b) for a, b in zip(ev0, ev1)])
+        stages = []
         if with_stages:
-            stages = np.array([[x * 1e3 for x in d.stage_ms()] for d in dbgs])
+            stages = np.array([[hev.us(mk[k], mk[k + 1]) for k in range(3)] for mk in marks])
         return times, stages
 
     torch.cuda.synchronize()
@@ -194,6 +201,44 @@ def main():
     if cpu is not None:
         res["cpu_baseline"] = cpu
     print(json.dumps(res), flush=True)
+
+
+class HipEvents:
+    """HIP events recorded with a device-scope release: the default event
+    record also writes back and invalidates the caches at system scope, which
+    adds several microseconds to every bracketed interval."""
+    RELEASE_TO_DEVICE = 0x40000000
+
+    def __init__(self, lib):
+        import ctypes
+        self.c = ctypes
+        self.L = lib
+        vp = ctypes.c_void_p
+        lib.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(vp), ctypes.c_uint]
+        lib.hipEventRecord.argtypes = [vp, vp]
+        lib.hipEventSynchronize.argtypes = [vp]
+        lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), vp, vp]
+        lib.hipEventDestroy.argtypes = [vp]
+        for f in (lib.hipEventCreateWithFlags, lib.hipEventRecord, lib.hipEventSynchronize,
+                  lib.hipEventElapsedTime, lib.hipEventDestroy):
+            f.restype = ctypes.c_int
+
+    def make(self):
+        e = self.c.c_void_p()
+        if self.L.hipEventCreateWithFlags(self.c.byref(e), self.RELEASE_TO_DEVICE) != 0:
+            raise RuntimeError("hipEventCreateWithFlags failed")
+        return e
+
+    def record(self, e, stream):
+        if self.L.hipEventRecord(e, stream) != 0:
+            raise RuntimeError("hipEventRecord failed")
+
+    def us(self, a, b):
+        t = self.c.c_float()
+        self.L.hipEventSynchronize(b)
+        if self.L.hipEventElapsedTime(self.c.byref(t), a, b) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return t.value * 1e3
 
 
 def upload(batch):

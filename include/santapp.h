@@ -68,6 +68,7 @@ typedef struct {
     const void* reps;        /* [B,Hkv,M,d] representative key of each team  */
     const int* team_begin;   /* [B,Hkv,M] first packed row of each team      */
     const int* team_size;    /* [B,Hkv,M] n_g                                */
+    const double* log_n;     /* [B,Hkv,M] log n_g (fp64)                     */
     const int* rep_token;    /* [B,Hkv,M] original token index of l_g        */
     const int* perm;         /* [B,Hkv,N] packed row -> original token index */
 } santapp_teams_desc;

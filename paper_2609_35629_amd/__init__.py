@@ -167,6 +167,7 @@ class DebugOut:
             self.union_teams = torch.zeros((B, Hkv), dtype=torch.int32, device=dev)
             self.union_rows = torch.zeros((B, Hkv), dtype=torch.int32, device=dev)
         self.events = None
+        self.raw_events = None  # caller-created hipEvent_t handles (ctypes.c_void_p)
         if events:
             # torch creates the underlying HIP event at its first record
             self.events = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
@@ -186,6 +187,9 @@ class DebugOut:
         if self.events is not None:
             for i, ev in enumerate(self.events):
                 d.events[i] = ev.cuda_event
+        if self.raw_events is not None:
+            for i, ev in enumerate(self.raw_events):
+                d.events[i] = ev.value
         return d
 
 

@@ -28,7 +28,7 @@ class TeamsDesc(ctypes.Structure):
         ("M", ctypes.c_int),
         ("packed_K", ctypes.c_void_p), ("packed_V", ctypes.c_void_p), ("reps", ctypes.c_void_p),
         ("team_begin", ctypes.c_void_p), ("team_size", ctypes.c_void_p),
-        ("rep_token", ctypes.c_void_p), ("perm", ctypes.c_void_p),
+        ("log_n", ctypes.c_void_p), ("rep_token", ctypes.c_void_p), ("perm", ctypes.c_void_p),
     ]
 
 

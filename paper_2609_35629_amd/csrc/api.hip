@@ -18,6 +18,7 @@ struct santapp_teams {
     void* reps;
     int* team_begin;
     int* team_size;
+    double* log_n;
     int* rep_token;
     int* perm;
 };
@@ -59,15 +60,22 @@ long long team_count(int N, int P, int R) {
     return (np - 1) * std::min<long long>(R, P) + std::min<long long>(R, last);
 }
 
+// Release device memory on clean-up paths, where a failure to free cannot be
+// reported any better than the error already being returned.
+void release(void* p) {
+    if (p) (void)hipFree(p);
+}
+
 void free_teams(santapp_teams* t) {
     if (!t) return;
-    hipFree(t->packed_K);
-    hipFree(t->packed_V);
-    hipFree(t->reps);
-    hipFree(t->team_begin);
-    hipFree(t->team_size);
-    hipFree(t->rep_token);
-    hipFree(t->perm);
+    release(t->packed_K);
+    release(t->packed_V);
+    release(t->reps);
+    release(t->team_begin);
+    release(t->team_size);
+    release(t->log_n);
+    release(t->rep_token);
+    release(t->perm);
     delete t;
 }
 
@@ -89,8 +97,10 @@ DecodeLayout decode_layout(int B, int Hq, int Hkv, int N, int T, int d, int M) {
     L.Y = take(BQ * M * sizeof(double));
     L.lc = take(BQ * M * sizeof(float));
     L.hdr = take(BH * 4 * sizeof(int));
+    L.ubeg = take(BH * M * sizeof(int));
+    L.urs = take(BH * (M + 1) * sizeof(int));
     L.ulogc = take(BH * M * kLogcStride * sizeof(float));
-    L.rowmap = take(BH * N * 2 * sizeof(int));
+    L.split = take(BH * L.max_split * sizeof(int));
     L.po = take(BQ * L.max_split * d * sizeof(float));
     L.pml = take(BQ * L.max_split * 2 * sizeof(float));
     L.total = off;
@@ -171,21 +181,22 @@ santapp_status santapp_build_teams(const void* K, const void* V, int B, int Hkv,
     alloc(&t->reps, BH * M * row);
     alloc(reinterpret_cast<void**>(&t->team_begin), BH * M * sizeof(int));
     alloc(reinterpret_cast<void**>(&t->team_size), BH * M * sizeof(int));
+    alloc(reinterpret_cast<void**>(&t->log_n), BH * M * sizeof(double));
     alloc(reinterpret_cast<void**>(&t->rep_token), BH * M * sizeof(int));
     alloc(reinterpret_cast<void**>(&t->perm), BH * N * sizeof(int));
     alloc(reinterpret_cast<void**>(&mind), BH * N * sizeof(double));
     alloc(reinterpret_cast<void**>(&owner), BH * N * sizeof(int));
     if (e != hipSuccess) {
-        hipFree(mind);
-        hipFree(owner);
+        release(mind);
+        release(owner);
         free_teams(t);
         (void)hipGetLastError();
         return fail(SANTAPP_ENOMEM, "device allocation failed: %s", hipGetErrorString(e));
     }
     const char* what = "team build";
     e = launch_build_parents(K, dtype, static_cast<int>(BH), N, d, parent_size, reps_per_parent,
-                             t->M, mind, owner, t->team_begin, t->team_size, t->rep_token, t->perm,
-                             s);
+                             t->M, mind, owner, t->team_begin, t->team_size, t->log_n,
+                             t->rep_token, t->perm, s);
     if (e == hipSuccess) {
         what = "packing K";
         e = launch_gather_rows(K, t->packed_K, t->perm, static_cast<int>(BH), N, N, row, s);
@@ -202,8 +213,8 @@ santapp_status santapp_build_teams(const void* K, const void* V, int B, int Hkv,
         what = "team build sync";
         e = hipStreamSynchronize(s);
     }
-    hipFree(mind);
-    hipFree(owner);
+    release(mind);
+    release(owner);
     if (e != hipSuccess) {
         free_teams(t);
         return hip_fail(e, what);
@@ -227,6 +238,7 @@ santapp_status santapp_teams_info(const santapp_teams* t, santapp_teams_desc* d)
     d->reps = t->reps;
     d->team_begin = t->team_begin;
     d->team_size = t->team_size;
+    d->log_n = t->log_n;
     d->rep_token = t->rep_token;
     d->perm = t->perm;
     return ok();
@@ -318,6 +330,7 @@ santapp_status santapp_decode(const santapp_teams* t, const float* q, const void
         RouteArgs R{};
         R.reps = t->reps;
         R.team_size = t->team_size;
+        R.log_n = t->log_n;
         R.team_begin = t->team_begin;
         R.q = q;
         R.B = t->B;

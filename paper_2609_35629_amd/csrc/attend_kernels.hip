@@ -16,8 +16,9 @@
 // bf16 keys use v_mfma_f32_16x16x32_bf16 with the fp32 query split into
 // three bf16 terms (exact to fp32 precision), fp32 keys v_mfma_f32_16x16x4_f32.
 // The softmax runs on the 16x16 accumulator (lanes = rows, registers =
-// heads); the value sum runs on the vector ALUs with every lane owning d/64
-// dimensions of all heads and the probabilities broadcast through LDS.
+// heads); the value sum runs on the vector ALUs with 16 lanes per row, each
+// owning d/16 dimensions of all heads, and the probabilities broadcast
+// through LDS.
 // Exponentials are base 2 with log2(e) folded into the query and the
 // corrections.  "No weight" is the finite logit kNeg, so differences of
 // logits never form inf - inf; a state that only ever saw kNeg logits gets
@@ -145,46 +146,59 @@ constexpr int frag_count() {
     return sizeof(T) == 2 ? D / 32 : D / 16;
 }
 
-// d / 64 value dimensions per lane: dims DPV l .. DPV l + DPV - 1 of a row.
-template <typename T, int DPV>
-struct VPart;
+// d / 16 consecutive value dims of a row for one of 16 lanes.
+template <typename T, int VPL>
+struct RowChunk;
 
 template <>
-struct VPart<bf16_t, 2> {
-    using raw = uint32_t;
-    static __device__ __forceinline__ raw load(const bf16_t* row, int lane) {
-        return reinterpret_cast<const uint32_t*>(row)[lane];
+struct RowChunk<bf16_t, 8> {  // d = 128: 8 bf16 = 16 bytes per lane
+    using raw = uint4;
+    static __device__ __forceinline__ raw load(const bf16_t* p) {
+        return *reinterpret_cast<const uint4*>(p);
     }
-    static __device__ __forceinline__ void unpack(raw r, float* x) {
-        x[0] = bf16lo(r);
-        x[1] = bf16hi(r);
-    }
-};
-
-template <>
-struct VPart<bf16_t, 1> {
-    using raw = uint16_t;
-    static __device__ __forceinline__ raw load(const bf16_t* row, int lane) { return row[lane].bits; }
-    static __device__ __forceinline__ void unpack(raw r, float* x) { x[0] = bf16_to_f32(r); }
-};
-
-template <>
-struct VPart<float, 2> {
-    using raw = float2;
-    static __device__ __forceinline__ raw load(const float* row, int lane) {
-        return reinterpret_cast<const float2*>(row)[lane];
-    }
-    static __device__ __forceinline__ void unpack(raw r, float* x) {
-        x[0] = r.x;
-        x[1] = r.y;
+    static __device__ __forceinline__ void unpack(const raw& u, float* x) {
+        x[0] = bf16lo(u.x); x[1] = bf16hi(u.x); x[2] = bf16lo(u.y); x[3] = bf16hi(u.y);
+        x[4] = bf16lo(u.z); x[5] = bf16hi(u.z); x[6] = bf16lo(u.w); x[7] = bf16hi(u.w);
     }
 };
 
 template <>
-struct VPart<float, 1> {
-    using raw = float;
-    static __device__ __forceinline__ raw load(const float* row, int lane) { return row[lane]; }
-    static __device__ __forceinline__ void unpack(raw r, float* x) { x[0] = r; }
+struct RowChunk<bf16_t, 4> {  // d = 64
+    using raw = uint2;
+    static __device__ __forceinline__ raw load(const bf16_t* p) {
+        return *reinterpret_cast<const uint2*>(p);
+    }
+    static __device__ __forceinline__ void unpack(const raw& u, float* x) {
+        x[0] = bf16lo(u.x); x[1] = bf16hi(u.x); x[2] = bf16lo(u.y); x[3] = bf16hi(u.y);
+    }
+};
+
+template <>
+struct RowChunk<float, 8> {
+    struct raw {
+        float4 a, b;
+    };
+    static __device__ __forceinline__ raw load(const float* p) {
+        raw r;
+        r.a = *reinterpret_cast<const float4*>(p);
+        r.b = *reinterpret_cast<const float4*>(p + 4);
+        return r;
+    }
+    static __device__ __forceinline__ void unpack(const raw& r, float* x) {
+        x[0] = r.a.x; x[1] = r.a.y; x[2] = r.a.z; x[3] = r.a.w;
+        x[4] = r.b.x; x[5] = r.b.y; x[6] = r.b.z; x[7] = r.b.w;
+    }
+};
+
+template <>
+struct RowChunk<float, 4> {
+    using raw = float4;
+    static __device__ __forceinline__ raw load(const float* p) {
+        return *reinterpret_cast<const float4*>(p);
+    }
+    static __device__ __forceinline__ void unpack(const raw& r, float* x) {
+        x[0] = r.x; x[1] = r.y; x[2] = r.z; x[3] = r.w;
+    }
 };
 
 // Rows of one KV head are [prompt rows ; suffix rows]; the prompt part holds
@@ -198,16 +212,20 @@ __global__ __launch_bounds__(kAttThreads) void k_attend(
     const T* __restrict__ K, const T* __restrict__ V, const T* __restrict__ sK,
     const T* __restrict__ sV, const float* __restrict__ q, int N, int T_suf, int M, int Hkv,
     int Hq, int Greal, float scale_log2, int max_split, const int* __restrict__ hdr,
-    const int2* __restrict__ rowmap, const float* __restrict__ ulogc,
-    float* __restrict__ part_o, float* __restrict__ part_ml) {
-    constexpr int DPV = D / 64;
+    const int* __restrict__ split_team, const int* __restrict__ ubeg,
+    const int* __restrict__ urs, const float* __restrict__ ulogc, float* __restrict__ part_o,
+    float* __restrict__ part_ml) {
     constexpr int NF = frag_count<T, D>();
+    constexpr int VPL = D / 16;  // value dims per lane (16 lanes per row)
     using QKT = QK<T, D>;
-    using VP = VPart<T, DPV>;
-    __shared__ int s_src[kSplitRows];  // prompt row, or -(suffix row) - 1
-    __shared__ float4 s_lc[kSplitRows][2];  // log2 corrections of heads 0..7
-    __shared__ float4 s_p[kAttWaves][16][2];  // probabilities of one tile
-    __shared__ float4 s_a[kAttWaves][2];      // rescale factors of one tile
+    using VC = RowChunk<T, VPL>;
+    __shared__ int s_src[kSplitRows];          // prompt row, or -(suffix row) - 1
+    __shared__ float4 s_lc[kSplitRows][2];     // log2 corrections of heads 0..7
+    __shared__ int s_trs[kSplitRows + 1];      // union slice: first row of each team
+    __shared__ int s_tbeg[kSplitRows];         //   its first packed row
+    __shared__ float4 s_tlc[kSplitRows][2];    //   its corrections
+    __shared__ float4 s_p[kAttWaves][16][2];   // probabilities of one tile
+    __shared__ float4 s_a[kAttWaves][2];       // rescale factors of one tile
     __shared__ float s_m[kAttWaves][8];
     __shared__ float s_l[kAttWaves][8];
     __shared__ float s_o[kAttWaves][G][D];
@@ -218,6 +236,13 @@ __global__ __launch_bounds__(kAttThreads) void k_attend(
     const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
     const int c = lane >> 4, j16 = lane & 15;
 
+    // plan header and the first union team of this range, in one round trip
+    int rows_u = N, U = 0, t0 = 0;
+    if (!DENSE) {
+        U = hdr[bh * 4 + 0];
+        rows_u = hdr[bh * 4 + 1];
+        t0 = split_team[static_cast<size_t>(bh) * max_split + s];
+    }
     // query fragments: head l % 16 of this KV head (zero for padding heads)
     QKT qk;
     {
@@ -225,13 +250,27 @@ __global__ __launch_bounds__(kAttThreads) void k_attend(
         const int hq = kv * Greal + (h < Greal ? h : 0);
         qk.load_q(q + (static_cast<size_t>(b) * Hq + hq) * D, h < Greal ? scale_log2 : 0.f, c);
     }
-
-    const int rows_u = DENSE ? N : hdr[bh * 4 + 1];
     const int total = rows_u + T_suf;
     if (s >= split_count(rows_u, T_suf)) return;  // uniform: nothing to read here
     const int r0 = s * kSplitRows;
     const int nrows = min(kSplitRows, total - r0);
 
+    if (!DENSE && r0 < rows_u) {
+        // union teams t0 .. t0 + kSplitRows - 1 hold every union row of the range
+        const int* ursb = urs + static_cast<size_t>(bh) * (M + 1);
+        for (int j = tid; j <= kSplitRows; j += kAttThreads) {
+            const int t = t0 + j;
+            s_trs[j] = (t <= U) ? ursb[t] : 0x7fffffff;
+        }
+        if (tid < kSplitRows) {
+            const int t = min(t0 + tid, U - 1);
+            s_tbeg[tid] = ubeg[static_cast<size_t>(bh) * M + t];
+            const float4* L = reinterpret_cast<const float4*>(ulogc + (static_cast<size_t>(bh) * M + t) * kLogcStride);
+            s_tlc[tid][0] = L[0];
+            s_tlc[tid][1] = L[1];
+        }
+        __syncthreads();
+    }
     if (tid < kSplitRows) {
         // rows past the range repeat the last row with no weight for any head
         const int r = r0 + min(tid, nrows - 1);
@@ -243,11 +282,16 @@ __global__ __launch_bounds__(kAttThreads) void k_attend(
             if (DENSE) {
                 src = r;
             } else {
-                const int2 e = rowmap[static_cast<size_t>(bh) * N + r];
-                src = e.x;
-                const float4* L = reinterpret_cast<const float4*>(
-                    ulogc + (static_cast<size_t>(bh) * M + e.y) * kLogcStride);
-                const float4 u = L[0], v = L[1];
+                int lo = 0, hi = min(kSplitRows, U - t0) - 1;  // largest j with s_trs[j] <= r
+                while (lo < hi) {
+                    const int mid = (lo + hi + 1) >> 1;
+                    if (s_trs[mid] <= r)
+                        lo = mid;
+                    else
+                        hi = mid - 1;
+                }
+                src = s_tbeg[lo] + (r - s_trs[lo]);
+                const float4 u = s_tlc[lo][0], v = s_tlc[lo][1];
                 const float x[8] = {u.x, u.y, u.z, u.w, v.x, v.y, v.z, v.w};
 #pragma unroll
                 for (int h = 0; h < 8; ++h)
@@ -268,9 +312,11 @@ __global__ __launch_bounds__(kAttThreads) void k_attend(
     const T* sVb = sV + static_cast<size_t>(bh) * T_suf * D;
     const int wrow = w * kWaveRows;
 
-    // every K and V load of the wave's 32 rows is issued before any math
+    // every K and V load of the wave's 32 rows is issued before any math:
+    // K as MFMA fragments (lane (c, j) -> row j of a 16-row tile), V with 16
+    // lanes per row (lane (c, j) -> dims VPL j .. of rows c, c + 4, ...)
     typename QKT::frag kf[kTiles][NF];
-    typename VP::raw vr[kWaveRows];
+    typename VC::raw vr[kWaveRows / 4];
 #pragma unroll
     for (int t = 0; t < kTiles; ++t) {
         const int src = s_src[wrow + 16 * t + j16];
@@ -279,14 +325,14 @@ __global__ __launch_bounds__(kAttThreads) void k_attend(
         qk.load_k(row, c, kf[t]);
     }
 #pragma unroll
-    for (int i = 0; i < kWaveRows; ++i) {
-        const int src = s_src[wrow + i];
+    for (int k = 0; k < kWaveRows / 4; ++k) {
+        const int src = s_src[wrow + 4 * k + c];
         const T* row = (src >= 0) ? Vb + static_cast<size_t>(src) * D
                                   : sVb + static_cast<size_t>(-src - 1) * D;
-        vr[i] = VP::load(row, lane);
+        vr[k] = VC::load(row + VPL * j16);
     }
 
-    float m[4], l[4], acc[G][DPV];
+    float m[4], l[4], acc[G][VPL];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         m[r] = kNeg;
@@ -295,7 +341,7 @@ __global__ __launch_bounds__(kAttThreads) void k_attend(
 #pragma unroll
     for (int h = 0; h < G; ++h)
 #pragma unroll
-        for (int e = 0; e < DPV; ++e) acc[h][e] = 0.f;
+        for (int e = 0; e < VPL; ++e) acc[h][e] = 0.f;
 
 #pragma unroll
     for (int t = 0; t < kTiles; ++t) {
@@ -326,25 +372,35 @@ __global__ __launch_bounds__(kAttThreads) void k_attend(
 #pragma unroll
             for (int h = 0; h < G; ++h)
 #pragma unroll
-                for (int e = 0; e < DPV; ++e) acc[h][e] *= av[h];
+                for (int e = 0; e < VPL; ++e) acc[h][e] *= av[h];
         }
+        // this lane group's rows of the tile: c, c + 4, c + 8, c + 12
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-            float v[DPV];
-            VP::unpack(vr[16 * t + j], v);
-            const float4 p0 = s_p[w][j][0], p1 = s_p[w][j][1];
+        for (int kk = 0; kk < 4; ++kk) {
+            float v[VPL];
+            VC::unpack(vr[4 * t + kk], v);
+            const float4 p0 = s_p[w][4 * kk + c][0], p1 = s_p[w][4 * kk + c][1];
             const float pv[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
 #pragma unroll
             for (int h = 0; h < G; ++h)
 #pragma unroll
-                for (int e = 0; e < DPV; ++e) acc[h][e] = fmaf(pv[h], v[e], acc[h][e]);
+                for (int e = 0; e < VPL; ++e) acc[h][e] = fmaf(pv[h], v[e], acc[h][e]);
         }
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
 
-    // per-wave state of each head, then the four waves combined
+    // the four lane groups share each head's maximum: their sums simply add
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+        for (int e = 0; e < VPL; ++e) {
+            float x = acc[h][e];
+            x += __shfl_xor(x, 16);
+            x += __shfl_xor(x, 32);
+            acc[h][e] = x;
+        }
     if (c < 2 && j16 == 0) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -352,10 +408,12 @@ __global__ __launch_bounds__(kAttThreads) void k_attend(
             s_l[w][4 * c + r] = l[r];
         }
     }
+    if (c == 0) {
 #pragma unroll
-    for (int h = 0; h < G; ++h)
+        for (int h = 0; h < G; ++h)
 #pragma unroll
-        for (int e = 0; e < DPV; ++e) s_o[w][h][DPV * lane + e] = acc[h][e];
+            for (int e = 0; e < VPL; ++e) s_o[w][h][VPL * j16 + e] = acc[h][e];
+    }
     __syncthreads();
     for (int idx = tid; idx < Greal * D; idx += kAttThreads) {
         const int h = idx / D, jd = idx - h * D;
@@ -446,12 +504,13 @@ hipError_t attend_g(const AttendArgs& a, hipStream_t s) {
     if (a.dense) {
         k_attend<T, D, G, true><<<grid, kAttThreads, 0, s>>>(
             K, V, sK, sV, a.q, a.N, a.T, 0, a.Hkv, a.Hq, a.G, sl2, a.max_split, nullptr, nullptr,
-            nullptr, a.part_o, a.part_ml);
+            nullptr, nullptr, nullptr, a.part_o, a.part_ml);
     } else {
         const DecodeLayout& L = *a.lay;
         k_attend<T, D, G, false><<<grid, kAttThreads, 0, s>>>(
             K, V, sK, sV, a.q, a.N, a.T, a.M, a.Hkv, a.Hq, a.G, sl2, a.max_split,
-            reinterpret_cast<const int*>(a.ws + L.hdr), reinterpret_cast<const int2*>(a.ws + L.rowmap),
+            reinterpret_cast<const int*>(a.ws + L.hdr), reinterpret_cast<const int*>(a.ws + L.split),
+            reinterpret_cast<const int*>(a.ws + L.ubeg), reinterpret_cast<const int*>(a.ws + L.urs),
             reinterpret_cast<const float*>(a.ws + L.ulogc), a.part_o, a.part_ml);
     }
     return hipGetLastError();

@@ -66,7 +66,7 @@ template <typename T>
 __global__ __launch_bounds__(kBuildThreads) void k_build_parent(
     const T* __restrict__ K, int N, int d, int P, int R, int M, double* __restrict__ mind_all,
     int* __restrict__ owner_all, int* __restrict__ team_begin, int* __restrict__ team_size,
-    int* __restrict__ rep_token, int* __restrict__ perm) {
+    double* __restrict__ log_n, int* __restrict__ rep_token, int* __restrict__ perm) {
 #pragma clang fp contract(off)
     __shared__ double s_vec[kMaxHeadDim];
     __shared__ ArgVal s_red[kBuildWaves];
@@ -158,6 +158,7 @@ __global__ __launch_bounds__(kBuildThreads) void k_build_parent(
     for (int u = tid; u < r; u += kBuildThreads) {
         team_begin[tbase + u] = start + s_off[u];
         team_size[tbase + u] = s_cnt[u];
+        log_n[tbase + u] = log(static_cast<double>(s_cnt[u]));
         rep_token[tbase + u] = start + s_reps[u];
     }
 
@@ -213,16 +214,17 @@ __global__ __launch_bounds__(256) void k_gather_rows(const uint4* __restrict__ s
 
 hipError_t launch_build_parents(const void* K, santapp_dtype dtype, int BH, int N, int d, int P,
                                 int R, int M, double* mind, int* owner, int* team_begin,
-                                int* team_size, int* rep_token, int* perm, hipStream_t s) {
+                                int* team_size, double* log_n, int* rep_token, int* perm,
+                                hipStream_t s) {
     const dim3 grid((N + P - 1) / P, BH);
     if (dtype == SANTAPP_BF16)
         k_build_parent<bf16_t><<<grid, kBuildThreads, 0, s>>>(
             static_cast<const bf16_t*>(K), N, d, P, R, M, mind, owner, team_begin, team_size,
-            rep_token, perm);
+            log_n, rep_token, perm);
     else
         k_build_parent<float><<<grid, kBuildThreads, 0, s>>>(
             static_cast<const float*>(K), N, d, P, R, M, mind, owner, team_begin, team_size,
-            rep_token, perm);
+            log_n, rep_token, perm);
     return hipGetLastError();
 }
 

@@ -47,7 +47,10 @@ __device__ __forceinline__ u64x4 philox4x64_10(uint64_t c0, uint64_t c1, uint64_
                                                uint64_t k0, uint64_t k1) {
     const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
     const uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
-#pragma unroll
+    // kept rolled: the round is a handful of 64-bit multiplies and the loop
+    // overhead is one scalar add and branch, so unrolling buys little code
+    // speed for ten times the code size
+#pragma unroll 1
     for (int r = 0; r < 10; ++r) {
         if (r) {
             k0 += W0;
@@ -76,7 +79,10 @@ __device__ __forceinline__ u64x4 philox4x64_10(uint64_t c0, uint64_t c1, uint64_
 __device__ __forceinline__ double team_gumbel(uint64_t seed, uint64_t step, uint64_t b, uint64_t h,
                                               uint64_t g) {
     const u64x4 r = philox4x64_10(g >> 2, h, b, step, seed, 0);
-    const uint64_t w = r.v[g & 3];
+    // word g % 4 by selects: an indexed read of the array would go through
+    // memory
+    const int sel = static_cast<int>(g & 3);
+    const uint64_t w = sel == 0 ? r.v[0] : sel == 1 ? r.v[1] : sel == 2 ? r.v[2] : r.v[3];
     const double u = (static_cast<double>(w >> 12) + 0.5) * 0x1.0p-52;
     return -log(-log(u));
 }
@@ -124,6 +130,92 @@ __device__ __forceinline__ float row16_sum(float v) {
     v += dpp_f32<0x121>(v);
     return v;
 }
+
+// Inclusive prefix sum over the 64 lanes of the wave (row shifts inside each
+// 16-lane row, then row broadcasts of lane 15 and lane 31).
+__device__ __forceinline__ int wave_incl_scan(int x) {
+    x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, true);  // row_shr:1
+    x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, true);  // row_shr:2
+    x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, true);  // row_shr:4
+    x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, true);  // row_shr:8
+    x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);  // row_bcast:15
+    x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);  // row_bcast:31
+    return x;
+}
+
+__device__ __forceinline__ int readlane(int x, int lane) { return __builtin_amdgcn_readlane(x, lane); }
+
+__device__ __forceinline__ uint64_t readlane(uint64_t x, int lane) {
+    const uint32_t lo = __builtin_amdgcn_readlane(static_cast<int>(x & 0xffffffffu), lane);
+    const uint32_t hi = __builtin_amdgcn_readlane(static_cast<int>(x >> 32), lane);
+    return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+// Sum over all 64 lanes; the result is wave-uniform.
+__device__ __forceinline__ int wave_sum(int x) {
+    x += __builtin_amdgcn_update_dpp(0, x, 0x128, 0xF, 0xF, false);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x124, 0xF, 0xF, false);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x122, 0xF, 0xF, false);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x121, 0xF, 0xF, false);
+    return readlane(x, 0) + readlane(x, 16) + readlane(x, 32) + readlane(x, 48);
+}
+
+template <bool kAnd>
+__device__ __forceinline__ uint32_t wave_bits32(uint32_t x) {
+    int v = static_cast<int>(x);
+#define SANTAPP_BITSTEP(CTRL)                                                            \
+    {                                                                                    \
+        const int t = __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);         \
+        v = kAnd ? (v & t) : (v | t);                                                    \
+    }
+    SANTAPP_BITSTEP(0x128)
+    SANTAPP_BITSTEP(0x124)
+    SANTAPP_BITSTEP(0x122)
+    SANTAPP_BITSTEP(0x121)
+#undef SANTAPP_BITSTEP
+    const uint32_t a = readlane(v, 0), b = readlane(v, 16), c = readlane(v, 32), d = readlane(v, 48);
+    return kAnd ? (a & b & c & d) : (a | b | c | d);
+}
+
+// Bitwise AND / OR of a 64-bit value over all 64 lanes (wave-uniform).
+__device__ __forceinline__ uint64_t wave_and64(uint64_t x) {
+    return (static_cast<uint64_t>(wave_bits32<true>(static_cast<uint32_t>(x >> 32))) << 32) |
+           wave_bits32<true>(static_cast<uint32_t>(x));
+}
+
+__device__ __forceinline__ uint64_t wave_or64(uint64_t x) {
+    return (static_cast<uint64_t>(wave_bits32<false>(static_cast<uint32_t>(x >> 32))) << 32) |
+           wave_bits32<false>(static_cast<uint32_t>(x));
+}
+
+template <bool kMin>
+__device__ __forceinline__ uint64_t wave_ext64(uint64_t x) {
+#define SANTAPP_EXTSTEP(CTRL)                                                                    \
+    {                                                                                            \
+        const uint32_t lo = __builtin_amdgcn_update_dpp(0, static_cast<int>(x & 0xffffffffu), CTRL, \
+                                                        0xF, 0xF, false);                         \
+        const uint32_t hi = __builtin_amdgcn_update_dpp(0, static_cast<int>(x >> 32), CTRL, 0xF,  \
+                                                        0xF, false);                              \
+        const uint64_t y = (static_cast<uint64_t>(hi) << 32) | lo;                               \
+        x = kMin ? (y < x ? y : x) : (y > x ? y : x);                                            \
+    }
+    SANTAPP_EXTSTEP(0x128)
+    SANTAPP_EXTSTEP(0x124)
+    SANTAPP_EXTSTEP(0x122)
+    SANTAPP_EXTSTEP(0x121)
+#undef SANTAPP_EXTSTEP
+    uint64_t r = readlane(x, 0);
+#pragma unroll
+    for (int row = 1; row < 4; ++row) {
+        const uint64_t y = readlane(x, 16 * row);
+        r = kMin ? (y < r ? y : r) : (y > r ? y : r);
+    }
+    return r;
+}
+
+// Unsigned 64-bit minimum / maximum over all 64 lanes (wave-uniform).
+__device__ __forceinline__ uint64_t wave_min64(uint64_t x) { return wave_ext64<true>(x); }
+__device__ __forceinline__ uint64_t wave_max64(uint64_t x) { return wave_ext64<false>(x); }
 
 __device__ __forceinline__ double row16_sum(double v) {
     v += dpp_f64<0x128>(v);

@@ -21,7 +21,8 @@ constexpr int kLogcStride = 8;     // floats per union team in the read plan
 // partials per head is at most max_split = ceil((N + T) / kSplitRows).
 struct DecodeLayout {
     int max_split = 0;
-    size_t phi = 0, Y = 0, lc = 0, hdr = 0, ulogc = 0, rowmap = 0, po = 0, pml = 0, total = 0;
+    size_t phi = 0, Y = 0, lc = 0, hdr = 0, ubeg = 0, urs = 0, ulogc = 0, split = 0, po = 0,
+           pml = 0, total = 0;
 };
 
 constexpr int kSplitRows = 128;  // rows per attention workgroup (16 groups x 8 rows)
@@ -31,7 +32,8 @@ DecodeLayout dense_layout(int B, int Hq, int Hkv, int N, int T, int d);
 
 hipError_t launch_build_parents(const void* K, santapp_dtype dtype, int BH, int N, int d, int P,
                                 int R, int M, double* mind, int* owner, int* team_begin,
-                                int* team_size, int* rep_token, int* perm, hipStream_t s);
+                                int* team_size, double* log_n, int* rep_token, int* perm,
+                                hipStream_t s);
 
 hipError_t launch_gather_rows(const void* src, void* dst, const int* index, int BH, int rows_out,
                               int rows_in, size_t row_bytes, hipStream_t s);
@@ -40,6 +42,7 @@ struct RouteArgs {
     const void* reps;       // [BH, M, d]
     const int* team_size;   // [BH, M]
     const int* team_begin;  // [BH, M]
+    const double* log_n;    // [BH, M]
     const float* q;         // [B, Hq, d]
     int B, Hkv, Hq, G, d, N, M, Kp, T;
     santapp_dtype dtype;
