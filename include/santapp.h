@@ -129,8 +129,10 @@ typedef struct {
 
 /*
  * Workspace for santapp_decode with these sizes (bytes, host-only query).
- * The workspace must be zero-filled before its first use (for instance with
- * santapp_workspace_zero); the library keeps that state between calls.
+ * It holds the step's routing scores, read plan and partial results; every
+ * entry a call reads is written earlier in the same call, so it needs no
+ * initialisation.  Calls that share a workspace must not overlap in time (use
+ * one workspace per stream).
  */
 santapp_status santapp_decode_workspace_bytes(const santapp_teams* teams, int Hq, int T, int K,
                                               size_t* bytes);

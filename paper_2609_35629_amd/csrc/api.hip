@@ -5,7 +5,9 @@
 #include <stdio.h>
 
 #include <algorithm>
+#include <functional>
 #include <string>
+#include <vector>
 
 #include "internal.h"
 
@@ -21,6 +23,10 @@ struct santapp_teams {
     double* log_n;
     int* rep_token;
     int* perm;
+    // cap[x]: the most attention chunks any x distinct teams of one (b, kv)
+    // need (sum of their x largest chunk counts, maximum over (b, kv))
+    std::vector<int> cap;
+    int cus;  // compute units of the device the handle was built on
 };
 
 namespace {
@@ -83,10 +89,12 @@ void free_teams(santapp_teams* t) {
 
 namespace santapp {
 
-DecodeLayout decode_layout(int B, int Hq, int Hkv, int N, int T, int d, int M) {
+DecodeLayout decode_layout(int B, int Hq, int Hkv, int T, int d, int M, int Kp, const int* cap) {
     DecodeLayout L;
     const size_t BH = static_cast<size_t>(B) * Hkv, BQ = static_cast<size_t>(B) * Hq;
-    L.max_split = (N + T + kSplitRows - 1) / kSplitRows;
+    const int G = Hq / Hkv;
+    const long long xs = std::min<long long>(M, static_cast<long long>(G) * Kp);
+    L.max_chunks = cap[xs] + chunk_count(T);
     size_t off = 0;
     auto take = [&](size_t bytes) {
         const size_t at = off;
@@ -96,13 +104,11 @@ DecodeLayout decode_layout(int B, int Hq, int Hkv, int N, int T, int d, int M) {
     L.phi = take(BQ * M * sizeof(double));
     L.Y = take(BQ * M * sizeof(double));
     L.lc = take(BQ * M * sizeof(float));
-    L.hdr = take(BH * 4 * sizeof(int));
-    L.ubeg = take(BH * M * sizeof(int));
-    L.urs = take(BH * (M + 1) * sizeof(int));
+    L.hdr = take(BH * sizeof(PlanHeader));
+    L.chunk = take(BH * L.max_chunks * sizeof(Chunk));
     L.ulogc = take(BH * M * kLogcStride * sizeof(float));
-    L.split = take(BH * L.max_split * sizeof(int));
-    L.po = take(BQ * L.max_split * d * sizeof(float));
-    L.pml = take(BQ * L.max_split * 2 * sizeof(float));
+    L.po = take(BQ * L.max_chunks * d * sizeof(float));
+    L.pml = take(BQ * L.max_chunks * 2 * sizeof(float));
     L.total = off;
     return L;
 }
@@ -111,12 +117,12 @@ DecodeLayout dense_layout(int B, int Hq, int Hkv, int N, int T, int d) {
     DecodeLayout L;
     const size_t BQ = static_cast<size_t>(B) * Hq;
     (void)Hkv;
-    L.max_split = (N + T + kSplitRows - 1) / kSplitRows;
+    L.max_chunks = dense_count(N) + dense_count(T);
     size_t off = 0;
     L.po = off;
-    off = align_up(off + BQ * L.max_split * d * sizeof(float));
+    off = align_up(off + BQ * L.max_chunks * d * sizeof(float));
     L.pml = off;
-    off = align_up(off + BQ * L.max_split * 2 * sizeof(float));
+    off = align_up(off + BQ * L.max_chunks * 2 * sizeof(float));
     L.total = off;
     return L;
 }
@@ -215,9 +221,32 @@ santapp_status santapp_build_teams(const void* K, const void* V, int B, int Hkv,
     }
     release(mind);
     release(owner);
+    std::vector<int> sizes;
+    if (e == hipSuccess) {
+        what = "team size copy";
+        sizes.resize(BH * t->M);
+        e = hipMemcpy(sizes.data(), t->team_size, sizes.size() * sizeof(int), hipMemcpyDeviceToHost);
+    }
     if (e != hipSuccess) {
         free_teams(t);
         return hip_fail(e, what);
+    }
+    int dev = 0;
+    t->cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&t->cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        t->cus = 0;
+    (void)hipGetLastError();
+    t->cap.assign(t->M + 1, 0);
+    std::vector<int> cnt(t->M);
+    for (size_t bh = 0; bh < BH; ++bh) {
+        for (int g = 0; g < t->M; ++g) cnt[g] = chunk_count(sizes[bh * t->M + g]);
+        std::sort(cnt.begin(), cnt.end(), std::greater<int>());
+        int run = 0;
+        for (int x = 1; x <= t->M; ++x) {
+            run += cnt[x - 1];
+            t->cap[x] = std::max(t->cap[x], run);
+        }
     }
     *out = t;
     return ok();
@@ -258,7 +287,9 @@ santapp_status santapp_decode_workspace_bytes(const santapp_teams* t, int Hq, in
     if (!t || !bytes) return fail(SANTAPP_EINVAL, "NULL argument");
     if (Hq < 1 || Hq % t->Hkv != 0) return fail(SANTAPP_EINVAL, "Hq must be a positive multiple of Hkv");
     if (T < 0 || K < 1) return fail(SANTAPP_EINVAL, "T must be >= 0 and K >= 1");
-    *bytes = decode_layout(t->B, Hq, t->Hkv, t->N, T, t->d, t->M).total;
+    const int Kp = std::min(K, t->M);
+    *bytes = Kp == t->M ? dense_layout(t->B, Hq, t->Hkv, t->N, T, t->d).total
+                        : decode_layout(t->B, Hq, t->Hkv, T, t->d, t->M, Kp, t->cap.data()).total;
     return ok();
 }
 
@@ -285,12 +316,13 @@ santapp_status santapp_decode(const santapp_teams* t, const float* q, const void
     if (K < 1) return fail(SANTAPP_EINVAL, "K must be >= 1 (got %d)", K);
     if (!(scale >= 0.0) || !isfinite(scale)) return fail(SANTAPP_EINVAL, "scale must be finite and >= 0");
     if (scale == 0.0) scale = 1.0 / sqrt(static_cast<double>(t->d));
-    const DecodeLayout L = decode_layout(t->B, Hq, t->Hkv, t->N, T, t->d, t->M);
+    const int Kp = std::min(K, t->M);
+    const DecodeLayout L = Kp == t->M ? dense_layout(t->B, Hq, t->Hkv, t->N, T, t->d)
+                                      : decode_layout(t->B, Hq, t->Hkv, T, t->d, t->M, Kp, t->cap.data());
     if (!workspace || ws_bytes < L.total)
         return fail(SANTAPP_EWORKSPACE, "workspace of %zu bytes needed (got %zu)", L.total, ws_bytes);
     hipStream_t s = static_cast<hipStream_t>(stream);
     char* ws = static_cast<char*>(workspace);
-    const int Kp = std::min(K, t->M);
 
     AttendArgs A{};
     A.K = t->packed_K;
@@ -306,7 +338,8 @@ santapp_status santapp_decode(const santapp_teams* t, const float* q, const void
     A.N = t->N;
     A.T = T;
     A.M = t->M;
-    A.max_split = L.max_split;
+    A.max_chunks = L.max_chunks;
+    A.grid_y = t->cus > 0 ? std::max(1, (t->cus * kAttendWavesPerCU + t->B * t->Hkv - 1) / (t->B * t->Hkv)) : 0;
     A.dtype = t->dtype;
     A.scale = static_cast<float>(scale);
     A.ws = ws;
@@ -338,7 +371,6 @@ santapp_status santapp_decode(const santapp_teams* t, const float* q, const void
         R.Hq = Hq;
         R.G = G;
         R.d = t->d;
-        R.N = t->N;
         R.M = t->M;
         R.Kp = Kp;
         R.T = T;
@@ -349,8 +381,7 @@ santapp_status santapp_decode(const santapp_teams* t, const float* q, const void
         R.lay = &L;
         R.ws = ws;
         R.dbg = dbg;
-        if ((e = launch_route(R, s)) != hipSuccess) return hip_fail(e, "routing kernel");
-        if ((e = launch_select(R, s)) != hipSuccess) return hip_fail(e, "sampling kernel");
+        if ((e = launch_route_select(R, s)) != hipSuccess) return hip_fail(e, "routing and sampling kernel");
         if (dbg && dbg->phi &&
             (e = hipMemcpyAsync(dbg->phi, ws + L.phi, sizeof(double) * t->B * Hq * t->M,
                                 hipMemcpyDeviceToDevice, s)) != hipSuccess)
@@ -402,7 +433,7 @@ santapp_status santapp_dense_decode(const float* q, const void* K, const void* V
     A.N = N;
     A.T = T;
     A.M = 0;
-    A.max_split = L.max_split;
+    A.max_chunks = L.max_chunks;
     A.dtype = dtype;
     A.scale = static_cast<float>(scale);
     A.dense = true;

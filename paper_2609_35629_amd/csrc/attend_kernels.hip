@@ -1,15 +1,18 @@
-// Split-K attention over the read plan, and the split merge.
+// Attention over the read plan, and the merge of the chunk partials.
 //
-// k_attend  eq. method-estimate in log space: every row read gets the logit
-//           w_{h,i} = scale q_h.k_i - log c_{g(i),h} for each query head h of
-//           the KV head (no weight when h did not select the team; no
-//           correction for suffix rows and on the dense path), and an online
-//           softmax accumulates (m, l, acc) per head.  The rows of one KV head,
-//           [union rows ; suffix rows], are cut into ranges of kSplitRows
-//           rows; one workgroup owns one range and writes one partial per
-//           head.  The query heads sharing the KV head share every K/V load.
-// k_merge   rescales the partials of a head to a common maximum and divides
-//           the weighted value sum by the mass.
+// k_attend  eq. method-estimate in log space.  One workgroup reads one chunk:
+//           up to kChunkRows consecutive packed rows of one union team, or of
+//           the suffix.  Every query head h of the KV head that selected the
+//           team gets the logits w_{h,i} = scale q_h.k_i over the chunk's rows
+//           and an online softmax state (m, l, acc); all rows of a chunk
+//           belong to one team, so the team's correction -log c_{g,h} enters
+//           as a shift of the state's maximum.  Heads that did not select the
+//           team skip the value sum and leave an empty state.  The query heads
+//           sharing the KV head share every K/V load.  The dense path (and the
+//           full budget) cuts [prompt rows ; suffix rows] into chunks with
+//           every head and no correction.
+// k_merge   rescales the chunk states of a head to a common maximum and
+//           divides the weighted value sum by the mass.
 //
 // Scores on the matrix cores: for a tile of 16 rows, S[head][row] = Q K^T
 // with the query heads of the KV head (padded to 16) as the M dimension.
@@ -22,9 +25,10 @@
 // Exponentials are base 2 with log2(e) folded into the query and the
 // corrections.  "No weight" is the finite logit kNeg, so differences of
 // logits never form inf - inf; a state that only ever saw kNeg logits gets
-// weight exp2(kNeg - m) = 0 as soon as it meets a real logit, and every head
-// has at least one real logit.
+// weight exp2(kNeg - m) = 0 as soon as it meets a real logit.
 #include <math.h>
+
+#include <algorithm>
 
 #include "common.h"
 #include "internal.h"
@@ -36,15 +40,16 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kAttThreads = 256;
-constexpr int kAttWaves = kAttThreads / kWave;
-constexpr int kWaveRows = kSplitRows / kAttWaves;  // 32 rows per wave
-constexpr int kTiles = kWaveRows / 16;             // two 16-row MFMA tiles
+static_assert(kChunkRows == 32, "a sampled unit is two 16-row tiles of one wave");
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNeg = -1.0e30f;   // logit of a row that carries no weight
-constexpr float kSkip = 1.0e30f;   // correction of a head that did not select the team
-constexpr int kMergeThreads = 256;
-constexpr int kMergeDims = 32;  // output dimensions per merge workgroup
+constexpr float kEmpty = -1.0e29f; // chunk states with a maximum below this are empty
+
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
@@ -72,42 +77,51 @@ struct QK;
 template <int D>
 struct QK<bf16_t, D> {
     // block kb, lane group c: 16-byte chunk 4 kb + c of the row (dims
-    // 8 (4 kb + c) .. + 8); the same dims of the query head l % 16
+    // 8 (4 kb + c) .. + 8); the same dims of the query head l % 16.  The
+    // query fragments (three bf16 terms per fp32 value, exact to fp32) live
+    // in LDS, shared by the workgroup's waves: sq[(kb * 3 + t) * 64 + lane].
     static constexpr int KB = D / 32;
+    static constexpr int kLdsFrags = KB * 3 * kWave;
     using frag = uint4;
-    bf16x8 qa[KB][3];
+    const bf16x8* sq;
 
-    __device__ __forceinline__ void load_q(const float* qrow, float scale, int c) {
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb) {
+    // fragments of lane `lane` for blocks kb = kb0, kb0 + step, ...
+    static __device__ __forceinline__ void build(bf16x8* s, const float* qrow, float scale, int lane,
+                                                 int kb0, int step) {
+        const int c = lane >> 4;
+        for (int kb = kb0; kb < KB; kb += step) {
             const float4* p = reinterpret_cast<const float4*>(qrow + 8 * (4 * kb + c));
             const float4 u = p[0], v = p[1];
             const float x[8] = {u.x, u.y, u.z, u.w, v.x, v.y, v.z, v.w};
+            bf16x8 a, b, r;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const float f = x[e] * scale;
-                const __bf16 a = static_cast<__bf16>(f);
-                const float r1 = f - static_cast<float>(a);
-                const __bf16 b = static_cast<__bf16>(r1);
-                const float r2 = r1 - static_cast<float>(b);
-                qa[kb][0][e] = a;
-                qa[kb][1][e] = b;
-                qa[kb][2][e] = static_cast<__bf16>(r2);
+                const __bf16 h0 = static_cast<__bf16>(f);
+                const float r1 = f - static_cast<float>(h0);
+                const __bf16 h1 = static_cast<__bf16>(r1);
+                const float r2 = r1 - static_cast<float>(h1);
+                a[e] = h0;
+                b[e] = h1;
+                r[e] = static_cast<__bf16>(r2);
             }
+            s[(kb * 3 + 0) * kWave + lane] = a;
+            s[(kb * 3 + 1) * kWave + lane] = b;
+            s[(kb * 3 + 2) * kWave + lane] = r;
         }
     }
     __device__ __forceinline__ void load_k(const bf16_t* row, int c, frag* f) const {
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb) f[kb] = *reinterpret_cast<const uint4*>(row + 8 * (4 * kb + c));
+        for (int kb = 0; kb < KB; ++kb) f[kb] = load_stream(row + 8 * (4 * kb + c));
     }
-    __device__ __forceinline__ f32x4 scores(const frag* f) const {
+    __device__ __forceinline__ f32x4 scores(const frag* f, int lane) const {
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb) {
             const bf16x8 k = __builtin_bit_cast(bf16x8, f[kb]);
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[kb][2], k, acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[kb][1], k, acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[kb][0], k, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sq[(kb * 3 + 2) * kWave + lane], k, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sq[(kb * 3 + 1) * kWave + lane], k, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sq[(kb * 3 + 0) * kWave + lane], k, acc, 0, 0, 0);
         }
         return acc;
     }
@@ -115,8 +129,9 @@ struct QK<bf16_t, D> {
 
 template <int D>
 struct QK<float, D> {
-    // block kb, lane group c: dim (D / 4) c + kb
+    // block kb, lane group c: dim (D / 4) c + kb; the query stays in registers
     static constexpr int KB = D / 4;
+    static constexpr int kLdsFrags = 1;
     using frag = float4;
     float qa[KB];
 
@@ -126,9 +141,9 @@ struct QK<float, D> {
     }
     __device__ __forceinline__ void load_k(const float* row, int c, frag* f) const {
 #pragma unroll
-        for (int i = 0; i < KB / 4; ++i) f[i] = *reinterpret_cast<const float4*>(row + (D / 4) * c + 4 * i);
+        for (int i = 0; i < KB / 4; ++i) f[i] = load_stream_f(row + (D / 4) * c + 4 * i);
     }
-    __device__ __forceinline__ f32x4 scores(const frag* f) const {
+    __device__ __forceinline__ f32x4 scores(const frag* f, int) const {
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int i = 0; i < KB / 4; ++i) {
@@ -153,9 +168,7 @@ struct RowChunk;
 template <>
 struct RowChunk<bf16_t, 8> {  // d = 128: 8 bf16 = 16 bytes per lane
     using raw = uint4;
-    static __device__ __forceinline__ raw load(const bf16_t* p) {
-        return *reinterpret_cast<const uint4*>(p);
-    }
+    static __device__ __forceinline__ raw load(const bf16_t* p) { return load_stream(p); }
     static __device__ __forceinline__ void unpack(const raw& u, float* x) {
         x[0] = bf16lo(u.x); x[1] = bf16hi(u.x); x[2] = bf16lo(u.y); x[3] = bf16hi(u.y);
         x[4] = bf16lo(u.z); x[5] = bf16hi(u.z); x[6] = bf16lo(u.w); x[7] = bf16hi(u.w);
@@ -165,9 +178,7 @@ struct RowChunk<bf16_t, 8> {  // d = 128: 8 bf16 = 16 bytes per lane
 template <>
 struct RowChunk<bf16_t, 4> {  // d = 64
     using raw = uint2;
-    static __device__ __forceinline__ raw load(const bf16_t* p) {
-        return *reinterpret_cast<const uint2*>(p);
-    }
+    static __device__ __forceinline__ raw load(const bf16_t* p) { return load_stream8(p); }
     static __device__ __forceinline__ void unpack(const raw& u, float* x) {
         x[0] = bf16lo(u.x); x[1] = bf16hi(u.x); x[2] = bf16lo(u.y); x[3] = bf16hi(u.y);
     }
@@ -180,8 +191,8 @@ struct RowChunk<float, 8> {
     };
     static __device__ __forceinline__ raw load(const float* p) {
         raw r;
-        r.a = *reinterpret_cast<const float4*>(p);
-        r.b = *reinterpret_cast<const float4*>(p + 4);
+        r.a = load_stream_f(p);
+        r.b = load_stream_f(p + 4);
         return r;
     }
     static __device__ __forceinline__ void unpack(const raw& r, float* x) {
@@ -193,295 +204,365 @@ struct RowChunk<float, 8> {
 template <>
 struct RowChunk<float, 4> {
     using raw = float4;
-    static __device__ __forceinline__ raw load(const float* p) {
-        return *reinterpret_cast<const float4*>(p);
-    }
+    static __device__ __forceinline__ raw load(const float* p) { return load_stream_f(p); }
     static __device__ __forceinline__ void unpack(const raw& r, float* x) {
         x[0] = r.x; x[1] = r.y; x[2] = r.z; x[3] = r.w;
     }
 };
 
-// Rows of one KV head are [prompt rows ; suffix rows]; the prompt part holds
-// rows_u rows (the union rows of the plan, or all N rows on the dense path).
-__device__ __forceinline__ int split_count(int rows_u, int T_suf) {
-    return (rows_u + T_suf + kSplitRows - 1) / kSplitRows;
-}
-
-template <typename T, int D, int G, bool DENSE>
-__global__ __launch_bounds__(kAttThreads) void k_attend(
+// One wave per workgroup.  The sampled path's units are chunks of at most
+// kChunkRows (32) consecutive rows of one union team or of the suffix, so
+// that every chunk of a step is resident at once and no wave waits for
+// another; the dense path's units are kDenseRows (128) rows, walked 32 rows
+// at a time with the softmax state carried along.  Workgroup (bh, y) takes
+// units y, y + gridDim.y, ... of KV head bh, a loop bounded by the plan's
+// unit count.
+template <typename T, int D, int GT, bool DENSE>
+__global__ __launch_bounds__(kWave) void k_attend(
     const T* __restrict__ K, const T* __restrict__ V, const T* __restrict__ sK,
-    const T* __restrict__ sV, const float* __restrict__ q, int N, int T_suf, int M, int Hkv,
-    int Hq, int Greal, float scale_log2, int max_split, const int* __restrict__ hdr,
-    const int* __restrict__ split_team, const int* __restrict__ ubeg,
-    const int* __restrict__ urs, const float* __restrict__ ulogc, float* __restrict__ part_o,
-    float* __restrict__ part_ml) {
+    const T* __restrict__ sV, const float* __restrict__ q, int N, int T_suf, int Hkv, int Hq,
+    int G, int M, float scale_log2, int max_chunks, const PlanHeader* __restrict__ hdr,
+    const Chunk* __restrict__ chunks, const float* __restrict__ ulogc,
+    float* __restrict__ part_o, float* __restrict__ part_ml) {
     constexpr int NF = frag_count<T, D>();
     constexpr int VPL = D / 16;  // value dims per lane (16 lanes per row)
+    constexpr int UR = DENSE ? kDenseRows : kChunkRows;
     using QKT = QK<T, D>;
     using VC = RowChunk<T, VPL>;
-    __shared__ int s_src[kSplitRows];          // prompt row, or -(suffix row) - 1
-    __shared__ float4 s_lc[kSplitRows][2];     // log2 corrections of heads 0..7
-    __shared__ int s_trs[kSplitRows + 1];      // union slice: first row of each team
-    __shared__ int s_tbeg[kSplitRows];         //   its first packed row
-    __shared__ float4 s_tlc[kSplitRows][2];    //   its corrections
-    __shared__ float4 s_p[kAttWaves][16][2];   // probabilities of one tile
-    __shared__ float4 s_a[kAttWaves][2];       // rescale factors of one tile
-    __shared__ float s_m[kAttWaves][8];
-    __shared__ float s_l[kAttWaves][8];
-    __shared__ float s_o[kAttWaves][G][D];
+    constexpr bool kLdsQ = sizeof(T) == 2;
+    __shared__ bf16x8 s_q[QKT::kLdsFrags];  // query fragments (bf16 keys)
+    __shared__ float4 s_p[16][2];           // probabilities of one tile
+    __shared__ float4 s_a[2];               // rescale factors of one tile
 
-    const int bh = blockIdx.x;  // KV heads vary fastest: active ranges dispatch first
-    const int s = blockIdx.y;
+    const int bh = blockIdx.x;  // KV heads vary fastest
     const int b = bh / Hkv, kv = bh - b * Hkv;
-    const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
+    const int lane = lane_id();
     const int c = lane >> 4, j16 = lane & 15;
+    const int ncp = (N + UR - 1) / UR;
+    auto dense_chunk = [&](int ci) {
+        const bool suf = ci >= ncp;
+        const int begin = (suf ? ci - ncp : ci) * UR;
+        return Chunk{begin, min(UR, (suf ? T_suf : N) - begin), suf ? -1 : 0, (1 << G) - 1};
+    };
 
-    // plan header and the first union team of this range, in one round trip
-    int rows_u = N, U = 0, t0 = 0;
-    if (!DENSE) {
-        U = hdr[bh * 4 + 0];
-        rows_u = hdr[bh * 4 + 1];
-        t0 = split_team[static_cast<size_t>(bh) * max_split + s];
+    // plan header and the first descriptor in one round trip
+    int nch;
+    Chunk ck;
+    if (DENSE) {
+        nch = ncp + (T_suf + UR - 1) / UR;
+        ck = dense_chunk(blockIdx.y);
+    } else {
+        nch = min(hdr[bh].chunks, max_chunks);
+        ck = chunks[static_cast<size_t>(bh) * max_chunks + blockIdx.y];
     }
     // query fragments: head l % 16 of this KV head (zero for padding heads)
     QKT qk;
     {
         const int h = j16;
-        const int hq = kv * Greal + (h < Greal ? h : 0);
-        qk.load_q(q + (static_cast<size_t>(b) * Hq + hq) * D, h < Greal ? scale_log2 : 0.f, c);
-    }
-    const int total = rows_u + T_suf;
-    if (s >= split_count(rows_u, T_suf)) return;  // uniform: nothing to read here
-    const int r0 = s * kSplitRows;
-    const int nrows = min(kSplitRows, total - r0);
-
-    if (!DENSE && r0 < rows_u) {
-        // union teams t0 .. t0 + kSplitRows - 1 hold every union row of the range
-        const int* ursb = urs + static_cast<size_t>(bh) * (M + 1);
-        for (int j = tid; j <= kSplitRows; j += kAttThreads) {
-            const int t = t0 + j;
-            s_trs[j] = (t <= U) ? ursb[t] : 0x7fffffff;
-        }
-        if (tid < kSplitRows) {
-            const int t = min(t0 + tid, U - 1);
-            s_tbeg[tid] = ubeg[static_cast<size_t>(bh) * M + t];
-            const float4* L = reinterpret_cast<const float4*>(ulogc + (static_cast<size_t>(bh) * M + t) * kLogcStride);
-            s_tlc[tid][0] = L[0];
-            s_tlc[tid][1] = L[1];
-        }
-        __syncthreads();
-    }
-    if (tid < kSplitRows) {
-        // rows past the range repeat the last row with no weight for any head
-        const int r = r0 + min(tid, nrows - 1);
-        float lcv[8];
-#pragma unroll
-        for (int h = 0; h < 8; ++h) lcv[h] = (h < Greal && tid < nrows) ? 0.f : kSkip;
-        int src;
-        if (r < rows_u) {
-            if (DENSE) {
-                src = r;
-            } else {
-                int lo = 0, hi = min(kSplitRows, U - t0) - 1;  // largest j with s_trs[j] <= r
-                while (lo < hi) {
-                    const int mid = (lo + hi + 1) >> 1;
-                    if (s_trs[mid] <= r)
-                        lo = mid;
-                    else
-                        hi = mid - 1;
-                }
-                src = s_tbeg[lo] + (r - s_trs[lo]);
-                const float4 u = s_tlc[lo][0], v = s_tlc[lo][1];
-                const float x[8] = {u.x, u.y, u.z, u.w, v.x, v.y, v.z, v.w};
-#pragma unroll
-                for (int h = 0; h < 8; ++h)
-                    if (h < Greal && tid < nrows) lcv[h] = x[h] * kLog2e;
-            }
+        const int hq = kv * G + (h < G ? h : 0);
+        const float* qrow = q + (static_cast<size_t>(b) * Hq + hq) * D;
+        const float sc = h < G ? scale_log2 : 0.f;
+        if constexpr (kLdsQ) {
+            QKT::build(s_q, qrow, sc, lane, 0, 1);
+            qk.sq = s_q;
+            wave_lds_sync();
         } else {
-            src = -(r - rows_u) - 1;
+            qk.load_q(qrow, sc, c);
         }
-        s_src[tid] = src;
-        s_lc[tid][0] = make_float4(lcv[0], lcv[1], lcv[2], lcv[3]);
-        s_lc[tid][1] = make_float4(lcv[4], lcv[5], lcv[6], lcv[7]);
-    }
-    __syncthreads();
-
-    const T* Kb = K + static_cast<size_t>(bh) * N * D;
-    const T* Vb = V + static_cast<size_t>(bh) * N * D;
-    const T* sKb = sK + static_cast<size_t>(bh) * T_suf * D;
-    const T* sVb = sV + static_cast<size_t>(bh) * T_suf * D;
-    const int wrow = w * kWaveRows;
-
-    // every K and V load of the wave's 32 rows is issued before any math:
-    // K as MFMA fragments (lane (c, j) -> row j of a 16-row tile), V with 16
-    // lanes per row (lane (c, j) -> dims VPL j .. of rows c, c + 4, ...)
-    typename QKT::frag kf[kTiles][NF];
-    typename VC::raw vr[kWaveRows / 4];
-#pragma unroll
-    for (int t = 0; t < kTiles; ++t) {
-        const int src = s_src[wrow + 16 * t + j16];
-        const T* row = (src >= 0) ? Kb + static_cast<size_t>(src) * D
-                                  : sKb + static_cast<size_t>(-src - 1) * D;
-        qk.load_k(row, c, kf[t]);
-    }
-#pragma unroll
-    for (int k = 0; k < kWaveRows / 4; ++k) {
-        const int src = s_src[wrow + 4 * k + c];
-        const T* row = (src >= 0) ? Vb + static_cast<size_t>(src) * D
-                                  : sVb + static_cast<size_t>(-src - 1) * D;
-        vr[k] = VC::load(row + VPL * j16);
     }
 
-    float m[4], l[4], acc[G][VPL];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        m[r] = kNeg;
-        l[r] = 0.f;
-    }
-#pragma unroll
-    for (int h = 0; h < G; ++h)
-#pragma unroll
-        for (int e = 0; e < VPL; ++e) acc[h][e] = 0.f;
-
-#pragma unroll
-    for (int t = 0; t < kTiles; ++t) {
-        const f32x4 sc = qk.scores(kf[t]);
-        // lane (c, j16): row j16 of the tile, heads 4 c .. 4 c + 3
-        const float4 lc = s_lc[wrow + 16 * t + j16][c & 1];
-        const float lcr[4] = {lc.x, lc.y, lc.z, lc.w};
-        float a[4], p[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const float x = (c < 2) ? sc[r] - lcr[r] : kNeg;
-            const float mn = fmaxf(m[r], row16_max(x));
-            a[r] = rebase(m[r], mn);
-            p[r] = fast_exp2(x - mn);
-            l[r] = l[r] * a[r] + row16_sum(p[r]);
-            m[r] = mn;
+    for (int ci = blockIdx.y; ci < nch; ci += gridDim.y) {
+        // the next descriptor is fetched while this unit is processed
+        const int cn = ci + gridDim.y;
+        const Chunk nx = DENSE ? dense_chunk(min(cn, nch - 1))
+                               : chunks[static_cast<size_t>(bh) * max_chunks + min(cn, max_chunks - 1)];
+        int begin = ck.begin, rows = ck.rows, slot = ck.slot;
+        const int hmask = ck.hmask & ((1 << G) - 1);
+        const bool suffix = slot < 0;
+        const int lim = suffix ? T_suf : N;
+        if (!DENSE) {
+            // a descriptor only ever addresses rows inside its buffer,
+            // whatever the workspace holds
+            rows = min(max(rows, 1), min(UR, max(lim, 1)));
+            begin = min(max(begin, 0), max(lim - rows, 0));
+            slot = min(slot, M - 1);
         }
-        if (c < 2) {
-            s_p[w][j16][c] = make_float4(p[0], p[1], p[2], p[3]);
-            if (j16 == 0) s_a[w][c] = make_float4(a[0], a[1], a[2], a[3]);
-        }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        const bool live_unit = lim >= 1;  // uniform
+        const T* Kb = suffix ? sK + (static_cast<size_t>(bh) * T_suf + begin) * D
+                             : K + (static_cast<size_t>(bh) * N + begin) * D;
+        const T* Vb = suffix ? sV + (static_cast<size_t>(bh) * T_suf + begin) * D
+                             : V + (static_cast<size_t>(bh) * N + begin) * D;
+        // the correction of this unit's team, one per head (zero for the suffix)
+        float lcv[8];
         {
-            const float4 a0 = s_a[w][0], a1 = s_a[w][1];
-            const float av[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
-#pragma unroll
-            for (int h = 0; h < G; ++h)
-#pragma unroll
-                for (int e = 0; e < VPL; ++e) acc[h][e] *= av[h];
+            float4 u = make_float4(0.f, 0.f, 0.f, 0.f), v = u;
+            if (!DENSE && !suffix) {
+                const float4* L = reinterpret_cast<const float4*>(
+                    ulogc + (static_cast<size_t>(bh) * M + slot) * kLogcStride);
+                u = L[0];
+                v = L[1];
+            }
+            lcv[0] = u.x; lcv[1] = u.y; lcv[2] = u.z; lcv[3] = u.w;
+            lcv[4] = v.x; lcv[5] = v.y; lcv[6] = v.z; lcv[7] = v.w;
         }
-        // this lane group's rows of the tile: c, c + 4, c + 8, c + 12
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-            float v[VPL];
-            VC::unpack(vr[4 * t + kk], v);
-            const float4 p0 = s_p[w][4 * kk + c][0], p1 = s_p[w][4 * kk + c][1];
-            const float pv[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
-#pragma unroll
-            for (int h = 0; h < G; ++h)
-#pragma unroll
-                for (int e = 0; e < VPL; ++e) acc[h][e] = fmaf(pv[h], v[e], acc[h][e]);
-        }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    }
 
-    // the four lane groups share each head's maximum: their sums simply add
-#pragma unroll
-    for (int h = 0; h < G; ++h)
-#pragma unroll
-        for (int e = 0; e < VPL; ++e) {
-            float x = acc[h][e];
-            x += __shfl_xor(x, 16);
-            x += __shfl_xor(x, 32);
-            acc[h][e] = x;
-        }
-    if (c < 2 && j16 == 0) {
+        float m[4], l[4], acc[GT][VPL];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            s_m[w][4 * c + r] = m[r];
-            s_l[w][4 * c + r] = l[r];
+            m[r] = kNeg;
+            l[r] = 0.f;
         }
-    }
-    if (c == 0) {
 #pragma unroll
-        for (int h = 0; h < G; ++h)
+        for (int h = 0; h < GT; ++h)
 #pragma unroll
-            for (int e = 0; e < VPL; ++e) s_o[w][h][VPL * j16 + e] = acc[h][e];
-    }
-    __syncthreads();
-    for (int idx = tid; idx < Greal * D; idx += kAttThreads) {
-        const int h = idx / D, jd = idx - h * D;
-        float mx = s_m[0][h];
+            for (int e = 0; e < VPL; ++e) acc[h][e] = 0.f;
+
+        // 32 rows at a time: two 16-row tiles whose K and V loads are all
+        // issued before any math.  K as MFMA fragments (lane (c, j) -> row j
+        // of the tile), V with 16 lanes per row (lane (c, j) -> dims VPL j ..
+        // of rows c, c + 4, ...).  Rows past the unit repeat its last row and
+        // get no weight.
+        for (int r0 = 0; live_unit && r0 < rows; r0 += 32) {
+            const bool has1 = r0 + 16 < rows;
+            typename QKT::frag kf[2][NF];
+            typename VC::raw vr[2][4];
 #pragma unroll
-        for (int v = 1; v < kAttWaves; ++v) mx = fmaxf(mx, s_m[v][h]);
-        float lsum = 0.f, osum = 0.f;
+            for (int k = 0; k < 2; ++k) {
+                if (k == 0 || has1) {
+                    const int t0 = r0 + 16 * k;
+                    qk.load_k(Kb + static_cast<size_t>(min(t0 + j16, rows - 1)) * D, c, kf[k]);
 #pragma unroll
-        for (int v = 0; v < kAttWaves; ++v) {
-            const float a = rebase(s_m[v][h], mx);
-            lsum += s_l[v][h] * a;
-            osum += s_o[v][h][jd] * a;
+                    for (int kk = 0; kk < 4; ++kk)
+                        vr[k][kk] = VC::load(Vb + static_cast<size_t>(min(t0 + 4 * kk + c, rows - 1)) * D + VPL * j16);
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < 2; ++k) {
+                if (k == 1 && !has1) continue;  // uniform
+                const int t0 = r0 + 16 * k;
+                const f32x4 sc = qk.scores(kf[k], lane);
+                // lane (c, j16): row j16 of the tile, heads 4 c .. 4 c + 3
+                const bool live = c < 2 && t0 + j16 < rows;
+                float a[4], p[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const float x = live ? sc[r] : kNeg;
+                    const float mn = fmaxf(m[r], row16_max(x));
+                    a[r] = rebase(m[r], mn);
+                    p[r] = fast_exp2(x - mn);
+                    l[r] = l[r] * a[r] + row16_sum(p[r]);
+                    m[r] = mn;
+                }
+                if (c < 2) {
+                    s_p[j16][c] = make_float4(p[0], p[1], p[2], p[3]);
+                    if (j16 == 0) s_a[c] = make_float4(a[0], a[1], a[2], a[3]);
+                }
+                wave_lds_sync();
+                float av[8];
+                {
+                    const float4 a0 = s_a[0], a1 = s_a[1];
+                    av[0] = a0.x; av[1] = a0.y; av[2] = a0.z; av[3] = a0.w;
+                    av[4] = a1.x; av[5] = a1.y; av[6] = a1.z; av[7] = a1.w;
+                }
+                // only the heads that read this unit accumulate
+#pragma unroll
+                for (int h = 0; h < GT; ++h) {
+                    if (!((hmask >> h) & 1)) continue;  // uniform
+#pragma unroll
+                    for (int e = 0; e < VPL; ++e) acc[h][e] *= av[h];
+                }
+                // this lane group's rows of the tile: c, c + 4, c + 8, c + 12
+#pragma unroll
+                for (int kk = 0; kk < 4; ++kk) {
+                    float vv[VPL];
+                    VC::unpack(vr[k][kk], vv);
+                    const float4 p0 = s_p[4 * kk + c][0], p1 = s_p[4 * kk + c][1];
+                    const float pv[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+#pragma unroll
+                    for (int h = 0; h < GT; ++h) {
+                        if (!((hmask >> h) & 1)) continue;
+#pragma unroll
+                        for (int e = 0; e < VPL; ++e) acc[h][e] = fmaf(pv[h], vv[e], acc[h][e]);
+                    }
+                }
+                wave_lds_sync();
+            }
         }
-        const size_t pidx = (static_cast<size_t>(b) * Hq + kv * Greal + h) * max_split + s;
-        part_o[pidx * D + jd] = osum;
-        if (jd == 0) {
-            part_ml[pidx * 2 + 0] = mx;
-            part_ml[pidx * 2 + 1] = lsum;
+
+        // the unit's state per head: the four lane groups share each head's
+        // maximum, so their value sums simply add; heads that do not read the
+        // unit leave an empty state
+        const size_t pbase = static_cast<size_t>(bh) * G * max_chunks + ci;
+#pragma unroll
+        for (int h = 0; h < GT; ++h) {
+            if (!(live_unit && ((hmask >> h) & 1))) continue;  // uniform
+            float x[VPL];
+#pragma unroll
+            for (int e = 0; e < VPL; ++e) {
+                float t = acc[h][e];
+                t += __shfl_xor(t, 16);
+                t += __shfl_xor(t, 32);
+                x[e] = t;
+            }
+            if (c == 0) {
+                float* o = part_o + (pbase + static_cast<size_t>(h) * max_chunks) * D + VPL * j16;
+#pragma unroll
+                for (int e = 0; e < VPL; e += 4) *reinterpret_cast<float4*>(o + e) = make_float4(x[e], x[e + 1], x[e + 2], x[e + 3]);
+            }
         }
+        if (c < 2 && j16 == 0) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int h = 4 * c + r;
+                if (h < G) {
+                    const bool on = live_unit && ((hmask >> h) & 1);
+                    // the correction enters as a shift of the unit's maximum:
+                    // every row of the unit belongs to the same team
+                    const float2 st = on ? make_float2(m[r] - lcv[h] * kLog2e, l[r]) : make_float2(kNeg, 0.f);
+                    *reinterpret_cast<float2*>(part_ml + (pbase + static_cast<size_t>(h) * max_chunks) * 2) = st;
+                }
+            }
+        }
+        ck = nx;
     }
 }
 
-// One workgroup per (sequence, query head, 32 output dimensions).
-__global__ __launch_bounds__(kMergeThreads) void k_merge(
-    const float* __restrict__ part_o, const float* __restrict__ part_ml,
-    const int* __restrict__ hdr, int N, int T_suf, int Hq, int Hkv, int max_split, int D,
-    float* __restrict__ out) {
-    __shared__ float s_red[kMergeThreads / kWave];
-    __shared__ float s_acc[kMergeThreads / kMergeDims][kMergeDims];
-    const int bhq = blockIdx.x;
-    const int b = bhq / Hq, h = bhq - b * Hq;
-    const int bh = b * Hkv + h / (Hq / Hkv);
-    const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
-    const int rows_u = hdr ? hdr[bh * 4 + 1] : N;
-    const int n = split_count(rows_u, T_suf);
-    const float* ml = part_ml + static_cast<size_t>(bhq) * max_split * 2;
-    const float* po = part_o + static_cast<size_t>(bhq) * max_split * D;
+// Workgroup (sequence and query head, slice of kMergeDims output dims):
+// the chunk states of the head are rescaled to the largest maximum; units
+// the head does not read carry the empty state and are skipped.  The states
+// come first (one round trip that does not wait for the header), then the
+// value sums of the units that count: lane group g of the workgroup takes
+// every kMergeGroups-th of them in order, all loads in flight at once, and
+// the groups' sums are added in group order (a fixed summation order).
+constexpr int kMergeThreads = 256;
+constexpr int kMergeDims = 32;
+constexpr int kMergeGroups = kMergeThreads / kMergeDims;  // 8
 
-    float mx = -INFINITY;
-    for (int s = tid; s < n; s += kMergeThreads) mx = fmaxf(mx, ml[2 * s]);
+__global__ __launch_bounds__(kMergeThreads) void k_merge(const float* __restrict__ part_o,
+                                                         const float* __restrict__ part_ml,
+                                                         const PlanHeader* __restrict__ hdr,
+                                                         int nch_dense, int Hkv, int Hq,
+                                                         int max_chunks, int D,
+                                                         float* __restrict__ out) {
+    constexpr int NW = kMergeThreads / kWave;
+    constexpr int PER = 4;                     // chunk states per thread and block of units
+    constexpr int CB = PER * kMergeThreads;    // units per block
+    constexpr int kBatch = 16;                 // value loads in flight per thread and pass
+    __shared__ float s_red[NW];
+    __shared__ int s_cnt[NW];
+    __shared__ int s_idx[CB];
+    __shared__ float s_wt[CB];
+    __shared__ float s_sum[kMergeGroups][kMergeDims];
+    const int bhq = blockIdx.x;
+    const int b = bhq / Hq, hq = bhq - b * Hq;
+    const int G = Hq / Hkv;
+    const int kv = hq / G, h = hq - kv * G;
+    const int bh = b * Hkv + kv;
+    const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
+    const int jd = tid % kMergeDims, grp = tid / kMergeDims;
+    const int dim = blockIdx.y * kMergeDims + jd;
+    const int nch = min(max(hdr ? hdr[bh].chunks : nch_dense, 0), max_chunks);
+    const float2* ml = reinterpret_cast<const float2*>(part_ml) + (static_cast<size_t>(bh) * G + h) * max_chunks;
+    const float* po = part_o + (static_cast<size_t>(bh) * G + h) * max_chunks * D + dim;
+    const float2 empty = make_float2(kNeg, 0.f);
+
+    // thread t owns units t PER .. t PER + PER - 1 of each block
+    float2 st[PER];
+#pragma unroll
+    for (int r = 0; r < PER; ++r) {
+        const int cc = tid * PER + r;
+        st[r] = cc < max_chunks ? ml[cc] : empty;
+    }
+    float mx = kNeg;
+#pragma unroll
+    for (int r = 0; r < PER; ++r)
+        if (tid * PER + r < nch) mx = fmaxf(mx, st[r].x);
+    for (int c0 = CB; c0 < nch; c0 += CB)
+        for (int r = 0; r < PER; ++r) {
+            const int cc = c0 + tid * PER + r;
+            if (cc < nch) mx = fmaxf(mx, ml[cc].x);
+        }
     for (int off = kWave / 2; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
     if (lane == 0) s_red[w] = mx;
     __syncthreads();
     mx = s_red[0];
-    for (int v = 1; v < kMergeThreads / kWave; ++v) mx = fmaxf(mx, s_red[v]);
+#pragma unroll
+    for (int v = 1; v < NW; ++v) mx = fmaxf(mx, s_red[v]);
     __syncthreads();
 
-    float lsum = 0.f;
-    for (int s = tid; s < n; s += kMergeThreads) lsum += ml[2 * s + 1] * rebase(ml[2 * s], mx);
+    float lsum = 0.f, acc = 0.f;
+    for (int c0 = 0; c0 < nch; c0 += CB) {
+        // this block's states: the registers for the first block, reloaded
+        // for later ones
+        float2 x[PER];
+        if (c0 == 0) {
+#pragma unroll
+            for (int r = 0; r < PER; ++r) x[r] = st[r];
+        } else {
+#pragma unroll
+            for (int r = 0; r < PER; ++r) {
+                const int cc = c0 + tid * PER + r;
+                x[r] = cc < nch ? ml[cc] : empty;
+            }
+        }
+        float wt[PER];
+        int nv = 0;
+#pragma unroll
+        for (int r = 0; r < PER; ++r) {
+            const bool valid = c0 + tid * PER + r < nch && x[r].x > kEmpty;
+            wt[r] = valid ? rebase(x[r].x, mx) : -1.f;
+            lsum += valid ? wt[r] * x[r].y : 0.f;
+            nv += valid ? 1 : 0;
+        }
+        // compaction in unit order: exclusive scan of the per-thread counts
+        const int inc = wave_incl_scan(nv);
+        if (lane == kWave - 1) s_cnt[w] = inc;
+        __syncthreads();
+        int off = 0, n = 0;
+#pragma unroll
+        for (int v = 0; v < NW; ++v) {
+            off += v < w ? s_cnt[v] : 0;
+            n += s_cnt[v];
+        }
+        int pos = off + inc - nv;
+#pragma unroll
+        for (int r = 0; r < PER; ++r) {
+            const bool valid = wt[r] >= 0.f;
+            if (valid) {
+                s_idx[pos] = c0 + tid * PER + r;
+                s_wt[pos] = wt[r];
+            }
+            pos += valid ? 1 : 0;
+        }
+        __syncthreads();
+        // group grp takes list entries grp, grp + kMergeGroups, ...
+        for (int k0 = grp; k0 < n; k0 += kBatch * kMergeGroups) {
+            int ix[kBatch];
+            float wv[kBatch], v[kBatch];
+#pragma unroll
+            for (int k = 0; k < kBatch; ++k) {
+                const int kk = min(k0 + k * kMergeGroups, n - 1);
+                ix[k] = s_idx[kk];
+                wv[k] = k0 + k * kMergeGroups < n ? s_wt[kk] : 0.f;
+            }
+#pragma unroll
+            for (int k = 0; k < kBatch; ++k) v[k] = po[static_cast<size_t>(ix[k]) * D];
+#pragma unroll
+            for (int k = 0; k < kBatch; ++k) acc = fmaf(v[k], wv[k], acc);
+        }
+        __syncthreads();
+    }
+    s_sum[grp][jd] = acc;
     for (int off = kWave / 2; off > 0; off >>= 1) lsum += __shfl_xor(lsum, off);
     if (lane == 0) s_red[w] = lsum;
     __syncthreads();
-    lsum = 0.f;
-    for (int v = 0; v < kMergeThreads / kWave; ++v) lsum += s_red[v];
-
-    const int j = blockIdx.y * kMergeDims + (tid % kMergeDims);
-    const int sl = tid / kMergeDims;
-    constexpr int kLanes = kMergeThreads / kMergeDims;
-    float acc = 0.f;
-#pragma unroll 4
-    for (int s = sl; s < n; s += kLanes) acc += po[static_cast<size_t>(s) * D + j] * rebase(ml[2 * s], mx);
-    s_acc[sl][tid % kMergeDims] = acc;
-    __syncthreads();
     if (tid < kMergeDims) {
         float t = 0.f;
+        for (int v = 0; v < NW; ++v) t += s_red[v];
+        float o = 0.f;
 #pragma unroll
-        for (int v = 0; v < kLanes; ++v) t += s_acc[v][tid];
-        out[static_cast<size_t>(bhq) * D + blockIdx.y * kMergeDims + tid] = t / lsum;
+        for (int g2 = 0; g2 < kMergeGroups; ++g2) o += s_sum[g2][jd];
+        out[static_cast<size_t>(bhq) * D + dim] = o / t;
     }
 }
 
@@ -493,24 +574,28 @@ __global__ void k_zero(uint4* __restrict__ p, size_t n16, unsigned char* __restr
     if (blockIdx.x == 0 && static_cast<int>(threadIdx.x) < ntail) tail[threadIdx.x] = 0;
 }
 
-template <typename T, int D, int G>
+template <typename T, int D, int GT>
 hipError_t attend_g(const AttendArgs& a, hipStream_t s) {
-    const dim3 grid(a.B * a.Hkv, a.max_split);
+    // sampled path: enough one-wave workgroups per KV head to keep the
+    // chip's resident capacity busy, each looping over its share of the
+    // units; dense path: one workgroup per unit
+    const int gy = (!a.dense && a.grid_y > 0) ? std::min(a.grid_y, a.max_chunks) : a.max_chunks;
+    const dim3 grid(a.B * a.Hkv, gy);
     const float sl2 = a.scale * kLog2e;
     const T* K = static_cast<const T*>(a.K);
     const T* V = static_cast<const T*>(a.V);
     const T* sK = static_cast<const T*>(a.sK);
     const T* sV = static_cast<const T*>(a.sV);
     if (a.dense) {
-        k_attend<T, D, G, true><<<grid, kAttThreads, 0, s>>>(
-            K, V, sK, sV, a.q, a.N, a.T, 0, a.Hkv, a.Hq, a.G, sl2, a.max_split, nullptr, nullptr,
-            nullptr, nullptr, nullptr, a.part_o, a.part_ml);
+        k_attend<T, D, GT, true><<<grid, kWave, 0, s>>>(
+            K, V, sK, sV, a.q, a.N, a.T, a.Hkv, a.Hq, a.G, 0, sl2, a.max_chunks, nullptr, nullptr,
+            nullptr, a.part_o, a.part_ml);
     } else {
         const DecodeLayout& L = *a.lay;
-        k_attend<T, D, G, false><<<grid, kAttThreads, 0, s>>>(
-            K, V, sK, sV, a.q, a.N, a.T, a.M, a.Hkv, a.Hq, a.G, sl2, a.max_split,
-            reinterpret_cast<const int*>(a.ws + L.hdr), reinterpret_cast<const int*>(a.ws + L.split),
-            reinterpret_cast<const int*>(a.ws + L.ubeg), reinterpret_cast<const int*>(a.ws + L.urs),
+        k_attend<T, D, GT, false><<<grid, kWave, 0, s>>>(
+            K, V, sK, sV, a.q, a.N, a.T, a.Hkv, a.Hq, a.G, a.M, sl2, a.max_chunks,
+            reinterpret_cast<const PlanHeader*>(a.ws + L.hdr),
+            reinterpret_cast<const Chunk*>(a.ws + L.chunk),
             reinterpret_cast<const float*>(a.ws + L.ulogc), a.part_o, a.part_ml);
     }
     return hipGetLastError();
@@ -547,10 +632,11 @@ hipError_t launch_attend(const AttendArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_merge(const AttendArgs& a, hipStream_t s) {
-    const int* hdr = a.dense ? nullptr : reinterpret_cast<const int*>(a.ws + a.lay->hdr);
-    const dim3 grid(a.B * a.Hq, a.d / kMergeDims);
-    k_merge<<<grid, kMergeThreads, 0, s>>>(a.part_o, a.part_ml, hdr, a.N, a.T, a.Hq, a.Hkv,
-                                           a.max_split, a.d, a.out);
+    const PlanHeader* hdr = a.dense ? nullptr : reinterpret_cast<const PlanHeader*>(a.ws + a.lay->hdr);
+    const int nch_dense = dense_count(a.N) + dense_count(a.T);
+    if (a.d % kMergeDims != 0) return hipErrorInvalidValue;
+    k_merge<<<dim3(a.B * a.Hq, a.d / kMergeDims), kMergeThreads, 0, s>>>(
+        a.part_o, a.part_ml, hdr, nch_dense, a.Hkv, a.Hq, a.max_chunks, a.d, a.out);
     return hipGetLastError();
 }
 

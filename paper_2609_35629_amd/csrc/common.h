@@ -21,6 +21,27 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t b) {
 __device__ __forceinline__ float bf16lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
+// 16-byte streaming loads: K/V rows are read once per decode step, so they
+// are fetched without displacing the rest of the cache contents.
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint4 load_stream(const void* p) {
+    const u32x4_t v = __builtin_nontemporal_load(static_cast<const u32x4_t*>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ float4 load_stream_f(const void* p) {
+    const f32x4_t v = __builtin_nontemporal_load(static_cast<const f32x4_t*>(p));
+    return make_float4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ uint2 load_stream8(const void* p) {
+    typedef unsigned u32x2_t __attribute__((ext_vector_type(2)));
+    const u32x2_t v = __builtin_nontemporal_load(static_cast<const u32x2_t*>(p));
+    return make_uint2(v.x, v.y);
+}
+
 template <typename T>
 __device__ __forceinline__ float load_elem(const T* p, size_t i);
 

@@ -11,24 +11,48 @@ namespace santapp {
 
 constexpr int kMaxHeadDim = 256;   // LDS vector in the team builder
 constexpr int kMaxReps = 1024;     // representatives per parent
-constexpr int kMaxTeams = 8192;    // teams per (b, kv) the sampler keeps in LDS
+constexpr int kMaxTeams = 8192;    // teams per (b, kv) the sampler handles
 constexpr int kMaxGroup = 8;       // query heads per KV head (8-bit head masks)
 constexpr int kLogcStride = 8;     // floats per union team in the read plan
+constexpr int kChunkRows = 32;     // rows per sampled attention unit (one wave)
+constexpr int kDenseRows = 128;    // rows per dense attention unit
+constexpr int kAttendWavesPerCU = 8; // resident attention waves per compute unit
 
-// Workspace layout of santapp_decode; byte offsets into the caller's buffer.
-// Rows of one KV head are [union rows ; suffix rows]; the attention kernel
-// splits them into ranges of at most kSplitRows rows, so the number of
-// partials per head is at most max_split = ceil((N + T) / kSplitRows).
-struct DecodeLayout {
-    int max_split = 0;
-    size_t phi = 0, Y = 0, lc = 0, hdr = 0, ubeg = 0, urs = 0, ulogc = 0, split = 0, po = 0,
-           pml = 0, total = 0;
+// Attention work unit: up to kChunkRows consecutive rows of one union team of
+// the packed cache, or of the suffix (slot < 0); the dense path cuts its rows
+// into units of kDenseRows.  hmask has bit h set for
+// each query head of the KV head that reads the rows.
+struct Chunk {
+    int begin;  // first packed row, or first suffix row when slot < 0
+    int rows;   // 1 .. kChunkRows
+    int slot;   // union slot (index of the team's corrections), -1 = suffix
+    int hmask;
 };
 
-constexpr int kSplitRows = 128;  // rows per attention workgroup (16 groups x 8 rows)
+// Plan header per (b, kv), written by the sampler.
+struct PlanHeader {
+    int teams;   // union teams U
+    int rows;    // union rows (excluding the suffix)
+    int chunks;  // chunks of the union and the suffix
+    int pad;
+};
 
-DecodeLayout decode_layout(int B, int Hq, int Hkv, int N, int T, int d, int M);
+// Workspace layout of santapp_decode; byte offsets into the caller's buffer.
+// max_chunks bounds the chunks of any (b, kv): the largest chunk count any
+// union of up to min(M, G K) teams can have, plus the suffix chunks.
+struct DecodeLayout {
+    int max_chunks = 0;
+    size_t phi = 0, Y = 0, lc = 0, hdr = 0, chunk = 0, ulogc = 0, po = 0, pml = 0,
+           total = 0;
+};
+
+// cap: host table with cap[x] = most chunks any x distinct teams of one
+// (b, kv) can need (x = 0 .. M); nullptr for the dense layout.
+DecodeLayout decode_layout(int B, int Hq, int Hkv, int T, int d, int M, int Kp, const int* cap);
 DecodeLayout dense_layout(int B, int Hq, int Hkv, int N, int T, int d);
+
+__host__ __device__ inline int chunk_count(int rows) { return (rows + kChunkRows - 1) / kChunkRows; }
+__host__ __device__ inline int dense_count(int rows) { return (rows + kDenseRows - 1) / kDenseRows; }
 
 hipError_t launch_build_parents(const void* K, santapp_dtype dtype, int BH, int N, int d, int P,
                                 int R, int M, double* mind, int* owner, int* team_begin,
@@ -44,7 +68,7 @@ struct RouteArgs {
     const int* team_begin;  // [BH, M]
     const double* log_n;    // [BH, M]
     const float* q;         // [B, Hq, d]
-    int B, Hkv, Hq, G, d, N, M, Kp, T;
+    int B, Hkv, Hq, G, d, M, Kp, T;
     santapp_dtype dtype;
     double scale;
     uint64_t seed, step;
@@ -53,8 +77,9 @@ struct RouteArgs {
     const santapp_decode_debug* dbg;
 };
 
-hipError_t launch_route(const RouteArgs& a, hipStream_t s);
-hipError_t launch_select(const RouteArgs& a, hipStream_t s);
+// Routing (k_route), then Gumbel-top-K, corrections and the read plan
+// (k_select): two launches on the stream.
+hipError_t launch_route_select(const RouteArgs& a, hipStream_t s);
 
 struct AttendArgs {
     const void* K;    // [BH, N, d] packed (sampled path) or original (dense path)
@@ -62,14 +87,15 @@ struct AttendArgs {
     const void* sK;   // [BH, T, d]
     const void* sV;
     const float* q;   // [B, Hq, d]
-    int B, Hkv, Hq, G, d, N, T, M, max_split;
+    int B, Hkv, Hq, G, d, N, T, M, max_chunks;
+    int grid_y;                 // workgroups per KV head on the sampled path (0: one per chunk)
     santapp_dtype dtype;
     float scale;
     bool dense;                 // every row, every head, correction 1
     const char* ws;             // plan (sampled path)
     const DecodeLayout* lay;    // plan offsets (sampled path)
-    float* part_o;              // [B, Hq, max_split, d]
-    float* part_ml;             // [B, Hq, max_split, 2]
+    float* part_o;              // [BH, G, max_chunks, d]
+    float* part_ml;             // [BH, G, max_chunks, 2]
     float* out;                 // [B, Hq, d]
 };
 

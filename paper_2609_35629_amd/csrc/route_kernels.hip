@@ -2,17 +2,21 @@
 //
 // k_route   eq. method-routing: phi_g = log n_g + scale q.l_g for every query
 //           head sharing the KV head (one representative load serves all of
-//           them), plus the Gumbel perturbation Y_g = phi_g + G_g.  The dot
-//           products accumulate in fp64 (every bf16 x fp32 product is exact in
-//           fp64), so phi differs from an fp64 reference only by summation
+//           them), and the Gumbel perturbation Y_g = phi_g + G_g.  The dot
+//           products accumulate in fp64 (every bf16 x fp32 product is exact
+//           in fp64), so phi differs from an fp64 reference only by summation
 //           order.
-// k_select  Gumbel-top-K per query head: tau = the (K+1)-th largest Y (radix
-//           select over order-preserving 64-bit keys), S = the K largest
-//           (ties to the lower team index), log c_g for g in S
-//           (eq. method-inclusion); then the union of the heads' selections
-//           per KV head with an 8-bit head mask and per-head log c, the row
-//           prefix of the union, and the row map the attention kernel reads:
-//           for each union row its packed row and its union slot.
+// k_select  Alg. "SANTA++ attention for one query head", eq.
+//           method-inclusion, one workgroup per (sequence, KV head): one wave
+//           per query head finds tau = the (K+1)-th largest Y with a
+//           two-level value histogram and an exact finish over the
+//           order-preserving 64-bit keys, selects the K largest (ties to the
+//           lower team index) and computes log c_g for the selected teams.
+//           Then the read plan: the union of the heads' selections in
+//           ascending team order with each team's per-head corrections, cut
+//           into chunks of at most kChunkRows consecutive packed rows (each
+//           chunk is one unit of attention work), followed by the chunks of
+//           the exactly attended suffix.
 #include <math.h>
 
 #include "common.h"
@@ -23,10 +27,10 @@ namespace santapp {
 namespace {
 
 constexpr int kRouteThreads = 256;
-constexpr int kRouteGroups = kRouteThreads / 16;  // 16 lanes per representative
-constexpr int kRouteTeamsPerBlock = kRouteGroups;  // one representative per lane group
+constexpr int kRouteTeams = kRouteThreads / 16;  // one representative per 16-lane group
 constexpr int kSelectThreads = 512;
 constexpr int kSelectWaves = kSelectThreads / kWave;
+constexpr int kFineBits = 16;                 // value-histogram resolution of the sampler
 
 template <typename T, int DPL>
 struct RepChunk;
@@ -34,9 +38,7 @@ struct RepChunk;
 template <>
 struct RepChunk<bf16_t, 8> {
     using raw = uint4;
-    static __device__ __forceinline__ raw load(const bf16_t* p) {
-        return *reinterpret_cast<const uint4*>(p);
-    }
+    static __device__ __forceinline__ raw load(const bf16_t* p) { return load_stream(p); }
     static __device__ __forceinline__ float get(const raw& r, int e) {
         const uint32_t w = (e < 2) ? r.x : (e < 4) ? r.y : (e < 6) ? r.z : r.w;
         return (e & 1) ? bf16hi(w) : bf16lo(w);
@@ -46,9 +48,7 @@ struct RepChunk<bf16_t, 8> {
 template <>
 struct RepChunk<bf16_t, 4> {
     using raw = uint2;
-    static __device__ __forceinline__ raw load(const bf16_t* p) {
-        return *reinterpret_cast<const uint2*>(p);
-    }
+    static __device__ __forceinline__ raw load(const bf16_t* p) { return load_stream8(p); }
     static __device__ __forceinline__ float get(const raw& r, int e) {
         const uint32_t w = (e < 2) ? r.x : r.y;
         return (e & 1) ? bf16hi(w) : bf16lo(w);
@@ -62,8 +62,8 @@ struct RepChunk<float, 8> {
     };
     static __device__ __forceinline__ raw load(const float* p) {
         raw r;
-        r.a = *reinterpret_cast<const float4*>(p);
-        r.b = *reinterpret_cast<const float4*>(p + 4);
+        r.a = load_stream_f(p);
+        r.b = load_stream_f(p + 4);
         return r;
     }
     static __device__ __forceinline__ float get(const raw& r, int e) {
@@ -76,71 +76,11 @@ struct RepChunk<float, 8> {
 template <>
 struct RepChunk<float, 4> {
     using raw = float4;
-    static __device__ __forceinline__ raw load(const float* p) {
-        return *reinterpret_cast<const float4*>(p);
-    }
+    static __device__ __forceinline__ raw load(const float* p) { return load_stream_f(p); }
     static __device__ __forceinline__ float get(const raw& r, int e) {
         return e == 0 ? r.x : e == 1 ? r.y : e == 2 ? r.z : r.w;
     }
 };
-
-template <typename T, int D, int G>
-__global__ __launch_bounds__(kRouteThreads) void k_route(
-    const T* __restrict__ reps, const double* __restrict__ log_n, const float* __restrict__ q,
-    int M, int Hkv, int Hq, double scale, uint64_t seed, uint64_t step, double* __restrict__ phi,
-    double* __restrict__ Y) {
-    constexpr int DPL = D / 16;
-    using Chunk = RepChunk<T, DPL>;
-    __shared__ double s_gum[G][kRouteTeamsPerBlock];
-    const int bh = blockIdx.y;
-    const int b = bh / Hkv, kv = bh - b * Hkv;
-    const int tid = threadIdx.x, grp = tid >> 4, sub = tid & 15;
-    const int g0 = blockIdx.x * kRouteTeamsPerBlock;
-
-    // 1) every load of the block is issued first: one representative per
-    //    16-lane group (clamped in range), its log n, this lane's query dims
-    const int gmine = min(g0 + grp, M - 1);
-    const typename Chunk::raw raw =
-        Chunk::load(reps + (static_cast<size_t>(bh) * M + gmine) * D + sub * DPL);
-    const double lnn = log_n[static_cast<size_t>(bh) * M + gmine];
-    double qd[G][DPL];
-    const float* qb = q + (static_cast<size_t>(b) * Hq + kv * G) * D + sub * DPL;
-#pragma unroll
-    for (int h = 0; h < G; ++h)
-#pragma unroll
-        for (int e = 0; e < DPL; ++e) qd[h][e] = static_cast<double>(qb[h * D + e]);
-
-    // 2) the Gumbel noise does not depend on the loads: one (head, team)
-    //    draw per thread while they are in flight
-    for (int p = tid; p < G * kRouteTeamsPerBlock; p += kRouteThreads) {
-        const int h = p / kRouteTeamsPerBlock, gi = p - h * kRouteTeamsPerBlock;
-        const int g = g0 + gi;
-        if (g < M) s_gum[h][gi] = team_gumbel(seed, step, b, kv * G + h, g);
-    }
-    __syncthreads();
-
-    // 3) fp64 dot products of the representative with the G queries
-    const int g = g0 + grp;
-    if (g >= M) return;  // uniform across the 16-lane group; no barrier follows
-    double acc[G];
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-        double a = 0.0;
-#pragma unroll
-        for (int e = 0; e < DPL; ++e) a = fma(qd[h][e], static_cast<double>(Chunk::get(raw, e)), a);
-        acc[h] = row16_sum(a);
-    }
-    if (sub < G) {
-        double dot = 0.0;
-#pragma unroll
-        for (int h = 0; h < G; ++h)
-            if (h == sub) dot = acc[h];
-        const double ph = lnn + scale * dot;
-        const size_t o = (static_cast<size_t>(b) * Hq + kv * G + sub) * M + g;
-        phi[o] = ph;
-        Y[o] = ph + s_gum[sub][grp];
-    }
-}
 
 // log c for c = 1 - exp(-exp(x)) in fp32 (eq. method-inclusion).  x >= -37
 // for a selected team (its perturbed score beats tau and a Gumbel draw is at
@@ -156,56 +96,55 @@ __device__ __forceinline__ float log_inclusion(float x) {
     return __builtin_amdgcn_logf(c) * kLn2;
 }
 
-// Exclusive scan of two counters over the workgroup; returns the totals.
-__device__ __forceinline__ void block_scan2(int a, int c, int& ea, int& ec, int& ta, int& tc,
-                                            int* s_w /* [2 * kSelectWaves] */) {
+// Exclusive scan of three counters over the workgroup; returns the totals.
+__device__ __forceinline__ void block_scan3(const int (&x)[3], int (&ex)[3], int (&tot)[3],
+                                           int* s_w /* [3 * kSelectWaves] */) {
     const int lane = lane_id(), w = wave_id();
-    const int ia = wave_incl_scan(a), ic = wave_incl_scan(c);
-    if (lane == kWave - 1) {
-        s_w[w] = ia;
-        s_w[kSelectWaves + w] = ic;
+    int inc[3];
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+        inc[k] = wave_incl_scan(x[k]);
+        if (lane == kWave - 1) s_w[k * kSelectWaves + w] = inc[k];
     }
     __syncthreads();
-    int pa = 0, pc = 0;
-    ta = 0;
-    tc = 0;
 #pragma unroll
-    for (int v = 0; v < kSelectWaves; ++v) {
-        const int xa = s_w[v], xc = s_w[kSelectWaves + v];
-        if (v < w) {
-            pa += xa;
-            pc += xc;
+    for (int k = 0; k < 3; ++k) {
+        int pre = 0, t = 0;
+#pragma unroll
+        for (int v = 0; v < kSelectWaves; ++v) {
+            const int y = s_w[k * kSelectWaves + v];
+            pre += (v < w) ? y : 0;
+            t += y;
         }
-        ta += xa;
-        tc += xc;
+        ex[k] = pre + inc[k] - x[k];
+        tot[k] = t;
     }
-    ea = pa + ia - a;
-    ec = pc + ic - c;
     __syncthreads();
 }
 
-// The perturbed scores of one head, as order-preserving keys.  PL > 0 keeps
-// element i = j * 64 + lane in register j (M <= 64 * PL); PL == 0 re-reads
-// them from global memory on every pass.
+// The perturbed scores of one head as order-preserving keys, with each key's
+// fine value bucket.  PL > 0 keeps element i = j * 64 + lane in register j
+// (M <= 64 PL); PL == 0 re-reads them from global memory on every pass.
 template <int PL>
 struct KeySet {
+    // phi stays in registers only for small PL; larger sets re-read it for
+    // the few selected keys
+    static constexpr bool kPhiRegs = PL <= 8;
     uint64_t k[PL];
-    double ph[PL];
-    const double* y;
+    double ph[kPhiRegs ? PL : 1];
+    int fine[PL];
     const double* p;
     int M;
-    // every load is issued before the first use (clamped addresses, no branch)
-    __device__ __forceinline__ void init(const double* yy, const double* pp, int MM) {
-        y = yy;
-        p = pp;
+    __device__ __forceinline__ void init(const double* y, const double* pp, int MM) {
         M = MM;
+        p = pp;
         const int lane = lane_id();
         double v[PL];
 #pragma unroll
         for (int j = 0; j < PL; ++j) {
-            const int i = min(j * kWave + lane, M - 1);
+            const int i = min(j * kWave + lane, M - 1);  // clamped: no branch around the loads
             v[j] = y[i];
-            ph[j] = p[i];
+            if constexpr (kPhiRegs) ph[j] = pp[i];
         }
 #pragma unroll
         for (int j = 0; j < PL; ++j) k[j] = order_key(v[j]);
@@ -213,7 +152,18 @@ struct KeySet {
     __device__ __forceinline__ int count() const { return PL; }
     __device__ __forceinline__ bool valid(int j) const { return j * kWave + lane_id() < M; }
     __device__ __forceinline__ uint64_t key(int j) const { return k[j]; }
-    __device__ __forceinline__ double phi(int j) const { return ph[j]; }
+    __device__ __forceinline__ double phi(int j) const {
+        if constexpr (kPhiRegs)
+            return ph[j];
+        else
+            return p[min(j * kWave + lane_id(), M - 1)];
+    }
+    __device__ __forceinline__ void set_fine(double ymin, double fs) {
+#pragma unroll
+        for (int j = 0; j < PL; ++j)
+            fine[j] = min((1 << kFineBits) - 1, static_cast<int>((key_value(k[j]) - ymin) * fs));
+    }
+    __device__ __forceinline__ int fine_of(int j, double, double) const { return fine[j]; }
 };
 
 template <>
@@ -231,16 +181,10 @@ struct KeySet<0> {
     __device__ __forceinline__ uint64_t key(int j) const {
         return order_key(y[min(j * kWave + lane_id(), M - 1)]);
     }
-    __device__ __forceinline__ double phi(int j) const { return p[j * kWave + lane_id()]; }
-};
-
-// Per-wave candidate bookkeeping of the selection: the value bucket of a key
-// (monotone in the key's value) and the candidates of the current pass.
-struct Buckets {
-    double ymin, scale;
-    __device__ __forceinline__ int of(uint64_t k) const {
-        const double t = (key_value(k) - ymin) * scale;
-        return min(255, static_cast<int>(t));
+    __device__ __forceinline__ double phi(int j) const { return p[min(j * kWave + lane_id(), M - 1)]; }
+    __device__ __forceinline__ void set_fine(double, double) {}
+    __device__ __forceinline__ int fine_of(int j, double ymin, double fs) const {
+        return min((1 << kFineBits) - 1, static_cast<int>((key_value(key(j)) - ymin) * fs));
     }
 };
 
@@ -275,37 +219,216 @@ __device__ __forceinline__ int hist_select(const uint32_t* hist, int want, int& 
     return readlane(digit, src);
 }
 
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// tau's key for one head: the key of rank `want` (0-based, descending) among
+// the valid keys.  Value histograms over [min Y, max Y] at 2^16 buckets (two
+// passes of 256); at most 64 candidates left are ranked directly; beyond that
+// (many nearly equal keys) an exact 8-bit radix over the 64-bit keys finishes.
 template <int PL>
+__device__ uint64_t select_key(KeySet<PL>& ks, int want, uint32_t* hist, uint64_t* cand) {
+    const int lane = lane_id();
+    const int nj = ks.count();
+    uint64_t kmin = ~0ull, kmax = 0;
+#pragma unroll
+    for (int j = 0; j < nj; ++j) {
+        if (ks.valid(j)) {
+            kmin = min(kmin, ks.key(j));
+            kmax = max(kmax, ks.key(j));
+        }
+    }
+    kmin = wave_min64(kmin);
+    kmax = wave_max64(kmax);
+    const double ymin = key_value(kmin);
+    const double range = key_value(kmax) - ymin;
+    if (!(range > 0.0)) return kmin;  // every key equal
+    const double fs = (static_cast<double>(1 << kFineBits) - 0.001) / range;
+    ks.set_fine(ymin, fs);
+
+    // pass 0: the top 8 bits of the fine bucket over every key; pass 1: its
+    // low 8 bits over the keys of the chosen top bin.  `target` is the part
+    // of the fine bucket fixed so far.
+    int target = 0;
+    for (int pass = 0; pass < 2; ++pass) {
+        const int shift = pass == 0 ? 8 : 0;
+        reinterpret_cast<uint4*>(hist)[lane] = make_uint4(0, 0, 0, 0);
+        wave_lds_sync();
+#pragma unroll
+        for (int j = 0; j < nj; ++j) {
+            const int f = ks.fine_of(j, ymin, fs);
+            if (ks.valid(j) && (pass == 0 || (f >> 8) == target)) atomicAdd(&hist[(f >> shift) & 255], 1u);
+        }
+        wave_lds_sync();
+        int above, cnt;
+        const int bin = hist_select(hist, want, above, cnt);
+        want -= above;
+        target = pass == 0 ? bin : (target << 8) | bin;
+        if (cnt <= kWave) {
+            // few candidates: gather them and rank them directly
+            const uint64_t lt = lanemask_lt();
+            int n = 0;
+#pragma unroll
+            for (int j = 0; j < nj; ++j) {
+                const bool c = ks.valid(j) && (ks.fine_of(j, ymin, fs) >> shift) == target;
+                const uint64_t cb = __ballot(c);
+                if (c) cand[n + __popcll(cb & lt)] = ks.key(j);
+                n += __popcll(cb);
+            }
+            wave_lds_sync();
+            // slots n .. 63 repeat the smallest possible key and never count
+            if (lane >= n) cand[lane] = 0;
+            wave_lds_sync();
+            const uint64_t mine = cand[min(lane, n - 1)];
+            int gt = 0, ge = 0;
+            const ulonglong2* c2 = reinterpret_cast<const ulonglong2*>(cand);
+#pragma unroll
+            for (int t = 0; t < kWave / 2; ++t) {
+                const ulonglong2 o = c2[t];
+                gt += (o.x > mine ? 1 : 0) + (o.y > mine ? 1 : 0);
+                ge += (2 * t < n && o.x >= mine ? 1 : 0) + (2 * t + 1 < n && o.y >= mine ? 1 : 0);
+            }
+            const bool owner = lane < n && gt <= want && want < ge;
+            const uint64_t r = readlane(mine, __ffsll(static_cast<unsigned long long>(__ballot(owner))) - 1);
+            wave_lds_sync();  // cand is reused by the caller
+            return r;
+        }
+    }
+
+    // many keys in one fine bucket: exact radix over their 64-bit keys
+    auto in_bucket = [&](int j) { return ks.valid(j) && ks.fine_of(j, ymin, fs) == target; };
+    uint64_t kand = ~0ull, kor = 0;
+#pragma unroll
+    for (int j = 0; j < nj; ++j) {
+        if (in_bucket(j)) {
+            kand &= ks.key(j);
+            kor |= ks.key(j);
+        }
+    }
+    const uint64_t all_and = wave_and64(kand), all_or = wave_or64(kor);
+    const uint64_t diff = all_or & ~all_and;
+    uint64_t prefix = 0, pmask = 0;
+    const int top = diff ? 63 - __clzll(static_cast<long long>(diff)) : 7;
+    int sh = top >= 7 ? top - 7 : 0;
+    if (sh + 8 < 64) {
+        pmask = ~0ull << (sh + 8);
+        prefix = all_and & pmask;
+    }
+    for (;;) {
+        reinterpret_cast<uint4*>(hist)[lane] = make_uint4(0, 0, 0, 0);
+        wave_lds_sync();
+#pragma unroll
+        for (int j = 0; j < nj; ++j) {
+            const uint64_t k = ks.key(j);
+            if (in_bucket(j) && (k & pmask) == prefix) atomicAdd(&hist[(k >> sh) & 255], 1u);
+        }
+        wave_lds_sync();
+        int above, cnt;
+        const int digit = hist_select(hist, want, above, cnt);
+        want -= above;
+        prefix |= static_cast<uint64_t>(digit) << sh;
+        pmask |= 0xffull << sh;
+        if (cnt == 1 || sh == 0) {
+            // the rank element is determined: fetch one key equal to it
+            uint64_t kk = 0;
+            bool have = false;
+#pragma unroll
+            for (int j = 0; j < nj; ++j) {
+                const uint64_t k = ks.key(j);
+                if (in_bucket(j) && (k & pmask) == prefix) {
+                    kk = k;
+                    have = true;
+                }
+            }
+            return readlane(kk, __ffsll(static_cast<unsigned long long>(__ballot(have))) - 1);
+        }
+        sh = sh >= 8 ? sh - 8 : 0;  // the last digit may overlap bits fixed before
+    }
+}
+
+template <typename T, int D, int G>
+__global__ __launch_bounds__(kRouteThreads) void k_route(
+    const T* __restrict__ reps, const double* __restrict__ log_n, const float* __restrict__ q,
+    int M, int Hkv, int Hq, double scale, uint64_t seed, uint64_t step, double* __restrict__ phi,
+    double* __restrict__ Y) {
+    constexpr int DPL = D / 16;
+    using RC = RepChunk<T, DPL>;
+    __shared__ double s_gum[G][kRouteTeams];
+    const int bh = blockIdx.y;
+    const int b = bh / Hkv, kv = bh - b * Hkv;
+    const int tid = threadIdx.x, grp = tid >> 4, sub = tid & 15;
+    const int g0 = blockIdx.x * kRouteTeams;
+    const size_t tb0 = static_cast<size_t>(bh) * M;
+
+    // every load first: one representative per 16-lane group (clamped in
+    // range), its log n, this lane's query dims
+    const int gmine = min(g0 + grp, M - 1);
+    const typename RC::raw raw = RC::load(reps + (tb0 + gmine) * D + sub * DPL);
+    const double lnn = log_n[tb0 + gmine];
+    double qd[G][DPL];
+    const float* qb = q + (static_cast<size_t>(b) * Hq + kv * G) * D + sub * DPL;
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) qd[h][e] = static_cast<double>(qb[h * D + e]);
+    // the Gumbel noise does not depend on the loads: one (head, team) draw
+    // per thread while they are in flight
+    for (int p = tid; p < G * kRouteTeams; p += kRouteThreads) {
+        const int h = p / kRouteTeams, gi = p - h * kRouteTeams;
+        const int g = g0 + gi;
+        if (g < M) s_gum[h][gi] = team_gumbel(seed, step, b, kv * G + h, g);
+    }
+    __syncthreads();
+    const int g = g0 + grp;
+    if (g >= M) return;  // uniform across the 16-lane group; no barrier follows
+    double acc[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+        double a = 0.0;
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) a = fma(qd[h][e], static_cast<double>(RC::get(raw, e)), a);
+        acc[h] = row16_sum(a);
+    }
+    if (sub < G) {
+        double dot = 0.0;
+#pragma unroll
+        for (int h = 0; h < G; ++h)
+            if (h == sub) dot = acc[h];
+        const double ph = lnn + scale * dot;
+        const size_t o = (static_cast<size_t>(b) * Hq + kv * G + sub) * M + g;
+        phi[o] = ph;
+        Y[o] = ph + s_gum[sub][grp];
+    }
+}
+
+template <int G, int PL>
 __global__ __launch_bounds__(kSelectThreads) void k_select(
-    const double* __restrict__ phi, const double* __restrict__ Y,
-    const int* __restrict__ team_begin, const int* __restrict__ team_size, int M, int Kp,
-    int Hkv, int G, int Hq, int T, int max_split, float* __restrict__ lc,
-    int* __restrict__ hdr, int* __restrict__ ubeg, int* __restrict__ urs,
-    float* __restrict__ ulogc, int* __restrict__ split_team, int* __restrict__ dbg_sel,
-    float* __restrict__ dbg_logc, double* __restrict__ dbg_tau, int* __restrict__ dbg_uteams,
-    int* __restrict__ dbg_urows) {
-    // dynamic LDS: 8-bit head mask per team, then (kLdsLc) log c per head and
-    // team; larger team counts keep log c in global memory
-    constexpr bool kLdsLc = PL > 0 && PL <= 16;
-    extern __shared__ uint32_t s_dyn[];
-    const int mask_words = (M + 3) >> 2;
-    uint32_t* s_mask = s_dyn;
-    float* s_lc = reinterpret_cast<float*>(s_dyn + mask_words);  // [G][M] when kLdsLc
+    const double* __restrict__ phi, const double* __restrict__ Y, const int* __restrict__ team_begin,
+    const int* __restrict__ team_size, int M, int Hkv, int Hq, int Kp, int T_suf, int max_chunks,
+    float* __restrict__ lc, PlanHeader* __restrict__ hdr, Chunk* __restrict__ chunks,
+    float* __restrict__ ulogc, int* __restrict__ dbg_sel, float* __restrict__ dbg_logc,
+    double* __restrict__ dbg_tau, int* __restrict__ dbg_uteams, int* __restrict__ dbg_urows) {
+    constexpr bool kLdsLc = PL > 0 && PL <= 8;  // log c of every (head, team) in LDS
+    extern __shared__ float s_lc[];  // [G][M] when kLdsLc
     __shared__ __align__(16) uint32_t s_hist[kSelectWaves][256];
-    __shared__ uint64_t s_cand[kSelectWaves][kWave];
-    __shared__ int s_w[2 * kSelectWaves];
+    __shared__ __align__(16) uint64_t s_cand[kSelectWaves][kWave];
+    __shared__ uint64_t s_bits[kMaxGroup][kMaxTeams / kWave];  // selection bits per head
+    __shared__ int s_w[3 * kSelectWaves];
 
     const int bh = blockIdx.x;
     const int b = bh / Hkv, kv = bh - b * Hkv;
     const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
-    for (int i = tid; i < mask_words; i += kSelectThreads) s_mask[i] = 0;
+    const size_t tb0 = static_cast<size_t>(bh) * M;
+
     // team sizes and starts of the first chunk of teams, fetched while the
     // heads select
-    const size_t tb0 = static_cast<size_t>(bh) * M;
     const int gc0 = min(tid, M - 1);
     const int size0 = team_size[tb0 + gc0];
     const int begin0 = team_begin[tb0 + gc0];
-    __syncthreads();
+    // (no barrier before the selection: nothing in LDS needs clearing)
 
     if (w < G) {
         const int hq = kv * G + w;
@@ -313,119 +436,7 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
         KeySet<PL> ks;
         ks.init(Y + hoff, phi + hoff, M);
         const int nj = ks.count();
-        uint32_t* hist = s_hist[w];
-        int want = Kp;  // rank of tau among the keys, 0-based from the top
-        uint64_t tkey = 0;
-
-        // pass 1: 256 value buckets over [min Y, max Y]
-        uint64_t kmin = ~0ull, kmax = 0;
-#pragma unroll
-        for (int j = 0; j < nj; ++j) {
-            if (ks.valid(j)) {
-                kmin = min(kmin, ks.key(j));
-                kmax = max(kmax, ks.key(j));
-            }
-        }
-        kmin = wave_min64(kmin);
-        kmax = wave_max64(kmax);
-        Buckets bk;
-        bk.ymin = key_value(kmin);
-        const double range = key_value(kmax) - bk.ymin;
-        bool found = !(range > 0.0);  // every key equal
-        if (found) tkey = kmin;
-        bk.scale = found ? 0.0 : 255.999 / range;
-        int bucket = -1;
-        if (!found) {
-            reinterpret_cast<uint4*>(hist)[lane] = make_uint4(0, 0, 0, 0);
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-#pragma unroll
-            for (int j = 0; j < nj; ++j)
-                if (ks.valid(j)) atomicAdd(&hist[bk.of(ks.key(j))], 1u);
-            __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            int above, cnt;
-            bucket = hist_select(hist, want, above, cnt);
-            want -= above;
-            if (cnt <= kWave) {
-                // few candidates left: gather them and rank them directly
-                const uint64_t lt = lanemask_lt();
-                int n = 0;
-#pragma unroll
-                for (int j = 0; j < nj; ++j) {
-                    const bool cand = ks.valid(j) && bk.of(ks.key(j)) == bucket;
-                    const uint64_t cb = __ballot(cand);
-                    if (cand) s_cand[w][n + __popcll(cb & lt)] = ks.key(j);
-                    n += __popcll(cb);
-                }
-                __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-                __builtin_amdgcn_wave_barrier();
-                const uint64_t mine = s_cand[w][min(lane, n - 1)];
-                int gt = 0, ge = 0;
-                for (int t = 0; t < n; ++t) {
-                    const uint64_t o = s_cand[w][t];
-                    gt += o > mine ? 1 : 0;
-                    ge += o >= mine ? 1 : 0;
-                }
-                const bool owner = lane < n && gt <= want && want < ge;
-                tkey = readlane(mine, __ffsll(static_cast<unsigned long long>(__ballot(owner))) - 1);
-                found = true;
-            }
-        }
-        if (!found) {
-            // many equal-bucket keys: exact radix over their 64-bit keys
-            uint64_t kand = ~0ull, kor = 0;
-#pragma unroll
-            for (int j = 0; j < nj; ++j) {
-                if (ks.valid(j) && bk.of(ks.key(j)) == bucket) {
-                    kand &= ks.key(j);
-                    kor |= ks.key(j);
-                }
-            }
-            const uint64_t all_and = wave_and64(kand), all_or = wave_or64(kor);
-            const uint64_t diff = all_or & ~all_and;
-            uint64_t prefix = 0, pmask = 0;
-            const int top = diff ? 63 - __clzll(static_cast<long long>(diff)) : 7;
-            int shift = top >= 7 ? top - 7 : 0;
-            if (shift + 8 < 64) {
-                pmask = ~0ull << (shift + 8);
-                prefix = all_and & pmask;
-            }
-            for (; !found; shift -= 8) {
-                reinterpret_cast<uint4*>(hist)[lane] = make_uint4(0, 0, 0, 0);
-                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-                __builtin_amdgcn_wave_barrier();
-#pragma unroll
-                for (int j = 0; j < nj; ++j) {
-                    const uint64_t k = ks.key(j);
-                    if (ks.valid(j) && bk.of(k) == bucket && (k & pmask) == prefix)
-                        atomicAdd(&hist[(k >> shift) & 255], 1u);
-                }
-                __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-                __builtin_amdgcn_wave_barrier();
-                int above, cnt;
-                const int digit = hist_select(hist, want, above, cnt);
-                want -= above;
-                prefix |= static_cast<uint64_t>(digit) << shift;
-                pmask |= 0xffull << shift;
-                if (cnt == 1 || shift == 0) {
-                    // the rank element is determined: fetch one key equal to it
-                    uint64_t kk = 0;
-                    bool have = false;
-#pragma unroll
-                    for (int j = 0; j < nj; ++j) {
-                        const uint64_t k = ks.key(j);
-                        if (ks.valid(j) && bk.of(k) == bucket && (k & pmask) == prefix) {
-                            kk = k;
-                            have = true;
-                        }
-                    }
-                    tkey = readlane(kk, __ffsll(static_cast<unsigned long long>(__ballot(have))) - 1);
-                    found = true;
-                }
-                if (shift < 8) shift = 8;  // the last digit may overlap earlier bits
-            }
-        }
+        const uint64_t tkey = select_key<PL>(ks, Kp, s_hist[w], s_cand[w]);
         const double tau = key_value(tkey);
 
         int above_cnt = 0;
@@ -433,53 +444,66 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
         for (int j = 0; j < nj; ++j) above_cnt += (ks.valid(j) && ks.key(j) > tkey) ? 1 : 0;
         const int need_ties = Kp - wave_sum(above_cnt);
 
-        // log c of every key in flight at once (independent chains), then
-        // the selection in index order: i = j * 64 + lane
-        float lcv[PL > 0 ? PL : 1];
-#pragma unroll
-        for (int j = 0; j < (PL > 0 ? PL : 0); ++j)
-            lcv[j] = log_inclusion(static_cast<float>(ks.phi(j) - tau));
+        // selection in index order i = j * 64 + lane: the keys above tau's
+        // key and the first need_ties keys equal to it
         const uint64_t lt = lanemask_lt();
+        const bool compact = Kp <= kWave;  // log c once per selected team, one lane each
         int nsel = 0, nties = 0;
+        uint32_t* cidx = reinterpret_cast<uint32_t*>(s_cand[w]);  // [64] team index
+        float* cx = reinterpret_cast<float*>(s_cand[w]) + kWave;  // [64] phi - tau
 #pragma unroll
         for (int j = 0; j < nj; ++j) {
             const int i = j * kWave + lane;
             const bool valid = ks.valid(j);
             const uint64_t k = ks.key(j);
-            const bool tie = valid && k == tkey;
-            const uint64_t tb = __ballot(tie);
-            const int trank = nties + __popcll(tb & lt);
-            nties += __popcll(tb);
-            const bool sel = valid && (k > tkey || (tie && trank < need_ties));
+            bool sel = valid && k > tkey;
+            if (need_ties > 0) {  // uniform
+                const bool tie = valid && k == tkey;
+                const uint64_t tb = __ballot(tie);
+                sel = sel || (tie && nties + __popcll(tb & lt) < need_ties);
+                nties += __popcll(tb);
+            }
             const uint64_t sb = __ballot(sel);
-            const int pos = nsel + __popcll(sb & lt);
-            nsel += __popcll(sb);
+            if (lane == 0) s_bits[w][j] = sb;
             if (sel) {
-                float v;
-                if constexpr (PL > 0)
-                    v = lcv[j];
-                else
-                    v = log_inclusion(static_cast<float>(ks.phi(j) - tau));
+                const int pos = nsel + __popcll(sb & lt);
+                const float x = static_cast<float>(ks.phi(j) - tau);
+                if (compact) {
+                    cidx[pos] = static_cast<uint32_t>(i);
+                    cx[pos] = x;
+                } else {
+                    const float v = log_inclusion(x);
+                    if constexpr (kLdsLc)
+                        s_lc[w * M + i] = v;
+                    else
+                        lc[hoff + i] = v;
+                    if (dbg_sel) dbg_sel[(static_cast<size_t>(b) * Hq + hq) * Kp + pos] = i;
+                    if (dbg_logc) dbg_logc[(static_cast<size_t>(b) * Hq + hq) * Kp + pos] = v;
+                }
+            }
+            nsel += __popcll(sb);
+        }
+        if (compact) {
+            wave_lds_sync();
+            if (lane < Kp) {
+                const int i = static_cast<int>(cidx[lane]);
+                const float v = log_inclusion(cx[lane]);
                 if constexpr (kLdsLc)
                     s_lc[w * M + i] = v;
                 else
                     lc[hoff + i] = v;
-                atomicOr(&s_mask[i >> 2], 1u << ((i & 3) * 8 + w));
-                if (pos < Kp) {
-                    if (dbg_sel) dbg_sel[(static_cast<size_t>(b) * Hq + hq) * Kp + pos] = i;
-                    if (dbg_logc) dbg_logc[(static_cast<size_t>(b) * Hq + hq) * Kp + pos] = v;
-                }
+                if (dbg_sel) dbg_sel[(static_cast<size_t>(b) * Hq + hq) * Kp + lane] = i;
+                if (dbg_logc) dbg_logc[(static_cast<size_t>(b) * Hq + hq) * Kp + lane] = v;
             }
         }
         if (lane == 0 && dbg_tau) dbg_tau[static_cast<size_t>(b) * Hq + hq] = tau;
     }
     __syncthreads();
 
-    // union of the heads' selections in ascending team order, its row prefix,
-    // and the first union team of every kSplitRows-row range of the rows
-    int* sp = split_team + static_cast<size_t>(bh) * max_split;
-    const size_t rs0 = static_cast<size_t>(bh) * (M + 1);
-    int run_u = 0, run_rows = 0;
+    // ---- union of the heads' selections in ascending team order -------------
+    // per union team: its corrections, then its chunks of <= kChunkRows rows
+    Chunk* cb = chunks + static_cast<size_t>(bh) * max_chunks;
+    int run_u = 0, run_rows = 0, run_c = 0;
     for (int base = 0; base < M; base += kSelectThreads) {
         const int g = base + tid;
         int tsz = size0, tbeg = begin0;
@@ -488,115 +512,115 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
             tsz = team_size[tb0 + gc];
             tbeg = team_begin[tb0 + gc];
         }
-        const uint32_t m = (g < M) ? ((s_mask[g >> 2] >> ((g & 3) * 8)) & 0xffu) : 0u;
-        const int f = m ? 1 : 0;
-        const int sz = f ? tsz : 0;
-        int ef, es, tf, ts;
-        block_scan2(f, sz, ef, es, tf, ts, s_w);
+        int hm = 0;
+        if (g < M) {
+#pragma unroll
+            for (int h = 0; h < G; ++h) hm |= static_cast<int>((s_bits[h][g >> 6] >> (g & 63)) & 1ull) << h;
+        }
+        const int f = hm ? 1 : 0;
+        const int x[3] = {f, f ? chunk_count(tsz) : 0, f ? tsz : 0};
+        int ex[3], tot[3];
+        block_scan3(x, ex, tot, s_w);
         if (f) {
-            const int slot = run_u + ef, rs = run_rows + es;
+            const int slot = run_u + ex[0];
             float v[kLogcStride];
 #pragma unroll
             for (int h = 0; h < kLogcStride; ++h) {
-                const int hc = min(h, G - 1);
-                if constexpr (kLdsLc)
-                    v[h] = s_lc[hc * M + g];
-                else
-                    v[h] = lc[(static_cast<size_t>(b) * Hq + kv * G + hc) * M + g];
+                float t = 0.f;
+                if (h < G && ((hm >> h) & 1)) {
+                    if constexpr (kLdsLc)
+                        t = s_lc[h * M + g];
+                    else
+                        t = lc[(static_cast<size_t>(b) * Hq + kv * G + h) * M + g];
+                }
+                v[h] = t;
             }
-#pragma unroll
-            for (int h = 0; h < kLogcStride; ++h)
-                if (!(h < G && ((m >> h) & 1u))) v[h] = 1.0e30f;  // no weight for this head
             float4* L = reinterpret_cast<float4*>(ulogc + (tb0 + slot) * kLogcStride);
             L[0] = make_float4(v[0], v[1], v[2], v[3]);
             L[1] = make_float4(v[4], v[5], v[6], v[7]);
-            ubeg[tb0 + slot] = tbeg;
-            urs[rs0 + slot] = rs;
-            // row ranges whose first row falls inside this team
-            for (int r = (rs + kSplitRows - 1) / kSplitRows * kSplitRows; r < rs + tsz; r += kSplitRows)
-                sp[r / kSplitRows] = slot;
+            const int c0 = run_c + ex[1];
+            for (int p = 0; p < x[1]; ++p) {
+                const int c = c0 + p;
+                if (c < max_chunks)
+                    cb[c] = Chunk{tbeg + p * kChunkRows, min(kChunkRows, tsz - p * kChunkRows), slot, hm};
+            }
         }
-        run_u += tf;
-        run_rows += ts;
+        run_u += tot[0];
+        run_c += tot[1];
+        run_rows += tot[2];
     }
-    // ranges that start in the suffix
-    const int nsp = (run_rows + T + kSplitRows - 1) / kSplitRows;
-    for (int q0 = (run_rows + kSplitRows - 1) / kSplitRows + tid; q0 < nsp; q0 += kSelectThreads)
-        sp[q0] = run_u;
+    // the suffix: every head, no correction
+    const int nsc = chunk_count(T_suf);
+    for (int p = tid; p < nsc; p += kSelectThreads) {
+        const int c = run_c + p;
+        if (c < max_chunks)
+            cb[c] = Chunk{p * kChunkRows, min(kChunkRows, T_suf - p * kChunkRows), -1, (1 << G) - 1};
+    }
     if (tid == 0) {
-        urs[rs0 + run_u] = run_rows;
-        hdr[bh * 4 + 0] = run_u;
-        hdr[bh * 4 + 1] = run_rows;
+        hdr[bh] = PlanHeader{run_u, run_rows, min(run_c + nsc, max_chunks), 0};
         if (dbg_uteams) dbg_uteams[bh] = run_u;
         if (dbg_urows) dbg_urows[bh] = run_rows;
     }
 }
 
-template <typename T, int D>
-hipError_t route_dispatch_d(const RouteArgs& a, hipStream_t s) {
-    const dim3 grid((a.M + kRouteTeamsPerBlock - 1) / kRouteTeamsPerBlock, a.B * a.Hkv);
-    double* phi = reinterpret_cast<double*>(a.ws + a.lay->phi);
-    double* Y = reinterpret_cast<double*>(a.ws + a.lay->Y);
-    const T* reps = static_cast<const T*>(a.reps);
-#define SANTAPP_ROUTE(GG)                                                                  \
-    k_route<T, D, GG><<<grid, kRouteThreads, 0, s>>>(reps, a.log_n, a.q, a.M, a.Hkv, a.Hq,  \
-                                                      a.scale, a.seed, a.step, phi, Y)
-    switch (a.G) {
-        case 1: SANTAPP_ROUTE(1); break;
-        case 2: SANTAPP_ROUTE(2); break;
-        case 3: SANTAPP_ROUTE(3); break;
-        case 4: SANTAPP_ROUTE(4); break;
-        case 5: SANTAPP_ROUTE(5); break;
-        case 6: SANTAPP_ROUTE(6); break;
-        case 7: SANTAPP_ROUTE(7); break;
-        case 8: SANTAPP_ROUTE(8); break;
-        default: return hipErrorInvalidValue;
-    }
-#undef SANTAPP_ROUTE
+template <typename T, int D, int G>
+hipError_t route_g(const RouteArgs& a, hipStream_t s) {
+    const DecodeLayout& L = *a.lay;
+    const santapp_decode_debug* d = a.dbg;
+    double* phi = reinterpret_cast<double*>(a.ws + L.phi);
+    double* Y = reinterpret_cast<double*>(a.ws + L.Y);
+    k_route<T, D, G><<<dim3((a.M + kRouteTeams - 1) / kRouteTeams, a.B * a.Hkv), kRouteThreads, 0, s>>>(
+        static_cast<const T*>(a.reps), a.log_n, a.q, a.M, a.Hkv, a.Hq, a.scale, a.seed, a.step, phi, Y);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    float* lc = reinterpret_cast<float*>(a.ws + L.lc);
+    PlanHeader* hdr = reinterpret_cast<PlanHeader*>(a.ws + L.hdr);
+    Chunk* ch = reinterpret_cast<Chunk*>(a.ws + L.chunk);
+    float* ulogc = reinterpret_cast<float*>(a.ws + L.ulogc);
+#define SANTAPP_SEL(PLV)                                                                          \
+    k_select<G, PLV><<<a.B * a.Hkv, kSelectThreads,                                               \
+                       (PLV > 0 && PLV <= 8) ? sizeof(float) * G * a.M : 0, s>>>(                \
+        phi, Y, a.team_begin, a.team_size, a.M, a.Hkv, a.Hq, a.Kp, a.T, L.max_chunks, lc, hdr,   \
+        ch, ulogc, d ? d->sel : nullptr, d ? d->logc : nullptr, d ? d->tau : nullptr,             \
+        d ? d->union_teams : nullptr, d ? d->union_rows : nullptr)
+    if (a.M <= 8 * kWave)
+        SANTAPP_SEL(8);
+    else if (a.M <= 32 * kWave)
+        SANTAPP_SEL(32);
+    else
+        SANTAPP_SEL(0);
+#undef SANTAPP_SEL
     return hipGetLastError();
 }
 
-template <typename T>
-hipError_t route_dispatch(const RouteArgs& a, hipStream_t s) {
-    switch (a.d) {
-        case 64: return route_dispatch_d<T, 64>(a, s);
-        case 128: return route_dispatch_d<T, 128>(a, s);
+template <typename T, int D>
+hipError_t route_d(const RouteArgs& a, hipStream_t s) {
+    switch (a.G) {
+        case 1: return route_g<T, D, 1>(a, s);
+        case 2: return route_g<T, D, 2>(a, s);
+        case 3: return route_g<T, D, 3>(a, s);
+        case 4: return route_g<T, D, 4>(a, s);
+        case 5: return route_g<T, D, 5>(a, s);
+        case 6: return route_g<T, D, 6>(a, s);
+        case 7: return route_g<T, D, 7>(a, s);
+        case 8: return route_g<T, D, 8>(a, s);
         default: return hipErrorInvalidValue;
     }
 }
 
-template <int PL>
-void select_launch(const RouteArgs& a, hipStream_t s) {
-    size_t lds = sizeof(uint32_t) * ((a.M + 3) / 4);
-    if (PL > 0 && PL <= 16) lds += sizeof(float) * static_cast<size_t>(a.G) * a.M;
-    const santapp_decode_debug* d = a.dbg;
-    const DecodeLayout& L = *a.lay;
-    k_select<PL><<<a.B * a.Hkv, kSelectThreads, lds, s>>>(
-        reinterpret_cast<const double*>(a.ws + L.phi), reinterpret_cast<const double*>(a.ws + L.Y),
-        a.team_begin, a.team_size, a.M, a.Kp, a.Hkv, a.G, a.Hq, a.T, L.max_split,
-        reinterpret_cast<float*>(a.ws + L.lc), reinterpret_cast<int*>(a.ws + L.hdr),
-        reinterpret_cast<int*>(a.ws + L.ubeg), reinterpret_cast<int*>(a.ws + L.urs),
-        reinterpret_cast<float*>(a.ws + L.ulogc), reinterpret_cast<int*>(a.ws + L.split),
-        d ? d->sel : nullptr, d ? d->logc : nullptr, d ? d->tau : nullptr,
-        d ? d->union_teams : nullptr, d ? d->union_rows : nullptr);
+template <typename T>
+hipError_t route_t(const RouteArgs& a, hipStream_t s) {
+    switch (a.d) {
+        case 64: return route_d<T, 64>(a, s);
+        case 128: return route_d<T, 128>(a, s);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 }  // namespace
 
-hipError_t launch_route(const RouteArgs& a, hipStream_t s) {
-    return a.dtype == SANTAPP_BF16 ? route_dispatch<bf16_t>(a, s) : route_dispatch<float>(a, s);
-}
-
-hipError_t launch_select(const RouteArgs& a, hipStream_t s) {
-    if (a.M <= 8 * kWave)
-        select_launch<8>(a, s);
-    else if (a.M <= 16 * kWave)
-        select_launch<16>(a, s);
-    else if (a.M <= 32 * kWave)
-        select_launch<32>(a, s);
-    else
-        select_launch<0>(a, s);
-    return hipGetLastError();
+hipError_t launch_route_select(const RouteArgs& a, hipStream_t s) {
+    return a.dtype == SANTAPP_BF16 ? route_t<bf16_t>(a, s) : route_t<float>(a, s);
 }
 
 }  // namespace santapp
