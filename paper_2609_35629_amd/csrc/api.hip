@@ -339,7 +339,7 @@ santapp_status santapp_decode(const santapp_teams* t, const float* q, const void
     A.T = T;
     A.M = t->M;
     A.max_chunks = L.max_chunks;
-    A.grid_y = t->cus > 0 ? std::max(1, (t->cus * kAttendWavesPerCU + t->B * t->Hkv - 1) / (t->B * t->Hkv)) : 0;
+    A.grid_waves = t->cus > 0 ? t->cus * kAttendWavesPerCU : 0;
     A.dtype = t->dtype;
     A.scale = static_cast<float>(scale);
     A.ws = ws;

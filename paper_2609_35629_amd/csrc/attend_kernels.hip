@@ -211,17 +211,17 @@ struct RowChunk<float, 4> {
 };
 
 // One wave per workgroup.  The sampled path's units are chunks of at most
-// kChunkRows (32) consecutive rows of one union team or of the suffix, so
-// that every chunk of a step is resident at once and no wave waits for
-// another; the dense path's units are kDenseRows (128) rows, walked 32 rows
-// at a time with the softmax state carried along.  Workgroup (bh, y) takes
-// units y, y + gridDim.y, ... of KV head bh, a loop bounded by the plan's
-// unit count.
+// kChunkRows (32) consecutive rows of one union team or of the suffix; the
+// dense path's units are kDenseRows (128) rows, walked 32 rows at a time with
+// the softmax state carried along.  The units of all (sequence, KV head)
+// pairs form one list, (b, kv)-major; wave w takes units w, w + gridDim.x, ...
+// (a loop bounded by the plan's unit count), so that a KV head whose heads
+// selected large teams does not leave the others idle.
 template <typename T, int D, int GT, bool DENSE>
 __global__ __launch_bounds__(kWave) void k_attend(
     const T* __restrict__ K, const T* __restrict__ V, const T* __restrict__ sK,
-    const T* __restrict__ sV, const float* __restrict__ q, int N, int T_suf, int Hkv, int Hq,
-    int G, int M, float scale_log2, int max_chunks, const PlanHeader* __restrict__ hdr,
+    const T* __restrict__ sV, const float* __restrict__ q, int N, int T_suf, int BH, int Hkv,
+    int Hq, int G, int M, float scale_log2, int max_chunks, const PlanHeader* __restrict__ hdr,
     const Chunk* __restrict__ chunks, const float* __restrict__ ulogc,
     float* __restrict__ part_o, float* __restrict__ part_ml) {
     constexpr int NF = frag_count<T, D>();
@@ -234,48 +234,62 @@ __global__ __launch_bounds__(kWave) void k_attend(
     __shared__ float4 s_p[16][2];           // probabilities of one tile
     __shared__ float4 s_a[2];               // rescale factors of one tile
 
-    const int bh = blockIdx.x;  // KV heads vary fastest
-    const int b = bh / Hkv, kv = bh - b * Hkv;
     const int lane = lane_id();
     const int c = lane >> 4, j16 = lane & 15;
     const int ncp = (N + UR - 1) / UR;
-    auto dense_chunk = [&](int ci) {
-        const bool suf = ci >= ncp;
-        const int begin = (suf ? ci - ncp : ci) * UR;
-        return Chunk{begin, min(UR, (suf ? T_suf : N) - begin), suf ? -1 : 0, (1 << G) - 1};
+    const int nchd = ncp + (T_suf + UR - 1) / UR;  // dense units per (b, kv)
+    // units of (b, kv) pair i: the plan's count (sampled), or nchd (dense)
+    auto units_of = [&](int i) { return DENSE ? nchd : min(max(hdr[i].chunks, 0), max_chunks); };
+    int total = 0;
+    for (int i = 0; i < BH; ++i) total += units_of(i);
+    // (b, kv) pair and unit index of list entry u
+    auto locate = [&](int u, int& bhx, int& cix) {
+        if (DENSE) {
+            bhx = u / nchd;
+            cix = u - bhx * nchd;
+        } else {
+            bhx = 0;
+            while (bhx < BH - 1 && u >= units_of(bhx)) u -= units_of(bhx++);
+            cix = u;
+        }
+    };
+    auto descriptor = [&](int bhx, int cix) {
+        if (DENSE) {
+            const bool suf = cix >= ncp;
+            const int begin = (suf ? cix - ncp : cix) * UR;
+            return Chunk{begin, min(UR, (suf ? T_suf : N) - begin), suf ? -1 : 0, (1 << G) - 1};
+        }
+        return chunks[static_cast<size_t>(bhx) * max_chunks + min(cix, max_chunks - 1)];
     };
 
-    // plan header and the first descriptor in one round trip
-    int nch;
-    Chunk ck;
-    if (DENSE) {
-        nch = ncp + (T_suf + UR - 1) / UR;
-        ck = dense_chunk(blockIdx.y);
-    } else {
-        nch = min(hdr[bh].chunks, max_chunks);
-        ck = chunks[static_cast<size_t>(bh) * max_chunks + blockIdx.y];
-    }
-    // query fragments: head l % 16 of this KV head (zero for padding heads)
+    int bh = -1, ci = 0;
+    if (blockIdx.x < total) locate(blockIdx.x, bh, ci);
+    Chunk ck = descriptor(max(bh, 0), ci);
+    int qbh = -1;  // the (b, kv) pair whose query fragments s_q holds
     QKT qk;
-    {
-        const int h = j16;
-        const int hq = kv * G + (h < G ? h : 0);
-        const float* qrow = q + (static_cast<size_t>(b) * Hq + hq) * D;
-        const float sc = h < G ? scale_log2 : 0.f;
-        if constexpr (kLdsQ) {
-            QKT::build(s_q, qrow, sc, lane, 0, 1);
-            qk.sq = s_q;
-            wave_lds_sync();
-        } else {
-            qk.load_q(qrow, sc, c);
-        }
-    }
 
-    for (int ci = blockIdx.y; ci < nch; ci += gridDim.y) {
-        // the next descriptor is fetched while this unit is processed
-        const int cn = ci + gridDim.y;
-        const Chunk nx = DENSE ? dense_chunk(min(cn, nch - 1))
-                               : chunks[static_cast<size_t>(bh) * max_chunks + min(cn, max_chunks - 1)];
+    for (int u = blockIdx.x; u < total; u += gridDim.x) {
+        const int b = bh / Hkv, kv = bh - b * Hkv;
+        if (bh != qbh) {  // uniform
+            // query fragments: head l % 16 of this KV head (zero for padding heads)
+            const int h = j16;
+            const int hq = kv * G + (h < G ? h : 0);
+            const float* qrow = q + (static_cast<size_t>(b) * Hq + hq) * D;
+            const float sc = h < G ? scale_log2 : 0.f;
+            if constexpr (kLdsQ) {
+                wave_lds_sync();
+                QKT::build(s_q, qrow, sc, lane, 0, 1);
+                qk.sq = s_q;
+                wave_lds_sync();
+            } else {
+                qk.load_q(qrow, sc, c);
+            }
+            qbh = bh;
+        }
+        // the next unit's descriptor is fetched while this one is processed
+        int nbh = bh, nci = ci;
+        if (u + gridDim.x < total) locate(u + gridDim.x, nbh, nci);
+        const Chunk nx = descriptor(nbh, nci);
         int begin = ck.begin, rows = ck.rows, slot = ck.slot;
         const int hmask = ck.hmask & ((1 << G) - 1);
         const bool suffix = slot < 0;
@@ -407,7 +421,7 @@ __global__ __launch_bounds__(kWave) void k_attend(
             if (c == 0) {
                 float* o = part_o + (pbase + static_cast<size_t>(h) * max_chunks) * D + VPL * j16;
 #pragma unroll
-                for (int e = 0; e < VPL; e += 4) *reinterpret_cast<float4*>(o + e) = make_float4(x[e], x[e + 1], x[e + 2], x[e + 3]);
+                for (int e = 0; e < VPL; e += 4) store_stream(o + e, make_float4(x[e], x[e + 1], x[e + 2], x[e + 3]));
             }
         }
         if (c < 2 && j16 == 0) {
@@ -419,11 +433,13 @@ __global__ __launch_bounds__(kWave) void k_attend(
                     // the correction enters as a shift of the unit's maximum:
                     // every row of the unit belongs to the same team
                     const float2 st = on ? make_float2(m[r] - lcv[h] * kLog2e, l[r]) : make_float2(kNeg, 0.f);
-                    *reinterpret_cast<float2*>(part_ml + (pbase + static_cast<size_t>(h) * max_chunks) * 2) = st;
+                    store_stream2(part_ml + (pbase + static_cast<size_t>(h) * max_chunks) * 2, st);
                 }
             }
         }
         ck = nx;
+        bh = nbh;
+        ci = nci;
     }
 }
 
@@ -546,7 +562,7 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(const float* __restrict
                 wv[k] = k0 + k * kMergeGroups < n ? s_wt[kk] : 0.f;
             }
 #pragma unroll
-            for (int k = 0; k < kBatch; ++k) v[k] = po[static_cast<size_t>(ix[k]) * D];
+            for (int k = 0; k < kBatch; ++k) v[k] = __builtin_nontemporal_load(po + static_cast<size_t>(ix[k]) * D);
 #pragma unroll
             for (int k = 0; k < kBatch; ++k) acc = fmaf(v[k], wv[k], acc);
         }
@@ -576,24 +592,28 @@ __global__ void k_zero(uint4* __restrict__ p, size_t n16, unsigned char* __restr
 
 template <typename T, int D, int GT>
 hipError_t attend_g(const AttendArgs& a, hipStream_t s) {
-    // sampled path: enough one-wave workgroups per KV head to keep the
-    // chip's resident capacity busy, each looping over its share of the
-    // units; dense path: one workgroup per unit
-    const int gy = (!a.dense && a.grid_y > 0) ? std::min(a.grid_y, a.max_chunks) : a.max_chunks;
-    const dim3 grid(a.B * a.Hkv, gy);
+    // one list of units over every (b, kv) pair; the sampled path runs as
+    // many one-wave workgroups as the chip keeps resident (each looping over
+    // its share), the dense path one workgroup per unit
+    const long long units = static_cast<long long>(a.B) * a.Hkv * a.max_chunks;
+    long long waves = units;
+    if (!a.dense && a.grid_waves > 0) waves = std::min<long long>(units, a.grid_waves);
+    if (waves < 1 || waves > 0x7fffffffLL) return hipErrorInvalidValue;
+    const dim3 grid(static_cast<unsigned>(waves));
     const float sl2 = a.scale * kLog2e;
     const T* K = static_cast<const T*>(a.K);
     const T* V = static_cast<const T*>(a.V);
     const T* sK = static_cast<const T*>(a.sK);
     const T* sV = static_cast<const T*>(a.sV);
+    const int BH = a.B * a.Hkv;
     if (a.dense) {
         k_attend<T, D, GT, true><<<grid, kWave, 0, s>>>(
-            K, V, sK, sV, a.q, a.N, a.T, a.Hkv, a.Hq, a.G, 0, sl2, a.max_chunks, nullptr, nullptr,
-            nullptr, a.part_o, a.part_ml);
+            K, V, sK, sV, a.q, a.N, a.T, BH, a.Hkv, a.Hq, a.G, 0, sl2, a.max_chunks, nullptr,
+            nullptr, nullptr, a.part_o, a.part_ml);
     } else {
         const DecodeLayout& L = *a.lay;
         k_attend<T, D, GT, false><<<grid, kWave, 0, s>>>(
-            K, V, sK, sV, a.q, a.N, a.T, a.Hkv, a.Hq, a.G, a.M, sl2, a.max_chunks,
+            K, V, sK, sV, a.q, a.N, a.T, BH, a.Hkv, a.Hq, a.G, a.M, sl2, a.max_chunks,
             reinterpret_cast<const PlanHeader*>(a.ws + L.hdr),
             reinterpret_cast<const Chunk*>(a.ws + L.chunk),
             reinterpret_cast<const float*>(a.ws + L.ulogc), a.part_o, a.part_ml);

@@ -42,6 +42,16 @@ __device__ __forceinline__ uint2 load_stream8(const void* p) {
     return make_uint2(v.x, v.y);
 }
 
+// Streaming stores of values written once and read once by the next kernel.
+__device__ __forceinline__ void store_stream(float* p, float4 v) {
+    __builtin_nontemporal_store(f32x4_t{v.x, v.y, v.z, v.w}, reinterpret_cast<f32x4_t*>(p));
+}
+
+__device__ __forceinline__ void store_stream2(float* p, float2 v) {
+    typedef float f32x2_t __attribute__((ext_vector_type(2)));
+    __builtin_nontemporal_store(f32x2_t{v.x, v.y}, reinterpret_cast<f32x2_t*>(p));
+}
+
 template <typename T>
 __device__ __forceinline__ float load_elem(const T* p, size_t i);
 

@@ -88,7 +88,7 @@ struct AttendArgs {
     const void* sV;
     const float* q;   // [B, Hq, d]
     int B, Hkv, Hq, G, d, N, T, M, max_chunks;
-    int grid_y;                 // workgroups per KV head on the sampled path (0: one per chunk)
+    int grid_waves;             // one-wave workgroups on the sampled path (0: one per unit)
     santapp_dtype dtype;
     float scale;
     bool dense;                 // every row, every head, correction 1
