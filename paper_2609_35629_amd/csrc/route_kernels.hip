@@ -279,17 +279,12 @@ __device__ uint64_t select_key(KeySet<PL>& ks, int want, uint32_t* hist, uint64_
                 n += __popcll(cb);
             }
             wave_lds_sync();
-            // slots n .. 63 repeat the smallest possible key and never count
-            if (lane >= n) cand[lane] = 0;
-            wave_lds_sync();
             const uint64_t mine = cand[min(lane, n - 1)];
             int gt = 0, ge = 0;
-            const ulonglong2* c2 = reinterpret_cast<const ulonglong2*>(cand);
-#pragma unroll
-            for (int t = 0; t < kWave / 2; ++t) {
-                const ulonglong2 o = c2[t];
-                gt += (o.x > mine ? 1 : 0) + (o.y > mine ? 1 : 0);
-                ge += (2 * t < n && o.x >= mine ? 1 : 0) + (2 * t + 1 < n && o.y >= mine ? 1 : 0);
+            for (int t = 0; t < n; ++t) {  // n is wave-uniform
+                const uint64_t o = readlane(mine, t);
+                gt += o > mine ? 1 : 0;
+                ge += o >= mine ? 1 : 0;
             }
             const bool owner = lane < n && gt <= want && want < ge;
             const uint64_t r = readlane(mine, __ffsll(static_cast<unsigned long long>(__ballot(owner))) - 1);
@@ -417,6 +412,7 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
     __shared__ __align__(16) uint64_t s_cand[kSelectWaves][kWave];
     __shared__ uint64_t s_bits[kMaxGroup][kMaxTeams / kWave];  // selection bits per head
     __shared__ int s_w[3 * kSelectWaves];
+    __shared__ int4 s_team[kSelectThreads];  // union teams of one pass: first chunk, begin, size, heads
 
     const int bh = blockIdx.x;
     const int b = bh / Hkv, kv = bh - b * Hkv;
@@ -538,13 +534,26 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
             float4* L = reinterpret_cast<float4*>(ulogc + (tb0 + slot) * kLogcStride);
             L[0] = make_float4(v[0], v[1], v[2], v[3]);
             L[1] = make_float4(v[4], v[5], v[6], v[7]);
-            const int c0 = run_c + ex[1];
-            for (int p = 0; p < x[1]; ++p) {
-                const int c = c0 + p;
-                if (c < max_chunks)
-                    cb[c] = Chunk{tbeg + p * kChunkRows, min(kChunkRows, tsz - p * kChunkRows), slot, hm};
-            }
+            s_team[ex[0]] = make_int4(ex[1], tbeg, tsz, hm);
         }
+        __syncthreads();
+        // the pass's chunks, one per thread: its team is the last with a
+        // first chunk at or before it
+        for (int c = tid; c < tot[1]; c += kSelectThreads) {
+            int lo = 0, hi = tot[0] - 1;
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (s_team[mid].x <= c)
+                    lo = mid;
+                else
+                    hi = mid - 1;
+            }
+            const int4 tm = s_team[lo];
+            const int p = c - tm.x;
+            if (run_c + c < max_chunks)
+                cb[run_c + c] = Chunk{tm.y + p * kChunkRows, min(kChunkRows, tm.z - p * kChunkRows), run_u + lo, tm.w};
+        }
+        __syncthreads();  // s_team is rewritten by the next pass
         run_u += tot[0];
         run_c += tot[1];
         run_rows += tot[2];
