@@ -101,6 +101,7 @@ DecodeLayout decode_layout(int B, int Hq, int Hkv, int T, int d, int M, int Kp, 
         off = align_up(off + bytes);
         return at;
     };
+    L.counter = take(sizeof(unsigned));  // units appended to the list this step
     L.phi = take(BQ * M * sizeof(double));
     L.Y = take(BQ * M * sizeof(double));
     L.lc = take(BQ * M * sizeof(float));
@@ -311,6 +312,8 @@ santapp_status santapp_decode(const santapp_teams* t, const float* q, const void
     if (Hq < 1 || Hq % t->Hkv != 0) return fail(SANTAPP_EINVAL, "Hq (%d) must be a positive multiple of Hkv (%d)", Hq, t->Hkv);
     const int G = Hq / t->Hkv;
     if (G > kMaxGroup) return fail(SANTAPP_ELIMIT, "%d query heads per KV head exceed %d", G, kMaxGroup);
+    if (static_cast<long long>(t->B) * t->Hkv > kMaxPairs)
+        return fail(SANTAPP_ELIMIT, "B * Hkv = %lld exceeds %d", static_cast<long long>(t->B) * t->Hkv, kMaxPairs);
     if (T < 0) return fail(SANTAPP_EINVAL, "T must be >= 0");
     if (T > 0 && (!suffix_K || !suffix_V)) return fail(SANTAPP_EINVAL, "suffix K/V are NULL with T > 0");
     if (K < 1) return fail(SANTAPP_EINVAL, "K must be >= 1 (got %d)", K);

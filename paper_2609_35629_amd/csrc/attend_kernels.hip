@@ -214,14 +214,15 @@ struct RowChunk<float, 4> {
 // kChunkRows (32) consecutive rows of one union team or of the suffix; the
 // dense path's units are kDenseRows (128) rows, walked 32 rows at a time with
 // the softmax state carried along.  The units of all (sequence, KV head)
-// pairs form one list, (b, kv)-major; wave w takes units w, w + gridDim.x, ...
-// (a loop bounded by the plan's unit count), so that a KV head whose heads
+// pairs form one list (the sampler appends each pair's units at a range it
+// claims; each entry names its pair); wave w takes units w, w + gridDim.x,
+// ... (a loop bounded by the list's length), so that a KV head whose heads
 // selected large teams does not leave the others idle.
 template <typename T, int D, int GT, bool DENSE>
 __global__ __launch_bounds__(kWave) void k_attend(
     const T* __restrict__ K, const T* __restrict__ V, const T* __restrict__ sK,
     const T* __restrict__ sV, const float* __restrict__ q, int N, int T_suf, int BH, int Hkv,
-    int Hq, int G, int M, float scale_log2, int max_chunks, const PlanHeader* __restrict__ hdr,
+    int Hq, int G, int M, float scale_log2, int max_chunks, const unsigned* __restrict__ counter,
     const Chunk* __restrict__ chunks, const float* __restrict__ ulogc,
     float* __restrict__ part_o, float* __restrict__ part_ml) {
     constexpr int NF = frag_count<T, D>();
@@ -238,37 +239,31 @@ __global__ __launch_bounds__(kWave) void k_attend(
     const int c = lane >> 4, j16 = lane & 15;
     const int ncp = (N + UR - 1) / UR;
     const int nchd = ncp + (T_suf + UR - 1) / UR;  // dense units per (b, kv)
-    // units of (b, kv) pair i: the plan's count (sampled), or nchd (dense)
-    auto units_of = [&](int i) { return DENSE ? nchd : min(max(hdr[i].chunks, 0), max_chunks); };
-    int total = 0;
-    for (int i = 0; i < BH; ++i) total += units_of(i);
-    // (b, kv) pair and unit index of list entry u
-    auto locate = [&](int u, int& bhx, int& cix) {
+    // the unit list: the sampler's (read with the count of units it
+    // appended), or the dense path's (b, kv)-major one
+    const int total = DENSE ? BH * nchd
+                            : static_cast<int>(min(__hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT),
+                                                   static_cast<unsigned>(BH) * static_cast<unsigned>(max_chunks)));
+    auto descriptor = [&](int u) {
         if (DENSE) {
-            bhx = u / nchd;
-            cix = u - bhx * nchd;
-        } else {
-            bhx = 0;
-            while (bhx < BH - 1 && u >= units_of(bhx)) u -= units_of(bhx++);
-            cix = u;
-        }
-    };
-    auto descriptor = [&](int bhx, int cix) {
-        if (DENSE) {
+            const int bhx = u / nchd, cix = u - bhx * nchd;
             const bool suf = cix >= ncp;
             const int begin = (suf ? cix - ncp : cix) * UR;
-            return Chunk{begin, min(UR, (suf ? T_suf : N) - begin), suf ? -1 : 0, (1 << G) - 1};
+            return Chunk{begin, suf ? -1 : 0, cix, chunk_meta(min(UR, (suf ? T_suf : N) - begin), (1 << G) - 1, bhx)};
         }
-        return chunks[static_cast<size_t>(bhx) * max_chunks + min(cix, max_chunks - 1)];
+        return chunks[min(u, BH * max_chunks - 1)];
     };
 
-    int bh = -1, ci = 0;
-    if (blockIdx.x < total) locate(blockIdx.x, bh, ci);
-    Chunk ck = descriptor(max(bh, 0), ci);
+    Chunk ck = descriptor(min(static_cast<int>(blockIdx.x), BH * max_chunks - 1));
     int qbh = -1;  // the (b, kv) pair whose query fragments s_q holds
     QKT qk;
 
     for (int u = blockIdx.x; u < total; u += gridDim.x) {
+        const int bh = meta_bh(ck.meta), ci = ck.ci;
+        if (bh >= BH || ci < 0 || ci >= max_chunks) {  // uniform; never for a plan of this step
+            ck = descriptor(u + gridDim.x);
+            continue;
+        }
         const int b = bh / Hkv, kv = bh - b * Hkv;
         if (bh != qbh) {  // uniform
             // query fragments: head l % 16 of this KV head (zero for padding heads)
@@ -287,11 +282,9 @@ __global__ __launch_bounds__(kWave) void k_attend(
             qbh = bh;
         }
         // the next unit's descriptor is fetched while this one is processed
-        int nbh = bh, nci = ci;
-        if (u + gridDim.x < total) locate(u + gridDim.x, nbh, nci);
-        const Chunk nx = descriptor(nbh, nci);
-        int begin = ck.begin, rows = ck.rows, slot = ck.slot;
-        const int hmask = ck.hmask & ((1 << G) - 1);
+        const Chunk nx = descriptor(min(u + static_cast<int>(gridDim.x), total - 1));
+        int begin = ck.begin, rows = meta_rows(ck.meta), slot = ck.slot;
+        const int hmask = meta_hmask(ck.meta) & ((1 << G) - 1);
         const bool suffix = slot < 0;
         const int lim = suffix ? T_suf : N;
         if (!DENSE) {
@@ -438,8 +431,6 @@ __global__ __launch_bounds__(kWave) void k_attend(
             }
         }
         ck = nx;
-        bh = nbh;
-        ci = nci;
     }
 }
 
@@ -614,7 +605,7 @@ hipError_t attend_g(const AttendArgs& a, hipStream_t s) {
         const DecodeLayout& L = *a.lay;
         k_attend<T, D, GT, false><<<grid, kWave, 0, s>>>(
             K, V, sK, sV, a.q, a.N, a.T, BH, a.Hkv, a.Hq, a.G, a.M, sl2, a.max_chunks,
-            reinterpret_cast<const PlanHeader*>(a.ws + L.hdr),
+            reinterpret_cast<const unsigned*>(a.ws + L.counter),
             reinterpret_cast<const Chunk*>(a.ws + L.chunk),
             reinterpret_cast<const float*>(a.ws + L.ulogc), a.part_o, a.part_ml);
     }

@@ -20,14 +20,24 @@ constexpr int kAttendWavesPerCU = 8; // resident attention waves per compute uni
 
 // Attention work unit: up to kChunkRows consecutive rows of one union team of
 // the packed cache, or of the suffix (slot < 0); the dense path cuts its rows
-// into units of kDenseRows.  hmask has bit h set for
-// each query head of the KV head that reads the rows.
+// into units of kDenseRows.  The sampler appends the units of each (b, kv)
+// to one list shared by all pairs; `meta` packs the row count (bits 0-7),
+// the mask of query heads of the KV head that read the rows (bits 8-15) and
+// the (b, kv) pair (bits 16-31).
 struct Chunk {
     int begin;  // first packed row, or first suffix row when slot < 0
-    int rows;   // 1 .. kChunkRows
     int slot;   // union slot (index of the team's corrections), -1 = suffix
-    int hmask;
+    int ci;     // index of the unit within its (b, kv) pair
+    int meta;
 };
+
+__host__ __device__ inline int chunk_meta(int rows, int hmask, int bh) {
+    return rows | (hmask << 8) | (bh << 16);
+}
+__host__ __device__ inline int meta_rows(int m) { return m & 255; }
+__host__ __device__ inline int meta_hmask(int m) { return (m >> 8) & 255; }
+__host__ __device__ inline int meta_bh(int m) { return static_cast<int>(static_cast<unsigned>(m) >> 16); }
+constexpr int kMaxPairs = 65536;  // (b, kv) pairs a unit can name
 
 // Plan header per (b, kv), written by the sampler.
 struct PlanHeader {
@@ -42,7 +52,7 @@ struct PlanHeader {
 // union of up to min(M, G K) teams can have, plus the suffix chunks.
 struct DecodeLayout {
     int max_chunks = 0;
-    size_t phi = 0, Y = 0, lc = 0, hdr = 0, chunk = 0, ulogc = 0, po = 0, pml = 0,
+    size_t counter = 0, phi = 0, Y = 0, lc = 0, hdr = 0, chunk = 0, ulogc = 0, po = 0, pml = 0,
            total = 0;
 };
 

@@ -348,10 +348,13 @@ template <typename T, int D, int G>
 __global__ __launch_bounds__(kRouteThreads) void k_route(
     const T* __restrict__ reps, const double* __restrict__ log_n, const float* __restrict__ q,
     int M, int Hkv, int Hq, double scale, uint64_t seed, uint64_t step, double* __restrict__ phi,
-    double* __restrict__ Y) {
+    double* __restrict__ Y, unsigned* __restrict__ counter) {
     constexpr int DPL = D / 16;
     using RC = RepChunk<T, DPL>;
     __shared__ double s_gum[G][kRouteTeams];
+    // the sampler appends this step's attention units to an empty list
+    if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0)
+        __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const int bh = blockIdx.y;
     const int b = bh / Hkv, kv = bh - b * Hkv;
     const int tid = threadIdx.x, grp = tid >> 4, sub = tid & 15;
@@ -403,9 +406,10 @@ template <int G, int PL>
 __global__ __launch_bounds__(kSelectThreads) void k_select(
     const double* __restrict__ phi, const double* __restrict__ Y, const int* __restrict__ team_begin,
     const int* __restrict__ team_size, int M, int Hkv, int Hq, int Kp, int T_suf, int max_chunks,
-    float* __restrict__ lc, PlanHeader* __restrict__ hdr, Chunk* __restrict__ chunks,
-    float* __restrict__ ulogc, int* __restrict__ dbg_sel, float* __restrict__ dbg_logc,
-    double* __restrict__ dbg_tau, int* __restrict__ dbg_uteams, int* __restrict__ dbg_urows) {
+    float* __restrict__ lc, unsigned* __restrict__ counter, PlanHeader* __restrict__ hdr,
+    Chunk* __restrict__ chunks, float* __restrict__ ulogc, int* __restrict__ dbg_sel,
+    float* __restrict__ dbg_logc, double* __restrict__ dbg_tau, int* __restrict__ dbg_uteams,
+    int* __restrict__ dbg_urows) {
     constexpr bool kLdsLc = PL > 0 && PL <= 8;  // log c of every (head, team) in LDS
     extern __shared__ float s_lc[];  // [G][M] when kLdsLc
     __shared__ __align__(16) uint32_t s_hist[kSelectWaves][256];
@@ -497,8 +501,40 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
     __syncthreads();
 
     // ---- union of the heads' selections in ascending team order -------------
-    // per union team: its corrections, then its chunks of <= kChunkRows rows
-    Chunk* cb = chunks + static_cast<size_t>(bh) * max_chunks;
+    // per union team: its corrections, then its units of <= kChunkRows rows,
+    // appended to the list shared by all (b, kv) pairs at a range claimed
+    // with one atomic add
+    auto heads_of = [&](int g) {
+        int hm = 0;
+        if (g < M) {
+#pragma unroll
+            for (int h = 0; h < G; ++h) hm |= static_cast<int>((s_bits[h][g >> 6] >> (g & 63)) & 1ull) << h;
+        }
+        return hm;
+    };
+    // the pair's unit count first
+    int nu = 0;
+    for (int base = 0; base < M; base += kSelectThreads) {
+        const int g = base + tid;
+        const int tsz = base == 0 ? size0 : team_size[tb0 + min(g, M - 1)];
+        nu += heads_of(g) ? chunk_count(tsz) : 0;
+    }
+    const int nsc = chunk_count(T_suf);
+    {
+        const int x[3] = {nu, 0, 0};
+        int ex[3], tot[3];
+        block_scan3(x, ex, tot, s_w);
+        if (tid == 0) {
+            const int total = min(tot[0] + nsc, max_chunks);
+            s_w[0] = static_cast<int>(
+                __hip_atomic_fetch_add(counter, static_cast<unsigned>(total), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+            s_w[1] = total;
+        }
+        __syncthreads();
+    }
+    const int ubase = s_w[0], utotal = s_w[1];
+    __syncthreads();
+    Chunk* cb = chunks + ubase;
     int run_u = 0, run_rows = 0, run_c = 0;
     for (int base = 0; base < M; base += kSelectThreads) {
         const int g = base + tid;
@@ -508,11 +544,7 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
             tsz = team_size[tb0 + gc];
             tbeg = team_begin[tb0 + gc];
         }
-        int hm = 0;
-        if (g < M) {
-#pragma unroll
-            for (int h = 0; h < G; ++h) hm |= static_cast<int>((s_bits[h][g >> 6] >> (g & 63)) & 1ull) << h;
-        }
+        const int hm = heads_of(g);
         const int f = hm ? 1 : 0;
         const int x[3] = {f, f ? chunk_count(tsz) : 0, f ? tsz : 0};
         int ex[3], tot[3];
@@ -537,8 +569,8 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
             s_team[ex[0]] = make_int4(ex[1], tbeg, tsz, hm);
         }
         __syncthreads();
-        // the pass's chunks, one per thread: its team is the last with a
-        // first chunk at or before it
+        // the pass's units, one per thread: its team is the last with a
+        // first unit at or before it
         for (int c = tid; c < tot[1]; c += kSelectThreads) {
             int lo = 0, hi = tot[0] - 1;
             while (lo < hi) {
@@ -550,8 +582,10 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
             }
             const int4 tm = s_team[lo];
             const int p = c - tm.x;
-            if (run_c + c < max_chunks)
-                cb[run_c + c] = Chunk{tm.y + p * kChunkRows, min(kChunkRows, tm.z - p * kChunkRows), run_u + lo, tm.w};
+            const int ci = run_c + c;
+            if (ci < utotal)
+                cb[ci] = Chunk{tm.y + p * kChunkRows, run_u + lo, ci,
+                               chunk_meta(min(kChunkRows, tm.z - p * kChunkRows), tm.w, bh)};
         }
         __syncthreads();  // s_team is rewritten by the next pass
         run_u += tot[0];
@@ -559,18 +593,18 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
         run_rows += tot[2];
     }
     // the suffix: every head, no correction
-    const int nsc = chunk_count(T_suf);
     for (int p = tid; p < nsc; p += kSelectThreads) {
-        const int c = run_c + p;
-        if (c < max_chunks)
-            cb[c] = Chunk{p * kChunkRows, min(kChunkRows, T_suf - p * kChunkRows), -1, (1 << G) - 1};
+        const int ci = run_c + p;
+        if (ci < utotal)
+            cb[ci] = Chunk{p * kChunkRows, -1, ci, chunk_meta(min(kChunkRows, T_suf - p * kChunkRows), (1 << G) - 1, bh)};
     }
     if (tid == 0) {
-        hdr[bh] = PlanHeader{run_u, run_rows, min(run_c + nsc, max_chunks), 0};
+        hdr[bh] = PlanHeader{run_u, run_rows, utotal, 0};
         if (dbg_uteams) dbg_uteams[bh] = run_u;
         if (dbg_urows) dbg_urows[bh] = run_rows;
     }
 }
+
 
 template <typename T, int D, int G>
 hipError_t route_g(const RouteArgs& a, hipStream_t s) {
@@ -579,7 +613,8 @@ hipError_t route_g(const RouteArgs& a, hipStream_t s) {
     double* phi = reinterpret_cast<double*>(a.ws + L.phi);
     double* Y = reinterpret_cast<double*>(a.ws + L.Y);
     k_route<T, D, G><<<dim3((a.M + kRouteTeams - 1) / kRouteTeams, a.B * a.Hkv), kRouteThreads, 0, s>>>(
-        static_cast<const T*>(a.reps), a.log_n, a.q, a.M, a.Hkv, a.Hq, a.scale, a.seed, a.step, phi, Y);
+        static_cast<const T*>(a.reps), a.log_n, a.q, a.M, a.Hkv, a.Hq, a.scale, a.seed, a.step, phi, Y,
+        reinterpret_cast<unsigned*>(a.ws + L.counter));
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     float* lc = reinterpret_cast<float*>(a.ws + L.lc);
@@ -589,7 +624,8 @@ hipError_t route_g(const RouteArgs& a, hipStream_t s) {
 #define SANTAPP_SEL(PLV)                                                                          \
     k_select<G, PLV><<<a.B * a.Hkv, kSelectThreads,                                               \
                        (PLV > 0 && PLV <= 8) ? sizeof(float) * G * a.M : 0, s>>>(                \
-        phi, Y, a.team_begin, a.team_size, a.M, a.Hkv, a.Hq, a.Kp, a.T, L.max_chunks, lc, hdr,   \
+        phi, Y, a.team_begin, a.team_size, a.M, a.Hkv, a.Hq, a.Kp, a.T, L.max_chunks, lc,       \
+        reinterpret_cast<unsigned*>(a.ws + L.counter), hdr,                                     \
         ch, ulogc, d ? d->sel : nullptr, d ? d->logc : nullptr, d ? d->tau : nullptr,             \
         d ? d->union_teams : nullptr, d ? d->union_rows : nullptr)
     if (a.M <= 8 * kWave)
