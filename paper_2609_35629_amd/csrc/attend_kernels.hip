@@ -77,23 +77,18 @@ struct QK;
 template <int D>
 struct QK<bf16_t, D> {
     // block kb, lane group c: 16-byte chunk 4 kb + c of the row (dims
-    // 8 (4 kb + c) .. + 8); the same dims of the query head l % 16.  The
-    // query fragments (three bf16 terms per fp32 value, exact to fp32) live
-    // in LDS, shared by the workgroup's waves: sq[(kb * 3 + t) * 64 + lane].
+    // 8 (4 kb + c) .. + 8); the same dims of the query head of M row
+    // l % 16, as three bf16 terms per fp32 value (exact to fp32).
     static constexpr int KB = D / 32;
-    static constexpr int kLdsFrags = KB * 3 * kWave;
     using frag = uint4;
-    const bf16x8* sq;
+    bf16x8 qa[KB][3];
 
-    // fragments of lane `lane` for blocks kb = kb0, kb0 + step, ...
-    static __device__ __forceinline__ void build(bf16x8* s, const float* qrow, float scale, int lane,
-                                                 int kb0, int step) {
-        const int c = lane >> 4;
-        for (int kb = kb0; kb < KB; kb += step) {
+    __device__ __forceinline__ void load_q(const float* qrow, float scale, int c) {
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) {
             const float4* p = reinterpret_cast<const float4*>(qrow + 8 * (4 * kb + c));
             const float4 u = p[0], v = p[1];
             const float x[8] = {u.x, u.y, u.z, u.w, v.x, v.y, v.z, v.w};
-            bf16x8 a, b, r;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const float f = x[e] * scale;
@@ -101,27 +96,24 @@ struct QK<bf16_t, D> {
                 const float r1 = f - static_cast<float>(h0);
                 const __bf16 h1 = static_cast<__bf16>(r1);
                 const float r2 = r1 - static_cast<float>(h1);
-                a[e] = h0;
-                b[e] = h1;
-                r[e] = static_cast<__bf16>(r2);
+                qa[kb][0][e] = h0;
+                qa[kb][1][e] = h1;
+                qa[kb][2][e] = static_cast<__bf16>(r2);
             }
-            s[(kb * 3 + 0) * kWave + lane] = a;
-            s[(kb * 3 + 1) * kWave + lane] = b;
-            s[(kb * 3 + 2) * kWave + lane] = r;
         }
     }
     __device__ __forceinline__ void load_k(const bf16_t* row, int c, frag* f) const {
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb) f[kb] = load_stream(row + 8 * (4 * kb + c));
     }
-    __device__ __forceinline__ f32x4 scores(const frag* f, int lane) const {
+    __device__ __forceinline__ f32x4 scores(const frag* f) const {
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb) {
             const bf16x8 k = __builtin_bit_cast(bf16x8, f[kb]);
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sq[(kb * 3 + 2) * kWave + lane], k, acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sq[(kb * 3 + 1) * kWave + lane], k, acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sq[(kb * 3 + 0) * kWave + lane], k, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[kb][2], k, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[kb][1], k, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[kb][0], k, acc, 0, 0, 0);
         }
         return acc;
     }
@@ -131,7 +123,6 @@ template <int D>
 struct QK<float, D> {
     // block kb, lane group c: dim (D / 4) c + kb; the query stays in registers
     static constexpr int KB = D / 4;
-    static constexpr int kLdsFrags = 1;
     using frag = float4;
     float qa[KB];
 
@@ -143,7 +134,7 @@ struct QK<float, D> {
 #pragma unroll
         for (int i = 0; i < KB / 4; ++i) f[i] = load_stream_f(row + (D / 4) * c + 4 * i);
     }
-    __device__ __forceinline__ f32x4 scores(const frag* f, int) const {
+    __device__ __forceinline__ f32x4 scores(const frag* f) const {
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int i = 0; i < KB / 4; ++i) {
@@ -210,6 +201,42 @@ struct RowChunk<float, 4> {
     }
 };
 
+// Value sum of a 32-row step on the matrix cores (bf16 values):
+// O[h][dim] += sum_row P[h][row] V[row][dim] as v_mfma_f32_16x16x32_bf16
+// with the step's rows as the K dimension, one product per 16 dims.
+//   A (probabilities): M row i < 8 holds the bf16 high part of head i, row
+//     i + 8 the bf16 low part (p - high), so a product carries p to 16
+//     significant bits; the two halves of the accumulator are added when
+//     the unit ends.
+//   B (values): 8 consecutive rows of one dim per lane, read from an LDS
+//     copy of the 32 x D tile with the transposing read ds_read_b64_tr_b16:
+//     lane 4 a + e of a 16-lane block receives element e of the 8-byte
+//     words that lanes a, a + 4, a + 8, a + 12 of the block address, so
+//     when lane s addresses row s / 4, dims 4 (s % 4) .. + 4 of a 16-dim
+//     block, lane n gets four consecutive rows of dim n.
+//   The tile's 32-byte pieces are XOR-swizzled per row so that the eight
+//   rows one half-wave reads fall in distinct LDS banks.
+template <int D>
+struct VTile {
+    static constexpr int NB = D / 16;  // 16-dim blocks = products per step
+    static constexpr int kBytes = 32 * D * 2;
+    static __device__ __forceinline__ int offset(int row, int byte) {
+        const int h = ((row & 3) | ((row >> 1) & 4)) & (NB - 1);
+        return row * (2 * D) + ((((byte >> 5) ^ h)) << 5) + (byte & 31);
+    }
+    // B operand of block nb for lane l
+    static __device__ __forceinline__ bf16x8 operand(const char* tile, int nb, int lane) {
+        const int blk = lane >> 4, s = lane & 15;
+        const int r = 8 * blk + (s >> 2);
+        const int byte = 32 * nb + 8 * (s & 3);
+        typedef short v4i16 __attribute__((ext_vector_type(4)));
+        typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+        const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(tile + offset(r, byte)));
+        const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(tile + offset(r + 4, byte)));
+        return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    }
+};
+
 // One wave per workgroup.  The sampled path's units are chunks of at most
 // kChunkRows (32) consecutive rows of one union team or of the suffix; the
 // dense path's units are kDenseRows (128) rows, walked 32 rows at a time with
@@ -218,8 +245,14 @@ struct RowChunk<float, 4> {
 // claims; each entry names its pair); wave w takes units w, w + gridDim.x,
 // ... (a loop bounded by the list's length), so that a KV head whose heads
 // selected large teams does not leave the others idle.
+//
+// Register layout of the softmax: lane l = 16 c + j holds, in register r,
+// M row 4 c + r of the score tile, i.e. query head (4 c + r) % 8 of row j
+// (the query fills M rows 8..15 with a copy of heads 0..7, so lane groups
+// 2 and 3 repeat the states of groups 0 and 1 and every lane has the
+// state of the heads its value accumulators hold).
 template <typename T, int D, int GT, bool DENSE>
-__global__ __launch_bounds__(kWave) void k_attend(
+__global__ __launch_bounds__(kWave, 2) void k_attend(
     const T* __restrict__ K, const T* __restrict__ V, const T* __restrict__ sK,
     const T* __restrict__ sV, const float* __restrict__ q, int N, int T_suf, int BH, int Hkv,
     int Hq, int G, int M, float scale_log2, int max_chunks, const unsigned* __restrict__ counter,
@@ -228,15 +261,19 @@ __global__ __launch_bounds__(kWave) void k_attend(
     constexpr int NF = frag_count<T, D>();
     constexpr int VPL = D / 16;  // value dims per lane (16 lanes per row)
     constexpr int UR = DENSE ? kDenseRows : kChunkRows;
+    constexpr bool kMfmaPV = sizeof(T) == 2;
     using QKT = QK<T, D>;
     using VC = RowChunk<T, VPL>;
-    constexpr bool kLdsQ = sizeof(T) == 2;
-    __shared__ bf16x8 s_q[QKT::kLdsFrags];  // query fragments (bf16 keys)
-    __shared__ float4 s_p[16][2];           // probabilities of one tile
-    __shared__ float4 s_a[2];               // rescale factors of one tile
+    using VT = VTile<D>;
+    constexpr int NB = VT::NB;
+    __shared__ __attribute__((aligned(16))) char s_v[kMfmaPV ? VT::kBytes : 16];  // value tile
+    __shared__ float4 s_pt[8][8];  // probabilities [head][row / 4] (bf16 values)
+    __shared__ float4 s_p[16][2];  // probabilities [row][head / 4] of one tile (fp32 values)
+    __shared__ float4 s_a[2];      // rescale factors of one tile (fp32 values)
 
     const int lane = lane_id();
     const int c = lane >> 4, j16 = lane & 15;
+    const int hsel = 4 * (c & 1);  // first head of this lane's registers
     const int ncp = (N + UR - 1) / UR;
     const int nchd = ncp + (T_suf + UR - 1) / UR;  // dense units per (b, kv)
     // the unit list: the sampler's (read with the count of units it
@@ -255,7 +292,7 @@ __global__ __launch_bounds__(kWave) void k_attend(
     };
 
     Chunk ck = descriptor(min(static_cast<int>(blockIdx.x), BH * max_chunks - 1));
-    int qbh = -1;  // the (b, kv) pair whose query fragments s_q holds
+    int qbh = -1;  // the (b, kv) pair whose query the registers hold
     QKT qk;
 
     for (int u = blockIdx.x; u < total; u += gridDim.x) {
@@ -266,19 +303,11 @@ __global__ __launch_bounds__(kWave) void k_attend(
         }
         const int b = bh / Hkv, kv = bh - b * Hkv;
         if (bh != qbh) {  // uniform
-            // query fragments: head l % 16 of this KV head (zero for padding heads)
-            const int h = j16;
+            // query of M row l % 16: head (l % 16) % 8 of this KV head
+            // (zero for heads past the group)
+            const int h = kMfmaPV ? (j16 & 7) : j16;
             const int hq = kv * G + (h < G ? h : 0);
-            const float* qrow = q + (static_cast<size_t>(b) * Hq + hq) * D;
-            const float sc = h < G ? scale_log2 : 0.f;
-            if constexpr (kLdsQ) {
-                wave_lds_sync();
-                QKT::build(s_q, qrow, sc, lane, 0, 1);
-                qk.sq = s_q;
-                wave_lds_sync();
-            } else {
-                qk.load_q(qrow, sc, c);
-            }
+            qk.load_q(q + (static_cast<size_t>(b) * Hq + hq) * D, h < G ? scale_log2 : 0.f, c);
             qbh = bh;
         }
         // the next unit's descriptor is fetched while this one is processed
@@ -314,6 +343,7 @@ __global__ __launch_bounds__(kWave) void k_attend(
         }
 
         float m[4], l[4], acc[GT][VPL];
+        f32x4 oacc[NB];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             m[r] = kNeg;
@@ -323,6 +353,8 @@ __global__ __launch_bounds__(kWave) void k_attend(
         for (int h = 0; h < GT; ++h)
 #pragma unroll
             for (int e = 0; e < VPL; ++e) acc[h][e] = 0.f;
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) oacc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
         // 32 rows at a time: two 16-row tiles whose K and V loads are all
         // issued before any math.  K as MFMA fragments (lane (c, j) -> row j
@@ -343,78 +375,163 @@ __global__ __launch_bounds__(kWave) void k_attend(
                         vr[k][kk] = VC::load(Vb + static_cast<size_t>(min(t0 + 4 * kk + c, rows - 1)) * D + VPL * j16);
                 }
             }
-#pragma unroll
-            for (int k = 0; k < 2; ++k) {
-                if (k == 1 && !has1) continue;  // uniform
-                const int t0 = r0 + 16 * k;
-                const f32x4 sc = qk.scores(kf[k], lane);
-                // lane (c, j16): row j16 of the tile, heads 4 c .. 4 c + 3
-                const bool live = c < 2 && t0 + j16 < rows;
-                float a[4], p[4];
+            if constexpr (kMfmaPV) {
+                // softmax over the step's 32 rows at once
+                const f32x4 s0 = qk.scores(kf[0]);
+                f32x4 s1 = {kNeg, kNeg, kNeg, kNeg};
+                if (has1) s1 = qk.scores(kf[1]);
+                const bool live0 = r0 + j16 < rows, live1 = r0 + 16 + j16 < rows;
+                float a[4], p0[4], p1[4];
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    const float x = live ? sc[r] : kNeg;
-                    const float mn = fmaxf(m[r], row16_max(x));
+                    const float x0 = live0 ? s0[r] : kNeg;
+                    const float x1 = live1 ? s1[r] : kNeg;
+                    const float mn = fmaxf(m[r], row16_max(fmaxf(x0, x1)));
                     a[r] = rebase(m[r], mn);
-                    p[r] = fast_exp2(x - mn);
-                    l[r] = l[r] * a[r] + row16_sum(p[r]);
+                    p0[r] = fast_exp2(x0 - mn);
+                    p1[r] = fast_exp2(x1 - mn);
+                    l[r] = l[r] * a[r] + row16_sum(p0[r] + p1[r]);
                     m[r] = mn;
                 }
+                wave_lds_sync();  // the previous step's reads of the tiles are done
+                // the value tile (zeros for a missing second tile: its rows
+                // carry no weight, and 0 x garbage could be NaN)
+#pragma unroll
+                for (int k = 0; k < 2; ++k)
+#pragma unroll
+                    for (int kk = 0; kk < 4; ++kk) {
+                        const int row = 16 * k + 4 * kk + c;
+                        typename VC::raw v = vr[k][kk];
+                        if (k == 1 && !has1) v = typename VC::raw{};
+                        *reinterpret_cast<typename VC::raw*>(s_v + VT::offset(row, 2 * VPL * j16)) = v;
+                    }
                 if (c < 2) {
-                    s_p[j16][c] = make_float4(p[0], p[1], p[2], p[3]);
-                    if (j16 == 0) s_a[c] = make_float4(a[0], a[1], a[2], a[3]);
-                }
-                wave_lds_sync();
-                float av[8];
-                {
-                    const float4 a0 = s_a[0], a1 = s_a[1];
-                    av[0] = a0.x; av[1] = a0.y; av[2] = a0.z; av[3] = a0.w;
-                    av[4] = a1.x; av[5] = a1.y; av[6] = a1.z; av[7] = a1.w;
-                }
-                // only the heads that read this unit accumulate
+                    float* pt = reinterpret_cast<float*>(s_pt);
 #pragma unroll
-                for (int h = 0; h < GT; ++h) {
-                    if (!((hmask >> h) & 1)) continue;  // uniform
-#pragma unroll
-                    for (int e = 0; e < VPL; ++e) acc[h][e] *= av[h];
-                }
-                // this lane group's rows of the tile: c, c + 4, c + 8, c + 12
-#pragma unroll
-                for (int kk = 0; kk < 4; ++kk) {
-                    float vv[VPL];
-                    VC::unpack(vr[k][kk], vv);
-                    const float4 p0 = s_p[4 * kk + c][0], p1 = s_p[4 * kk + c][1];
-                    const float pv[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
-#pragma unroll
-                    for (int h = 0; h < GT; ++h) {
-                        if (!((hmask >> h) & 1)) continue;
-#pragma unroll
-                        for (int e = 0; e < VPL; ++e) acc[h][e] = fmaf(pv[h], vv[e], acc[h][e]);
+                    for (int r = 0; r < 4; ++r) {
+                        pt[(hsel + r) * 32 + j16] = p0[r];
+                        pt[(hsel + r) * 32 + 16 + j16] = p1[r];
                     }
                 }
                 wave_lds_sync();
+                // A operand: rows 8 c .. 8 c + 7 of head (l % 16) % 8, high
+                // or low bf16 part
+                bf16x8 pa;
+                {
+                    const float4 x0 = s_pt[j16 & 7][2 * c], x1 = s_pt[j16 & 7][2 * c + 1];
+                    const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+                    const bool low = j16 >= 8;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const __bf16 hi = static_cast<__bf16>(x[e]);
+                        pa[e] = low ? static_cast<__bf16>(x[e] - static_cast<float>(hi)) : hi;
+                    }
+                }
+                if (r0 > 0) {  // uniform; the first step starts from zero
+#pragma unroll
+                    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) oacc[nb][r] *= a[r];
+                }
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb)
+                    oacc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, VT::operand(s_v, nb, lane), oacc[nb], 0, 0, 0);
+            } else {
+#pragma unroll
+                for (int k = 0; k < 2; ++k) {
+                    if (k == 1 && !has1) continue;  // uniform
+                    const int t0 = r0 + 16 * k;
+                    const f32x4 sc = qk.scores(kf[k]);
+                    // lane (c, j16): row j16 of the tile, heads 4 c .. 4 c + 3
+                    const bool live = c < 2 && t0 + j16 < rows;
+                    float a[4], p[4];
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const float x = live ? sc[r] : kNeg;
+                        const float mn = fmaxf(m[r], row16_max(x));
+                        a[r] = rebase(m[r], mn);
+                        p[r] = fast_exp2(x - mn);
+                        l[r] = l[r] * a[r] + row16_sum(p[r]);
+                        m[r] = mn;
+                    }
+                    if (c < 2) {
+                        s_p[j16][c] = make_float4(p[0], p[1], p[2], p[3]);
+                        if (j16 == 0) s_a[c] = make_float4(a[0], a[1], a[2], a[3]);
+                    }
+                    wave_lds_sync();
+                    float av[8];
+                    {
+                        const float4 a0 = s_a[0], a1 = s_a[1];
+                        av[0] = a0.x; av[1] = a0.y; av[2] = a0.z; av[3] = a0.w;
+                        av[4] = a1.x; av[5] = a1.y; av[6] = a1.z; av[7] = a1.w;
+                    }
+                    // only the heads that read this unit accumulate
+#pragma unroll
+                    for (int h = 0; h < GT; ++h) {
+                        if (!((hmask >> h) & 1)) continue;  // uniform
+#pragma unroll
+                        for (int e = 0; e < VPL; ++e) acc[h][e] *= av[h];
+                    }
+                    // this lane group's rows of the tile: c, c + 4, c + 8, c + 12
+#pragma unroll
+                    for (int kk = 0; kk < 4; ++kk) {
+                        float vv[VPL];
+                        VC::unpack(vr[k][kk], vv);
+                        const float4 pp0 = s_p[4 * kk + c][0], pp1 = s_p[4 * kk + c][1];
+                        const float pv[8] = {pp0.x, pp0.y, pp0.z, pp0.w, pp1.x, pp1.y, pp1.z, pp1.w};
+#pragma unroll
+                        for (int h = 0; h < GT; ++h) {
+                            if (!((hmask >> h) & 1)) continue;
+#pragma unroll
+                            for (int e = 0; e < VPL; ++e) acc[h][e] = fmaf(pv[h], vv[e], acc[h][e]);
+                        }
+                    }
+                    wave_lds_sync();
+                }
             }
         }
 
-        // the unit's state per head: the four lane groups share each head's
-        // maximum, so their value sums simply add; heads that do not read the
-        // unit leave an empty state
+        // the unit's state per head; heads that do not read the unit leave
+        // an empty state
         const size_t pbase = static_cast<size_t>(bh) * G * max_chunks + ci;
+        if constexpr (kMfmaPV) {
+            // high + low halves: lane groups c and c ^ 2 hold the same
+            // heads; group c < 2 finishes dim blocks 0 .. NB/2 - 1, group
+            // c >= 2 blocks NB/2 .. NB - 1
+            const bool lower = c < 2;
 #pragma unroll
-        for (int h = 0; h < GT; ++h) {
-            if (!(live_unit && ((hmask >> h) & 1))) continue;  // uniform
-            float x[VPL];
+            for (int nb = 0; nb < NB / 2; ++nb) {
 #pragma unroll
-            for (int e = 0; e < VPL; ++e) {
-                float t = acc[h][e];
-                t += __shfl_xor(t, 16);
-                t += __shfl_xor(t, 32);
-                x[e] = t;
+                for (int r = 0; r < 4; ++r) {
+                    const float keep = lower ? oacc[nb][r] : oacc[nb + NB / 2][r];
+                    const float send = lower ? oacc[nb + NB / 2][r] : oacc[nb][r];
+                    const float x = keep + __shfl_xor(send, 32);
+                    const int h = hsel + r;
+                    if (live_unit && h < G && ((hmask >> h) & 1)) {
+                        const int dim = (lower ? 0 : D / 2) + 16 * nb + j16;
+                        __builtin_nontemporal_store(x, part_o + (pbase + static_cast<size_t>(h) * max_chunks) * D + dim);
+                    }
+                }
             }
-            if (c == 0) {
-                float* o = part_o + (pbase + static_cast<size_t>(h) * max_chunks) * D + VPL * j16;
+        } else {
+            // the four lane groups share each head's maximum, so their value
+            // sums simply add
 #pragma unroll
-                for (int e = 0; e < VPL; e += 4) store_stream(o + e, make_float4(x[e], x[e + 1], x[e + 2], x[e + 3]));
+            for (int h = 0; h < GT; ++h) {
+                if (!(live_unit && ((hmask >> h) & 1))) continue;  // uniform
+                float x[VPL];
+#pragma unroll
+                for (int e = 0; e < VPL; ++e) {
+                    float t = acc[h][e];
+                    t += __shfl_xor(t, 16);
+                    t += __shfl_xor(t, 32);
+                    x[e] = t;
+                }
+                if (c == 0) {
+                    float* o = part_o + (pbase + static_cast<size_t>(h) * max_chunks) * D + VPL * j16;
+#pragma unroll
+                    for (int e = 0; e < VPL; e += 4) store_stream(o + e, make_float4(x[e], x[e + 1], x[e + 2], x[e + 3]));
+                }
             }
         }
         if (c < 2 && j16 == 0) {
