@@ -571,7 +571,7 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(const float* __restrict
     constexpr int NW = kMergeThreads / kWave;
     constexpr int PER = 4;                     // chunk states per thread and block of units
     constexpr int CB = PER * kMergeThreads;    // units per block
-    constexpr int kBatch = 16;                 // value loads in flight per thread and pass
+    constexpr int kBatch = 32;                 // value loads in flight per thread and pass
     __shared__ float s_red[NW];
     __shared__ int s_cnt[NW];
     __shared__ int s_idx[CB];

@@ -19,6 +19,8 @@
 //           the exactly attended suffix.
 #include <math.h>
 
+#include <type_traits>
+
 #include "common.h"
 #include "internal.h"
 
@@ -140,11 +142,13 @@ struct KeySet {
         p = pp;
         const int lane = lane_id();
         double v[PL];
+        // clamped indices: no branch around the loads; the keys' loads
+        // first, phi (needed only once tau is known) after them
 #pragma unroll
-        for (int j = 0; j < PL; ++j) {
-            const int i = min(j * kWave + lane, M - 1);  // clamped: no branch around the loads
-            v[j] = y[i];
-            if constexpr (kPhiRegs) ph[j] = pp[i];
+        for (int j = 0; j < PL; ++j) v[j] = y[min(j * kWave + lane, M - 1)];
+        if constexpr (kPhiRegs) {
+#pragma unroll
+            for (int j = 0; j < PL; ++j) ph[j] = pp[min(j * kWave + lane, M - 1)];
         }
 #pragma unroll
         for (int j = 0; j < PL; ++j) k[j] = order_key(v[j]);
@@ -445,46 +449,41 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
         const int need_ties = Kp - wave_sum(above_cnt);
 
         // selection in index order i = j * 64 + lane: the keys above tau's
-        // key and the first need_ties keys equal to it
+        // key and the first need_ties keys equal to it (exactly equal Y
+        // values; the tie path is kept out of the common loop)
         const uint64_t lt = lanemask_lt();
         const bool compact = Kp <= kWave;  // log c once per selected team, one lane each
-        int nsel = 0, nties = 0;
         uint32_t* cidx = reinterpret_cast<uint32_t*>(s_cand[w]);  // [64] team index
         float* cx = reinterpret_cast<float*>(s_cand[w]) + kWave;  // [64] phi - tau
+        auto select_pass = [&](auto with_ties) {
+            int nsel = 0, nties = 0;
 #pragma unroll
-        for (int j = 0; j < nj; ++j) {
-            const int i = j * kWave + lane;
-            const bool valid = ks.valid(j);
-            const uint64_t k = ks.key(j);
-            bool sel = valid && k > tkey;
-            if (need_ties > 0) {  // uniform
-                const bool tie = valid && k == tkey;
-                const uint64_t tb = __ballot(tie);
-                sel = sel || (tie && nties + __popcll(tb & lt) < need_ties);
-                nties += __popcll(tb);
-            }
-            const uint64_t sb = __ballot(sel);
-            if (lane == 0) s_bits[w][j] = sb;
-            if (sel) {
-                const int pos = nsel + __popcll(sb & lt);
-                const float x = static_cast<float>(ks.phi(j) - tau);
-                if (compact) {
-                    cidx[pos] = static_cast<uint32_t>(i);
-                    cx[pos] = x;
-                } else {
-                    const float v = log_inclusion(x);
-                    if constexpr (kLdsLc)
-                        s_lc[w * M + i] = v;
-                    else
-                        lc[hoff + i] = v;
-                    if (dbg_sel) dbg_sel[(static_cast<size_t>(b) * Hq + hq) * Kp + pos] = i;
-                    if (dbg_logc) dbg_logc[(static_cast<size_t>(b) * Hq + hq) * Kp + pos] = v;
+            for (int j = 0; j < nj; ++j) {
+                const bool valid = ks.valid(j);
+                const uint64_t k = ks.key(j);
+                bool sel = valid && k > tkey;
+                if constexpr (decltype(with_ties)::value) {
+                    const bool tie = valid && k == tkey;
+                    const uint64_t tb = __ballot(tie);
+                    sel = sel || (tie && nties + __popcll(tb & lt) < need_ties);
+                    nties += __popcll(tb);
                 }
+                const uint64_t sb = __ballot(sel);
+                if (lane == 0) s_bits[w][j] = sb;
+                if (compact && sel) {
+                    const int pos = nsel + __popcll(sb & lt);
+                    cidx[pos] = static_cast<uint32_t>(j * kWave + lane);
+                    cx[pos] = static_cast<float>(ks.phi(j) - tau);
+                }
+                nsel += __popcll(sb);
             }
-            nsel += __popcll(sb);
-        }
+        };
+        if (need_ties > 0)  // uniform
+            select_pass(std::true_type{});
+        else
+            select_pass(std::false_type{});
+        wave_lds_sync();
         if (compact) {
-            wave_lds_sync();
             if (lane < Kp) {
                 const int i = static_cast<int>(cidx[lane]);
                 const float v = log_inclusion(cx[lane]);
@@ -494,6 +493,24 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
                     lc[hoff + i] = v;
                 if (dbg_sel) dbg_sel[(static_cast<size_t>(b) * Hq + hq) * Kp + lane] = i;
                 if (dbg_logc) dbg_logc[(static_cast<size_t>(b) * Hq + hq) * Kp + lane] = v;
+            }
+        } else {
+            // large budgets: every lane its selected keys, from the ballots
+            int nsel = 0;
+            for (int j = 0; j < nj; ++j) {
+                const uint64_t sb = s_bits[w][j];
+                if ((sb >> lane) & 1ull) {
+                    const int i = j * kWave + lane;
+                    const int pos = nsel + __popcll(sb & lt);
+                    const float v = log_inclusion(static_cast<float>(ks.phi(j) - tau));
+                    if constexpr (kLdsLc)
+                        s_lc[w * M + i] = v;
+                    else
+                        lc[hoff + i] = v;
+                    if (dbg_sel) dbg_sel[(static_cast<size_t>(b) * Hq + hq) * Kp + pos] = i;
+                    if (dbg_logc) dbg_logc[(static_cast<size_t>(b) * Hq + hq) * Kp + pos] = v;
+                }
+                nsel += __popcll(sb);
             }
         }
         if (lane == 0 && dbg_tau) dbg_tau[static_cast<size_t>(b) * Hq + hq] = tau;
@@ -512,14 +529,78 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
         }
         return hm;
     };
-    // the pair's unit count first
+    auto write_logc = [&](int g, int slot, int hm) {
+        float v[kLogcStride];
+#pragma unroll
+        for (int h = 0; h < kLogcStride; ++h) {
+            float t = 0.f;
+            if (h < G && ((hm >> h) & 1)) {
+                if constexpr (kLdsLc)
+                    t = s_lc[h * M + g];
+                else
+                    t = lc[(static_cast<size_t>(b) * Hq + kv * G + h) * M + g];
+            }
+            v[h] = t;
+        }
+        float4* L = reinterpret_cast<float4*>(ulogc + (tb0 + slot) * kLogcStride);
+        L[0] = make_float4(v[0], v[1], v[2], v[3]);
+        L[1] = make_float4(v[4], v[5], v[6], v[7]);
+    };
+    const int nsc = chunk_count(T_suf);
+    if (M <= kSelectThreads) {
+        // one pass, thread g owns team g: one scan gives every union team
+        // its slot and first unit and the pair's totals, and the range claim
+        // is issued as soon as the total is known
+        const int hm = heads_of(tid);
+        const int f = hm ? 1 : 0;
+        const int x[3] = {f, f ? chunk_count(size0) : 0, f ? size0 : 0};
+        int ex[3], tot[3];
+        block_scan3(x, ex, tot, s_w);
+        const int utotal = min(tot[1] + nsc, max_chunks);
+        if (tid == 0)
+            s_w[0] = static_cast<int>(__hip_atomic_fetch_add(counter, static_cast<unsigned>(utotal), __ATOMIC_RELAXED,
+                                                             __HIP_MEMORY_SCOPE_AGENT));
+        if (f) {
+            write_logc(tid, ex[0], hm);
+            s_team[ex[0]] = make_int4(ex[1], begin0, size0, hm);
+        }
+        __syncthreads();
+        Chunk* cb = chunks + s_w[0];
+        // units of the union teams and of the suffix, cooperatively: unit c
+        // belongs to the last union team whose first unit is at or before it
+        for (int c = tid; c < utotal; c += kSelectThreads) {
+            if (c < tot[1]) {
+                int lo = 0, hi = tot[0] - 1;
+                while (lo < hi) {
+                    const int mid = (lo + hi + 1) >> 1;
+                    if (s_team[mid].x <= c)
+                        lo = mid;
+                    else
+                        hi = mid - 1;
+                }
+                const int4 tm = s_team[lo];
+                const int p = c - tm.x;
+                cb[c] = Chunk{tm.y + p * kChunkRows, lo, c, chunk_meta(min(kChunkRows, tm.z - p * kChunkRows), tm.w, bh)};
+            } else {
+                const int p = c - tot[1];
+                cb[c] = Chunk{p * kChunkRows, -1, c, chunk_meta(min(kChunkRows, T_suf - p * kChunkRows), (1 << G) - 1, bh)};
+            }
+        }
+        if (tid == 0) {
+            hdr[bh] = PlanHeader{tot[0], tot[2], utotal, 0};
+            if (dbg_uteams) dbg_uteams[bh] = tot[0];
+            if (dbg_urows) dbg_urows[bh] = tot[2];
+        }
+        return;
+    }
+
+    // several passes of kSelectThreads teams: the pair's unit count first
     int nu = 0;
     for (int base = 0; base < M; base += kSelectThreads) {
         const int g = base + tid;
         const int tsz = base == 0 ? size0 : team_size[tb0 + min(g, M - 1)];
         nu += heads_of(g) ? chunk_count(tsz) : 0;
     }
-    const int nsc = chunk_count(T_suf);
     {
         const int x[3] = {nu, 0, 0};
         int ex[3], tot[3];
@@ -550,22 +631,7 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
         int ex[3], tot[3];
         block_scan3(x, ex, tot, s_w);
         if (f) {
-            const int slot = run_u + ex[0];
-            float v[kLogcStride];
-#pragma unroll
-            for (int h = 0; h < kLogcStride; ++h) {
-                float t = 0.f;
-                if (h < G && ((hm >> h) & 1)) {
-                    if constexpr (kLdsLc)
-                        t = s_lc[h * M + g];
-                    else
-                        t = lc[(static_cast<size_t>(b) * Hq + kv * G + h) * M + g];
-                }
-                v[h] = t;
-            }
-            float4* L = reinterpret_cast<float4*>(ulogc + (tb0 + slot) * kLogcStride);
-            L[0] = make_float4(v[0], v[1], v[2], v[3]);
-            L[1] = make_float4(v[4], v[5], v[6], v[7]);
+            write_logc(g, run_u + ex[0], hm);
             s_team[ex[0]] = make_int4(ex[1], tbeg, tsz, hm);
         }
         __syncthreads();
