@@ -95,6 +95,7 @@ DecodeLayout decode_layout(int B, int Hq, int Hkv, int T, int d, int M, int Kp, 
     const int G = Hq / Hkv;
     const long long xs = std::min<long long>(M, static_cast<long long>(G) * Kp);
     L.max_chunks = cap[xs] + chunk_count(T);
+    L.max_hunits = cap[std::min(M, Kp)] + chunk_count(T);
     size_t off = 0;
     auto take = [&](size_t bytes) {
         const size_t at = off;
@@ -108,8 +109,8 @@ DecodeLayout decode_layout(int B, int Hq, int Hkv, int T, int d, int M, int Kp, 
     L.hdr = take(BH * sizeof(PlanHeader));
     L.chunk = take(BH * L.max_chunks * sizeof(Chunk));
     L.ulogc = take(BH * M * kLogcStride * sizeof(float));
-    L.po = take(BQ * L.max_chunks * d * sizeof(float));
-    L.pml = take(BQ * L.max_chunks * 2 * sizeof(float));
+    L.po = take(BQ * L.max_hunits * d * sizeof(float));
+    L.pml = take(BQ * L.max_hunits * 2 * sizeof(float));
     L.total = off;
     return L;
 }
@@ -119,6 +120,7 @@ DecodeLayout dense_layout(int B, int Hq, int Hkv, int N, int T, int d) {
     const size_t BQ = static_cast<size_t>(B) * Hq;
     (void)Hkv;
     L.max_chunks = dense_count(N) + dense_count(T);
+    L.max_hunits = L.max_chunks;  // every head reads every unit
     size_t off = 0;
     L.po = off;
     off = align_up(off + BQ * L.max_chunks * d * sizeof(float));
@@ -342,6 +344,7 @@ santapp_status santapp_decode(const santapp_teams* t, const float* q, const void
     A.T = T;
     A.M = t->M;
     A.max_chunks = L.max_chunks;
+    A.max_hunits = L.max_hunits;
     A.grid_waves = t->cus > 0 ? t->cus * kAttendWavesPerCU : 0;
     A.dtype = t->dtype;
     A.scale = static_cast<float>(scale);
@@ -357,6 +360,8 @@ santapp_status santapp_decode(const santapp_teams* t, const float* q, const void
         return hipSuccess;
     };
     if ((e = mark(0)) != hipSuccess) return hip_fail(e, "event record");
+    if (L.max_hunits > kMaxHeadUnits)
+        return fail(SANTAPP_ELIMIT, "a head would read %d units (at most %d)", L.max_hunits, kMaxHeadUnits);
     if (Kp == t->M) {
         // every team selected with correction 1: dense attention over the cache
         A.dense = true;
@@ -437,6 +442,7 @@ santapp_status santapp_dense_decode(const float* q, const void* K, const void* V
     A.T = T;
     A.M = 0;
     A.max_chunks = L.max_chunks;
+    A.max_hunits = L.max_hunits;
     A.dtype = dtype;
     A.scale = static_cast<float>(scale);
     A.dense = true;

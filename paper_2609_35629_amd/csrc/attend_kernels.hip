@@ -244,20 +244,22 @@ struct VTile {
 // pairs form one list (the sampler appends each pair's units at a range it
 // claims; each entry names its pair); wave w takes units w, w + gridDim.x,
 // ... (a loop bounded by the list's length), so that a KV head whose heads
-// selected large teams does not leave the others idle.
+// selected large teams does not leave the others idle.  A unit's state for
+// head h goes to position pos[h] of that head's list (its unit index on the
+// dense path, where every head reads every unit).
 //
 // Register layout of the softmax: lane l = 16 c + j holds, in register r,
 // M row 4 c + r of the score tile, i.e. query head (4 c + r) % 8 of row j
-// (the query fills M rows 8..15 with a copy of heads 0..7, so lane groups
-// 2 and 3 repeat the states of groups 0 and 1 and every lane has the
+// (for bf16 the query fills M rows 8..15 with a copy of heads 0..7, so lane
+// groups 2 and 3 repeat the states of groups 0 and 1 and every lane has the
 // state of the heads its value accumulators hold).
 template <typename T, int D, int GT, bool DENSE>
 __global__ __launch_bounds__(kWave, 2) void k_attend(
     const T* __restrict__ K, const T* __restrict__ V, const T* __restrict__ sK,
     const T* __restrict__ sV, const float* __restrict__ q, int N, int T_suf, int BH, int Hkv,
-    int Hq, int G, int M, float scale_log2, int max_chunks, const unsigned* __restrict__ counter,
-    const Chunk* __restrict__ chunks, const float* __restrict__ ulogc,
-    float* __restrict__ part_o, float* __restrict__ part_ml) {
+    int Hq, int G, int M, float scale_log2, int max_chunks, int max_hunits,
+    const unsigned* __restrict__ counter, const Chunk* __restrict__ chunks,
+    const float* __restrict__ ulogc, float* __restrict__ part_o, float* __restrict__ part_ml) {
     constexpr int NF = frag_count<T, D>();
     constexpr int VPL = D / 16;  // value dims per lane (16 lanes per row)
     constexpr int UR = DENSE ? kDenseRows : kChunkRows;
@@ -286,19 +288,30 @@ __global__ __launch_bounds__(kWave, 2) void k_attend(
             const int bhx = u / nchd, cix = u - bhx * nchd;
             const bool suf = cix >= ncp;
             const int begin = (suf ? cix - ncp : cix) * UR;
-            return Chunk{begin, suf ? -1 : 0, cix, chunk_meta(min(UR, (suf ? T_suf : N) - begin), (1 << G) - 1, bhx)};
+            Chunk d;
+            d.begin = begin;
+            d.slot = suf ? -1 : 0;
+            d.meta = chunk_meta(min(UR, (suf ? T_suf : N) - begin), (1 << G) - 1, bhx);
+            d.ci = cix;
+            d.p01 = d.p23 = d.p45 = d.p67 = 0u;
+            return d;
         }
         return chunks[min(u, BH * max_chunks - 1)];
     };
+    // the sampled path fetches the next unit's descriptor while it processes
+    // one; the dense path computes it in place
+    const int stride = static_cast<int>(gridDim.x);
+    const int u0 = static_cast<int>(blockIdx.x);
 
-    Chunk ck = descriptor(min(static_cast<int>(blockIdx.x), BH * max_chunks - 1));
+    Chunk ck = descriptor(DENSE ? 0 : min(u0, BH * max_chunks - 1));
     int qbh = -1;  // the (b, kv) pair whose query the registers hold
     QKT qk;
 
-    for (int u = blockIdx.x; u < total; u += gridDim.x) {
+    for (int u = u0; u < total; u += stride) {
+        if (DENSE) ck = descriptor(u);
         const int bh = meta_bh(ck.meta), ci = ck.ci;
         if (bh >= BH || ci < 0 || ci >= max_chunks) {  // uniform; never for a plan of this step
-            ck = descriptor(u + gridDim.x);
+            ck = descriptor(min(u + stride, total - 1));
             continue;
         }
         const int b = bh / Hkv, kv = bh - b * Hkv;
@@ -310,8 +323,7 @@ __global__ __launch_bounds__(kWave, 2) void k_attend(
             qk.load_q(q + (static_cast<size_t>(b) * Hq + hq) * D, h < G ? scale_log2 : 0.f, c);
             qbh = bh;
         }
-        // the next unit's descriptor is fetched while this one is processed
-        const Chunk nx = descriptor(min(u + static_cast<int>(gridDim.x), total - 1));
+        const Chunk nx = DENSE ? ck : descriptor(min(u + stride, total - 1));
         int begin = ck.begin, rows = meta_rows(ck.meta), slot = ck.slot;
         const int hmask = meta_hmask(ck.meta) & ((1 << G) - 1);
         const bool suffix = slot < 0;
@@ -328,18 +340,13 @@ __global__ __launch_bounds__(kWave, 2) void k_attend(
                              : K + (static_cast<size_t>(bh) * N + begin) * D;
         const T* Vb = suffix ? sV + (static_cast<size_t>(bh) * T_suf + begin) * D
                              : V + (static_cast<size_t>(bh) * N + begin) * D;
-        // the correction of this unit's team, one per head (zero for the suffix)
-        float lcv[8];
-        {
-            float4 u = make_float4(0.f, 0.f, 0.f, 0.f), v = u;
-            if (!DENSE && !suffix) {
-                const float4* L = reinterpret_cast<const float4*>(
-                    ulogc + (static_cast<size_t>(bh) * M + slot) * kLogcStride);
-                u = L[0];
-                v = L[1];
-            }
-            lcv[0] = u.x; lcv[1] = u.y; lcv[2] = u.z; lcv[3] = u.w;
-            lcv[4] = v.x; lcv[5] = v.y; lcv[6] = v.z; lcv[7] = v.w;
+        // the correction of this unit's team for heads 0..3 (lc03) and 4..7
+        // (lc47), zero for the suffix
+        float4 lc03 = make_float4(0.f, 0.f, 0.f, 0.f), lc47 = lc03;
+        if (!DENSE && !suffix) {
+            const float4* L = reinterpret_cast<const float4*>(ulogc + (static_cast<size_t>(bh) * M + slot) * kLogcStride);
+            lc03 = L[0];
+            lc47 = L[1];
         }
 
         float m[4], l[4], acc[GT][VPL];
@@ -491,14 +498,30 @@ __global__ __launch_bounds__(kWave, 2) void k_attend(
             }
         }
 
-        // the unit's state per head; heads that do not read the unit leave
-        // an empty state
-        const size_t pbase = static_cast<size_t>(bh) * G * max_chunks + ci;
+        // the unit's state for each head that reads it, at the unit's
+        // position in that head's list (rows of this pair's lists)
+        float* const po_bh = part_o + static_cast<size_t>(bh) * G * max_hunits * D;
+        float* const pml_bh = part_ml + static_cast<size_t>(bh) * G * max_hunits * 2;
+        auto list_row = [&](int h, int pos) { return h * max_hunits + min(DENSE ? ci : pos, max_hunits - 1); };
+        // positions of this lane's register heads hsel .. hsel + 3: the
+        // descriptor words as wave-uniform values, picked by selects (an
+        // indexed read would move the descriptor to scratch memory)
+        int hp[4];
+        {
+            const unsigned w01 = __builtin_amdgcn_readfirstlane(ck.p01), w23 = __builtin_amdgcn_readfirstlane(ck.p23);
+            const unsigned w45 = __builtin_amdgcn_readfirstlane(ck.p45), w67 = __builtin_amdgcn_readfirstlane(ck.p67);
+            const unsigned wa = hsel ? w45 : w01, wb = hsel ? w67 : w23;
+            hp[0] = static_cast<int>(wa & 0xffffu);
+            hp[1] = static_cast<int>(wa >> 16);
+            hp[2] = static_cast<int>(wb & 0xffffu);
+            hp[3] = static_cast<int>(wb >> 16);
+        }
         if constexpr (kMfmaPV) {
             // high + low halves: lane groups c and c ^ 2 hold the same
             // heads; group c < 2 finishes dim blocks 0 .. NB/2 - 1, group
             // c >= 2 blocks NB/2 .. NB - 1
             const bool lower = c < 2;
+            const int dim0 = (lower ? 0 : D / 2) + j16;
 #pragma unroll
             for (int nb = 0; nb < NB / 2; ++nb) {
 #pragma unroll
@@ -507,10 +530,8 @@ __global__ __launch_bounds__(kWave, 2) void k_attend(
                     const float send = lower ? oacc[nb + NB / 2][r] : oacc[nb][r];
                     const float x = keep + __shfl_xor(send, 32);
                     const int h = hsel + r;
-                    if (live_unit && h < G && ((hmask >> h) & 1)) {
-                        const int dim = (lower ? 0 : D / 2) + 16 * nb + j16;
-                        __builtin_nontemporal_store(x, part_o + (pbase + static_cast<size_t>(h) * max_chunks) * D + dim);
-                    }
+                    if (live_unit && h < G && ((hmask >> h) & 1))
+                        __builtin_nontemporal_store(x, po_bh + list_row(h, hp[r]) * D + dim0 + 16 * nb);
                 }
             }
         } else {
@@ -518,7 +539,7 @@ __global__ __launch_bounds__(kWave, 2) void k_attend(
             // sums simply add
 #pragma unroll
             for (int h = 0; h < GT; ++h) {
-                if (!(live_unit && ((hmask >> h) & 1))) continue;  // uniform
+                if (!(live_unit && h < G && ((hmask >> h) & 1))) continue;  // uniform
                 float x[VPL];
 #pragma unroll
                 for (int e = 0; e < VPL; ++e) {
@@ -528,54 +549,61 @@ __global__ __launch_bounds__(kWave, 2) void k_attend(
                     x[e] = t;
                 }
                 if (c == 0) {
-                    float* o = part_o + (pbase + static_cast<size_t>(h) * max_chunks) * D + VPL * j16;
+                    float* o = po_bh + list_row(h, chunk_pos(ck, h)) * D + VPL * j16;
 #pragma unroll
                     for (int e = 0; e < VPL; e += 4) store_stream(o + e, make_float4(x[e], x[e + 1], x[e + 2], x[e + 3]));
                 }
             }
         }
         if (c < 2 && j16 == 0) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
+            // register r of lane group c is head 4 c + r; the correction
+            // enters as a shift of the unit's maximum (every row of the unit
+            // belongs to the same team).  Written out per register so that
+            // every index is a constant (a lane-dependent index into a
+            // register array would put the array in scratch memory).
+            auto put = [&](int r, float lc_lo, float lc_hi, float mr, float lr, int pos) {
                 const int h = 4 * c + r;
-                if (h < G) {
-                    const bool on = live_unit && ((hmask >> h) & 1);
-                    // the correction enters as a shift of the unit's maximum:
-                    // every row of the unit belongs to the same team
-                    const float2 st = on ? make_float2(m[r] - lcv[h] * kLog2e, l[r]) : make_float2(kNeg, 0.f);
-                    store_stream2(part_ml + (pbase + static_cast<size_t>(h) * max_chunks) * 2, st);
-                }
-            }
+                if (live_unit && h < G && ((hmask >> h) & 1))
+                    store_stream2(pml_bh + list_row(h, pos) * 2, make_float2(mr - (c ? lc_hi : lc_lo) * kLog2e, lr));
+            };
+            put(0, lc03.x, lc47.x, m[0], l[0], hp[0]);
+            put(1, lc03.y, lc47.y, m[1], l[1], hp[1]);
+            put(2, lc03.z, lc47.z, m[2], l[2], hp[2]);
+            put(3, lc03.w, lc47.w, m[3], l[3], hp[3]);
         }
         ck = nx;
     }
 }
 
-// Workgroup (sequence and query head, slice of kMergeDims output dims):
-// the chunk states of the head are rescaled to the largest maximum; units
-// the head does not read carry the empty state and are skipped.  The states
-// come first (one round trip that does not wait for the header), then the
-// value sums of the units that count: lane group g of the workgroup takes
-// every kMergeGroups-th of them in order, all loads in flight at once, and
-// the groups' sums are added in group order (a fixed summation order).
-constexpr int kMergeThreads = 256;
+// Merge of one query head's list of n unit states (m_p: log2-domain maximum
+// with the team's correction folded in, l_p: mass) and value sums o_p:
+// out = sum_p 2^(m_p - mx) o_p / sum_p 2^(m_p - mx) l_p with mx = max_p m_p.
+// Workgroup (sequence and query head, slice of kMergeDims output dims): a
+// pass covers kMergePass positions; its states go to LDS (each loaded once,
+// by one thread), and lane group g loads the value sums of positions g,
+// g + kMergeGroups, ... of its dims.  Every load of the first pass, the
+// sampled path's list length included, is issued before any is used (they
+// are issued for every position the list can have; those past its length
+// are masked), and the groups' sums add in group order.
+// The dense path knows its lists' length and loads exactly that (in one pass
+// up to 320 positions); the sampled path's first pass covers 160 positions,
+// the length of a list of a few dozen teams, so that few of its loads are
+// wasted on positions past the list.
 constexpr int kMergeDims = 32;
-constexpr int kMergeGroups = kMergeThreads / kMergeDims;  // 8
+constexpr int kMergeGroups = kMergeThreads / kMergeDims;
 
+template <bool DENSE>
 __global__ __launch_bounds__(kMergeThreads) void k_merge(const float* __restrict__ part_o,
                                                          const float* __restrict__ part_ml,
                                                          const PlanHeader* __restrict__ hdr,
-                                                         int nch_dense, int Hkv, int Hq,
-                                                         int max_chunks, int D,
-                                                         float* __restrict__ out) {
+                                                         int n_dense, int Hkv, int Hq, int max_hunits,
+                                                         int D, float* __restrict__ out) {
+    constexpr int kMergeBatch = DENSE ? 40 : 20;                 // positions per lane group and pass
+    constexpr int kMergePass = kMergeGroups * kMergeBatch;       // positions per pass
+    constexpr int kMergeStates = (kMergePass + kMergeThreads - 1) / kMergeThreads;  // per thread
     constexpr int NW = kMergeThreads / kWave;
-    constexpr int PER = 4;                     // chunk states per thread and block of units
-    constexpr int CB = PER * kMergeThreads;    // units per block
-    constexpr int kBatch = 32;                 // value loads in flight per thread and pass
-    __shared__ float s_red[NW];
-    __shared__ int s_cnt[NW];
-    __shared__ int s_idx[CB];
-    __shared__ float s_wt[CB];
+    __shared__ float2 s_st[kMergePass];
+    __shared__ float s_red[2][NW];
     __shared__ float s_sum[kMergeGroups][kMergeDims];
     const int bhq = blockIdx.x;
     const int b = bhq / Hq, hq = bhq - b * Hq;
@@ -584,109 +612,83 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(const float* __restrict
     const int bh = b * Hkv + kv;
     const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
     const int jd = tid % kMergeDims, grp = tid / kMergeDims;
-    const int dim = blockIdx.y * kMergeDims + jd;
-    const int nch = min(max(hdr ? hdr[bh].chunks : nch_dense, 0), max_chunks);
-    const float2* ml = reinterpret_cast<const float2*>(part_ml) + (static_cast<size_t>(bh) * G + h) * max_chunks;
-    const float* po = part_o + (static_cast<size_t>(bh) * G + h) * max_chunks * D + dim;
-    const float2 empty = make_float2(kNeg, 0.f);
+    const size_t row0 = (static_cast<size_t>(bh) * G + h) * max_hunits;
+    const float2* ml = reinterpret_cast<const float2*>(part_ml) + row0;
+    const float* po = part_o + row0 * D + blockIdx.y * kMergeDims + jd;
+    // the list length as a vector load (the index is 0 on every lane, but
+    // not provably uniform), so that it travels with the first pass's loads
+    // instead of holding them back
+    int n_list = n_dense;
+    if (!DENSE) n_list = hdr[bh].hunits[h + static_cast<int>(__builtin_amdgcn_mbcnt_lo(0u, 0u))];
+    // positions the loads may touch: the list on the dense path, the list's
+    // capacity on the sampled path
+    const int lim = DENSE ? min(n_dense, max_hunits) : max_hunits;
 
-    // thread t owns units t PER .. t PER + PER - 1 of each block
-    float2 st[PER];
+    float mx = kNeg, lsum = 0.f, acc = 0.f;
+    float2 st[kMergeStates];
+    float v[kMergeBatch];
+    auto load = [&](int p0) {
 #pragma unroll
-    for (int r = 0; r < PER; ++r) {
-        const int cc = tid * PER + r;
-        st[r] = cc < max_chunks ? ml[cc] : empty;
-    }
-    float mx = kNeg;
+        for (int k = 0; k < kMergeStates; ++k) st[k] = ml[min(p0 + tid + k * kMergeThreads, lim - 1)];
 #pragma unroll
-    for (int r = 0; r < PER; ++r)
-        if (tid * PER + r < nch) mx = fmaxf(mx, st[r].x);
-    for (int c0 = CB; c0 < nch; c0 += CB)
-        for (int r = 0; r < PER; ++r) {
-            const int cc = c0 + tid * PER + r;
-            if (cc < nch) mx = fmaxf(mx, ml[cc].x);
-        }
-    for (int off = kWave / 2; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
-    if (lane == 0) s_red[w] = mx;
-    __syncthreads();
-    mx = s_red[0];
+        for (int k = 0; k < kMergeBatch; ++k)
+            v[k] = __builtin_nontemporal_load(po + static_cast<size_t>(min(p0 + grp + k * kMergeGroups, lim - 1)) * D);
+    };
+    auto consume = [&](int p0, int n) {
+        float pm = kNeg;
 #pragma unroll
-    for (int v = 1; v < NW; ++v) mx = fmaxf(mx, s_red[v]);
-    __syncthreads();
-
-    float lsum = 0.f, acc = 0.f;
-    for (int c0 = 0; c0 < nch; c0 += CB) {
-        // this block's states: the registers for the first block, reloaded
-        // for later ones
-        float2 x[PER];
-        if (c0 == 0) {
-#pragma unroll
-            for (int r = 0; r < PER; ++r) x[r] = st[r];
-        } else {
-#pragma unroll
-            for (int r = 0; r < PER; ++r) {
-                const int cc = c0 + tid * PER + r;
-                x[r] = cc < nch ? ml[cc] : empty;
+        for (int k = 0; k < kMergeStates; ++k) {
+            const int i = tid + k * kMergeThreads;
+            if (i < kMergePass) {
+                const bool valid = p0 + i < n;
+                s_st[i] = valid ? st[k] : make_float2(kNeg, 0.f);
+                pm = fmaxf(pm, valid ? st[k].x : kNeg);
             }
         }
-        float wt[PER];
-        int nv = 0;
-#pragma unroll
-        for (int r = 0; r < PER; ++r) {
-            const bool valid = c0 + tid * PER + r < nch && x[r].x > kEmpty;
-            wt[r] = valid ? rebase(x[r].x, mx) : -1.f;
-            lsum += valid ? wt[r] * x[r].y : 0.f;
-            nv += valid ? 1 : 0;
-        }
-        // compaction in unit order: exclusive scan of the per-thread counts
-        const int inc = wave_incl_scan(nv);
-        if (lane == kWave - 1) s_cnt[w] = inc;
+        for (int off = kWave / 2; off > 0; off >>= 1) pm = fmaxf(pm, __shfl_xor(pm, off));
+        if (lane == 0) s_red[0][w] = pm;
         __syncthreads();
-        int off = 0, n = 0;
 #pragma unroll
-        for (int v = 0; v < NW; ++v) {
-            off += v < w ? s_cnt[v] : 0;
-            n += s_cnt[v];
+        for (int k = 0; k < NW; ++k) pm = fmaxf(pm, s_red[0][k]);
+        const float nmx = fmaxf(mx, pm);
+        const float sc = rebase(mx, nmx);
+        acc *= sc;
+        lsum *= sc;
+        // the masses: each thread its own states; the value sums: each lane
+        // group its positions (masked states have no weight)
+#pragma unroll
+        for (int k = 0; k < kMergeStates; ++k) {
+            const int i = tid + k * kMergeThreads;
+            if (i < kMergePass && p0 + i < n) lsum = fmaf(rebase(st[k].x, nmx), st[k].y, lsum);
         }
-        int pos = off + inc - nv;
 #pragma unroll
-        for (int r = 0; r < PER; ++r) {
-            const bool valid = wt[r] >= 0.f;
-            if (valid) {
-                s_idx[pos] = c0 + tid * PER + r;
-                s_wt[pos] = wt[r];
-            }
-            pos += valid ? 1 : 0;
+        for (int k = 0; k < kMergeBatch; ++k) {
+            const int i = grp + k * kMergeGroups;
+            if (p0 + i < n) acc = fmaf(rebase(s_st[i].x, nmx), v[k], acc);
         }
-        __syncthreads();
-        // group grp takes list entries grp, grp + kMergeGroups, ...
-        for (int k0 = grp; k0 < n; k0 += kBatch * kMergeGroups) {
-            int ix[kBatch];
-            float wv[kBatch], v[kBatch];
-#pragma unroll
-            for (int k = 0; k < kBatch; ++k) {
-                const int kk = min(k0 + k * kMergeGroups, n - 1);
-                ix[k] = s_idx[kk];
-                wv[k] = k0 + k * kMergeGroups < n ? s_wt[kk] : 0.f;
-            }
-#pragma unroll
-            for (int k = 0; k < kBatch; ++k) v[k] = __builtin_nontemporal_load(po + static_cast<size_t>(ix[k]) * D);
-#pragma unroll
-            for (int k = 0; k < kBatch; ++k) acc = fmaf(v[k], wv[k], acc);
-        }
-        __syncthreads();
+        mx = nmx;
+    };
+    // the first pass in straight-line code: its loads go out together with
+    // the length's; later passes (lists longer than kMergePass) follow
+    load(0);
+    const int n = min(n_list, max_hunits);
+    consume(0, n);
+    for (int p0 = kMergePass; p0 < n; p0 += kMergePass) {  // uniform
+        __syncthreads();  // s_st and s_red are rewritten
+        load(p0);
+        consume(p0, n);
     }
     s_sum[grp][jd] = acc;
     for (int off = kWave / 2; off > 0; off >>= 1) lsum += __shfl_xor(lsum, off);
-    if (lane == 0) s_red[w] = lsum;
+    if (lane == 0) s_red[1][w] = lsum;
     __syncthreads();
     if (tid < kMergeDims) {
-        float t = 0.f;
-        for (int v = 0; v < NW; ++v) t += s_red[v];
-        float o = 0.f;
+        float o = 0.f, L = 0.f;
 #pragma unroll
-        for (int g2 = 0; g2 < kMergeGroups; ++g2) o += s_sum[g2][jd];
-        out[static_cast<size_t>(bhq) * D + dim] = o / t;
+        for (int g2 = 0; g2 < kMergeGroups; ++g2) o += s_sum[g2][tid];
+#pragma unroll
+        for (int k = 0; k < NW; ++k) L += s_red[1][k];
+        out[static_cast<size_t>(bhq) * D + blockIdx.y * kMergeDims + tid] = o / L;
     }
 }
 
@@ -715,15 +717,14 @@ hipError_t attend_g(const AttendArgs& a, hipStream_t s) {
     const T* sV = static_cast<const T*>(a.sV);
     const int BH = a.B * a.Hkv;
     if (a.dense) {
-        k_attend<T, D, GT, true><<<grid, kWave, 0, s>>>(
-            K, V, sK, sV, a.q, a.N, a.T, BH, a.Hkv, a.Hq, a.G, 0, sl2, a.max_chunks, nullptr,
-            nullptr, nullptr, a.part_o, a.part_ml);
+        k_attend<T, D, GT, true><<<grid, kWave, 0, s>>>(K, V, sK, sV, a.q, a.N, a.T, BH, a.Hkv, a.Hq, a.G, 0, sl2,
+                                                        a.max_chunks, a.max_hunits, nullptr, nullptr, nullptr,
+                                                        a.part_o, a.part_ml);
     } else {
         const DecodeLayout& L = *a.lay;
         k_attend<T, D, GT, false><<<grid, kWave, 0, s>>>(
-            K, V, sK, sV, a.q, a.N, a.T, BH, a.Hkv, a.Hq, a.G, a.M, sl2, a.max_chunks,
-            reinterpret_cast<const unsigned*>(a.ws + L.counter),
-            reinterpret_cast<const Chunk*>(a.ws + L.chunk),
+            K, V, sK, sV, a.q, a.N, a.T, BH, a.Hkv, a.Hq, a.G, a.M, sl2, a.max_chunks, a.max_hunits,
+            reinterpret_cast<const unsigned*>(a.ws + L.counter), reinterpret_cast<const Chunk*>(a.ws + L.chunk),
             reinterpret_cast<const float*>(a.ws + L.ulogc), a.part_o, a.part_ml);
     }
     return hipGetLastError();
@@ -731,16 +732,21 @@ hipError_t attend_g(const AttendArgs& a, hipStream_t s) {
 
 template <typename T, int D>
 hipError_t attend_d(const AttendArgs& a, hipStream_t s) {
-    switch (a.G) {
-        case 1: return attend_g<T, D, 1>(a, s);
-        case 2: return attend_g<T, D, 2>(a, s);
-        case 3:
-        case 4: return attend_g<T, D, 4>(a, s);
-        case 5:
-        case 6:
-        case 7: return attend_g<T, D, 7>(a, s);
-        case 8: return attend_g<T, D, 8>(a, s);
-        default: return hipErrorInvalidValue;
+    if constexpr (sizeof(T) == 2) {
+        // the matrix-core value sum computes every head of the group at once
+        return a.G >= 1 && a.G <= kMaxGroup ? attend_g<T, D, kMaxGroup>(a, s) : hipErrorInvalidValue;
+    } else {
+        switch (a.G) {
+            case 1: return attend_g<T, D, 1>(a, s);
+            case 2: return attend_g<T, D, 2>(a, s);
+            case 3:
+            case 4: return attend_g<T, D, 4>(a, s);
+            case 5:
+            case 6:
+            case 7: return attend_g<T, D, 7>(a, s);
+            case 8: return attend_g<T, D, 8>(a, s);
+            default: return hipErrorInvalidValue;
+        }
     }
 }
 
@@ -760,11 +766,15 @@ hipError_t launch_attend(const AttendArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_merge(const AttendArgs& a, hipStream_t s) {
-    const PlanHeader* hdr = a.dense ? nullptr : reinterpret_cast<const PlanHeader*>(a.ws + a.lay->hdr);
-    const int nch_dense = dense_count(a.N) + dense_count(a.T);
     if (a.d % kMergeDims != 0) return hipErrorInvalidValue;
-    k_merge<<<dim3(a.B * a.Hq, a.d / kMergeDims), kMergeThreads, 0, s>>>(
-        a.part_o, a.part_ml, hdr, nch_dense, a.Hkv, a.Hq, a.max_chunks, a.d, a.out);
+    const dim3 grid(a.B * a.Hq, a.d / kMergeDims);
+    if (a.dense)
+        k_merge<true><<<grid, kMergeThreads, 0, s>>>(a.part_o, a.part_ml, nullptr, a.max_chunks, a.Hkv, a.Hq,
+                                                     a.max_hunits, a.d, a.out);
+    else
+        k_merge<false><<<grid, kMergeThreads, 0, s>>>(a.part_o, a.part_ml,
+                                                      reinterpret_cast<const PlanHeader*>(a.ws + a.lay->hdr), 0,
+                                                      a.Hkv, a.Hq, a.max_hunits, a.d, a.out);
     return hipGetLastError();
 }
 

@@ -17,19 +17,44 @@ constexpr int kLogcStride = 8;     // floats per union team in the read plan
 constexpr int kChunkRows = 32;     // rows per sampled attention unit (one wave)
 constexpr int kDenseRows = 128;    // rows per dense attention unit
 constexpr int kAttendWavesPerCU = 8; // resident attention waves per compute unit
+constexpr int kMergeThreads = 256;   // threads of a merge workgroup
 
 // Attention work unit: up to kChunkRows consecutive rows of one union team of
 // the packed cache, or of the suffix (slot < 0); the dense path cuts its rows
 // into units of kDenseRows.  The sampler appends the units of each (b, kv)
 // to one list shared by all pairs; `meta` packs the row count (bits 0-7),
 // the mask of query heads of the KV head that read the rows (bits 8-15) and
-// the (b, kv) pair (bits 16-31).
+// the (b, kv) pair (bits 16-31); pos[h] is the unit's position in the list
+// of units head h reads (for the heads of the mask), where its partial
+// state goes.
 struct Chunk {
     int begin;  // first packed row, or first suffix row when slot < 0
     int slot;   // union slot (index of the team's corrections), -1 = suffix
-    int ci;     // index of the unit within its (b, kv) pair
     int meta;
+    int ci;     // index of the unit within its (b, kv) pair
+    // head h's position in bits 16 (h % 2) .. of p01 (h < 2), p23, p45, p67
+    unsigned p01, p23, p45, p67;
 };
+static_assert(sizeof(Chunk) == 32, "unit descriptors are two 16-byte words");
+
+// Position of a unit in head h's list (h may differ across lanes: named
+// fields and selects, so the descriptor stays in registers).
+__host__ __device__ inline int chunk_pos(const Chunk& c, int h) {
+    const unsigned lo = (h & 2) ? c.p23 : c.p01;
+    const unsigned hi = (h & 2) ? c.p67 : c.p45;
+    const unsigned wd = (h & 4) ? hi : lo;
+    return static_cast<int>((wd >> (16 * (h & 1))) & 0xffffu);
+}
+// Positions of heads 0 .. 7 (a head outside the unit's mask gets 0).
+__host__ __device__ inline void set_chunk_pos(Chunk& c, const int (&p)[8]) {
+    auto pack = [](int a, int b) {
+        return static_cast<unsigned>(a & 0xffff) | (static_cast<unsigned>(b & 0xffff) << 16);
+    };
+    c.p01 = pack(p[0], p[1]);
+    c.p23 = pack(p[2], p[3]);
+    c.p45 = pack(p[4], p[5]);
+    c.p67 = pack(p[6], p[7]);
+}
 
 __host__ __device__ inline int chunk_meta(int rows, int hmask, int bh) {
     return rows | (hmask << 8) | (bh << 16);
@@ -37,23 +62,27 @@ __host__ __device__ inline int chunk_meta(int rows, int hmask, int bh) {
 __host__ __device__ inline int meta_rows(int m) { return m & 255; }
 __host__ __device__ inline int meta_hmask(int m) { return (m >> 8) & 255; }
 __host__ __device__ inline int meta_bh(int m) { return static_cast<int>(static_cast<unsigned>(m) >> 16); }
-constexpr int kMaxPairs = 65536;  // (b, kv) pairs a unit can name
+constexpr int kMaxPairs = 65536;       // (b, kv) pairs a unit can name
+constexpr int kMaxHeadUnits = 65535;   // units one head can read (16-bit positions)
 
 // Plan header per (b, kv), written by the sampler.
 struct PlanHeader {
     int teams;   // union teams U
     int rows;    // union rows (excluding the suffix)
-    int chunks;  // chunks of the union and the suffix
+    int chunks;  // units of the union and the suffix
     int pad;
+    int hunits[kMaxGroup];  // units each query head reads (its teams and the suffix)
 };
 
 // Workspace layout of santapp_decode; byte offsets into the caller's buffer.
-// max_chunks bounds the chunks of any (b, kv): the largest chunk count any
-// union of up to min(M, G K) teams can have, plus the suffix chunks.
+// max_chunks bounds the units of any (b, kv): the largest unit count any
+// union of up to min(M, G K) teams can have, plus the suffix units;
+// max_hunits bounds the units one head reads (K teams and the suffix), the
+// length of each head's partial-state list.
 struct DecodeLayout {
-    int max_chunks = 0;
-    size_t counter = 0, phi = 0, Y = 0, lc = 0, hdr = 0, chunk = 0, ulogc = 0, po = 0, pml = 0,
-           total = 0;
+    int max_chunks = 0, max_hunits = 0;
+    size_t counter = 0, phi = 0, Y = 0, lc = 0, hdr = 0, chunk = 0, ulogc = 0, po = 0,
+           pml = 0, total = 0;
 };
 
 // cap: host table with cap[x] = most chunks any x distinct teams of one
@@ -97,15 +126,15 @@ struct AttendArgs {
     const void* sK;   // [BH, T, d]
     const void* sV;
     const float* q;   // [B, Hq, d]
-    int B, Hkv, Hq, G, d, N, T, M, max_chunks;
-    int grid_waves;             // one-wave workgroups on the sampled path (0: one per unit)
+    int B, Hkv, Hq, G, d, N, T, M, max_chunks, max_hunits;
+    int grid_waves;             // resident attention waves of the device (0: one per unit)
     santapp_dtype dtype;
     float scale;
     bool dense;                 // every row, every head, correction 1
     const char* ws;             // plan (sampled path)
     const DecodeLayout* lay;    // plan offsets (sampled path)
-    float* part_o;              // [BH, G, max_chunks, d]
-    float* part_ml;             // [BH, G, max_chunks, 2]
+    float* part_o;              // [BH, G, max_hunits, d]
+    float* part_ml;             // [BH, G, max_hunits, 2]
     float* out;                 // [B, Hq, d]
 };
 

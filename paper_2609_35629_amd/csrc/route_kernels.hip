@@ -98,25 +98,30 @@ __device__ __forceinline__ float log_inclusion(float x) {
     return __builtin_amdgcn_logf(c) * kLn2;
 }
 
-// Exclusive scan of three counters over the workgroup; returns the totals.
-__device__ __forceinline__ void block_scan3(const int (&x)[3], int (&ex)[3], int (&tot)[3],
-                                           int* s_w /* [3 * kSelectWaves] */) {
+// Exclusive scan of NV counters over the workgroup; returns the totals.
+// s_w holds NV x kSelectWaves wave totals.
+template <int NV>
+__device__ __forceinline__ void block_scan(const int (&x)[NV], int (&ex)[NV], int (&tot)[NV],
+                                           int* s_w /* [NV * kSelectWaves] */) {
+    static_assert(kSelectWaves == 8, "wave totals are read as two int4 per counter");
     const int lane = lane_id(), w = wave_id();
-    int inc[3];
+    int inc[NV];
 #pragma unroll
-    for (int k = 0; k < 3; ++k) {
+    for (int k = 0; k < NV; ++k) {
         inc[k] = wave_incl_scan(x[k]);
         if (lane == kWave - 1) s_w[k * kSelectWaves + w] = inc[k];
     }
     __syncthreads();
 #pragma unroll
-    for (int k = 0; k < 3; ++k) {
+    for (int k = 0; k < NV; ++k) {
+        const int4 a = reinterpret_cast<const int4*>(s_w)[2 * k];
+        const int4 c = reinterpret_cast<const int4*>(s_w)[2 * k + 1];
+        const int y[8] = {a.x, a.y, a.z, a.w, c.x, c.y, c.z, c.w};
         int pre = 0, t = 0;
 #pragma unroll
         for (int v = 0; v < kSelectWaves; ++v) {
-            const int y = s_w[k * kSelectWaves + v];
-            pre += (v < w) ? y : 0;
-            t += y;
+            pre += (v < w) ? y[v] : 0;
+            t += y[v];
         }
         ex[k] = pre + inc[k] - x[k];
         tot[k] = t;
@@ -419,8 +424,10 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
     __shared__ __align__(16) uint32_t s_hist[kSelectWaves][256];
     __shared__ __align__(16) uint64_t s_cand[kSelectWaves][kWave];
     __shared__ uint64_t s_bits[kMaxGroup][kMaxTeams / kWave];  // selection bits per head
-    __shared__ int s_w[3 * kSelectWaves];
-    __shared__ int4 s_team[kSelectThreads];  // union teams of one pass: first chunk, begin, size, heads
+    __shared__ __align__(16) int s_w[(3 + kMaxGroup) * kSelectWaves];
+    __shared__ int s_base;
+    __shared__ int4 s_team[kSelectThreads];  // union teams of one pass: first unit, begin, size, heads
+    __shared__ unsigned short s_tpos[kSelectThreads][kMaxGroup];  // first position in each head's list
 
     const int bh = blockIdx.x;
     const int b = bh / Hkv, kv = bh - b * Hkv;
@@ -547,76 +554,35 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
         L[1] = make_float4(v[4], v[5], v[6], v[7]);
     };
     const int nsc = chunk_count(T_suf);
-    if (M <= kSelectThreads) {
-        // one pass, thread g owns team g: one scan gives every union team
-        // its slot and first unit and the pair's totals, and the range claim
-        // is issued as soon as the total is known
-        const int hm = heads_of(tid);
-        const int f = hm ? 1 : 0;
-        const int x[3] = {f, f ? chunk_count(size0) : 0, f ? size0 : 0};
-        int ex[3], tot[3];
-        block_scan3(x, ex, tot, s_w);
-        const int utotal = min(tot[1] + nsc, max_chunks);
+    // One pass per kSelectThreads teams, thread tid owning team base + tid:
+    // a scan gives every union team its slot, its first unit, and its first
+    // position in the list of each head that selected it; a unit's team is
+    // the last union team whose first unit is at or before it.  The pair's
+    // range in the shared unit list is claimed once its total is known (in
+    // the first pass when one pass covers every team, else after a counting
+    // pre-pass).
+    constexpr int NV = 3 + G;
+    const bool one_pass = M <= kSelectThreads;
+    int utotal = 0;
+    if (!one_pass) {
+        int nu = 0;
+        for (int base = 0; base < M; base += kSelectThreads) {
+            const int g = base + tid;
+            const int tsz = base == 0 ? size0 : team_size[tb0 + min(g, M - 1)];
+            nu += heads_of(g) ? chunk_count(tsz) : 0;
+        }
+        const int x[1] = {nu};
+        int ex[1], tot[1];
+        block_scan<1>(x, ex, tot, s_w);
+        utotal = min(tot[0] + nsc, max_chunks);
         if (tid == 0)
-            s_w[0] = static_cast<int>(__hip_atomic_fetch_add(counter, static_cast<unsigned>(utotal), __ATOMIC_RELAXED,
-                                                             __HIP_MEMORY_SCOPE_AGENT));
-        if (f) {
-            write_logc(tid, ex[0], hm);
-            s_team[ex[0]] = make_int4(ex[1], begin0, size0, hm);
-        }
-        __syncthreads();
-        Chunk* cb = chunks + s_w[0];
-        // units of the union teams and of the suffix, cooperatively: unit c
-        // belongs to the last union team whose first unit is at or before it
-        for (int c = tid; c < utotal; c += kSelectThreads) {
-            if (c < tot[1]) {
-                int lo = 0, hi = tot[0] - 1;
-                while (lo < hi) {
-                    const int mid = (lo + hi + 1) >> 1;
-                    if (s_team[mid].x <= c)
-                        lo = mid;
-                    else
-                        hi = mid - 1;
-                }
-                const int4 tm = s_team[lo];
-                const int p = c - tm.x;
-                cb[c] = Chunk{tm.y + p * kChunkRows, lo, c, chunk_meta(min(kChunkRows, tm.z - p * kChunkRows), tm.w, bh)};
-            } else {
-                const int p = c - tot[1];
-                cb[c] = Chunk{p * kChunkRows, -1, c, chunk_meta(min(kChunkRows, T_suf - p * kChunkRows), (1 << G) - 1, bh)};
-            }
-        }
-        if (tid == 0) {
-            hdr[bh] = PlanHeader{tot[0], tot[2], utotal, 0};
-            if (dbg_uteams) dbg_uteams[bh] = tot[0];
-            if (dbg_urows) dbg_urows[bh] = tot[2];
-        }
-        return;
+            s_base = static_cast<int>(
+                __hip_atomic_fetch_add(counter, static_cast<unsigned>(utotal), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
     }
-
-    // several passes of kSelectThreads teams: the pair's unit count first
-    int nu = 0;
-    for (int base = 0; base < M; base += kSelectThreads) {
-        const int g = base + tid;
-        const int tsz = base == 0 ? size0 : team_size[tb0 + min(g, M - 1)];
-        nu += heads_of(g) ? chunk_count(tsz) : 0;
-    }
-    {
-        const int x[3] = {nu, 0, 0};
-        int ex[3], tot[3];
-        block_scan3(x, ex, tot, s_w);
-        if (tid == 0) {
-            const int total = min(tot[0] + nsc, max_chunks);
-            s_w[0] = static_cast<int>(
-                __hip_atomic_fetch_add(counter, static_cast<unsigned>(total), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-            s_w[1] = total;
-        }
-        __syncthreads();
-    }
-    const int ubase = s_w[0], utotal = s_w[1];
-    __syncthreads();
-    Chunk* cb = chunks + ubase;
     int run_u = 0, run_rows = 0, run_c = 0;
+    int run_h[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) run_h[h] = 0;
     for (int base = 0; base < M; base += kSelectThreads) {
         const int g = base + tid;
         int tsz = size0, tbeg = begin0;
@@ -627,16 +593,30 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
         }
         const int hm = heads_of(g);
         const int f = hm ? 1 : 0;
-        const int x[3] = {f, f ? chunk_count(tsz) : 0, f ? tsz : 0};
-        int ex[3], tot[3];
-        block_scan3(x, ex, tot, s_w);
+        const int nc = f ? chunk_count(tsz) : 0;
+        int x[NV];
+        x[0] = f;
+        x[1] = nc;
+        x[2] = f ? tsz : 0;
+#pragma unroll
+        for (int h = 0; h < G; ++h) x[3 + h] = ((hm >> h) & 1) ? nc : 0;
+        int ex[NV], tot[NV];
+        block_scan<NV>(x, ex, tot, s_w);
+        if (one_pass) {
+            utotal = min(tot[1] + nsc, max_chunks);
+            if (tid == 0)
+                s_base = static_cast<int>(__hip_atomic_fetch_add(counter, static_cast<unsigned>(utotal), __ATOMIC_RELAXED,
+                                                                 __HIP_MEMORY_SCOPE_AGENT));
+        }
         if (f) {
             write_logc(g, run_u + ex[0], hm);
             s_team[ex[0]] = make_int4(ex[1], tbeg, tsz, hm);
+#pragma unroll
+            for (int h = 0; h < kMaxGroup; ++h)
+                s_tpos[ex[0]][h] = static_cast<unsigned short>(h < G ? run_h[h] + ex[3 + h] : 0);
         }
         __syncthreads();
-        // the pass's units, one per thread: its team is the last with a
-        // first unit at or before it
+        Chunk* cb = chunks + s_base;
         for (int c = tid; c < tot[1]; c += kSelectThreads) {
             int lo = 0, hi = tot[0] - 1;
             while (lo < hi) {
@@ -649,28 +629,56 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
             const int4 tm = s_team[lo];
             const int p = c - tm.x;
             const int ci = run_c + c;
-            if (ci < utotal)
-                cb[ci] = Chunk{tm.y + p * kChunkRows, run_u + lo, ci,
-                               chunk_meta(min(kChunkRows, tm.z - p * kChunkRows), tm.w, bh)};
+            if (ci < utotal) {
+                Chunk ch;
+                ch.begin = tm.y + p * kChunkRows;
+                ch.slot = run_u + lo;
+                ch.meta = chunk_meta(min(kChunkRows, tm.z - p * kChunkRows), tm.w, bh);
+                ch.ci = ci;
+                int ps[kMaxGroup];
+#pragma unroll
+                for (int h = 0; h < kMaxGroup; ++h) ps[h] = ((tm.w >> h) & 1) ? s_tpos[lo][h] + p : 0;
+                set_chunk_pos(ch, ps);
+                cb[ci] = ch;
+            }
         }
-        __syncthreads();  // s_team is rewritten by the next pass
         run_u += tot[0];
         run_c += tot[1];
         run_rows += tot[2];
+#pragma unroll
+        for (int h = 0; h < G; ++h) run_h[h] += tot[3 + h];
+        if (base + kSelectThreads < M) __syncthreads();  // s_team is rewritten by the next pass
     }
-    // the suffix: every head, no correction
+    // the suffix: every head, no correction, after each head's teams
+    Chunk* cb = chunks + s_base;
     for (int p = tid; p < nsc; p += kSelectThreads) {
         const int ci = run_c + p;
-        if (ci < utotal)
-            cb[ci] = Chunk{p * kChunkRows, -1, ci, chunk_meta(min(kChunkRows, T_suf - p * kChunkRows), (1 << G) - 1, bh)};
+        if (ci < utotal) {
+            Chunk ch;
+            ch.begin = p * kChunkRows;
+            ch.slot = -1;
+            ch.meta = chunk_meta(min(kChunkRows, T_suf - p * kChunkRows), (1 << G) - 1, bh);
+            ch.ci = ci;
+            int ps[kMaxGroup];
+#pragma unroll
+            for (int h = 0; h < kMaxGroup; ++h) ps[h] = h < G ? run_h[h] + p : 0;
+            set_chunk_pos(ch, ps);
+            cb[ci] = ch;
+        }
     }
     if (tid == 0) {
-        hdr[bh] = PlanHeader{run_u, run_rows, utotal, 0};
+        PlanHeader ph;
+        ph.teams = run_u;
+        ph.rows = run_rows;
+        ph.chunks = utotal;
+        ph.pad = 0;
+#pragma unroll
+        for (int h = 0; h < kMaxGroup; ++h) ph.hunits[h] = h < G ? run_h[h] + nsc : 0;
+        hdr[bh] = ph;
         if (dbg_uteams) dbg_uteams[bh] = run_u;
         if (dbg_urows) dbg_urows[bh] = run_rows;
     }
 }
-
 
 template <typename T, int D, int G>
 hipError_t route_g(const RouteArgs& a, hipStream_t s) {

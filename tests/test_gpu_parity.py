@@ -191,6 +191,29 @@ def test_bitwise_deterministic():
     assert not torch.equal(a, d)  # a fresh step draws fresh noise
 
 
+@pytest.mark.parametrize("name", ["qwen8k", "tiny"])
+def test_workspace_reuse_across_shapes_of_steps(name):
+    # one workspace for several steps, each list of partial states shorter or
+    # longer than the one before: a step reads only what it wrote itself
+    wl = datagen.WORKLOADS[name]
+    log(f"[gpu] workspace reuse workload={wl.name}")
+    b = datagen.generate(wl)
+    db = dev_batch(b)
+    teams = sp.build_teams(db.K, db.V, wl.P, wl.R)
+    ws = sp.decode_workspace(teams, wl.Hq, wl.T, wl.K)
+    fresh = sp.decode(teams, db.q, db.sK, db.sV, wl.K, seed=5, step=2, scale=wl.scale).clone()
+    for step in (0, 1, 2):
+        got = sp.decode(teams, db.q, db.sK, db.sV, wl.K, seed=5, step=step, scale=wl.scale,
+                        workspace=ws).clone()
+    torch.cuda.synchronize()
+    assert torch.equal(got, fresh)
+    pairs = [(bi, h) for bi in range(wl.B) for h in range(wl.Hq)]
+    ot = oracle_teams(b, sorted(set((bi, h // wl.G) for (bi, h) in pairs)))
+    so = oracle.decode(b.q, b.f32(b.K), b.f32(b.V), b.f32(b.sK), b.f32(b.sV), ot, wl.K, 5, 2,
+                       wl.scale, heads=pairs)
+    assert oracle.rel_l2(got.cpu().numpy(), so.out) <= REL_BAR
+
+
 def test_device_side_argument_errors():
     wl = datagen.WORKLOADS["tiny"]
     b = datagen.generate(wl)
