@@ -102,7 +102,7 @@ struct QK<bf16_t, D> {
             }
         }
     }
-    __device__ __forceinline__ void load_k(const bf16_t* row, int c, frag* f) const {
+    static __device__ __forceinline__ void load_k(const bf16_t* row, int c, frag* f) {
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb) f[kb] = load_stream(row + 8 * (4 * kb + c));
     }
@@ -220,9 +220,9 @@ template <int D>
 struct VTile {
     static constexpr int NB = D / 16;  // 16-dim blocks = products per step
     static constexpr int kBytes = 32 * D * 2;
+    static __device__ __forceinline__ int swz(int row) { return ((row & 3) | ((row >> 1) & 4)) & (NB - 1); }
     static __device__ __forceinline__ int offset(int row, int byte) {
-        const int h = ((row & 3) | ((row >> 1) & 4)) & (NB - 1);
-        return row * (2 * D) + ((((byte >> 5) ^ h)) << 5) + (byte & 31);
+        return row * (2 * D) + ((((byte >> 5) ^ swz(row))) << 5) + (byte & 31);
     }
     // B operand of block nb for lane l
     static __device__ __forceinline__ bf16x8 operand(const char* tile, int nb, int lane) {
@@ -575,6 +575,292 @@ __global__ __launch_bounds__(kWave, 2) void k_attend(
     }
 }
 
+// bf16 keys and values: the units, arithmetic and results of k_attend, with
+// the loads software-pipelined across the 32-row steps of a wave's units
+// (unit after unit).  Each step waits for its own data, issues the next
+// step's, and computes while those fly: K as MFMA fragments into the other
+// of two register sets, V by the LDS DMA (global_load_lds, 16 bytes per
+// lane, lane l to byte 16 l of a 1 KB block, each lane fetching the
+// 16-byte segment that the tile's swizzle puts at its position) into the
+// other of two tiles.  Loads complete in issue order and a step's V copies
+// go out before its K loads, so waiting for its K fragments covers its
+// value tile too.  Rows past a unit's end repeat its last row: finite, and
+// weighted 0.
+// Order of this wave's LDS accesses for the compiler only: the LDS executes
+// one wave's instructions in order, so no wait is needed (a fence would also
+// wait for the value copies in flight).
+__device__ __forceinline__ void lds_order() { asm volatile("" ::: "memory"); }
+
+template <int D, bool DENSE>
+__global__ __launch_bounds__(kWave, 2) void k_attend_mfma(
+    const bf16_t* __restrict__ K, const bf16_t* __restrict__ V, const bf16_t* __restrict__ sK,
+    const bf16_t* __restrict__ sV, const float* __restrict__ q, int N, int T_suf, int BH, int Hkv,
+    int Hq, int G, int M, float scale_log2, int max_chunks, int max_hunits,
+    const unsigned* __restrict__ counter, const Chunk* __restrict__ chunks,
+    const float* __restrict__ ulogc, float* __restrict__ part_o, float* __restrict__ part_ml) {
+    constexpr int UR = DENSE ? kDenseRows : kChunkRows;
+    using QKT = QK<bf16_t, D>;
+    using VT = VTile<D>;
+    constexpr int NF = QKT::KB;         // K fragments per 16-row tile
+    constexpr int NB = VT::NB;
+    constexpr int SPR = D / 8;          // 16-byte segments per row
+    constexpr int RPI = kWave / SPR;    // rows per DMA instruction (1 KB)
+    constexpr int NDMA = 32 / RPI;      // DMA instructions per step
+    static_assert(RPI * SPR == kWave && NDMA * RPI == 32, "a step's tile is whole 1 KB DMA blocks");
+    constexpr int kNT = 2;              // cache policy of the value copies: streaming
+    // value tiles, double-buffered (two objects, so that the compiler can
+    // tell the copies into one from the reads of the other)
+    __shared__ __attribute__((aligned(16))) char s_v0[VT::kBytes];
+    __shared__ __attribute__((aligned(16))) char s_v1[VT::kBytes];
+    __shared__ float4 s_pt[8][8];  // probabilities [head][row / 4]
+
+    const int lane = lane_id();
+    const int c = lane >> 4, j16 = lane & 15;
+    const int hsel = 4 * (c & 1);  // first head of this lane's registers
+    const int ncp = (N + UR - 1) / UR;
+    const int nchd = ncp + (T_suf + UR - 1) / UR;
+    const int total = DENSE ? BH * nchd
+                            : static_cast<int>(min(__hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT),
+                                                   static_cast<unsigned>(BH) * static_cast<unsigned>(max_chunks)));
+    const int stride = static_cast<int>(gridDim.x);
+    auto descriptor = [&](int u) {
+        if (DENSE) {
+            const int bhx = u / nchd, cix = u - bhx * nchd;
+            const bool suf = cix >= ncp;
+            const int begin = (suf ? cix - ncp : cix) * UR;
+            Chunk d;
+            d.begin = begin;
+            d.slot = suf ? -1 : 0;
+            d.meta = chunk_meta(min(UR, (suf ? T_suf : N) - begin), (1 << G) - 1, bhx);
+            d.ci = cix;
+            d.p01 = d.p23 = d.p45 = d.p67 = 0u;
+            return d;
+        }
+        return chunks[min(u, BH * max_chunks - 1)];
+    };
+    // a unit's rows, clamped to its buffer whatever the workspace holds
+    struct Unit {
+        const bf16_t* Kb;
+        const bf16_t* Vb;
+        int bh, rows, slot, hmask, ci;
+        bool suffix, live;
+        unsigned p01, p23, p45, p67;
+    };
+    auto unit_of = [&](const Chunk& ck) {
+        Unit U;
+        U.bh = min(max(meta_bh(ck.meta), 0), BH - 1);
+        U.ci = ck.ci;
+        int begin = ck.begin, rows = meta_rows(ck.meta);
+        U.slot = min(ck.slot, M - 1);
+        U.hmask = meta_hmask(ck.meta) & ((1 << G) - 1);
+        U.suffix = ck.slot < 0;
+        const int lim = U.suffix ? T_suf : N;
+        U.live = lim >= 1;
+        rows = min(max(rows, 1), min(UR, max(lim, 1)));
+        begin = min(max(begin, 0), max(lim - rows, 0));
+        U.rows = rows;
+        U.Kb = U.suffix ? sK + (static_cast<size_t>(U.bh) * T_suf + begin) * D : K + (static_cast<size_t>(U.bh) * N + begin) * D;
+        U.Vb = U.suffix ? sV + (static_cast<size_t>(U.bh) * T_suf + begin) * D : V + (static_cast<size_t>(U.bh) * N + begin) * D;
+        U.p01 = __builtin_amdgcn_readfirstlane(ck.p01);
+        U.p23 = __builtin_amdgcn_readfirstlane(ck.p23);
+        U.p45 = __builtin_amdgcn_readfirstlane(ck.p45);
+        U.p67 = __builtin_amdgcn_readfirstlane(ck.p67);
+        return U;
+    };
+    auto corrections = [&](const Unit& U, float4& lo, float4& hi) {
+        lo = make_float4(0.f, 0.f, 0.f, 0.f);
+        hi = lo;
+        if (!DENSE && !U.suffix) {
+            const float4* L = reinterpret_cast<const float4*>(ulogc + (static_cast<size_t>(U.bh) * M + U.slot) * kLogcStride);
+            lo = L[0];
+            hi = L[1];
+        }
+    };
+    // V copies, then K loads, of rows r0 .. r0 + 31 of unit U.  Every step
+    // issues the same loads whether or not a next step exists (then every
+    // lane fetches the unit's first 16 bytes: one cache line per
+    // instruction), so that the compiler's count of loads in flight, and
+    // with it the wait before each step, is the same on every path.
+    auto issue = [&](const Unit& U, int r0, char* tile, typename QKT::frag (&kf)[2][NF], bool real) {
+        const int ls = real ? lane : 0;
+#pragma unroll
+        for (int j = 0; j < NDMA; ++j) {
+            const int row = real ? RPI * j + lane / SPR : 0;
+            const int seg = real ? (ls % SPR) ^ (2 * VT::swz(row)) : 0;
+            const bf16_t* src = U.Vb + static_cast<size_t>(min(r0 + row, U.rows - 1)) * D + 8 * seg;
+            __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)(tile + 1024 * j), 16, 0, kNT);
+        }
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            const bf16_t* row = U.Kb + (real ? static_cast<size_t>(min(r0 + 16 * k + j16, U.rows - 1)) * D : 0);
+            QKT::load_k(row, real ? c : 0, kf[k]);
+        }
+    };
+
+    int u = static_cast<int>(blockIdx.x);
+    if (u >= total) return;  // uniform
+    Unit cur = unit_of(descriptor(u));
+    Chunk nxck = DENSE ? Chunk{} : descriptor(min(u + stride, total - 1));
+    float4 lc_lo, lc_hi;
+    corrections(cur, lc_lo, lc_hi);
+    QKT qk;
+    int qbh = cur.bh;
+    {
+        const int h = j16 & 7;
+        const int b = cur.bh / Hkv, kv = cur.bh - b * Hkv;
+        qk.load_q(q + (static_cast<size_t>(b) * Hq + kv * G + (h < G ? h : 0)) * D, h < G ? scale_log2 : 0.f, c);
+    }
+    typename QKT::frag kf0[2][NF], kf1[2][NF];
+    issue(cur, 0, s_v0, kf0, true);
+
+    float m[4], l[4];
+    f32x4 oacc[NB];
+    auto reset = [&]() {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            m[r] = kNeg;
+            l[r] = 0.f;
+        }
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) oacc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    };
+    reset();
+    int r0 = 0;
+    bool done = false;
+
+    // one step from tile `tile` and fragments kf (rows r0 .. of unit cur),
+    // with the next step issued into the other buffer first
+    auto step = [&](char* tile, typename QKT::frag (&kf)[2][NF], char* ntile, typename QKT::frag (&nkf)[2][NF]) {
+        // the next step: the same unit's next 32 rows, or the next unit's first
+        const bool more = r0 + 32 < cur.rows;
+        const int un = u + stride;
+        const bool has_next = more || (!DENSE && un < total);
+        Unit nxt = cur;
+        int nr0 = r0 + 32;
+        if (!more && has_next) {
+            nxt = unit_of(nxck);
+            nr0 = 0;
+        }
+        // this step's data first: its K fragments, and with them (issued
+        // before them) its value copies; nothing later is in flight yet, so
+        // the wait is exact.  Then the next step goes out and flies while
+        // this one computes.  No load or read of a tile moves above here.
+        asm volatile("" ::"v"(kf[1][NF - 1].w) : "memory");
+        issue(nxt, has_next ? nr0 : 0, ntile, nkf, has_next);
+
+        // scores and softmax over the step's 32 rows
+        const f32x4 s0 = qk.scores(kf[0]);
+        const f32x4 s1 = qk.scores(kf[1]);
+        const bool live0 = r0 + j16 < cur.rows, live1 = r0 + 16 + j16 < cur.rows;
+        float a[4], p0[4], p1[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const float x0 = live0 ? s0[r] : kNeg;
+            const float x1 = live1 ? s1[r] : kNeg;
+            const float mn = fmaxf(m[r], row16_max(fmaxf(x0, x1)));
+            a[r] = rebase(m[r], mn);
+            p0[r] = fast_exp2(x0 - mn);
+            p1[r] = fast_exp2(x1 - mn);
+            l[r] = l[r] * a[r] + row16_sum(p0[r] + p1[r]);
+            m[r] = mn;
+        }
+        lds_order();  // the previous step's reads of s_pt come first
+        if (c < 2) {
+            float* pt = reinterpret_cast<float*>(s_pt);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                pt[(hsel + r) * 32 + j16] = p0[r];
+                pt[(hsel + r) * 32 + 16 + j16] = p1[r];
+            }
+        }
+        lds_order();
+        bf16x8 pa;
+        {
+            const float4 x0 = s_pt[j16 & 7][2 * c], x1 = s_pt[j16 & 7][2 * c + 1];
+            const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+            const bool low = j16 >= 8;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const __bf16 hi = static_cast<__bf16>(x[e]);
+                pa[e] = low ? static_cast<__bf16>(x[e] - static_cast<float>(hi)) : hi;
+            }
+        }
+        if (r0 > 0) {  // uniform; a unit's first step starts from zero
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) oacc[nb][r] *= a[r];
+        }
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+            oacc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, VT::operand(tile, nb, lane), oacc[nb], 0, 0, 0);
+
+        if (!more) {
+            // the unit's state for each head that reads it, at the unit's
+            // position in that head's list
+            float* const po_bh = part_o + static_cast<size_t>(cur.bh) * G * max_hunits * D;
+            float* const pml_bh = part_ml + static_cast<size_t>(cur.bh) * G * max_hunits * 2;
+            auto list_row = [&](int h, int pos) { return h * max_hunits + min(DENSE ? cur.ci : pos, max_hunits - 1); };
+            const unsigned wa = hsel ? cur.p45 : cur.p01, wb = hsel ? cur.p67 : cur.p23;
+            const int hp[4] = {static_cast<int>(wa & 0xffffu), static_cast<int>(wa >> 16),
+                               static_cast<int>(wb & 0xffffu), static_cast<int>(wb >> 16)};
+            // high + low halves: lane groups c and c ^ 2 hold the same heads
+            const bool lower = c < 2;
+            const int dim0 = (lower ? 0 : D / 2) + j16;
+#pragma unroll
+            for (int nb = 0; nb < NB / 2; ++nb) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const float keep = lower ? oacc[nb][r] : oacc[nb + NB / 2][r];
+                    const float send = lower ? oacc[nb + NB / 2][r] : oacc[nb][r];
+                    const float x = keep + __shfl_xor(send, 32);
+                    const int h = hsel + r;
+                    if (cur.live && h < G && ((cur.hmask >> h) & 1))
+                        __builtin_nontemporal_store(x, po_bh + list_row(h, hp[r]) * D + dim0 + 16 * nb);
+                }
+            }
+            if (c < 2 && j16 == 0) {
+                // the correction enters as a shift of the unit's maximum
+                // (every row of the unit belongs to the same team); written
+                // out per register so that every index is a constant
+                auto put = [&](int r, float lc0, float lc1, float mr, float lr, int pos) {
+                    const int h = 4 * c + r;
+                    if (cur.live && h < G && ((cur.hmask >> h) & 1))
+                        store_stream2(pml_bh + list_row(h, pos) * 2, make_float2(mr - (c ? lc1 : lc0) * kLog2e, lr));
+                };
+                put(0, lc_lo.x, lc_hi.x, m[0], l[0], hp[0]);
+                put(1, lc_lo.y, lc_hi.y, m[1], l[1], hp[1]);
+                put(2, lc_lo.z, lc_hi.z, m[2], l[2], hp[2]);
+                put(3, lc_lo.w, lc_hi.w, m[3], l[3], hp[3]);
+            }
+        }
+        if (!has_next) {
+            done = true;
+            return;
+        }
+        if (!more) {  // the next unit becomes current
+            cur = nxt;
+            u = un;
+            if (!DENSE) nxck = descriptor(min(u + stride, total - 1));
+            corrections(cur, lc_lo, lc_hi);
+            if (cur.bh != qbh) {
+                const int h = j16 & 7;
+                const int b = cur.bh / Hkv, kv = cur.bh - b * Hkv;
+                qk.load_q(q + (static_cast<size_t>(b) * Hq + kv * G + (h < G ? h : 0)) * D, h < G ? scale_log2 : 0.f, c);
+                qbh = cur.bh;
+            }
+            reset();
+        }
+        r0 = nr0;
+    };
+    for (;;) {
+        step(s_v0, kf0, s_v1, kf1);
+        if (done) break;
+        step(s_v1, kf1, s_v0, kf0);
+        if (done) break;
+    }
+}
+
 // Merge of one query head's list of n unit states (m_p: log2-domain maximum
 // with the team's correction folded in, l_p: mass) and value sums o_p:
 // out = sum_p 2^(m_p - mx) o_p / sum_p 2^(m_p - mx) l_p with mx = max_p m_p.
@@ -700,6 +986,33 @@ __global__ void k_zero(uint4* __restrict__ p, size_t n16, unsigned char* __restr
     if (blockIdx.x == 0 && static_cast<int>(threadIdx.x) < ntail) tail[threadIdx.x] = 0;
 }
 
+template <int D>
+hipError_t attend_mfma(const AttendArgs& a, hipStream_t s) {
+    const long long units = static_cast<long long>(a.B) * a.Hkv * a.max_chunks;
+    long long waves = units;
+    if (!a.dense && a.grid_waves > 0) waves = std::min<long long>(units, a.grid_waves);
+    if (waves < 1 || waves > 0x7fffffffLL) return hipErrorInvalidValue;
+    const dim3 grid(static_cast<unsigned>(waves));
+    const float sl2 = a.scale * kLog2e;
+    const bf16_t* K = static_cast<const bf16_t*>(a.K);
+    const bf16_t* V = static_cast<const bf16_t*>(a.V);
+    const bf16_t* sK = static_cast<const bf16_t*>(a.sK);
+    const bf16_t* sV = static_cast<const bf16_t*>(a.sV);
+    const int BH = a.B * a.Hkv;
+    if (a.dense) {
+        k_attend_mfma<D, true><<<grid, kWave, 0, s>>>(K, V, sK, sV, a.q, a.N, a.T, BH, a.Hkv, a.Hq, a.G, 0, sl2,
+                                                      a.max_chunks, a.max_hunits, nullptr, nullptr, nullptr,
+                                                      a.part_o, a.part_ml);
+    } else {
+        const DecodeLayout& L = *a.lay;
+        k_attend_mfma<D, false><<<grid, kWave, 0, s>>>(
+            K, V, sK, sV, a.q, a.N, a.T, BH, a.Hkv, a.Hq, a.G, a.M, sl2, a.max_chunks, a.max_hunits,
+            reinterpret_cast<const unsigned*>(a.ws + L.counter), reinterpret_cast<const Chunk*>(a.ws + L.chunk),
+            reinterpret_cast<const float*>(a.ws + L.ulogc), a.part_o, a.part_ml);
+    }
+    return hipGetLastError();
+}
+
 template <typename T, int D, int GT>
 hipError_t attend_g(const AttendArgs& a, hipStream_t s) {
     // one list of units over every (b, kv) pair; the sampled path runs as
@@ -734,7 +1047,7 @@ template <typename T, int D>
 hipError_t attend_d(const AttendArgs& a, hipStream_t s) {
     if constexpr (sizeof(T) == 2) {
         // the matrix-core value sum computes every head of the group at once
-        return a.G >= 1 && a.G <= kMaxGroup ? attend_g<T, D, kMaxGroup>(a, s) : hipErrorInvalidValue;
+        return a.G >= 1 && a.G <= kMaxGroup ? attend_mfma<D>(a, s) : hipErrorInvalidValue;
     } else {
         switch (a.G) {
             case 1: return attend_g<T, D, 1>(a, s);
