@@ -5,6 +5,7 @@
 #include <stdio.h>
 
 #include <algorithm>
+#include <atomic>
 #include <functional>
 #include <string>
 #include <vector>
@@ -58,6 +59,27 @@ bool dtype_ok(santapp_dtype dt) { return dt == SANTAPP_BF16 || dt == SANTAPP_FP3
 
 size_t align_up(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
+// Compute units of the current device (0 if the query fails), looked up once
+// per device.
+int device_cus() {
+    constexpr int kDevs = 64;
+    static std::atomic<int> cache[kDevs];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return 0;
+    }
+    if (dev < 0 || dev >= kDevs) return 0;
+    int n = cache[dev].load(std::memory_order_relaxed);
+    if (n > 0) return n;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 0) {
+        (void)hipGetLastError();
+        return 0;
+    }
+    cache[dev].store(n, std::memory_order_relaxed);
+    return n;
+}
+
 // Teams per (b, kv) for contiguous parents: every parent but the last has P
 // members and min(R, P) teams.
 long long team_count(int N, int P, int R) {
@@ -102,7 +124,6 @@ DecodeLayout decode_layout(int B, int Hq, int Hkv, int T, int d, int M, int Kp, 
         off = align_up(off + bytes);
         return at;
     };
-    L.counter = take(sizeof(unsigned));  // units appended to the list this step
     L.phi = take(BQ * M * sizeof(double));
     L.Y = take(BQ * M * sizeof(double));
     L.lc = take(BQ * M * sizeof(float));
@@ -346,6 +367,7 @@ santapp_status santapp_decode(const santapp_teams* t, const float* q, const void
     A.max_chunks = L.max_chunks;
     A.max_hunits = L.max_hunits;
     A.grid_waves = t->cus > 0 ? t->cus * kAttendWavesPerCU : 0;
+    A.cus = t->cus;
     A.dtype = t->dtype;
     A.scale = static_cast<float>(scale);
     A.ws = ws;
@@ -443,6 +465,8 @@ santapp_status santapp_dense_decode(const float* q, const void* K, const void* V
     A.M = 0;
     A.max_chunks = L.max_chunks;
     A.max_hunits = L.max_hunits;
+    A.cus = device_cus();
+    A.grid_waves = A.cus * kAttendWavesPerCU;
     A.dtype = dtype;
     A.scale = static_cast<float>(scale);
     A.dense = true;

@@ -258,7 +258,7 @@ __global__ __launch_bounds__(kWave, 2) void k_attend(
     const T* __restrict__ K, const T* __restrict__ V, const T* __restrict__ sK,
     const T* __restrict__ sV, const float* __restrict__ q, int N, int T_suf, int BH, int Hkv,
     int Hq, int G, int M, float scale_log2, int max_chunks, int max_hunits,
-    const unsigned* __restrict__ counter, const Chunk* __restrict__ chunks,
+    const PlanHeader* __restrict__ hdr, const Chunk* __restrict__ chunks,
     const float* __restrict__ ulogc, float* __restrict__ part_o, float* __restrict__ part_ml) {
     constexpr int NF = frag_count<T, D>();
     constexpr int VPL = D / 16;  // value dims per lane (16 lanes per row)
@@ -278,11 +278,12 @@ __global__ __launch_bounds__(kWave, 2) void k_attend(
     const int hsel = 4 * (c & 1);  // first head of this lane's registers
     const int ncp = (N + UR - 1) / UR;
     const int nchd = ncp + (T_suf + UR - 1) / UR;  // dense units per (b, kv)
-    // the unit list: the sampler's (read with the count of units it
-    // appended), or the dense path's (b, kv)-major one
-    const int total = DENSE ? BH * nchd
-                            : static_cast<int>(min(__hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT),
-                                                   static_cast<unsigned>(BH) * static_cast<unsigned>(max_chunks)));
+    // the sampled path's wave serves one (b, kv) pair: entries
+    // blockIdx.x / BH, + gridDim.x / BH, ... of the pair's region of the
+    // sampler's unit list; the dense path walks its (b, kv)-major list
+    const int pbh = DENSE ? 0 : static_cast<int>(blockIdx.x) % BH;
+    const Chunk* const pchunks = chunks + static_cast<size_t>(pbh) * max_chunks;
+    const int total = DENSE ? BH * nchd : min(hdr[pbh].chunks, max_chunks);
     auto descriptor = [&](int u) {
         if (DENSE) {
             const int bhx = u / nchd, cix = u - bhx * nchd;
@@ -296,20 +297,20 @@ __global__ __launch_bounds__(kWave, 2) void k_attend(
             d.p01 = d.p23 = d.p45 = d.p67 = 0u;
             return d;
         }
-        return chunks[min(u, BH * max_chunks - 1)];
+        return pchunks[min(u, max_chunks - 1)];
     };
     // the sampled path fetches the next unit's descriptor while it processes
     // one; the dense path computes it in place
-    const int stride = static_cast<int>(gridDim.x);
-    const int u0 = static_cast<int>(blockIdx.x);
+    const int stride = DENSE ? static_cast<int>(gridDim.x) : static_cast<int>(gridDim.x) / BH;
+    const int u0 = DENSE ? static_cast<int>(blockIdx.x) : static_cast<int>(blockIdx.x) / BH;
 
-    Chunk ck = descriptor(DENSE ? 0 : min(u0, BH * max_chunks - 1));
+    Chunk ck = descriptor(DENSE ? 0 : u0);
     int qbh = -1;  // the (b, kv) pair whose query the registers hold
     QKT qk;
 
     for (int u = u0; u < total; u += stride) {
         if (DENSE) ck = descriptor(u);
-        const int bh = meta_bh(ck.meta), ci = ck.ci;
+        const int bh = DENSE ? meta_bh(ck.meta) : pbh, ci = ck.ci;
         if (bh >= BH || ci < 0 || ci >= max_chunks) {  // uniform; never for a plan of this step
             ck = descriptor(min(u + stride, total - 1));
             continue;
@@ -591,12 +592,20 @@ __global__ __launch_bounds__(kWave, 2) void k_attend(
 // wait for the value copies in flight).
 __device__ __forceinline__ void lds_order() { asm volatile("" ::: "memory"); }
 
+// Workgroups of kAttendWaves independent waves, one workgroup per compute
+// unit: the waves share nothing but the workgroup's LDS allocation (each has
+// its own tiles) and never synchronise.  Wave k of workgroup b is wave
+// k gridDim.x + b of the launch, so the launch's first waves, which get work
+// first, are spread over every compute unit (one-wave workgroups were
+// placed several to a compute unit, leaving others idle).
+constexpr int kAttendWaves = 8;
+
 template <int D, bool DENSE>
-__global__ __launch_bounds__(kWave, 2) void k_attend_mfma(
+__global__ __launch_bounds__(kAttendWaves * kWave, 1) void k_attend_mfma(
     const bf16_t* __restrict__ K, const bf16_t* __restrict__ V, const bf16_t* __restrict__ sK,
     const bf16_t* __restrict__ sV, const float* __restrict__ q, int N, int T_suf, int BH, int Hkv,
     int Hq, int G, int M, float scale_log2, int max_chunks, int max_hunits,
-    const unsigned* __restrict__ counter, const Chunk* __restrict__ chunks,
+    const PlanHeader* __restrict__ hdr, const Chunk* __restrict__ chunks,
     const float* __restrict__ ulogc, float* __restrict__ part_o, float* __restrict__ part_ml) {
     constexpr int UR = DENSE ? kDenseRows : kChunkRows;
     using QKT = QK<bf16_t, D>;
@@ -610,19 +619,28 @@ __global__ __launch_bounds__(kWave, 2) void k_attend_mfma(
     constexpr int kNT = 2;              // cache policy of the value copies: streaming
     // value tiles, double-buffered (two objects, so that the compiler can
     // tell the copies into one from the reads of the other)
-    __shared__ __attribute__((aligned(16))) char s_v0[VT::kBytes];
-    __shared__ __attribute__((aligned(16))) char s_v1[VT::kBytes];
-    __shared__ float4 s_pt[8][8];  // probabilities [head][row / 4]
+    __shared__ __attribute__((aligned(16))) char s_v0[kAttendWaves][VT::kBytes];
+    __shared__ __attribute__((aligned(16))) char s_v1[kAttendWaves][VT::kBytes];
+    __shared__ float4 s_pt[kAttendWaves][8][8];  // probabilities [head][row / 4]
 
     const int lane = lane_id();
+    const int wv = __builtin_amdgcn_readfirstlane(wave_id());  // uniform: keeps the tile bases scalar
     const int c = lane >> 4, j16 = lane & 15;
     const int hsel = 4 * (c & 1);  // first head of this lane's registers
     const int ncp = (N + UR - 1) / UR;
     const int nchd = ncp + (T_suf + UR - 1) / UR;
-    const int total = DENSE ? BH * nchd
-                            : static_cast<int>(min(__hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT),
-                                                   static_cast<unsigned>(BH) * static_cast<unsigned>(max_chunks)));
-    const int stride = static_cast<int>(gridDim.x);
+    const int gw = wv * static_cast<int>(gridDim.x) + static_cast<int>(blockIdx.x);  // wave of the launch
+    const int nw = kAttendWaves * static_cast<int>(gridDim.x);                       // waves of the launch
+    // Wave gw takes units gw, gw + nw, ... of the step's list: the dense
+    // path's (b, kv)-major list, or the sampled path's units of all pairs in
+    // pair order (each pair's units sit in its own region of the sampler's
+    // list; every wave reads the pairs' unit counts and maps a unit to its
+    // pair by a prefix sum).  Every compute unit so gets the same number of
+    // units to within one, however the pairs' counts differ.
+    const int stride = nw;
+    char* const tile0 = s_v0[wv];
+    char* const tile1 = s_v1[wv];
+    float4 (*const ptile)[8] = s_pt[wv];
     auto descriptor = [&](int u) {
         if (DENSE) {
             const int bhx = u / nchd, cix = u - bhx * nchd;
@@ -636,7 +654,35 @@ __global__ __launch_bounds__(kWave, 2) void k_attend_mfma(
             d.p01 = d.p23 = d.p45 = d.p67 = 0u;
             return d;
         }
-        return chunks[min(u, BH * max_chunks - 1)];
+        // unit u of the pairs' concatenated lists: lanes hold the counts of
+        // 64 pairs at a time and their inclusive prefix sums
+        int base = 0, p = BH - 1, idx = 0;
+        for (int p0 = 0; p0 < BH; p0 += kWave) {  // uniform
+            const int cnt = p0 + lane < BH ? min(max(hdr[p0 + lane].chunks, 0), max_chunks) : 0;
+            const int incl = wave_incl_scan(cnt) + base;
+            const uint64_t before = __ballot(p0 + lane < BH && incl <= u);  // pairs wholly before unit u
+            const int nb = __popcll(before);
+            if (nb < kWave && p0 + nb < BH) {  // unit u is in pair p0 + nb
+                p = p0 + nb;
+                idx = u - (__builtin_amdgcn_readlane(incl, nb) - __builtin_amdgcn_readlane(cnt, nb));
+                break;
+            }
+            base = __builtin_amdgcn_readlane(incl, kWave - 1);
+        }
+        Chunk d = chunks[static_cast<size_t>(p) * max_chunks + min(max(idx, 0), max_chunks - 1)];
+        d.meta = (d.meta & 0xffff) | (p << 16);  // the pair the unit was found in
+        return d;
+    };
+    // units of the step: the dense list's length, or the sum of the pairs'
+    // counts (a wave-wide sum over the headers)
+    auto unit_total = [&]() {
+        if (DENSE) return BH * nchd;
+        int t = 0;
+        for (int p0 = 0; p0 < BH; p0 += kWave) {  // uniform
+            const int cnt = p0 + lane < BH ? min(max(hdr[p0 + lane].chunks, 0), max_chunks) : 0;
+            t += __builtin_amdgcn_readlane(wave_incl_scan(cnt), kWave - 1);
+        }
+        return t;
     };
     // a unit's rows, clamped to its buffer whatever the workspace holds
     struct Unit {
@@ -697,9 +743,12 @@ __global__ __launch_bounds__(kWave, 2) void k_attend_mfma(
         }
     };
 
-    int u = static_cast<int>(blockIdx.x);
+    int u = gw;
+    const int total = unit_total();
     if (u >= total) return;  // uniform
     Unit cur = unit_of(descriptor(u));
+    // the sampled path fetches the next unit's descriptor while it
+    // processes one; the dense path computes it when it needs it
     Chunk nxck = DENSE ? Chunk{} : descriptor(min(u + stride, total - 1));
     float4 lc_lo, lc_hi;
     corrections(cur, lc_lo, lc_hi);
@@ -711,7 +760,7 @@ __global__ __launch_bounds__(kWave, 2) void k_attend_mfma(
         qk.load_q(q + (static_cast<size_t>(b) * Hq + kv * G + (h < G ? h : 0)) * D, h < G ? scale_log2 : 0.f, c);
     }
     typename QKT::frag kf0[2][NF], kf1[2][NF];
-    issue(cur, 0, s_v0, kf0, true);
+    issue(cur, 0, tile0, kf0, true);
 
     float m[4], l[4];
     f32x4 oacc[NB];
@@ -734,11 +783,11 @@ __global__ __launch_bounds__(kWave, 2) void k_attend_mfma(
         // the next step: the same unit's next 32 rows, or the next unit's first
         const bool more = r0 + 32 < cur.rows;
         const int un = u + stride;
-        const bool has_next = more || (!DENSE && un < total);
+        const bool has_next = more || un < total;
         Unit nxt = cur;
         int nr0 = r0 + 32;
         if (!more && has_next) {
-            nxt = unit_of(nxck);
+            nxt = unit_of(DENSE ? descriptor(un) : nxck);
             nr0 = 0;
         }
         // this step's data first: its K fragments, and with them (issued
@@ -766,7 +815,7 @@ __global__ __launch_bounds__(kWave, 2) void k_attend_mfma(
         }
         lds_order();  // the previous step's reads of s_pt come first
         if (c < 2) {
-            float* pt = reinterpret_cast<float*>(s_pt);
+            float* pt = reinterpret_cast<float*>(ptile);
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 pt[(hsel + r) * 32 + j16] = p0[r];
@@ -776,7 +825,7 @@ __global__ __launch_bounds__(kWave, 2) void k_attend_mfma(
         lds_order();
         bf16x8 pa;
         {
-            const float4 x0 = s_pt[j16 & 7][2 * c], x1 = s_pt[j16 & 7][2 * c + 1];
+            const float4 x0 = ptile[j16 & 7][2 * c], x1 = ptile[j16 & 7][2 * c + 1];
             const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
             const bool low = j16 >= 8;
 #pragma unroll
@@ -854,9 +903,9 @@ __global__ __launch_bounds__(kWave, 2) void k_attend_mfma(
         r0 = nr0;
     };
     for (;;) {
-        step(s_v0, kf0, s_v1, kf1);
+        step(tile0, kf0, tile1, kf1);
         if (done) break;
-        step(s_v1, kf1, s_v0, kf0);
+        step(tile1, kf1, tile0, kf0);
         if (done) break;
     }
 }
@@ -986,13 +1035,31 @@ __global__ void k_zero(uint4* __restrict__ p, size_t n16, unsigned char* __restr
     if (blockIdx.x == 0 && static_cast<int>(threadIdx.x) < ntail) tail[threadIdx.x] = 0;
 }
 
+// Waves of an attention launch: one per unit on the dense path; on the
+// sampled path W per (b, kv) pair, where W spreads the device's resident
+// waves over the pairs and never exceeds the units a pair can have.
+long long attend_waves(const AttendArgs& a) {
+    const long long BH = static_cast<long long>(a.B) * a.Hkv;
+    if (a.dense) return BH * a.max_chunks;
+    long long W = a.max_chunks;
+    if (a.grid_waves > 0) W = std::min<long long>(W, std::max<long long>(1, a.grid_waves / BH));
+    return BH * W;
+}
+
+// Workgroups of an attention launch on the matrix cores: one per compute
+// unit, fewer when the step cannot have that many units of work.
+long long attend_blocks(const AttendArgs& a) {
+    const long long units = static_cast<long long>(a.B) * a.Hkv * a.max_chunks;
+    const long long blocks = a.cus > 0 ? std::min<long long>(a.cus, units) : (units + kAttendWaves - 1) / kAttendWaves;
+    return std::max<long long>(blocks, 1);
+}
+
 template <int D>
 hipError_t attend_mfma(const AttendArgs& a, hipStream_t s) {
-    const long long units = static_cast<long long>(a.B) * a.Hkv * a.max_chunks;
-    long long waves = units;
-    if (!a.dense && a.grid_waves > 0) waves = std::min<long long>(units, a.grid_waves);
-    if (waves < 1 || waves > 0x7fffffffLL) return hipErrorInvalidValue;
-    const dim3 grid(static_cast<unsigned>(waves));
+    const long long blocks = attend_blocks(a);
+    if (blocks > 0x7fffffffLL / kAttendWaves) return hipErrorInvalidValue;
+    const dim3 grid(static_cast<unsigned>(blocks));
+    constexpr int kThreads = kAttendWaves * kWave;
     const float sl2 = a.scale * kLog2e;
     const bf16_t* K = static_cast<const bf16_t*>(a.K);
     const bf16_t* V = static_cast<const bf16_t*>(a.V);
@@ -1000,14 +1067,14 @@ hipError_t attend_mfma(const AttendArgs& a, hipStream_t s) {
     const bf16_t* sV = static_cast<const bf16_t*>(a.sV);
     const int BH = a.B * a.Hkv;
     if (a.dense) {
-        k_attend_mfma<D, true><<<grid, kWave, 0, s>>>(K, V, sK, sV, a.q, a.N, a.T, BH, a.Hkv, a.Hq, a.G, 0, sl2,
+        k_attend_mfma<D, true><<<grid, kThreads, 0, s>>>(K, V, sK, sV, a.q, a.N, a.T, BH, a.Hkv, a.Hq, a.G, 0, sl2,
                                                       a.max_chunks, a.max_hunits, nullptr, nullptr, nullptr,
                                                       a.part_o, a.part_ml);
     } else {
         const DecodeLayout& L = *a.lay;
-        k_attend_mfma<D, false><<<grid, kWave, 0, s>>>(
+        k_attend_mfma<D, false><<<grid, kThreads, 0, s>>>(
             K, V, sK, sV, a.q, a.N, a.T, BH, a.Hkv, a.Hq, a.G, a.M, sl2, a.max_chunks, a.max_hunits,
-            reinterpret_cast<const unsigned*>(a.ws + L.counter), reinterpret_cast<const Chunk*>(a.ws + L.chunk),
+            reinterpret_cast<const PlanHeader*>(a.ws + L.hdr), reinterpret_cast<const Chunk*>(a.ws + L.chunk),
             reinterpret_cast<const float*>(a.ws + L.ulogc), a.part_o, a.part_ml);
     }
     return hipGetLastError();
@@ -1018,9 +1085,7 @@ hipError_t attend_g(const AttendArgs& a, hipStream_t s) {
     // one list of units over every (b, kv) pair; the sampled path runs as
     // many one-wave workgroups as the chip keeps resident (each looping over
     // its share), the dense path one workgroup per unit
-    const long long units = static_cast<long long>(a.B) * a.Hkv * a.max_chunks;
-    long long waves = units;
-    if (!a.dense && a.grid_waves > 0) waves = std::min<long long>(units, a.grid_waves);
+    const long long waves = attend_waves(a);
     if (waves < 1 || waves > 0x7fffffffLL) return hipErrorInvalidValue;
     const dim3 grid(static_cast<unsigned>(waves));
     const float sl2 = a.scale * kLog2e;
@@ -1037,7 +1102,7 @@ hipError_t attend_g(const AttendArgs& a, hipStream_t s) {
         const DecodeLayout& L = *a.lay;
         k_attend<T, D, GT, false><<<grid, kWave, 0, s>>>(
             K, V, sK, sV, a.q, a.N, a.T, BH, a.Hkv, a.Hq, a.G, a.M, sl2, a.max_chunks, a.max_hunits,
-            reinterpret_cast<const unsigned*>(a.ws + L.counter), reinterpret_cast<const Chunk*>(a.ws + L.chunk),
+            reinterpret_cast<const PlanHeader*>(a.ws + L.hdr), reinterpret_cast<const Chunk*>(a.ws + L.chunk),
             reinterpret_cast<const float*>(a.ws + L.ulogc), a.part_o, a.part_ml);
     }
     return hipGetLastError();

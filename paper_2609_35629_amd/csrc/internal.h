@@ -21,8 +21,8 @@ constexpr int kMergeThreads = 256;   // threads of a merge workgroup
 
 // Attention work unit: up to kChunkRows consecutive rows of one union team of
 // the packed cache, or of the suffix (slot < 0); the dense path cuts its rows
-// into units of kDenseRows.  The sampler appends the units of each (b, kv)
-// to one list shared by all pairs; `meta` packs the row count (bits 0-7),
+// into units of kDenseRows.  The sampler writes the units of each (b, kv)
+// to that pair's region of the unit list; `meta` packs the row count (bits 0-7),
 // the mask of query heads of the KV head that read the rows (bits 8-15) and
 // the (b, kv) pair (bits 16-31); pos[h] is the unit's position in the list
 // of units head h reads (for the heads of the mask), where its partial
@@ -81,7 +81,7 @@ struct PlanHeader {
 // length of each head's partial-state list.
 struct DecodeLayout {
     int max_chunks = 0, max_hunits = 0;
-    size_t counter = 0, phi = 0, Y = 0, lc = 0, hdr = 0, chunk = 0, ulogc = 0, po = 0,
+    size_t phi = 0, Y = 0, lc = 0, hdr = 0, chunk = 0, ulogc = 0, po = 0,
            pml = 0, total = 0;
 };
 
@@ -127,7 +127,8 @@ struct AttendArgs {
     const void* sV;
     const float* q;   // [B, Hq, d]
     int B, Hkv, Hq, G, d, N, T, M, max_chunks, max_hunits;
-    int grid_waves;             // resident attention waves of the device (0: one per unit)
+    int grid_waves;             // resident one-wave workgroups of the device (0: one per unit)
+    int cus;                    // compute units of the device (0: unknown)
     santapp_dtype dtype;
     float scale;
     bool dense;                 // every row, every head, correction 1

@@ -16,7 +16,9 @@
 //           ascending team order with each team's per-head corrections, cut
 //           into chunks of at most kChunkRows consecutive packed rows (each
 //           chunk is one unit of attention work), followed by the chunks of
-//           the exactly attended suffix.
+//           the exactly attended suffix.  Each (sequence, KV head) pair owns a
+//           fixed region of the unit list, so the plan needs no global
+//           atomics.
 #include <math.h>
 
 #include <type_traits>
@@ -357,13 +359,10 @@ template <typename T, int D, int G>
 __global__ __launch_bounds__(kRouteThreads) void k_route(
     const T* __restrict__ reps, const double* __restrict__ log_n, const float* __restrict__ q,
     int M, int Hkv, int Hq, double scale, uint64_t seed, uint64_t step, double* __restrict__ phi,
-    double* __restrict__ Y, unsigned* __restrict__ counter) {
+    double* __restrict__ Y) {
     constexpr int DPL = D / 16;
     using RC = RepChunk<T, DPL>;
     __shared__ double s_gum[G][kRouteTeams];
-    // the sampler appends this step's attention units to an empty list
-    if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0)
-        __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const int bh = blockIdx.y;
     const int b = bh / Hkv, kv = bh - b * Hkv;
     const int tid = threadIdx.x, grp = tid >> 4, sub = tid & 15;
@@ -415,7 +414,7 @@ template <int G, int PL>
 __global__ __launch_bounds__(kSelectThreads) void k_select(
     const double* __restrict__ phi, const double* __restrict__ Y, const int* __restrict__ team_begin,
     const int* __restrict__ team_size, int M, int Hkv, int Hq, int Kp, int T_suf, int max_chunks,
-    float* __restrict__ lc, unsigned* __restrict__ counter, PlanHeader* __restrict__ hdr,
+    float* __restrict__ lc, PlanHeader* __restrict__ hdr,
     Chunk* __restrict__ chunks, float* __restrict__ ulogc, int* __restrict__ dbg_sel,
     float* __restrict__ dbg_logc, double* __restrict__ dbg_tau, int* __restrict__ dbg_uteams,
     int* __restrict__ dbg_urows) {
@@ -425,7 +424,6 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
     __shared__ __align__(16) uint64_t s_cand[kSelectWaves][kWave];
     __shared__ uint64_t s_bits[kMaxGroup][kMaxTeams / kWave];  // selection bits per head
     __shared__ __align__(16) int s_w[(3 + kMaxGroup) * kSelectWaves];
-    __shared__ int s_base;
     __shared__ int4 s_team[kSelectThreads];  // union teams of one pass: first unit, begin, size, heads
     __shared__ unsigned short s_tpos[kSelectThreads][kMaxGroup];  // first position in each head's list
 
@@ -557,28 +555,11 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
     // One pass per kSelectThreads teams, thread tid owning team base + tid:
     // a scan gives every union team its slot, its first unit, and its first
     // position in the list of each head that selected it; a unit's team is
-    // the last union team whose first unit is at or before it.  The pair's
-    // range in the shared unit list is claimed once its total is known (in
-    // the first pass when one pass covers every team, else after a counting
-    // pre-pass).
+    // the last union team whose first unit is at or before it.  The units go
+    // to the pair's own region of the list (max_chunks entries, which bound
+    // the units of any union of this size).
     constexpr int NV = 3 + G;
-    const bool one_pass = M <= kSelectThreads;
-    int utotal = 0;
-    if (!one_pass) {
-        int nu = 0;
-        for (int base = 0; base < M; base += kSelectThreads) {
-            const int g = base + tid;
-            const int tsz = base == 0 ? size0 : team_size[tb0 + min(g, M - 1)];
-            nu += heads_of(g) ? chunk_count(tsz) : 0;
-        }
-        const int x[1] = {nu};
-        int ex[1], tot[1];
-        block_scan<1>(x, ex, tot, s_w);
-        utotal = min(tot[0] + nsc, max_chunks);
-        if (tid == 0)
-            s_base = static_cast<int>(
-                __hip_atomic_fetch_add(counter, static_cast<unsigned>(utotal), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-    }
+    Chunk* const cb = chunks + static_cast<size_t>(bh) * max_chunks;
     int run_u = 0, run_rows = 0, run_c = 0;
     int run_h[G];
 #pragma unroll
@@ -602,12 +583,6 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
         for (int h = 0; h < G; ++h) x[3 + h] = ((hm >> h) & 1) ? nc : 0;
         int ex[NV], tot[NV];
         block_scan<NV>(x, ex, tot, s_w);
-        if (one_pass) {
-            utotal = min(tot[1] + nsc, max_chunks);
-            if (tid == 0)
-                s_base = static_cast<int>(__hip_atomic_fetch_add(counter, static_cast<unsigned>(utotal), __ATOMIC_RELAXED,
-                                                                 __HIP_MEMORY_SCOPE_AGENT));
-        }
         if (f) {
             write_logc(g, run_u + ex[0], hm);
             s_team[ex[0]] = make_int4(ex[1], tbeg, tsz, hm);
@@ -616,7 +591,6 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
                 s_tpos[ex[0]][h] = static_cast<unsigned short>(h < G ? run_h[h] + ex[3 + h] : 0);
         }
         __syncthreads();
-        Chunk* cb = chunks + s_base;
         for (int c = tid; c < tot[1]; c += kSelectThreads) {
             int lo = 0, hi = tot[0] - 1;
             while (lo < hi) {
@@ -629,7 +603,7 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
             const int4 tm = s_team[lo];
             const int p = c - tm.x;
             const int ci = run_c + c;
-            if (ci < utotal) {
+            if (ci < max_chunks) {
                 Chunk ch;
                 ch.begin = tm.y + p * kChunkRows;
                 ch.slot = run_u + lo;
@@ -649,11 +623,11 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
         for (int h = 0; h < G; ++h) run_h[h] += tot[3 + h];
         if (base + kSelectThreads < M) __syncthreads();  // s_team is rewritten by the next pass
     }
+    const int utotal = min(run_c + nsc, max_chunks);
     // the suffix: every head, no correction, after each head's teams
-    Chunk* cb = chunks + s_base;
     for (int p = tid; p < nsc; p += kSelectThreads) {
         const int ci = run_c + p;
-        if (ci < utotal) {
+        if (ci < max_chunks) {
             Chunk ch;
             ch.begin = p * kChunkRows;
             ch.slot = -1;
@@ -687,8 +661,7 @@ hipError_t route_g(const RouteArgs& a, hipStream_t s) {
     double* phi = reinterpret_cast<double*>(a.ws + L.phi);
     double* Y = reinterpret_cast<double*>(a.ws + L.Y);
     k_route<T, D, G><<<dim3((a.M + kRouteTeams - 1) / kRouteTeams, a.B * a.Hkv), kRouteThreads, 0, s>>>(
-        static_cast<const T*>(a.reps), a.log_n, a.q, a.M, a.Hkv, a.Hq, a.scale, a.seed, a.step, phi, Y,
-        reinterpret_cast<unsigned*>(a.ws + L.counter));
+        static_cast<const T*>(a.reps), a.log_n, a.q, a.M, a.Hkv, a.Hq, a.scale, a.seed, a.step, phi, Y);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     float* lc = reinterpret_cast<float*>(a.ws + L.lc);
@@ -699,7 +672,7 @@ hipError_t route_g(const RouteArgs& a, hipStream_t s) {
     k_select<G, PLV><<<a.B * a.Hkv, kSelectThreads,                                               \
                        (PLV > 0 && PLV <= 8) ? sizeof(float) * G * a.M : 0, s>>>(                \
         phi, Y, a.team_begin, a.team_size, a.M, a.Hkv, a.Hq, a.Kp, a.T, L.max_chunks, lc,       \
-        reinterpret_cast<unsigned*>(a.ws + L.counter), hdr,                                     \
+        hdr,                                     \
         ch, ulogc, d ? d->sel : nullptr, d ? d->logc : nullptr, d ? d->tau : nullptr,             \
         d ? d->union_teams : nullptr, d ? d->union_rows : nullptr)
     if (a.M <= 8 * kWave)
