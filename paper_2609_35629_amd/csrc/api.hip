@@ -127,6 +127,7 @@ DecodeLayout decode_layout(int B, int Hq, int Hkv, int T, int d, int M, int Kp, 
     L.phi = take(BQ * M * sizeof(double));
     L.Y = take(BQ * M * sizeof(double));
     L.lc = take(BQ * M * sizeof(float));
+    L.lpos = take(BQ * M * sizeof(unsigned short));
     L.hdr = take(BH * sizeof(PlanHeader));
     L.chunk = take(BH * L.max_chunks * sizeof(Chunk));
     L.ulogc = take(BH * M * kLogcStride * sizeof(float));

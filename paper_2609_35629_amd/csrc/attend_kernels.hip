@@ -913,72 +913,66 @@ __global__ __launch_bounds__(kAttendWaves * kWave, 1) void k_attend_mfma(
 // Merge of one query head's list of n unit states (m_p: log2-domain maximum
 // with the team's correction folded in, l_p: mass) and value sums o_p:
 // out = sum_p 2^(m_p - mx) o_p / sum_p 2^(m_p - mx) l_p with mx = max_p m_p.
-// Workgroup (sequence and query head, slice of kMergeDims output dims): a
-// pass covers kMergePass positions; its states go to LDS (each loaded once,
-// by one thread), and lane group g loads the value sums of positions g,
-// g + kMergeGroups, ... of its dims.  Every load of the first pass, the
-// sampled path's list length included, is issued before any is used (they
-// are issued for every position the list can have; those past its length
-// are masked), and the groups' sums add in group order.
-// The dense path knows its lists' length and loads exactly that (in one pass
-// up to 320 positions); the sampled path's first pass covers 160 positions,
-// the length of a list of a few dozen teams, so that few of its loads are
-// wasted on positions past the list.
+// Workgroup = (sequence and query head, slice of kMergeDims output dims).
+// A pass covers 32 NPL positions: thread t loads the states of positions
+// t, t + 256, ... (to LDS, weights computed once per position) and 16 bytes
+// of values (four dims) of positions t / 8 + 32 k, k < NPL, so a pass is
+// NPL + 1 loads per thread, all issued before any is used (the sampled
+// path's list length travels with them; positions past it are masked).  The
+// host picks NPL from the longest list a step can have, so one pass covers
+// every list in the common case.  The value sums reduce over the 32
+// position groups in a fixed order.
 constexpr int kMergeDims = 32;
-constexpr int kMergeGroups = kMergeThreads / kMergeDims;
+constexpr int kMergeQuads = kMergeDims / 4;             // threads per position (16 bytes each)
+constexpr int kMergeRowsPerLoad = kMergeThreads / kMergeQuads;  // positions per load instruction (32)
 
-template <bool DENSE>
+template <bool DENSE, int NPL>
 __global__ __launch_bounds__(kMergeThreads) void k_merge(const float* __restrict__ part_o,
                                                          const float* __restrict__ part_ml,
                                                          const PlanHeader* __restrict__ hdr,
                                                          int n_dense, int Hkv, int Hq, int max_hunits,
                                                          int D, float* __restrict__ out) {
-    constexpr int kMergeBatch = DENSE ? 40 : 20;                 // positions per lane group and pass
-    constexpr int kMergePass = kMergeGroups * kMergeBatch;       // positions per pass
-    constexpr int kMergeStates = (kMergePass + kMergeThreads - 1) / kMergeThreads;  // per thread
+    constexpr int PP = kMergeRowsPerLoad * NPL;                              // positions per pass
+    constexpr int NST = (PP + kMergeThreads - 1) / kMergeThreads;            // states per thread
     constexpr int NW = kMergeThreads / kWave;
-    __shared__ float2 s_st[kMergePass];
+    __shared__ float2 s_st[PP];       // (weight exponent, mass) of the pass's positions
     __shared__ float s_red[2][NW];
-    __shared__ float s_sum[kMergeGroups][kMergeDims];
+    __shared__ float4 s_acc[NW][kMergeQuads];
     const int bhq = blockIdx.x;
     const int b = bhq / Hq, hq = bhq - b * Hq;
     const int G = Hq / Hkv;
     const int kv = hq / G, h = hq - kv * G;
     const int bh = b * Hkv + kv;
     const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
-    const int jd = tid % kMergeDims, grp = tid / kMergeDims;
+    const int dq = tid % kMergeQuads, pg = tid / kMergeQuads;
     const size_t row0 = (static_cast<size_t>(bh) * G + h) * max_hunits;
     const float2* ml = reinterpret_cast<const float2*>(part_ml) + row0;
-    const float* po = part_o + row0 * D + blockIdx.y * kMergeDims + jd;
+    const float* po = part_o + row0 * D + blockIdx.y * kMergeDims + 4 * dq;
     // the list length as a vector load (the index is 0 on every lane, but
-    // not provably uniform), so that it travels with the first pass's loads
-    // instead of holding them back
+    // not provably uniform), so that it travels with the pass's loads
     int n_list = n_dense;
     if (!DENSE) n_list = hdr[bh].hunits[h + static_cast<int>(__builtin_amdgcn_mbcnt_lo(0u, 0u))];
     // positions the loads may touch: the list on the dense path, the list's
     // capacity on the sampled path
     const int lim = DENSE ? min(n_dense, max_hunits) : max_hunits;
 
-    float mx = kNeg, lsum = 0.f, acc = 0.f;
-    float2 st[kMergeStates];
-    float v[kMergeBatch];
+    float mx = kNeg, lsum = 0.f;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    float2 st[NST];
+    float4 v[NPL];
     auto load = [&](int p0) {
 #pragma unroll
-        for (int k = 0; k < kMergeStates; ++k) st[k] = ml[min(p0 + tid + k * kMergeThreads, lim - 1)];
+        for (int k = 0; k < NST; ++k) st[k] = ml[min(p0 + tid + k * kMergeThreads, lim - 1)];
 #pragma unroll
-        for (int k = 0; k < kMergeBatch; ++k)
-            v[k] = __builtin_nontemporal_load(po + static_cast<size_t>(min(p0 + grp + k * kMergeGroups, lim - 1)) * D);
+        for (int k = 0; k < NPL; ++k)
+            v[k] = load_stream_f(po + static_cast<size_t>(min(p0 + pg + k * kMergeRowsPerLoad, lim - 1)) * D);
     };
     auto consume = [&](int p0, int n) {
         float pm = kNeg;
 #pragma unroll
-        for (int k = 0; k < kMergeStates; ++k) {
+        for (int k = 0; k < NST; ++k) {
             const int i = tid + k * kMergeThreads;
-            if (i < kMergePass) {
-                const bool valid = p0 + i < n;
-                s_st[i] = valid ? st[k] : make_float2(kNeg, 0.f);
-                pm = fmaxf(pm, valid ? st[k].x : kNeg);
-            }
+            if (i < PP) pm = fmaxf(pm, p0 + i < n ? st[k].x : kNeg);
         }
         for (int off = kWave / 2; off > 0; off >>= 1) pm = fmaxf(pm, __shfl_xor(pm, off));
         if (lane == 0) s_red[0][w] = pm;
@@ -987,43 +981,68 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(const float* __restrict
         for (int k = 0; k < NW; ++k) pm = fmaxf(pm, s_red[0][k]);
         const float nmx = fmaxf(mx, pm);
         const float sc = rebase(mx, nmx);
-        acc *= sc;
+        acc.x *= sc;
+        acc.y *= sc;
+        acc.z *= sc;
+        acc.w *= sc;
         lsum *= sc;
-        // the masses: each thread its own states; the value sums: each lane
-        // group its positions (masked states have no weight)
+        // each state's weight once, by the thread that loaded it
 #pragma unroll
-        for (int k = 0; k < kMergeStates; ++k) {
+        for (int k = 0; k < NST; ++k) {
             const int i = tid + k * kMergeThreads;
-            if (i < kMergePass && p0 + i < n) lsum = fmaf(rebase(st[k].x, nmx), st[k].y, lsum);
+            if (i < PP) {
+                const float wt = p0 + i < n ? rebase(st[k].x, nmx) : 0.f;
+                lsum = fmaf(wt, p0 + i < n ? st[k].y : 0.f, lsum);
+                s_st[i].x = wt;
+            }
         }
+        __syncthreads();
 #pragma unroll
-        for (int k = 0; k < kMergeBatch; ++k) {
-            const int i = grp + k * kMergeGroups;
-            if (p0 + i < n) acc = fmaf(rebase(s_st[i].x, nmx), v[k], acc);
+        for (int k = 0; k < NPL; ++k) {
+            const float wt = s_st[pg + k * kMergeRowsPerLoad].x;  // zero past the list
+            acc.x = fmaf(wt, v[k].x, acc.x);
+            acc.y = fmaf(wt, v[k].y, acc.y);
+            acc.z = fmaf(wt, v[k].z, acc.z);
+            acc.w = fmaf(wt, v[k].w, acc.w);
         }
         mx = nmx;
     };
-    // the first pass in straight-line code: its loads go out together with
-    // the length's; later passes (lists longer than kMergePass) follow
     load(0);
     const int n = min(n_list, max_hunits);
     consume(0, n);
-    for (int p0 = kMergePass; p0 < n; p0 += kMergePass) {  // uniform
+    for (int p0 = PP; p0 < n; p0 += PP) {  // uniform; lists longer than one pass
         __syncthreads();  // s_st and s_red are rewritten
         load(p0);
         consume(p0, n);
     }
-    s_sum[grp][jd] = acc;
+    // value sums: lanes l, l + 8, ..., l + 56 of a wave hold the same four
+    // dims; then the waves in order
+#pragma unroll
+    for (int off = kMergeQuads; off < kWave; off <<= 1) {
+        acc.x += __shfl_xor(acc.x, off);
+        acc.y += __shfl_xor(acc.y, off);
+        acc.z += __shfl_xor(acc.z, off);
+        acc.w += __shfl_xor(acc.w, off);
+    }
+    if (lane < kMergeQuads) s_acc[w][lane] = acc;
     for (int off = kWave / 2; off > 0; off >>= 1) lsum += __shfl_xor(lsum, off);
     if (lane == 0) s_red[1][w] = lsum;
     __syncthreads();
-    if (tid < kMergeDims) {
-        float o = 0.f, L = 0.f;
+    if (tid < kMergeQuads) {
+        float4 o = s_acc[0][tid];
 #pragma unroll
-        for (int g2 = 0; g2 < kMergeGroups; ++g2) o += s_sum[g2][tid];
+        for (int k = 1; k < NW; ++k) {
+            o.x += s_acc[k][tid].x;
+            o.y += s_acc[k][tid].y;
+            o.z += s_acc[k][tid].z;
+            o.w += s_acc[k][tid].w;
+        }
+        float L = 0.f;
 #pragma unroll
         for (int k = 0; k < NW; ++k) L += s_red[1][k];
-        out[static_cast<size_t>(bhq) * D + blockIdx.y * kMergeDims + tid] = o / L;
+        const float inv = 1.f / L;
+        *reinterpret_cast<float4*>(out + static_cast<size_t>(bhq) * D + blockIdx.y * kMergeDims + 4 * tid) =
+            make_float4(o.x * inv, o.y * inv, o.z * inv, o.w * inv);
     }
 }
 
@@ -1146,13 +1165,25 @@ hipError_t launch_attend(const AttendArgs& a, hipStream_t s) {
 hipError_t launch_merge(const AttendArgs& a, hipStream_t s) {
     if (a.d % kMergeDims != 0) return hipErrorInvalidValue;
     const dim3 grid(a.B * a.Hq, a.d / kMergeDims);
-    if (a.dense)
-        k_merge<true><<<grid, kMergeThreads, 0, s>>>(a.part_o, a.part_ml, nullptr, a.max_chunks, a.Hkv, a.Hq,
-                                                     a.max_hunits, a.d, a.out);
-    else
-        k_merge<false><<<grid, kMergeThreads, 0, s>>>(a.part_o, a.part_ml,
-                                                      reinterpret_cast<const PlanHeader*>(a.ws + a.lay->hdr), 0,
-                                                      a.Hkv, a.Hq, a.max_hunits, a.d, a.out);
+    // positions per pass: enough for the longest list the step can have, up
+    // to 640 (longer lists take several passes)
+    const int longest = a.dense ? a.max_chunks : a.max_hunits;
+    const PlanHeader* hdr = a.dense ? nullptr : reinterpret_cast<const PlanHeader*>(a.ws + a.lay->hdr);
+    const int nd = a.dense ? a.max_chunks : 0;
+#define SANTAPP_MERGE(DN, NPL)                                                                      \
+    k_merge<DN, NPL><<<grid, kMergeThreads, 0, s>>>(a.part_o, a.part_ml, hdr, nd, a.Hkv, a.Hq, \
+                                                    a.max_hunits, a.d, a.out)
+    const int npl = longest <= 5 * kMergeRowsPerLoad ? 5 : longest <= 10 * kMergeRowsPerLoad ? 10 : 20;
+    if (a.dense) {
+        if (npl == 5) SANTAPP_MERGE(true, 5);
+        else if (npl == 10) SANTAPP_MERGE(true, 10);
+        else SANTAPP_MERGE(true, 20);
+    } else {
+        if (npl == 5) SANTAPP_MERGE(false, 5);
+        else if (npl == 10) SANTAPP_MERGE(false, 10);
+        else SANTAPP_MERGE(false, 20);
+    }
+#undef SANTAPP_MERGE
     return hipGetLastError();
 }
 

@@ -81,7 +81,7 @@ struct PlanHeader {
 // length of each head's partial-state list.
 struct DecodeLayout {
     int max_chunks = 0, max_hunits = 0;
-    size_t phi = 0, Y = 0, lc = 0, hdr = 0, chunk = 0, ulogc = 0, po = 0,
+    size_t phi = 0, Y = 0, lc = 0, lpos = 0, hdr = 0, chunk = 0, ulogc = 0, po = 0,
            pml = 0, total = 0;
 };
 

@@ -35,6 +35,7 @@ constexpr int kRouteTeams = kRouteThreads / 16;  // one representative per 16-la
 constexpr int kSelectThreads = 512;
 constexpr int kSelectWaves = kSelectThreads / kWave;
 constexpr int kFineBits = 16;                 // value-histogram resolution of the sampler
+constexpr int kSelectUnits = 4096;            // units of a plan pass resolved through an LDS table
 
 template <typename T, int DPL>
 struct RepChunk;
@@ -414,36 +415,55 @@ template <int G, int PL>
 __global__ __launch_bounds__(kSelectThreads) void k_select(
     const double* __restrict__ phi, const double* __restrict__ Y, const int* __restrict__ team_begin,
     const int* __restrict__ team_size, int M, int Hkv, int Hq, int Kp, int T_suf, int max_chunks,
-    float* __restrict__ lc, PlanHeader* __restrict__ hdr,
+    float* __restrict__ lc, unsigned short* __restrict__ lpos, PlanHeader* __restrict__ hdr,
     Chunk* __restrict__ chunks, float* __restrict__ ulogc, int* __restrict__ dbg_sel,
     float* __restrict__ dbg_logc, double* __restrict__ dbg_tau, int* __restrict__ dbg_uteams,
     int* __restrict__ dbg_urows) {
-    constexpr bool kLdsLc = PL > 0 && PL <= 8;  // log c of every (head, team) in LDS
-    extern __shared__ float s_lc[];  // [G][M] when kLdsLc
+    // per (head, team): log c and the team's first position in the head's
+    // list of units, in LDS for small team counts, else in the workspace
+    constexpr bool kLds = PL > 0 && PL <= 8;
+    extern __shared__ float s_dyn[];  // [G][M] floats, then [G][M] ushorts, when kLds
     __shared__ __align__(16) uint32_t s_hist[kSelectWaves][256];
     __shared__ __align__(16) uint64_t s_cand[kSelectWaves][kWave];
     __shared__ uint64_t s_bits[kMaxGroup][kMaxTeams / kWave];  // selection bits per head
-    __shared__ __align__(16) int s_w[(3 + kMaxGroup) * kSelectWaves];
-    __shared__ int4 s_team[kSelectThreads];  // union teams of one pass: first unit, begin, size, heads
-    __shared__ unsigned short s_tpos[kSelectThreads][kMaxGroup];  // first position in each head's list
+    __shared__ __align__(16) int s_w[3 * kSelectWaves];
+    __shared__ int s_hunits[kMaxGroup];  // units of each head's teams
+    __shared__ int s_size[kSelectThreads];  // sizes of the first kSelectThreads teams
+    __shared__ int4 s_team[kSelectThreads];  // union teams of a pass: first unit, begin, size, heads
+    __shared__ int s_tg[kSelectThreads];     // their team indices
+    __shared__ unsigned short s_u2t[kSelectUnits];  // union slot of each unit of a pass
 
     const int bh = blockIdx.x;
     const int b = bh / Hkv, kv = bh - b * Hkv;
     const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
     const size_t tb0 = static_cast<size_t>(bh) * M;
+    const size_t hq0 = static_cast<size_t>(b) * Hq + kv * G;  // first query head of the pair
+    float* const s_lc = s_dyn;
+    unsigned short* const s_pos = reinterpret_cast<unsigned short*>(s_dyn + G * M);
+    auto lc_at = [&](int h, int g) -> float& {
+        if constexpr (kLds) return s_lc[h * M + g];
+        else return lc[(hq0 + h) * M + g];
+    };
+    auto pos_at = [&](int h, int g) -> unsigned short& {
+        if constexpr (kLds) return s_pos[h * M + g];
+        else return lpos[(hq0 + h) * M + g];
+    };
 
-    // team sizes and starts of the first chunk of teams, fetched while the
-    // heads select
+    // loads first: team sizes and starts of the first kSelectThreads teams,
+    // and each head wave's perturbed scores; the sizes go to LDS for the
+    // heads' list positions
     const int gc0 = min(tid, M - 1);
     const int size0 = team_size[tb0 + gc0];
     const int begin0 = team_begin[tb0 + gc0];
-    // (no barrier before the selection: nothing in LDS needs clearing)
+    const int hq = kv * G + min(w, G - 1);
+    const size_t hoff = (static_cast<size_t>(b) * Hq + hq) * M;
+    KeySet<PL> ks;
+    if (w < G) ks.init(Y + hoff, phi + hoff, M);
+    s_size[tid] = size0;
+    __syncthreads();
+    auto size_of = [&](int g) { return g < kSelectThreads ? s_size[g] : team_size[tb0 + g]; };
 
     if (w < G) {
-        const int hq = kv * G + w;
-        const size_t hoff = (static_cast<size_t>(b) * Hq + hq) * M;
-        KeySet<PL> ks;
-        ks.init(Y + hoff, phi + hoff, M);
         const int nj = ks.count();
         const uint64_t tkey = select_key<PL>(ks, Kp, s_hist[w], s_cand[w]);
         const double tau = key_value(tkey);
@@ -455,13 +475,35 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
 
         // selection in index order i = j * 64 + lane: the keys above tau's
         // key and the first need_ties keys equal to it (exactly equal Y
-        // values; the tie path is kept out of the common loop)
+        // values; the tie path is kept out of the common loop), compacted
+        // in team order into batches of 64 (LDS)
         const uint64_t lt = lanemask_lt();
-        const bool compact = Kp <= kWave;  // log c once per selected team, one lane each
         uint32_t* cidx = reinterpret_cast<uint32_t*>(s_cand[w]);  // [64] team index
         float* cx = reinterpret_cast<float*>(s_cand[w]) + kWave;  // [64] phi - tau
+        int nsel = 0, npos = 0;
+        // per batch of 64 selected teams, one per lane in team order: log c
+        // and the team's first position in the head's list (a scan of the
+        // selected teams' unit counts)
+        auto flush = [&](int cnt) {
+            wave_lds_sync();
+            const bool on = lane < cnt;
+            const int i = on ? static_cast<int>(cidx[lane]) : 0;
+            const int nc = on ? chunk_count(size_of(i)) : 0;
+            const int incl = wave_incl_scan(nc);
+            if (on) {
+                const float v = log_inclusion(cx[lane]);
+                lc_at(w, i) = v;
+                pos_at(w, i) = static_cast<unsigned short>(npos + incl - nc);
+                const size_t r = (static_cast<size_t>(b) * Hq + hq) * Kp + nsel + lane;
+                if (dbg_sel) dbg_sel[r] = i;
+                if (dbg_logc) dbg_logc[r] = v;
+            }
+            npos += __builtin_amdgcn_readlane(incl, kWave - 1);
+            nsel += cnt;
+            wave_lds_sync();  // cidx / cx are refilled
+        };
         auto select_pass = [&](auto with_ties) {
-            int nsel = 0, nties = 0;
+            int nties = 0, fill = 0;
 #pragma unroll
             for (int j = 0; j < nj; ++j) {
                 const bool valid = ks.valid(j);
@@ -475,57 +517,41 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
                 }
                 const uint64_t sb = __ballot(sel);
                 if (lane == 0) s_bits[w][j] = sb;
-                if (compact && sel) {
-                    const int pos = nsel + __popcll(sb & lt);
-                    cidx[pos] = static_cast<uint32_t>(j * kWave + lane);
-                    cx[pos] = static_cast<float>(ks.phi(j) - tau);
+                const int cnt = __popcll(sb);
+                if (fill + cnt > kWave) {  // uniform: the batch is full
+                    flush(fill);
+                    fill = 0;
                 }
-                nsel += __popcll(sb);
+                if (sel) {
+                    const int p = fill + __popcll(sb & lt);
+                    cidx[p] = static_cast<uint32_t>(j * kWave + lane);
+                    cx[p] = static_cast<float>(ks.phi(j) - tau);
+                }
+                fill += cnt;
             }
+            if (fill > 0) flush(fill);
         };
         if (need_ties > 0)  // uniform
             select_pass(std::true_type{});
         else
             select_pass(std::false_type{});
-        wave_lds_sync();
-        if (compact) {
-            if (lane < Kp) {
-                const int i = static_cast<int>(cidx[lane]);
-                const float v = log_inclusion(cx[lane]);
-                if constexpr (kLdsLc)
-                    s_lc[w * M + i] = v;
-                else
-                    lc[hoff + i] = v;
-                if (dbg_sel) dbg_sel[(static_cast<size_t>(b) * Hq + hq) * Kp + lane] = i;
-                if (dbg_logc) dbg_logc[(static_cast<size_t>(b) * Hq + hq) * Kp + lane] = v;
-            }
-        } else {
-            // large budgets: every lane its selected keys, from the ballots
-            int nsel = 0;
-            for (int j = 0; j < nj; ++j) {
-                const uint64_t sb = s_bits[w][j];
-                if ((sb >> lane) & 1ull) {
-                    const int i = j * kWave + lane;
-                    const int pos = nsel + __popcll(sb & lt);
-                    const float v = log_inclusion(static_cast<float>(ks.phi(j) - tau));
-                    if constexpr (kLdsLc)
-                        s_lc[w * M + i] = v;
-                    else
-                        lc[hoff + i] = v;
-                    if (dbg_sel) dbg_sel[(static_cast<size_t>(b) * Hq + hq) * Kp + pos] = i;
-                    if (dbg_logc) dbg_logc[(static_cast<size_t>(b) * Hq + hq) * Kp + pos] = v;
-                }
-                nsel += __popcll(sb);
-            }
+        if (lane == 0) {
+            s_hunits[w] = npos;
+            if (dbg_tau) dbg_tau[static_cast<size_t>(b) * Hq + hq] = tau;
         }
-        if (lane == 0 && dbg_tau) dbg_tau[static_cast<size_t>(b) * Hq + hq] = tau;
     }
     __syncthreads();
 
     // ---- union of the heads' selections in ascending team order -------------
-    // per union team: its corrections, then its units of <= kChunkRows rows,
-    // appended to the list shared by all (b, kv) pairs at a range claimed
-    // with one atomic add
+    // One pass per kSelectThreads teams, thread tid owning team base + tid: a
+    // scan gives every union team its slot, its first unit and its rows; the
+    // team writes its corrections and enters itself in LDS (its record, and
+    // its slot at each of its units); then thread c writes unit c of the
+    // pass to the pair's own region of the unit list (max_chunks entries,
+    // which bound the units of any union of this size).  Passes whose units
+    // exceed the LDS table fall back to a search over the records.  A unit's
+    // position in the list of a head that reads it is the team's first
+    // position there plus the unit's index within the team.
     auto heads_of = [&](int g) {
         int hm = 0;
         if (g < M) {
@@ -534,36 +560,8 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
         }
         return hm;
     };
-    auto write_logc = [&](int g, int slot, int hm) {
-        float v[kLogcStride];
-#pragma unroll
-        for (int h = 0; h < kLogcStride; ++h) {
-            float t = 0.f;
-            if (h < G && ((hm >> h) & 1)) {
-                if constexpr (kLdsLc)
-                    t = s_lc[h * M + g];
-                else
-                    t = lc[(static_cast<size_t>(b) * Hq + kv * G + h) * M + g];
-            }
-            v[h] = t;
-        }
-        float4* L = reinterpret_cast<float4*>(ulogc + (tb0 + slot) * kLogcStride);
-        L[0] = make_float4(v[0], v[1], v[2], v[3]);
-        L[1] = make_float4(v[4], v[5], v[6], v[7]);
-    };
-    const int nsc = chunk_count(T_suf);
-    // One pass per kSelectThreads teams, thread tid owning team base + tid:
-    // a scan gives every union team its slot, its first unit, and its first
-    // position in the list of each head that selected it; a unit's team is
-    // the last union team whose first unit is at or before it.  The units go
-    // to the pair's own region of the list (max_chunks entries, which bound
-    // the units of any union of this size).
-    constexpr int NV = 3 + G;
     Chunk* const cb = chunks + static_cast<size_t>(bh) * max_chunks;
     int run_u = 0, run_rows = 0, run_c = 0;
-    int run_h[G];
-#pragma unroll
-    for (int h = 0; h < G; ++h) run_h[h] = 0;
     for (int base = 0; base < M; base += kSelectThreads) {
         const int g = base + tid;
         int tsz = size0, tbeg = begin0;
@@ -575,43 +573,53 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
         const int hm = heads_of(g);
         const int f = hm ? 1 : 0;
         const int nc = f ? chunk_count(tsz) : 0;
-        int x[NV];
-        x[0] = f;
-        x[1] = nc;
-        x[2] = f ? tsz : 0;
-#pragma unroll
-        for (int h = 0; h < G; ++h) x[3 + h] = ((hm >> h) & 1) ? nc : 0;
-        int ex[NV], tot[NV];
-        block_scan<NV>(x, ex, tot, s_w);
+        const int x[3] = {f, nc, f ? tsz : 0};
+        int ex[3], tot[3];
+        block_scan<3>(x, ex, tot, s_w);
+        const bool table = tot[1] <= kSelectUnits;  // uniform
         if (f) {
-            write_logc(g, run_u + ex[0], hm);
-            s_team[ex[0]] = make_int4(ex[1], tbeg, tsz, hm);
+            const int slot = ex[0];
+            float lv[kLogcStride];
 #pragma unroll
-            for (int h = 0; h < kMaxGroup; ++h)
-                s_tpos[ex[0]][h] = static_cast<unsigned short>(h < G ? run_h[h] + ex[3 + h] : 0);
+            for (int h = 0; h < kMaxGroup; ++h) lv[h] = (h < G && ((hm >> h) & 1)) ? lc_at(h, g) : 0.f;
+            float4* L = reinterpret_cast<float4*>(ulogc + (tb0 + run_u + slot) * kLogcStride);
+            L[0] = make_float4(lv[0], lv[1], lv[2], lv[3]);
+            L[1] = make_float4(lv[4], lv[5], lv[6], lv[7]);
+            s_team[slot] = make_int4(ex[1], tbeg, tsz, hm);
+            s_tg[slot] = g;
+            if (table)
+                for (int c = 0; c < nc; ++c) s_u2t[ex[1] + c] = static_cast<unsigned short>(slot);
         }
         __syncthreads();
         for (int c = tid; c < tot[1]; c += kSelectThreads) {
-            int lo = 0, hi = tot[0] - 1;
-            while (lo < hi) {
-                const int mid = (lo + hi + 1) >> 1;
-                if (s_team[mid].x <= c)
-                    lo = mid;
-                else
-                    hi = mid - 1;
+            int slot;
+            if (table) {
+                slot = s_u2t[c];
+            } else {  // the last record whose first unit is at or before c
+                int lo = 0, hi = tot[0] - 1;
+                while (lo < hi) {
+                    const int mid = (lo + hi + 1) >> 1;
+                    if (s_team[mid].x <= c)
+                        lo = mid;
+                    else
+                        hi = mid - 1;
+                }
+                slot = lo;
             }
-            const int4 tm = s_team[lo];
+            const int4 tm = s_team[slot];
+            const int gg = s_tg[slot];
             const int p = c - tm.x;
             const int ci = run_c + c;
             if (ci < max_chunks) {
                 Chunk ch;
                 ch.begin = tm.y + p * kChunkRows;
-                ch.slot = run_u + lo;
+                ch.slot = run_u + slot;
                 ch.meta = chunk_meta(min(kChunkRows, tm.z - p * kChunkRows), tm.w, bh);
                 ch.ci = ci;
                 int ps[kMaxGroup];
 #pragma unroll
-                for (int h = 0; h < kMaxGroup; ++h) ps[h] = ((tm.w >> h) & 1) ? s_tpos[lo][h] + p : 0;
+                for (int h = 0; h < kMaxGroup; ++h)
+                    ps[h] = (h < G && ((tm.w >> h) & 1)) ? static_cast<int>(pos_at(h, gg)) + p : 0;
                 set_chunk_pos(ch, ps);
                 cb[ci] = ch;
             }
@@ -619,10 +627,9 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
         run_u += tot[0];
         run_c += tot[1];
         run_rows += tot[2];
-#pragma unroll
-        for (int h = 0; h < G; ++h) run_h[h] += tot[3 + h];
-        if (base + kSelectThreads < M) __syncthreads();  // s_team is rewritten by the next pass
+        if (base + kSelectThreads < M) __syncthreads();  // the LDS records are rewritten by the next pass
     }
+    const int nsc = chunk_count(T_suf);
     const int utotal = min(run_c + nsc, max_chunks);
     // the suffix: every head, no correction, after each head's teams
     for (int p = tid; p < nsc; p += kSelectThreads) {
@@ -635,7 +642,7 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
             ch.ci = ci;
             int ps[kMaxGroup];
 #pragma unroll
-            for (int h = 0; h < kMaxGroup; ++h) ps[h] = h < G ? run_h[h] + p : 0;
+            for (int h = 0; h < kMaxGroup; ++h) ps[h] = h < G ? s_hunits[h] + p : 0;
             set_chunk_pos(ch, ps);
             cb[ci] = ch;
         }
@@ -647,7 +654,7 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
         ph.chunks = utotal;
         ph.pad = 0;
 #pragma unroll
-        for (int h = 0; h < kMaxGroup; ++h) ph.hunits[h] = h < G ? run_h[h] + nsc : 0;
+        for (int h = 0; h < kMaxGroup; ++h) ph.hunits[h] = h < G ? s_hunits[h] + nsc : 0;
         hdr[bh] = ph;
         if (dbg_uteams) dbg_uteams[bh] = run_u;
         if (dbg_urows) dbg_urows[bh] = run_rows;
@@ -670,9 +677,9 @@ hipError_t route_g(const RouteArgs& a, hipStream_t s) {
     float* ulogc = reinterpret_cast<float*>(a.ws + L.ulogc);
 #define SANTAPP_SEL(PLV)                                                                          \
     k_select<G, PLV><<<a.B * a.Hkv, kSelectThreads,                                               \
-                       (PLV > 0 && PLV <= 8) ? sizeof(float) * G * a.M : 0, s>>>(                \
+                       (PLV > 0 && PLV <= 8) ? (sizeof(float) + sizeof(unsigned short)) * G * a.M : 0, s>>>( \
         phi, Y, a.team_begin, a.team_size, a.M, a.Hkv, a.Hq, a.Kp, a.T, L.max_chunks, lc,       \
-        hdr,                                     \
+        reinterpret_cast<unsigned short*>(a.ws + L.lpos), hdr,                                  \
         ch, ulogc, d ? d->sel : nullptr, d ? d->logc : nullptr, d ? d->tau : nullptr,             \
         d ? d->union_teams : nullptr, d ? d->union_rows : nullptr)
     if (a.M <= 8 * kWave)
