@@ -21,6 +21,7 @@
 //           atomics.
 #include <math.h>
 
+#include <atomic>
 #include <type_traits>
 
 #include "common.h"
@@ -180,6 +181,7 @@ struct KeySet {
 
 template <>
 struct KeySet<0> {
+    static constexpr bool kPhiRegs = false;
     const double* y;
     const double* p;
     int M;
@@ -419,16 +421,17 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
     Chunk* __restrict__ chunks, float* __restrict__ ulogc, int* __restrict__ dbg_sel,
     float* __restrict__ dbg_logc, double* __restrict__ dbg_tau, int* __restrict__ dbg_uteams,
     int* __restrict__ dbg_urows) {
-    // per (head, team): log c and the team's first position in the head's
-    // list of units, in LDS for small team counts, else in the workspace
-    constexpr bool kLds = PL > 0 && PL <= 8;
-    extern __shared__ float s_dyn[];  // [G][M] floats, then [G][M] ushorts, when kLds
+    // Team sizes and starts, and per (head, team) log c and the team's
+    // first position in the head's list of units: in LDS up to
+    // kSelectLdsTeams teams, else sizes and starts are read from the table
+    // and the per-head values go to the workspace.
+    constexpr bool kLds = PL > 0;
+    extern __shared__ int s_dyn[];  // kLds: [M] sizes, [M] starts, [G][M] floats, [G][M] ushorts
     __shared__ __align__(16) uint32_t s_hist[kSelectWaves][256];
     __shared__ __align__(16) uint64_t s_cand[kSelectWaves][kWave];
     __shared__ uint64_t s_bits[kMaxGroup][kMaxTeams / kWave];  // selection bits per head
     __shared__ __align__(16) int s_w[3 * kSelectWaves];
     __shared__ int s_hunits[kMaxGroup];  // units of each head's teams
-    __shared__ int s_size[kSelectThreads];  // sizes of the first kSelectThreads teams
     __shared__ int4 s_team[kSelectThreads];  // union teams of a pass: first unit, begin, size, heads
     __shared__ int s_tg[kSelectThreads];     // their team indices
     __shared__ unsigned short s_u2t[kSelectUnits];  // union slot of each unit of a pass
@@ -438,8 +441,10 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
     const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
     const size_t tb0 = static_cast<size_t>(bh) * M;
     const size_t hq0 = static_cast<size_t>(b) * Hq + kv * G;  // first query head of the pair
-    float* const s_lc = s_dyn;
-    unsigned short* const s_pos = reinterpret_cast<unsigned short*>(s_dyn + G * M);
+    int* const s_size = s_dyn;
+    int* const s_begin = s_dyn + M;
+    float* const s_lc = reinterpret_cast<float*>(s_dyn + 2 * M);
+    unsigned short* const s_pos = reinterpret_cast<unsigned short*>(s_lc + G * M);
     auto lc_at = [&](int h, int g) -> float& {
         if constexpr (kLds) return s_lc[h * M + g];
         else return lc[(hq0 + h) * M + g];
@@ -449,19 +454,33 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
         else return lpos[(hq0 + h) * M + g];
     };
 
-    // loads first: team sizes and starts of the first kSelectThreads teams,
-    // and each head wave's perturbed scores; the sizes go to LDS for the
-    // heads' list positions
-    const int gc0 = min(tid, M - 1);
-    const int size0 = team_size[tb0 + gc0];
-    const int begin0 = team_begin[tb0 + gc0];
+    // loads first: the team table (into LDS) and each head wave's perturbed
+    // scores
     const int hq = kv * G + min(w, G - 1);
     const size_t hoff = (static_cast<size_t>(b) * Hq + hq) * M;
     KeySet<PL> ks;
     if (w < G) ks.init(Y + hoff, phi + hoff, M);
-    s_size[tid] = size0;
+    if constexpr (kLds) {
+        constexpr int NT = (PL * kWave + kSelectThreads - 1) / kSelectThreads;  // teams per thread
+        int sz[NT], bg[NT];
+#pragma unroll
+        for (int k = 0; k < NT; ++k) {
+            const int g = min(tid + k * kSelectThreads, M - 1);
+            sz[k] = team_size[tb0 + g];
+            bg[k] = team_begin[tb0 + g];
+        }
+#pragma unroll
+        for (int k = 0; k < NT; ++k) {
+            const int g = tid + k * kSelectThreads;
+            if (g < M) {
+                s_size[g] = sz[k];
+                s_begin[g] = bg[k];
+            }
+        }
+    }
     __syncthreads();
-    auto size_of = [&](int g) { return g < kSelectThreads ? s_size[g] : team_size[tb0 + g]; };
+    auto size_of = [&](int g) { return kLds ? s_size[g] : team_size[tb0 + g]; };
+    auto begin_of = [&](int g) { return kLds ? s_begin[g] : team_begin[tb0 + g]; };
 
     if (w < G) {
         const int nj = ks.count();
@@ -488,10 +507,13 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
             wave_lds_sync();
             const bool on = lane < cnt;
             const int i = on ? static_cast<int>(cidx[lane]) : 0;
+            // phi - tau: kept from the pass when phi sits in registers, else
+            // one gather per batch
+            const float x = KeySet<PL>::kPhiRegs ? cx[lane] : static_cast<float>(phi[hoff + i] - tau);
             const int nc = on ? chunk_count(size_of(i)) : 0;
             const int incl = wave_incl_scan(nc);
             if (on) {
-                const float v = log_inclusion(cx[lane]);
+                const float v = log_inclusion(x);
                 lc_at(w, i) = v;
                 pos_at(w, i) = static_cast<unsigned short>(npos + incl - nc);
                 const size_t r = (static_cast<size_t>(b) * Hq + hq) * Kp + nsel + lane;
@@ -525,7 +547,7 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
                 if (sel) {
                     const int p = fill + __popcll(sb & lt);
                     cidx[p] = static_cast<uint32_t>(j * kWave + lane);
-                    cx[p] = static_cast<float>(ks.phi(j) - tau);
+                    if constexpr (KeySet<PL>::kPhiRegs) cx[p] = static_cast<float>(ks.phi(j) - tau);
                 }
                 fill += cnt;
             }
@@ -564,12 +586,8 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
     int run_u = 0, run_rows = 0, run_c = 0;
     for (int base = 0; base < M; base += kSelectThreads) {
         const int g = base + tid;
-        int tsz = size0, tbeg = begin0;
-        if (base > 0) {
-            const int gc = min(g, M - 1);
-            tsz = team_size[tb0 + gc];
-            tbeg = team_begin[tb0 + gc];
-        }
+        const int gc = min(g, M - 1);
+        const int tsz = size_of(gc), tbeg = begin_of(gc);
         const int hm = heads_of(g);
         const int f = hm ? 1 : 0;
         const int nc = f ? chunk_count(tsz) : 0;
@@ -661,6 +679,22 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
     }
 }
 
+// Raise a kernel's dynamic LDS limit to `bytes` (once per kernel and limit;
+// the select kernel keeps up to ~115 KB of team tables in LDS).
+template <typename F>
+hipError_t allow_dynamic_lds(F* kernel, size_t bytes) {
+    static std::atomic<size_t> granted{0};
+    if (bytes <= granted.load(std::memory_order_relaxed)) return hipSuccess;
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(bytes));
+    if (e == hipSuccess) {
+        size_t cur = granted.load(std::memory_order_relaxed);
+        while (bytes > cur && !granted.compare_exchange_weak(cur, bytes)) {
+        }
+    }
+    return e;
+}
+
 template <typename T, int D, int G>
 hipError_t route_g(const RouteArgs& a, hipStream_t s) {
     const DecodeLayout& L = *a.lay;
@@ -676,12 +710,16 @@ hipError_t route_g(const RouteArgs& a, hipStream_t s) {
     Chunk* ch = reinterpret_cast<Chunk*>(a.ws + L.chunk);
     float* ulogc = reinterpret_cast<float*>(a.ws + L.ulogc);
 #define SANTAPP_SEL(PLV)                                                                          \
-    k_select<G, PLV><<<a.B * a.Hkv, kSelectThreads,                                               \
-                       (PLV > 0 && PLV <= 8) ? (sizeof(float) + sizeof(unsigned short)) * G * a.M : 0, s>>>( \
-        phi, Y, a.team_begin, a.team_size, a.M, a.Hkv, a.Hq, a.Kp, a.T, L.max_chunks, lc,       \
-        reinterpret_cast<unsigned short*>(a.ws + L.lpos), hdr,                                  \
-        ch, ulogc, d ? d->sel : nullptr, d ? d->logc : nullptr, d ? d->tau : nullptr,             \
-        d ? d->union_teams : nullptr, d ? d->union_rows : nullptr)
+    do {                                                                                          \
+        const size_t dyn = PLV > 0 ? (2 * sizeof(int) + (sizeof(float) + sizeof(unsigned short)) * G) * a.M : 0; \
+        hipError_t ea = allow_dynamic_lds(k_select<G, PLV>, dyn);                                 \
+        if (ea != hipSuccess) return ea;                                                          \
+        k_select<G, PLV><<<a.B * a.Hkv, kSelectThreads, dyn, s>>>(                                \
+            phi, Y, a.team_begin, a.team_size, a.M, a.Hkv, a.Hq, a.Kp, a.T, L.max_chunks, lc,   \
+            reinterpret_cast<unsigned short*>(a.ws + L.lpos), hdr, ch, ulogc, d ? d->sel : nullptr, \
+            d ? d->logc : nullptr, d ? d->tau : nullptr, d ? d->union_teams : nullptr,            \
+            d ? d->union_rows : nullptr);                                                         \
+    } while (0)
     if (a.M <= 8 * kWave)
         SANTAPP_SEL(8);
     else if (a.M <= 32 * kWave)
