@@ -47,6 +47,9 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="budget of the oracle CPU-baseline sample (0 disables it)")
     p.add_argument("--no-dense", action="store_true")
+    p.add_argument("--calibrate-copy", action="store_true",
+                   help="only run a plain 256 MiB device-to-device copy five times (the reference "
+                        "kernel for scaling the FETCH_SIZE / WRITE_SIZE counters) and exit")
     return p.parse_args()
 
 
@@ -66,6 +69,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
     sp._lib.load()  # raises when the HIP library is not built
 
     wl = datagen.WORKLOADS[args.workload]
@@ -239,6 +245,21 @@ class HipEvents:
         if self.L.hipEventElapsedTime(self.c.byref(t), a, b) != 0:
             raise RuntimeError("hipEventElapsedTime failed")
         return t.value * 1e3
+
+
+def calibrate_copy():
+    """A plain copy of known size: 256 MiB read and 256 MiB written per
+    launch (torch's device-to-device copy kernel), five launches."""
+    import torch
+    n = 64 << 20  # floats
+    src = torch.empty(n, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibrate_copy": {"bytes_read": n * 4, "bytes_written": n * 4, "launches": 5}}),
+          flush=True)
 
 
 def upload(batch):

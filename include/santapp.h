@@ -112,9 +112,11 @@ santapp_status santapp_budget_to_K(int S, int P, int R, int M, int* K);
 
 /* Optional diagnostic outputs of santapp_decode (device pointers; each may be
  * NULL).  The arrays are written only when the step samples (K < M).
- * events[0..3], when non-NULL, are hipEvent_t handles created by the caller;
- * the call records them on `stream` before the routing/sampling kernels,
- * before the attention kernel, before the merge kernel and after it, so that
+ * events[0..3], when non-NULL, are hipEvent_t handles created by the caller:
+ * events[0] is recorded on `stream` before the routing/sampling kernels,
+ * events[1] and events[2] are stamped by the attention kernel's launch at
+ * that kernel's start and end (its execution time, without the dispatch gap
+ * before it), and events[3] is recorded after the merge kernel, so that
  * hipEventElapsedTime gives the time of each stage. */
 typedef struct {
     double* phi;      /* [B,Hq,M] routing logits log n_g + scale q.l_g          */

@@ -423,9 +423,13 @@ santapp_status santapp_decode(const santapp_teams* t, const float* q, const void
             return hip_fail(e, "debug copy");
         A.dense = false;
     }
-    if ((e = mark(1)) != hipSuccess) return hip_fail(e, "event record");
+    // events 1 and 2 are stamped by the attention kernel's launch itself,
+    // at the kernel's start and end
+    if (dbg) {
+        A.ev_start = static_cast<hipEvent_t>(dbg->events[1]);
+        A.ev_stop = static_cast<hipEvent_t>(dbg->events[2]);
+    }
     if ((e = launch_attend(A, s)) != hipSuccess) return hip_fail(e, "attention kernel");
-    if ((e = mark(2)) != hipSuccess) return hip_fail(e, "event record");
     if ((e = launch_merge(A, s)) != hipSuccess) return hip_fail(e, "merge kernel");
     if ((e = mark(3)) != hipSuccess) return hip_fail(e, "event record");
     return ok();

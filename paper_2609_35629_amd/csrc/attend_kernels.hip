@@ -30,6 +30,8 @@
 
 #include <algorithm>
 
+#include <hip/hip_ext.h>
+
 #include "common.h"
 #include "internal.h"
 
@@ -917,11 +919,12 @@ __global__ __launch_bounds__(kAttendWaves * kWave, 1) void k_attend_mfma(
 // A pass covers 32 NPL positions: thread t loads the states of positions
 // t, t + 256, ... (to LDS, weights computed once per position) and 16 bytes
 // of values (four dims) of positions t / 8 + 32 k, k < NPL, so a pass is
-// NPL + 1 loads per thread, all issued before any is used (the sampled
-// path's list length travels with them; positions past it are masked).  The
-// host picks NPL from the longest list a step can have, so one pass covers
-// every list in the common case.  The value sums reduce over the 32
-// position groups in a fixed order.
+// NPL + 1 loads per thread, all issued before any is used.  Positions are
+// clamped to the list (the sampled path reads its list length from the
+// plan header first), so a pass reads each of the list's states once
+// whatever NPL is; the host picks NPL from the longest list a step can
+// have, so one pass covers every list in the common case.  The value sums
+// reduce over the 32 position groups in a fixed order.
 constexpr int kMergeDims = 32;
 constexpr int kMergeQuads = kMergeDims / 4;             // threads per position (16 bytes each)
 constexpr int kMergeRowsPerLoad = kMergeThreads / kMergeQuads;  // positions per load instruction (32)
@@ -948,13 +951,10 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(const float* __restrict
     const size_t row0 = (static_cast<size_t>(bh) * G + h) * max_hunits;
     const float2* ml = reinterpret_cast<const float2*>(part_ml) + row0;
     const float* po = part_o + row0 * D + blockIdx.y * kMergeDims + 4 * dq;
-    // the list length as a vector load (the index is 0 on every lane, but
-    // not provably uniform), so that it travels with the pass's loads
-    int n_list = n_dense;
-    if (!DENSE) n_list = hdr[bh].hunits[h + static_cast<int>(__builtin_amdgcn_mbcnt_lo(0u, 0u))];
-    // positions the loads may touch: the list on the dense path, the list's
-    // capacity on the sampled path
-    const int lim = DENSE ? min(n_dense, max_hunits) : max_hunits;
+    // the list length (a uniform load of the plan header on the sampled
+    // path); the loads touch only the list's positions
+    const int n_list = DENSE ? n_dense : hdr[bh].hunits[h];
+    const int lim = max(1, min(n_list, max_hunits));
 
     float mx = kNeg, lsum = 0.f;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -1054,6 +1054,18 @@ __global__ void k_zero(uint4* __restrict__ p, size_t n16, unsigned char* __restr
     if (blockIdx.x == 0 && static_cast<int>(threadIdx.x) < ntail) tail[threadIdx.x] = 0;
 }
 
+// Launch an attention kernel; with stage events, the launch itself stamps
+// them at the kernel's start and end (so they time the kernel's execution,
+// not the dispatch gap before it).
+template <typename F, typename... Args>
+hipError_t launch_timed(const AttendArgs& a, F kernel, dim3 grid, dim3 block, hipStream_t s, Args... args) {
+    if (a.ev_start || a.ev_stop)
+        hipExtLaunchKernelGGL(kernel, grid, block, 0, s, a.ev_start, a.ev_stop, 0, args...);
+    else
+        hipLaunchKernelGGL(kernel, grid, block, 0, s, args...);
+    return hipGetLastError();
+}
+
 // Waves of an attention launch: one per unit on the dense path; on the
 // sampled path W per (b, kv) pair, where W spreads the device's resident
 // waves over the pairs and never exceeds the units a pair can have.
@@ -1086,15 +1098,17 @@ hipError_t attend_mfma(const AttendArgs& a, hipStream_t s) {
     const bf16_t* sV = static_cast<const bf16_t*>(a.sV);
     const int BH = a.B * a.Hkv;
     if (a.dense) {
-        k_attend_mfma<D, true><<<grid, kThreads, 0, s>>>(K, V, sK, sV, a.q, a.N, a.T, BH, a.Hkv, a.Hq, a.G, 0, sl2,
-                                                      a.max_chunks, a.max_hunits, nullptr, nullptr, nullptr,
-                                                      a.part_o, a.part_ml);
+        return launch_timed(a, k_attend_mfma<D, true>, grid, dim3(kThreads), s, K, V, sK, sV, a.q, a.N, a.T, BH,
+                            a.Hkv, a.Hq, a.G, 0, sl2, a.max_chunks, a.max_hunits,
+                            static_cast<const PlanHeader*>(nullptr), static_cast<const Chunk*>(nullptr),
+                            static_cast<const float*>(nullptr), a.part_o, a.part_ml);
     } else {
         const DecodeLayout& L = *a.lay;
-        k_attend_mfma<D, false><<<grid, kThreads, 0, s>>>(
-            K, V, sK, sV, a.q, a.N, a.T, BH, a.Hkv, a.Hq, a.G, a.M, sl2, a.max_chunks, a.max_hunits,
-            reinterpret_cast<const PlanHeader*>(a.ws + L.hdr), reinterpret_cast<const Chunk*>(a.ws + L.chunk),
-            reinterpret_cast<const float*>(a.ws + L.ulogc), a.part_o, a.part_ml);
+        return launch_timed(a, k_attend_mfma<D, false>, grid, dim3(kThreads), s, K, V, sK, sV, a.q, a.N, a.T,
+                            BH, a.Hkv, a.Hq, a.G, a.M, sl2, a.max_chunks, a.max_hunits,
+                            reinterpret_cast<const PlanHeader*>(a.ws + L.hdr),
+                            reinterpret_cast<const Chunk*>(a.ws + L.chunk),
+                            reinterpret_cast<const float*>(a.ws + L.ulogc), a.part_o, a.part_ml);
     }
     return hipGetLastError();
 }
@@ -1114,15 +1128,17 @@ hipError_t attend_g(const AttendArgs& a, hipStream_t s) {
     const T* sV = static_cast<const T*>(a.sV);
     const int BH = a.B * a.Hkv;
     if (a.dense) {
-        k_attend<T, D, GT, true><<<grid, kWave, 0, s>>>(K, V, sK, sV, a.q, a.N, a.T, BH, a.Hkv, a.Hq, a.G, 0, sl2,
-                                                        a.max_chunks, a.max_hunits, nullptr, nullptr, nullptr,
-                                                        a.part_o, a.part_ml);
+        return launch_timed(a, k_attend<T, D, GT, true>, grid, dim3(kWave), s, K, V, sK, sV, a.q, a.N, a.T, BH,
+                            a.Hkv, a.Hq, a.G, 0, sl2, a.max_chunks, a.max_hunits,
+                            static_cast<const PlanHeader*>(nullptr), static_cast<const Chunk*>(nullptr),
+                            static_cast<const float*>(nullptr), a.part_o, a.part_ml);
     } else {
         const DecodeLayout& L = *a.lay;
-        k_attend<T, D, GT, false><<<grid, kWave, 0, s>>>(
-            K, V, sK, sV, a.q, a.N, a.T, BH, a.Hkv, a.Hq, a.G, a.M, sl2, a.max_chunks, a.max_hunits,
-            reinterpret_cast<const PlanHeader*>(a.ws + L.hdr), reinterpret_cast<const Chunk*>(a.ws + L.chunk),
-            reinterpret_cast<const float*>(a.ws + L.ulogc), a.part_o, a.part_ml);
+        return launch_timed(a, k_attend<T, D, GT, false>, grid, dim3(kWave), s, K, V, sK, sV, a.q, a.N, a.T, BH,
+                            a.Hkv, a.Hq, a.G, a.M, sl2, a.max_chunks, a.max_hunits,
+                            reinterpret_cast<const PlanHeader*>(a.ws + L.hdr),
+                            reinterpret_cast<const Chunk*>(a.ws + L.chunk),
+                            reinterpret_cast<const float*>(a.ws + L.ulogc), a.part_o, a.part_ml);
     }
     return hipGetLastError();
 }

@@ -137,6 +137,8 @@ struct AttendArgs {
     float* part_o;              // [BH, G, max_hunits, d]
     float* part_ml;             // [BH, G, max_hunits, 2]
     float* out;                 // [B, Hq, d]
+    hipEvent_t ev_start;        // stamped at the attention kernel's start (nullable)
+    hipEvent_t ev_stop;         // stamped at its end (nullable)
 };
 
 hipError_t launch_attend(const AttendArgs& a, hipStream_t s);
