@@ -165,6 +165,13 @@ def main():
     # eq. qwen-logical-access: one key per representative, key + value per row read
     read_fraction = float(np.mean(rep_bytes + attend_bytes) / (BH * (wl.N + wl.T) * row_bytes))
 
+    # HBM bytes per launch of the attention kernel (rocprofv3 counters,
+    # copy-calibrated), for the workload they were measured on, while the
+    # kernel's sources are unchanged since
+    traffic = None
+    if wl.name == "qwen32k" and wl.K == 32 and wl.B == 1 and not args.no_evict:
+        traffic = measured_traffic()
+
     cpu = None
     if args.cpu_seconds > 0:
         cpu = cpu_baseline(wl, batch, args.cpu_seconds)
@@ -185,9 +192,9 @@ def main():
         "config": {"workload": f"{wl.name}: Qwen2.5-7B-shaped layer, {wl.N}-token prompt, B={wl.B}",
                    "B": wl.B, "Hq": wl.Hq, "Hkv": wl.Hkv, "d": wl.d, "N": wl.N, "T": wl.T,
                    "P": wl.P, "R": wl.R, "M": M, "K": wl.K, "evict_1GiB": not args.no_evict},
-        "roofline": {"bound": "hbm", "kernel": "k_attend", "achieved": round(achieved, 1),
+        "roofline": {"bound": "hbm", "kernel": "k_attend_mfma<128, false>", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": None},
+                     "traffic": traffic},
         "step_gbs": round(float(np.mean(step_bytes) / value / 1e3), 1),
         "step_hbm_frac": round(float(np.mean(step_bytes) / value / 1e3) / HBM_PEAK_GBS, 4),
         "step_bytes_mean": int(np.mean(step_bytes)),
@@ -245,6 +252,27 @@ class HipEvents:
         if self.L.hipEventElapsedTime(self.c.byref(t), a, b) != 0:
             raise RuntimeError("hipEventElapsedTime failed")
         return t.value * 1e3
+
+
+def measured_traffic():
+    """Read + write bytes per launch of the sparse attention kernel from
+    profiles/traffic_k_attend_qwen32k_K32.md, or None when the kernel's
+    sources no longer hash to the value recorded there."""
+    import hashlib
+    import re
+    path = os.path.join(ROOT, "profiles", "traffic_k_attend_qwen32k_K32.md")
+    try:
+        text = open(path).read()
+    except OSError:
+        return None
+    vals = dict(re.findall(r"^(sources_sha256|read_bytes_per_launch|write_bytes_per_launch): (\S+)$", text, re.M))
+    if len(vals) != 3:
+        return None
+    csrc = os.path.join(ROOT, "paper_2609_35629_amd", "csrc")
+    src = b"".join(open(os.path.join(csrc, f), "rb").read() for f in ("attend_kernels.hip", "common.h", "internal.h"))
+    if hashlib.sha256(src).hexdigest() != vals["sources_sha256"]:
+        return None
+    return int(vals["read_bytes_per_launch"]) + int(vals["write_bytes_per_launch"])
 
 
 def calibrate_copy():
