@@ -643,6 +643,7 @@ __global__ __launch_bounds__(kAttendWaves * kWave, 1) void k_attend_mfma(
     char* const tile0 = s_v0[wv];
     char* const tile1 = s_v1[wv];
     float4 (*const ptile)[8] = s_pt[wv];
+    int pc_cnt = 0, pc_incl = 0;  // sampled path: lane p's pair count and inclusive prefix (p < 64)
     auto descriptor = [&](int u) {
         if (DENSE) {
             const int bhx = u / nchd, cix = u - bhx * nchd;
@@ -657,9 +658,14 @@ __global__ __launch_bounds__(kAttendWaves * kWave, 1) void k_attend_mfma(
             return d;
         }
         // unit u of the pairs' concatenated lists: lanes hold the counts of
-        // 64 pairs at a time and their inclusive prefix sums
+        // 64 pairs at a time and their inclusive prefix sums (kept in
+        // registers from the start when there are at most 64 pairs)
         int base = 0, p = BH - 1, idx = 0;
-        for (int p0 = 0; p0 < BH; p0 += kWave) {  // uniform
+        if (BH <= kWave) {  // uniform
+            const int nb = __popcll(__ballot(lane < BH && pc_incl <= u));  // pairs wholly before unit u
+            p = min(nb, BH - 1);
+            idx = u - (__builtin_amdgcn_readlane(pc_incl, p) - __builtin_amdgcn_readlane(pc_cnt, p));
+        } else for (int p0 = 0; p0 < BH; p0 += kWave) {  // uniform
             const int cnt = p0 + lane < BH ? min(max(hdr[p0 + lane].chunks, 0), max_chunks) : 0;
             const int incl = wave_incl_scan(cnt) + base;
             const uint64_t before = __ballot(p0 + lane < BH && incl <= u);  // pairs wholly before unit u
@@ -676,13 +682,19 @@ __global__ __launch_bounds__(kAttendWaves * kWave, 1) void k_attend_mfma(
         return d;
     };
     // units of the step: the dense list's length, or the sum of the pairs'
-    // counts (a wave-wide sum over the headers)
+    // counts (a wave-wide sum over the headers; the first 64 pairs' counts
+    // and prefix sums stay in registers for the unit lookups)
     auto unit_total = [&]() {
         if (DENSE) return BH * nchd;
         int t = 0;
         for (int p0 = 0; p0 < BH; p0 += kWave) {  // uniform
             const int cnt = p0 + lane < BH ? min(max(hdr[p0 + lane].chunks, 0), max_chunks) : 0;
-            t += __builtin_amdgcn_readlane(wave_incl_scan(cnt), kWave - 1);
+            const int incl = wave_incl_scan(cnt);
+            if (p0 == 0) {
+                pc_cnt = cnt;
+                pc_incl = incl;
+            }
+            t += __builtin_amdgcn_readlane(incl, kWave - 1);
         }
         return t;
     };

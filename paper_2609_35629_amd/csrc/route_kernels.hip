@@ -454,21 +454,40 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
         else return lpos[(hq0 + h) * M + g];
     };
 
-    // loads first: the team table (into LDS) and each head wave's perturbed
-    // scores
+    // loads first: each head wave's perturbed scores, then the team table
+    // (into LDS once the heads have found tau, so that its load overlaps
+    // the search: the search waits only for the earlier loads)
     const int hq = kv * G + min(w, G - 1);
     const size_t hoff = (static_cast<size_t>(b) * Hq + hq) * M;
     KeySet<PL> ks;
     if (w < G) ks.init(Y + hoff, phi + hoff, M);
+    asm volatile("" ::: "memory");  // the scores' loads are issued before the table's
+    constexpr int NT = kLds ? (PL * kWave + kSelectThreads - 1) / kSelectThreads : 1;  // teams per thread
+    int sz[NT], bg[NT];
     if constexpr (kLds) {
-        constexpr int NT = (PL * kWave + kSelectThreads - 1) / kSelectThreads;  // teams per thread
-        int sz[NT], bg[NT];
 #pragma unroll
         for (int k = 0; k < NT; ++k) {
             const int g = min(tid + k * kSelectThreads, M - 1);
             sz[k] = team_size[tb0 + g];
             bg[k] = team_begin[tb0 + g];
         }
+    }
+    auto size_of = [&](int g) { return kLds ? s_size[g] : team_size[tb0 + g]; };
+    auto begin_of = [&](int g) { return kLds ? s_begin[g] : team_begin[tb0 + g]; };
+
+    const int nj = ks.count();
+    uint64_t tkey = 0;
+    double tau = 0.0;
+    int need_ties = 0;
+    if (w < G) {
+        tkey = select_key<PL>(ks, Kp, s_hist[w], s_cand[w]);
+        tau = key_value(tkey);
+        int above_cnt = 0;
+#pragma unroll
+        for (int j = 0; j < nj; ++j) above_cnt += (ks.valid(j) && ks.key(j) > tkey) ? 1 : 0;
+        need_ties = Kp - wave_sum(above_cnt);
+    }
+    if constexpr (kLds) {
 #pragma unroll
         for (int k = 0; k < NT; ++k) {
             const int g = tid + k * kSelectThreads;
@@ -479,18 +498,8 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
         }
     }
     __syncthreads();
-    auto size_of = [&](int g) { return kLds ? s_size[g] : team_size[tb0 + g]; };
-    auto begin_of = [&](int g) { return kLds ? s_begin[g] : team_begin[tb0 + g]; };
 
     if (w < G) {
-        const int nj = ks.count();
-        const uint64_t tkey = select_key<PL>(ks, Kp, s_hist[w], s_cand[w]);
-        const double tau = key_value(tkey);
-
-        int above_cnt = 0;
-#pragma unroll
-        for (int j = 0; j < nj; ++j) above_cnt += (ks.valid(j) && ks.key(j) > tkey) ? 1 : 0;
-        const int need_ties = Kp - wave_sum(above_cnt);
 
         // selection in index order i = j * 64 + lane: the keys above tau's
         // key and the first need_ties keys equal to it (exactly equal Y
