@@ -1,8 +1,9 @@
 // Attention over the read plan, and the merge of the chunk partials.
 //
-// k_attend  eq. method-estimate in log space.  One workgroup reads one chunk:
-//           up to kChunkRows consecutive packed rows of one union team, or of
-//           the suffix.  Every query head h of the KV head that selected the
+// k_attend_mfma (bf16) / k_attend (fp32)
+//           eq. method-estimate in log space.  A wave reads one chunk at a
+//           time: up to kChunkRows consecutive packed rows of one union team,
+//           or of the suffix.  Every query head h of the KV head that selected the
 //           team gets the logits w_{h,i} = scale q_h.k_i over the chunk's rows
 //           and an online softmax state (m, l, acc); all rows of a chunk
 //           belong to one team, so the team's correction -log c_{g,h} enters
@@ -42,7 +43,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-static_assert(kChunkRows == 32, "a sampled unit is two 16-row tiles of one wave");
+static_assert(kChunkRows % 32 == 0, "a sampled unit is whole 32-row steps");
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNeg = -1.0e30f;   // logit of a row that carries no weight
 constexpr float kEmpty = -1.0e29f; // chunk states with a maximum below this are empty
@@ -239,16 +240,15 @@ struct VTile {
     }
 };
 
-// One wave per workgroup.  The sampled path's units are chunks of at most
-// kChunkRows (32) consecutive rows of one union team or of the suffix; the
-// dense path's units are kDenseRows (128) rows, walked 32 rows at a time with
-// the softmax state carried along.  The units of all (sequence, KV head)
-// pairs form one list (the sampler appends each pair's units at a range it
-// claims; each entry names its pair); wave w takes units w, w + gridDim.x,
-// ... (a loop bounded by the list's length), so that a KV head whose heads
-// selected large teams does not leave the others idle.  A unit's state for
-// head h goes to position pos[h] of that head's list (its unit index on the
-// dense path, where every head reads every unit).
+// One wave per workgroup (the fp32 kernel).  The sampled path's units are
+// chunks of at most kChunkRows consecutive rows of one union team or of the
+// suffix; the dense path's units are kDenseRows rows; both are walked 32 rows
+// at a time with the softmax state carried along.  Each (sequence, KV head)
+// pair's units sit in that pair's region of the sampler's list; wave w serves
+// pair w % BH and takes its units w / BH, + gridDim.x / BH, ... (a loop
+// bounded by the pair's count).  A unit's state for head h goes to position
+// pos[h] of that head's list (its unit index on the dense path, where every
+// head reads every unit).
 //
 // Register layout of the softmax: lane l = 16 c + j holds, in register r,
 // M row 4 c + r of the score tile, i.e. query head (4 c + r) % 8 of row j

@@ -14,7 +14,7 @@ constexpr int kMaxReps = 1024;     // representatives per parent
 constexpr int kMaxTeams = 8192;    // teams per (b, kv) the sampler handles
 constexpr int kMaxGroup = 8;       // query heads per KV head (8-bit head masks)
 constexpr int kLogcStride = 8;     // floats per union team in the read plan
-constexpr int kChunkRows = 32;     // rows per sampled attention unit (one wave)
+constexpr int kChunkRows = 64;     // rows per sampled attention unit (two 32-row steps of one wave)
 constexpr int kDenseRows = 128;    // rows per dense attention unit
 constexpr int kAttendWavesPerCU = 8; // resident attention waves per compute unit
 constexpr int kMergeThreads = 256;   // threads of a merge workgroup
