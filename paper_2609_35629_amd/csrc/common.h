@@ -104,19 +104,16 @@ __device__ __forceinline__ u64x4 philox4x64_10(uint64_t c0, uint64_t c1, uint64_
     return o;
 }
 
-// Standard Gumbel variate of team g for (seed, step, b, h): word g % 4 of the
-// block at counter (g / 4, h, b, step), key (seed, 0); U = ((w >> 12) + 1/2)
+// Standard Gumbel variate of a 64-bit Philox word w: U = ((w >> 12) + 1/2)
 // 2^-52 is exact and inside (0, 1); G = -log(-log U).
-__device__ __forceinline__ double team_gumbel(uint64_t seed, uint64_t step, uint64_t b, uint64_t h,
-                                              uint64_t g) {
-    const u64x4 r = philox4x64_10(g >> 2, h, b, step, seed, 0);
-    // word g % 4 by selects: an indexed read of the array would go through
-    // memory
-    const int sel = static_cast<int>(g & 3);
-    const uint64_t w = sel == 0 ? r.v[0] : sel == 1 ? r.v[1] : sel == 2 ? r.v[2] : r.v[3];
+__device__ __forceinline__ double gumbel_of_word(uint64_t w) {
     const double u = (static_cast<double>(w >> 12) + 0.5) * 0x1.0p-52;
     return -log(-log(u));
 }
+
+// The variate of team g for (seed, step, b, h) is that of word g % 4 of the
+// block at counter (g / 4, h, b, step), key (seed, 0); one block serves
+// teams 4 (g / 4) .. 4 (g / 4) + 3.
 
 // Order-preserving map of a double onto uint64 (larger value -> larger key).
 __device__ __forceinline__ uint64_t order_key(double y) {

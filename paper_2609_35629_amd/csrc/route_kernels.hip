@@ -366,6 +366,7 @@ __global__ __launch_bounds__(kRouteThreads) void k_route(
     constexpr int DPL = D / 16;
     using RC = RepChunk<T, DPL>;
     __shared__ double s_gum[G][kRouteTeams];
+    __shared__ uint64_t s_word[G][kRouteTeams];
     const int bh = blockIdx.y;
     const int b = bh / Hkv, kv = bh - b * Hkv;
     const int tid = threadIdx.x, grp = tid >> 4, sub = tid & 15;
@@ -383,12 +384,22 @@ __global__ __launch_bounds__(kRouteThreads) void k_route(
     for (int h = 0; h < G; ++h)
 #pragma unroll
         for (int e = 0; e < DPL; ++e) qd[h][e] = static_cast<double>(qb[h * D + e]);
-    // the Gumbel noise does not depend on the loads: one (head, team) draw
-    // per thread while they are in flight
+    // the Gumbel noise does not depend on the loads, so it is drawn while
+    // they are in flight: one Philox block per (head, 4 teams) (the block at
+    // counter (g / 4, h, b, step) holds the words of teams 4 (g / 4) ..
+    // + 3), then one (head, team) variate per thread from its word
+    static_assert(kRouteTeams % 4 == 0, "a workgroup's teams are whole Philox blocks");
+    for (int p = tid; p < G * (kRouteTeams / 4); p += kRouteThreads) {
+        const int h = p / (kRouteTeams / 4), qd = p - h * (kRouteTeams / 4);
+        const u64x4 r = philox4x64_10(static_cast<uint64_t>(g0 / 4 + qd), static_cast<uint64_t>(kv * G + h),
+                                      static_cast<uint64_t>(b), step, seed, 0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) s_word[h][4 * qd + e] = r.v[e];
+    }
+    __syncthreads();
     for (int p = tid; p < G * kRouteTeams; p += kRouteThreads) {
         const int h = p / kRouteTeams, gi = p - h * kRouteTeams;
-        const int g = g0 + gi;
-        if (g < M) s_gum[h][gi] = team_gumbel(seed, step, b, kv * G + h, g);
+        if (g0 + gi < M) s_gum[h][gi] = gumbel_of_word(s_word[h][gi]);
     }
     __syncthreads();
     const int g = g0 + grp;
