@@ -143,6 +143,18 @@ def test_long_skewed_sampled_heads():
     _run(wl, pairs=pairs)
 
 
+def test_plan_beyond_unit_table():
+    # a few very large teams (8 teams of ~65K rows): one plan pass holds more
+    # units than the sampler's LDS unit-to-team table (4096 entries), so the
+    # units find their teams by search over the union records
+    wl = datagen.WORKLOADS["qwen8k"].with_(name="huge-teams", N=524288, P=131072, R=2, Hq=2, Hkv=1,
+                                           K=6, T=64, n_clusters=16)
+    teams, res = _run(wl, steps=(0,))
+    assert teams.M == 8
+    cmp, dbg, so = res[0]
+    assert int(dbg.union_rows.sum().item()) > 4096 * 64
+
+
 def test_short_last_parent_and_odd_groups():
     # N not a multiple of P, R > |last parent|, 3 query heads per KV head
     wl = datagen.WORKLOADS["qwen8k"].with_(name="odd", N=2050, P=512, R=24, Hq=6, Hkv=2, K=20, T=7)
