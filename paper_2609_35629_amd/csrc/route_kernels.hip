@@ -37,6 +37,7 @@ constexpr int kSelectThreads = 512;
 constexpr int kSelectWaves = kSelectThreads / kWave;
 constexpr int kFineBits = 16;                 // value-histogram resolution of the sampler
 constexpr int kSelectUnits = 4096;            // units of a plan pass resolved through an LDS table
+constexpr int kSelectRecs = 2048;             // union teams of a plan pass (M <= 2048: one pass)
 
 template <typename T, int DPL>
 struct RepChunk;
@@ -443,8 +444,7 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
     __shared__ uint64_t s_bits[kMaxGroup][kMaxTeams / kWave];  // selection bits per head
     __shared__ __align__(16) int s_w[3 * kSelectWaves];
     __shared__ int s_hunits[kMaxGroup];  // units of each head's teams
-    __shared__ int4 s_team[kSelectThreads];  // union teams of a pass: first unit, begin, size, heads
-    __shared__ int s_tg[kSelectThreads];     // their team indices
+    __shared__ int2 s_rec[kSelectRecs];      // union teams of a pass: first unit, team index
     __shared__ unsigned short s_u2t[kSelectUnits];  // union slot of each unit of a pass
 
     const int bh = blockIdx.x;
@@ -546,8 +546,7 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
         };
         auto select_pass = [&](auto with_ties) {
             int nties = 0, fill = 0;
-#pragma unroll
-            for (int j = 0; j < nj; ++j) {
+            auto ballot_word = [&](int j) {
                 const bool valid = ks.valid(j);
                 const uint64_t k = ks.key(j);
                 bool sel = valid && k > tkey;
@@ -559,6 +558,10 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
                 }
                 const uint64_t sb = __ballot(sel);
                 if (lane == 0) s_bits[w][j] = sb;
+                return sb;
+            };
+            auto compact = [&](int j, uint64_t sb) {
+                const bool sel = (sb >> lane) & 1ull;
                 const int cnt = __popcll(sb);
                 if (fill + cnt > kWave) {  // uniform: the batch is full
                     flush(fill);
@@ -570,6 +573,18 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
                     if constexpr (KeySet<PL>::kPhiRegs) cx[p] = static_cast<float>(ks.phi(j) - tau);
                 }
                 fill += cnt;
+            };
+            if constexpr (KeySet<PL>::kPhiRegs) {
+#pragma unroll
+                for (int j = 0; j < nj; ++j) compact(j, ballot_word(j));
+            } else {
+                // ballots first (unrolled over the registers), then the
+                // compaction (rolled, so that the batch flush is one copy)
+#pragma unroll
+                for (int j = 0; j < nj; ++j) ballot_word(j);
+                wave_lds_sync();
+#pragma unroll 1
+                for (int j = 0; j < nj; ++j) compact(j, s_bits[w][j]);
             }
             if (fill > 0) flush(fill);
         };
@@ -585,15 +600,16 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
     __syncthreads();
 
     // ---- union of the heads' selections in ascending team order -------------
-    // One pass per kSelectThreads teams, thread tid owning team base + tid: a
-    // scan gives every union team its slot, its first unit and its rows; the
-    // team writes its corrections and enters itself in LDS (its record, and
-    // its slot at each of its units); then thread c writes unit c of the
-    // pass to the pair's own region of the unit list (max_chunks entries,
-    // which bound the units of any union of this size).  Passes whose units
-    // exceed the LDS table fall back to a search over the records.  A unit's
-    // position in the list of a head that reads it is the team's first
-    // position there plus the unit's index within the team.
+    // One pass per kPass teams (all of them when the team table is in LDS),
+    // thread tid owning TPT consecutive teams: a scan gives every union team
+    // its slot, its first unit and its rows; the team writes its corrections
+    // and enters itself in LDS (its record, and its slot at each of its
+    // units); then thread c writes unit c of the pass to the pair's own
+    // region of the unit list (max_chunks entries, which bound the units of
+    // any union of this size).  Passes whose units exceed the LDS table fall
+    // back to a search over the records.  A unit's position in the list of a
+    // head that reads it is the team's first position there plus the unit's
+    // index within the team.
     auto heads_of = [&](int g) {
         int hm = 0;
         if (g < M) {
@@ -602,62 +618,76 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
         }
         return hm;
     };
+    constexpr int TPT = kLds ? PL / 8 : 1;  // teams per thread and pass (M <= 512 TPT with LDS tables)
+    constexpr int kPass = kSelectThreads * TPT;
+    static_assert(kPass <= kSelectRecs, "a pass's union teams fit the LDS records");
     Chunk* const cb = chunks + static_cast<size_t>(bh) * max_chunks;
     int run_u = 0, run_rows = 0, run_c = 0;
-    for (int base = 0; base < M; base += kSelectThreads) {
-        const int g = base + tid;
-        const int gc = min(g, M - 1);
-        const int tsz = size_of(gc), tbeg = begin_of(gc);
-        const int hm = heads_of(g);
-        const int f = hm ? 1 : 0;
-        const int nc = f ? chunk_count(tsz) : 0;
-        const int x[3] = {f, nc, f ? tsz : 0};
+    for (int base = 0; base < M; base += kPass) {
+        int hmk[TPT], nck[TPT];
+        int lf = 0, lnc = 0, lrows = 0;
+#pragma unroll
+        for (int k = 0; k < TPT; ++k) {
+            const int g = base + tid * TPT + k;
+            hmk[k] = heads_of(g);  // 0 past the last team
+            const int tsz = hmk[k] ? size_of(g) : 0;
+            nck[k] = hmk[k] ? chunk_count(tsz) : 0;
+            lf += hmk[k] ? 1 : 0;
+            lnc += nck[k];
+            lrows += tsz;
+        }
+        const int x[3] = {lf, lnc, lrows};
         int ex[3], tot[3];
         block_scan<3>(x, ex, tot, s_w);
         const bool table = tot[1] <= kSelectUnits;  // uniform
-        if (f) {
-            const int slot = ex[0];
-            float lv[kLogcStride];
+        int slot = ex[0], ust = ex[1];
 #pragma unroll
-            for (int h = 0; h < kMaxGroup; ++h) lv[h] = (h < G && ((hm >> h) & 1)) ? lc_at(h, g) : 0.f;
-            float4* L = reinterpret_cast<float4*>(ulogc + (tb0 + run_u + slot) * kLogcStride);
-            L[0] = make_float4(lv[0], lv[1], lv[2], lv[3]);
-            L[1] = make_float4(lv[4], lv[5], lv[6], lv[7]);
-            s_team[slot] = make_int4(ex[1], tbeg, tsz, hm);
-            s_tg[slot] = g;
-            if (table)
-                for (int c = 0; c < nc; ++c) s_u2t[ex[1] + c] = static_cast<unsigned short>(slot);
+        for (int k = 0; k < TPT; ++k) {
+            if (hmk[k]) {
+                const int g = base + tid * TPT + k;
+                float lv[kLogcStride];
+#pragma unroll
+                for (int h = 0; h < kMaxGroup; ++h) lv[h] = (h < G && ((hmk[k] >> h) & 1)) ? lc_at(h, g) : 0.f;
+                float4* L = reinterpret_cast<float4*>(ulogc + (tb0 + run_u + slot) * kLogcStride);
+                L[0] = make_float4(lv[0], lv[1], lv[2], lv[3]);
+                L[1] = make_float4(lv[4], lv[5], lv[6], lv[7]);
+                s_rec[slot] = make_int2(ust, g);
+                if (table)
+                    for (int c = 0; c < nck[k]; ++c) s_u2t[ust + c] = static_cast<unsigned short>(slot);
+                ++slot;
+                ust += nck[k];
+            }
         }
         __syncthreads();
         for (int c = tid; c < tot[1]; c += kSelectThreads) {
-            int slot;
+            int sl;
             if (table) {
-                slot = s_u2t[c];
+                sl = s_u2t[c];
             } else {  // the last record whose first unit is at or before c
                 int lo = 0, hi = tot[0] - 1;
                 while (lo < hi) {
                     const int mid = (lo + hi + 1) >> 1;
-                    if (s_team[mid].x <= c)
+                    if (s_rec[mid].x <= c)
                         lo = mid;
                     else
                         hi = mid - 1;
                 }
-                slot = lo;
+                sl = lo;
             }
-            const int4 tm = s_team[slot];
-            const int gg = s_tg[slot];
-            const int p = c - tm.x;
+            const int2 rc = s_rec[sl];
+            const int g = rc.y, p = c - rc.x;
+            const int hm = heads_of(g), tsz = size_of(g);
             const int ci = run_c + c;
             if (ci < max_chunks) {
                 Chunk ch;
-                ch.begin = tm.y + p * kChunkRows;
-                ch.slot = run_u + slot;
-                ch.meta = chunk_meta(min(kChunkRows, tm.z - p * kChunkRows), tm.w, bh);
+                ch.begin = begin_of(g) + p * kChunkRows;
+                ch.slot = run_u + sl;
+                ch.meta = chunk_meta(min(kChunkRows, tsz - p * kChunkRows), hm, bh);
                 ch.ci = ci;
                 int ps[kMaxGroup];
 #pragma unroll
                 for (int h = 0; h < kMaxGroup; ++h)
-                    ps[h] = (h < G && ((tm.w >> h) & 1)) ? static_cast<int>(pos_at(h, gg)) + p : 0;
+                    ps[h] = (h < G && ((hm >> h) & 1)) ? static_cast<int>(pos_at(h, g)) + p : 0;
                 set_chunk_pos(ch, ps);
                 cb[ci] = ch;
             }
@@ -665,7 +695,7 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
         run_u += tot[0];
         run_c += tot[1];
         run_rows += tot[2];
-        if (base + kSelectThreads < M) __syncthreads();  // the LDS records are rewritten by the next pass
+        if (base + kPass < M) __syncthreads();  // the LDS records are rewritten by the next pass
     }
     const int nsc = chunk_count(T_suf);
     const int utotal = min(run_c + nsc, max_chunks);
