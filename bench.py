@@ -172,6 +172,17 @@ def main():
     if wl.name == "qwen32k" and wl.K == 32 and wl.B == 1 and not args.no_evict:
         traffic = measured_traffic()
 
+    # preparation per prompt, excluded from the step as in the paper: host
+    # time of santapp_build_teams (device allocations, team build, packed
+    # copies; the call returns once its kernels are done), median of three
+    prep_us = []
+    for _ in range(3):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        extra = sp.build_teams(db["K"], db["V"], wl.P, wl.R)
+        prep_us.append((time.perf_counter() - t0) * 1e6)
+        extra.close()
+
     cpu = None
     if args.cpu_seconds > 0:
         cpu = cpu_baseline(wl, batch, args.cpu_seconds)
@@ -195,6 +206,7 @@ def main():
         "roofline": {"bound": "hbm", "kernel": "k_attend_mfma<128, false>", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic},
+        "prep_us": round(float(np.median(prep_us)), 1),
         "step_gbs": round(float(np.mean(step_bytes) / value / 1e3), 1),
         "step_hbm_frac": round(float(np.mean(step_bytes) / value / 1e3) / HBM_PEAK_GBS, 4),
         "step_bytes_mean": int(np.mean(step_bytes)),

@@ -19,7 +19,8 @@
  *
  * Conventions
  *   - Every tensor argument is a DEVICE pointer owned by the caller unless
- *     stated otherwise; layouts are dense row-major.
+ *     stated otherwise; layouts are dense row-major.  Tensor and workspace
+ *     pointers must be 16-byte aligned (else SANTAPP_EINVAL).
  *   - K/V element type is bf16 (raw 16-bit patterns) or fp32, chosen by
  *     santapp_dtype; queries are fp32; outputs are fp32.
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).

@@ -59,6 +59,9 @@ bool dtype_ok(santapp_dtype dt) { return dt == SANTAPP_BF16 || dt == SANTAPP_FP3
 
 size_t align_up(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
+// Device buffers are read and written with 16-byte vector accesses.
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
 // Compute units of the current device (0 if the query fails), looked up once
 // per device.
 int device_cus() {
@@ -177,6 +180,7 @@ santapp_status santapp_build_teams(const void* K, const void* V, int B, int Hkv,
     if (!out) return fail(SANTAPP_EINVAL, "out is NULL");
     *out = nullptr;
     if (!K || !V) return fail(SANTAPP_EINVAL, "K and V must be device pointers");
+    if (!aligned16(K) || !aligned16(V)) return fail(SANTAPP_EINVAL, "K and V must be 16-byte aligned");
     if (B < 1 || Hkv < 1 || N < 1) return fail(SANTAPP_EINVAL, "B, Hkv, N must be >= 1");
     if (parent_size < 1) return fail(SANTAPP_EINVAL, "parent_size must be >= 1");
     if (reps_per_parent < 1) return fail(SANTAPP_EINVAL, "reps_per_parent must be >= 1");
@@ -340,6 +344,8 @@ santapp_status santapp_decode(const santapp_teams* t, const float* q, const void
         return fail(SANTAPP_ELIMIT, "B * Hkv = %lld exceeds %d", static_cast<long long>(t->B) * t->Hkv, kMaxPairs);
     if (T < 0) return fail(SANTAPP_EINVAL, "T must be >= 0");
     if (T > 0 && (!suffix_K || !suffix_V)) return fail(SANTAPP_EINVAL, "suffix K/V are NULL with T > 0");
+    if (!aligned16(q) || !aligned16(out) || !aligned16(workspace) || (T > 0 && (!aligned16(suffix_K) || !aligned16(suffix_V))))
+        return fail(SANTAPP_EINVAL, "q, out, suffix K/V and workspace must be 16-byte aligned");
     if (K < 1) return fail(SANTAPP_EINVAL, "K must be >= 1 (got %d)", K);
     if (!(scale >= 0.0) || !isfinite(scale)) return fail(SANTAPP_EINVAL, "scale must be finite and >= 0");
     if (scale == 0.0) scale = 1.0 / sqrt(static_cast<double>(t->d));
@@ -444,6 +450,9 @@ santapp_status santapp_dense_decode(const float* q, const void* K, const void* V
         return fail(SANTAPP_EINVAL, "invalid sizes");
     if (N > 0 && (!K || !V)) return fail(SANTAPP_EINVAL, "K and V are NULL with N > 0");
     if (T > 0 && (!suffix_K || !suffix_V)) return fail(SANTAPP_EINVAL, "suffix K/V are NULL with T > 0");
+    if (!aligned16(q) || !aligned16(out) || !aligned16(workspace) || (N > 0 && (!aligned16(K) || !aligned16(V))) ||
+        (T > 0 && (!aligned16(suffix_K) || !aligned16(suffix_V))))
+        return fail(SANTAPP_EINVAL, "q, out, K/V, suffix K/V and workspace must be 16-byte aligned");
     if (Hq < 1 || Hq % Hkv != 0) return fail(SANTAPP_EINVAL, "Hq must be a positive multiple of Hkv");
     if (Hq / Hkv > kMaxGroup) return fail(SANTAPP_ELIMIT, "more than %d query heads per KV head", kMaxGroup);
     if (!dtype_ok(dtype)) return fail(SANTAPP_EDTYPE, "unsupported dtype %d", static_cast<int>(dtype));

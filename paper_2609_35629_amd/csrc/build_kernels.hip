@@ -10,6 +10,8 @@
 // rule (ties to the earliest-chosen representative) once all r rounds ran.
 // Distances are fp64 sums in dimension order with no fused multiply-add, so
 // every comparison sees the value the definition gives.
+#include <algorithm>
+
 #include "common.h"
 #include "internal.h"
 
@@ -101,7 +103,9 @@ __global__ __launch_bounds__(kBuildThreads) void k_build_parent(
         best = pick_min(best, c);
     }
     best = block_arg<false>(best, s_red);
-    int rep = best.i;
+    // a reduction without a winner (NaN keys) falls back to member 0, so
+    // that every index stays inside the parent
+    int rep = best.i < n ? best.i : 0;
 
     for (int u = 0; u < r; ++u) {
         if (tid == 0) s_reps[u] = rep;
@@ -135,7 +139,7 @@ __global__ __launch_bounds__(kBuildThreads) void k_build_parent(
         }
         if (u + 1 < r) {
             far = block_arg<true>(far, s_red);
-            rep = far.i;
+            rep = far.i < n ? far.i : 0;
         } else {
             __syncthreads();
         }
@@ -192,6 +196,338 @@ __global__ __launch_bounds__(kBuildThreads) void k_build_parent(
     }
 }
 
+// ---------------------------------------------------------------------------
+// Register-resident variant of the same construction for parents of at most
+// kRegThreads members whose rows fit 64 registers (d * element size <= 256 B).
+// Thread i holds member i's key row in registers for the whole build, so each
+// round reads only the new representative (an LDS broadcast) instead of every
+// member's row from memory.  The arithmetic, its order and the tie rules are
+// those of k_build_parent, so both kernels produce identical tables.
+constexpr int kRegThreads = 512;
+constexpr int kRegWaves = kRegThreads / kWave;
+constexpr int kRankBlock = kWave;  // representatives ranked per ballot block
+
+// A member row as 32-bit words: packed bf16 pairs, or fp32 values.
+template <typename T, int D>
+struct RegRow;
+
+template <int D>
+struct RegRow<bf16_t, D> {
+    static constexpr int kWords = D / 2;
+    uint32_t w[kWords];
+    __device__ __forceinline__ void load(const bf16_t* row) {
+        const uint4* p = reinterpret_cast<const uint4*>(row);
+#pragma unroll
+        for (int k = 0; k < kWords / 4; ++k) {
+            const uint4 v = p[k];
+            w[4 * k] = v.x;
+            w[4 * k + 1] = v.y;
+            w[4 * k + 2] = v.z;
+            w[4 * k + 3] = v.w;
+        }
+    }
+    __device__ __forceinline__ float elem(int j) const {
+        return (j & 1) ? bf16hi(w[j >> 1]) : bf16lo(w[j >> 1]);
+    }
+    // hides the words from code motion: widening the row to fp64 ahead of
+    // its use would need 4 D registers
+    __device__ __forceinline__ void opaque() {
+#pragma unroll
+        for (int k = 0; k < kWords; ++k) asm volatile("" : "+v"(w[k]));
+    }
+    // the same for the words of dimensions j0 .. j0 + 7
+    __device__ __forceinline__ void opaque8(int j0) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) asm volatile("" : "+v"(w[j0 / 2 + k]));
+    }
+};
+
+template <int D>
+struct RegRow<float, D> {
+    static constexpr int kWords = D;
+    float w[kWords];
+    __device__ __forceinline__ void load(const float* row) {
+        const float4* p = reinterpret_cast<const float4*>(row);
+#pragma unroll
+        for (int k = 0; k < kWords / 4; ++k) {
+            const float4 v = p[k];
+            w[4 * k] = v.x;
+            w[4 * k + 1] = v.y;
+            w[4 * k + 2] = v.z;
+            w[4 * k + 3] = v.w;
+        }
+    }
+    __device__ __forceinline__ float elem(int j) const { return w[j]; }
+    __device__ __forceinline__ void opaque() {
+#pragma unroll
+        for (int k = 0; k < kWords; ++k) asm volatile("" : "+v"(w[k]));
+    }
+    __device__ __forceinline__ void opaque8(int j0) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) asm volatile("" : "+v"(w[j0 + k]));
+    }
+};
+
+// |k - c|^2 with c an fp64 vector in LDS (read as broadcasts), summed in
+// dimension order without contraction.
+template <typename T, int D>
+__device__ __forceinline__ double reg_sqdist(const RegRow<T, D>& r, const double* c) {
+#pragma clang fp contract(off)
+    double acc = 0.0;
+#pragma unroll
+    for (int j = 0; j < D; j += 2) {
+        // LDS reads are kept in groups of four (eight dims): hoisting them
+        // all would need 256 registers for c
+        if (j % 8 == 0) asm volatile("" ::: "memory");
+        const double2 cc = *reinterpret_cast<const double2*>(c + j);
+        const double t0 = static_cast<double>(r.elem(j)) - cc.x;
+        acc = acc + t0 * t0;
+        const double t1 = static_cast<double>(r.elem(j + 1)) - cc.y;
+        acc = acc + t1 * t1;
+    }
+    return acc;
+}
+
+// (value, index) reduction over the workgroup's waves; s_red holds one
+// entry per wave.  The caller separates reuses of s_red by a barrier.
+template <bool kMax>
+__device__ __forceinline__ ArgVal reg_block_arg(ArgVal x, ArgVal* s_red, int nw) {
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+        ArgVal y;
+        y.v = __shfl_xor(x.v, off);
+        y.i = __shfl_xor(x.i, off);
+        x = kMax ? pick_max(x, y) : pick_min(x, y);
+    }
+    if (lane_id() == 0) s_red[wave_id()] = x;
+    __syncthreads();
+    ArgVal r = s_red[0];
+    for (int w = 1; w < nw; ++w) r = kMax ? pick_max(r, s_red[w]) : pick_min(r, s_red[w]);
+    return r;
+}
+
+// Thread t owns members t + k * blockDim.x, k < MPT, and is launched with
+// max(D, ceil(members / MPT) rounded up to a wave) threads.  Two members per
+// thread let one LDS read of the representative serve two distances.
+template <typename T, int D, int MPT>
+__global__ __launch_bounds__(kRegThreads) void k_build_parent_regs(
+    const T* __restrict__ K, int N, int P, int R, int M, int* __restrict__ team_begin,
+    int* __restrict__ team_size, double* __restrict__ log_n, int* __restrict__ rep_token,
+    int* __restrict__ perm) {
+#pragma clang fp contract(off)
+    __shared__ __align__(16) double s_vec[2][D];  // the mean, then each new representative
+    __shared__ __align__(16) float s_tile[kWave][D];  // one wave's rows, for the mean
+    __shared__ ArgVal s_red[2][kRegWaves];
+    __shared__ int s_reps[kMaxReps];
+    __shared__ int s_cnt[kMaxReps];
+    __shared__ int s_off[kMaxReps];
+    __shared__ int s_wsum[kRegWaves];
+    __shared__ int s_wcnt[MPT][kRegWaves][kRankBlock];
+
+    const int p = blockIdx.x;
+    const int bh = blockIdx.y;
+    const int tid = threadIdx.x;
+    const int nt = blockDim.x;
+    const int nw = nt / kWave;
+    const int w = wave_id(), lane = lane_id();
+    const int start = p * P;
+    const int n = min(P, N - start);
+    const int r = min(R, n);
+    const int team0 = p * min(R, P);  // every earlier parent is full-size
+    const T* Kc = K + (static_cast<size_t>(bh) * N + start) * D;
+
+    RegRow<T, D> row[MPT];
+    bool member[MPT];
+#pragma unroll
+    for (int k = 0; k < MPT; ++k) {
+        const int i = tid + k * nt;
+        member[k] = i < n;
+        if (member[k]) row[k].load(Kc + static_cast<size_t>(i) * D);
+    }
+
+    // parent mean, summed over members in token order: the rows pass
+    // through LDS 64 members (one wave's slot) at a time, and thread j < D
+    // adds dimension j of each staged row in turn
+    double msum = 0.0;
+    for (int g = 0; g * kWave < n; ++g) {
+        const int gk = g / nw, gw = g - gk * nw;  // slot and wave holding members 64g..
+#pragma unroll
+        for (int k = 0; k < MPT; ++k) {
+            row[k].opaque();
+            if (k == gk && w == gw && member[k]) {
+#pragma unroll
+                for (int j = 0; j < D; j += 4)
+                    *reinterpret_cast<float4*>(&s_tile[lane][j]) =
+                        make_float4(row[k].elem(j), row[k].elem(j + 1), row[k].elem(j + 2), row[k].elem(j + 3));
+            }
+        }
+        __syncthreads();
+        if (tid < D) {
+            const int cnt = min(kWave, n - g * kWave);
+            for (int i = 0; i < cnt; ++i) msum = msum + static_cast<double>(s_tile[i][tid]);
+        }
+        __syncthreads();
+    }
+    if (tid < D) s_vec[0][tid] = msum / static_cast<double>(n);
+    __syncthreads();
+
+    // distances of this thread's members to the vector c in LDS: |k - c|^2
+    // summed in dimension order without contraction, one LDS read of c for
+    // all MPT members, eight dimensions per scheduling group (hoisting the
+    // reads or the widening of all dimensions would need 4 D registers)
+    auto distances = [&](const double* c, double (&dd)[MPT]) {
+#pragma unroll
+        for (int k = 0; k < MPT; ++k) {
+            row[k].opaque();
+            dd[k] = 0.0;
+        }
+#pragma unroll
+        for (int j = 0; j < D; j += 2) {
+            if (j % 8 == 0) {
+                // the sums so far are complete before the group's LDS reads
+                // and widening (no group's work moves past another's)
+#pragma unroll
+                for (int k = 0; k < MPT; ++k) {
+                    asm volatile("" : "+v"(dd[k])::"memory");
+                    row[k].opaque8(j);
+                }
+            }
+            const double2 cc = *reinterpret_cast<const double2*>(c + j);
+#pragma unroll
+            for (int k = 0; k < MPT; ++k) {
+                const double t0 = static_cast<double>(row[k].elem(j)) - cc.x;
+                dd[k] = dd[k] + t0 * t0;
+                const double t1 = static_cast<double>(row[k].elem(j + 1)) - cc.y;
+                dd[k] = dd[k] + t1 * t1;
+            }
+        }
+    };
+
+    // first representative: the member nearest the mean
+    double dd[MPT];
+    distances(s_vec[0], dd);
+    ArgVal best{INFINITY, 0x7fffffff};
+#pragma unroll
+    for (int k = 0; k < MPT; ++k)
+        if (member[k]) best = pick_min(best, ArgVal{dd[k], tid + k * nt});
+    int rep = reg_block_arg<false>(best, s_red[0], nw).i;
+    if (rep >= n) rep = 0;  // no winner (NaN keys): stay inside the parent
+
+    // farthest-first rounds with a running minimum; a chosen representative
+    // gets -1 so that it is never chosen again.  Round u uses buffer
+    // (u + 1) & 1 of s_vec and s_red (the mean used buffer 0): a buffer is
+    // rewritten two rounds after it was read, past both barriers of the
+    // round between.
+    double m[MPT];
+    int o[MPT];
+#pragma unroll
+    for (int k = 0; k < MPT; ++k) {
+        m[k] = 0.0;
+        o[k] = 0;
+    }
+    for (int u = 0; u < r; ++u) {
+        const int b = (u + 1) & 1;
+        const int rk = rep / nt;
+        if (tid == rep - rk * nt) {
+            s_reps[u] = rep;
+#pragma unroll
+            for (int k = 0; k < MPT; ++k) {
+                if (k == rk) {
+#pragma unroll
+                    for (int j = 0; j < D; j += 2) {
+                        if (j % 8 == 0) row[k].opaque8(j);
+                        *reinterpret_cast<double2*>(&s_vec[b][j]) = make_double2(
+                            static_cast<double>(row[k].elem(j)), static_cast<double>(row[k].elem(j + 1)));
+                    }
+                }
+            }
+        }
+        __syncthreads();
+        distances(s_vec[b], dd);
+        ArgVal far{-INFINITY, 0x7fffffff};
+#pragma unroll
+        for (int k = 0; k < MPT; ++k) {
+            const int i = tid + k * nt;
+            if (member[k]) {
+                if (u == 0 || dd[k] < m[k]) {
+                    m[k] = dd[k];
+                    o[k] = u;
+                }
+                if (i == rep) {
+                    m[k] = -1.0;
+                    o[k] = u;
+                }
+                far = pick_max(far, ArgVal{m[k], i});
+            }
+        }
+        if (u + 1 < r) {
+            rep = reg_block_arg<true>(far, s_red[b], nw).i;
+            if (rep >= n) rep = 0;
+        }
+    }
+    __syncthreads();
+
+    // team sizes and their exclusive scan (r <= blockDim.x: one team per
+    // thread)
+    for (int u = tid; u < r; u += nt) s_cnt[u] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < MPT; ++k)
+        if (member[k]) atomicAdd(&s_cnt[o[k]], 1);
+    __syncthreads();
+    for (int base = 0; base < r; base += nt) {
+        const int u = base + tid;
+        const int c = u < r ? s_cnt[u] : 0;
+        const int inc = wave_incl_scan(c);
+        if (lane == kWave - 1) s_wsum[w] = inc;
+        __syncthreads();
+        int pre = base > 0 ? s_off[base - 1] + s_cnt[base - 1] : 0;
+        for (int v = 0; v < w; ++v) pre += s_wsum[v];
+        if (u < r) s_off[u] = pre + inc - c;
+        __syncthreads();
+    }
+    const size_t tbase = static_cast<size_t>(bh) * M + team0;
+    for (int u = tid; u < r; u += nt) {
+        team_begin[tbase + u] = start + s_off[u];
+        team_size[tbase + u] = s_cnt[u];
+        log_n[tbase + u] = log(static_cast<double>(s_cnt[u]));
+        rep_token[tbase + u] = start + s_reps[u];
+    }
+
+    // packed position of each member: its team's offset plus its rank among
+    // the team's members in token order (slot k of wave v holds members
+    // k nt + 64 v ..), per block of 64 representatives with one ballot per
+    // representative, slot and wave
+    int* pperm = perm + static_cast<size_t>(bh) * N + start;
+    const uint64_t lt = lanemask_lt();
+    for (int ub = 0; ub < r; ub += kRankBlock) {
+        const int nb = min(kRankBlock, r - ub);
+        int rank_in_wave[MPT];
+#pragma unroll
+        for (int k = 0; k < MPT; ++k) {
+            const int ok = member[k] ? o[k] : -1;
+            rank_in_wave[k] = 0;
+            for (int q = 0; q < nb; ++q) {
+                const uint64_t bm = __ballot(ok == ub + q);
+                if (ok == ub + q) rank_in_wave[k] = __popcll(bm & lt);
+                if (lane == 0) s_wcnt[k][w][q] = __popcll(bm);
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < MPT; ++k) {
+            const int ok = member[k] ? o[k] : -1;
+            if (ok >= ub && ok < ub + nb) {
+                int pos = s_off[ok] + rank_in_wave[k];
+                for (int kk = 0; kk < k; ++kk)
+                    for (int v = 0; v < nw; ++v) pos += s_wcnt[kk][v][ok - ub];
+                for (int v = 0; v < w; ++v) pos += s_wcnt[k][v][ok - ub];
+                pperm[pos] = start + tid + k * nt;
+            }
+        }
+        __syncthreads();
+    }
+}
+
 // Row gather into team order: packed[bh][pos] = src[bh][perm[bh][pos]], and the
 // representative keys reps[bh][g] = K[bh][rep_token[bh][g]].  One thread per
 // 16-byte chunk of a row.
@@ -217,6 +553,29 @@ hipError_t launch_build_parents(const void* K, santapp_dtype dtype, int BH, int 
                                 int* team_size, double* log_n, int* rep_token, int* perm,
                                 hipStream_t s) {
     const dim3 grid((N + P - 1) / P, BH);
+    // register-resident kernel where a parent fits 2 kRegThreads members and
+    // a row 64 registers (two members per thread above kRegThreads); the
+    // general kernel otherwise.  At least one thread per dimension: they sum
+    // the parent mean.
+    const int members = std::min(P, N);
+    if (members <= 2 * kRegThreads && R <= kMaxReps) {
+        const int mpt = members > kRegThreads ? 2 : 1;
+        const int threads = std::max(d, ((members + mpt - 1) / mpt + kWave - 1) / kWave * kWave);
+#define SANTAPP_REGS(TT, DD)                                                                        \
+    do {                                                                                           \
+        if (mpt == 1)                                                                              \
+            k_build_parent_regs<TT, DD, 1><<<grid, threads, 0, s>>>(                               \
+                static_cast<const TT*>(K), N, P, R, M, team_begin, team_size, log_n, rep_token, perm); \
+        else                                                                                       \
+            k_build_parent_regs<TT, DD, 2><<<grid, threads, 0, s>>>(                               \
+                static_cast<const TT*>(K), N, P, R, M, team_begin, team_size, log_n, rep_token, perm); \
+        return hipGetLastError();                                                                  \
+    } while (0)
+        if (dtype == SANTAPP_BF16 && d == 128) SANTAPP_REGS(bf16_t, 128);
+        if (dtype == SANTAPP_BF16 && d == 64) SANTAPP_REGS(bf16_t, 64);
+        if (dtype == SANTAPP_FP32 && d == 64) SANTAPP_REGS(float, 64);
+#undef SANTAPP_REGS
+    }
     if (dtype == SANTAPP_BF16)
         k_build_parent<bf16_t><<<grid, kBuildThreads, 0, s>>>(
             static_cast<const bf16_t*>(K), N, d, P, R, M, mind, owner, team_begin, team_size,

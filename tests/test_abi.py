@@ -65,6 +65,14 @@ def test_host_argument_checks():
     assert L.santapp_build_teams(fake, fake, 1, 1, 16, 64, 7, 4, 2, None, ctypes.byref(h)) == _lib.EDTYPE
     assert L.santapp_build_teams(fake, fake, 1, 1, 16, 96, 0, 4, 2, None, ctypes.byref(h)) == _lib.ELIMIT
     assert L.santapp_build_teams(fake, fake, 1, 1, 16, 64, 0, 4, 2000, None, ctypes.byref(h)) == _lib.ELIMIT
+    # misaligned device pointers (16-byte vector accesses)
+    odd = vp(0x1008)
+    assert L.santapp_build_teams(odd, fake, 1, 1, 16, 64, 0, 4, 2, None, ctypes.byref(h)) == _lib.EINVAL
+    assert b"aligned" in L.santapp_last_error()
+    assert L.santapp_dense_decode(odd, fake, fake, 1, 4, 100, 128, 0, None, None, 0, 28, 0.0,
+                                  fake, fake, 1 << 30, None) == _lib.EINVAL
+    assert L.santapp_dense_decode(fake, fake, fake, 1, 4, 100, 128, 0, None, None, 0, 28, 0.0,
+                                  fake, odd, 1 << 30, None) == _lib.EINVAL
     # decode without a table
     assert L.santapp_decode(None, fake, None, None, 0, 1, 1, 0, 0, 0.0, fake, fake, 10, None, None) == _lib.EINVAL
     # dense workspace query is pure host arithmetic

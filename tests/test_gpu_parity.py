@@ -241,3 +241,43 @@ def test_device_side_argument_errors():
     with pytest.raises(sp.SantappError) as e:
         sp.decode(teams, db.q, db.sK, db.sV, wl.K, scale=float("nan"), workspace=ws)
     assert e.value.status == sp._lib.EINVAL
+
+
+@pytest.mark.parametrize("name,base,kw", [
+    # bf16, d = 64, two members per thread, 70 representatives (two rank
+    # blocks), a short last parent
+    ("b64", "qwen8k", dict(d=64, N=3000, P=700, R=70, Hq=4, Hkv=2)),
+    # fp32 rows of 64 values, two members per thread
+    ("f32w", "tiny", dict(N=2000, P=600, R=9)),
+    # more teams per parent than threads (600 > 512): the team-size scan
+    # takes two passes
+    ("manyreps", "qwen8k", dict(N=2048, P=1024, R=600, Hq=2, Hkv=1)),
+    # one representative per parent, a parent just past one member per thread
+    ("onerep", "qwen8k", dict(N=1500, P=513, R=1, Hq=2, Hkv=1)),
+])
+def test_build_tables_shapes(name, base, kw):
+    wl = datagen.WORKLOADS[base].with_(name=name, **kw)
+    log(f"[gpu] build tables {name}: d={wl.d} N={wl.N} P={wl.P} R={wl.R} dtype={wl.dtype}")
+    b = datagen.generate(wl)
+    db = dev_batch(b)
+    kv_pairs = [(bi, kv) for bi in range(wl.B) for kv in range(wl.Hkv)]
+    ot = oracle_teams(b, kv_pairs)
+    teams = sp.build_teams(db.K, db.V, wl.P, wl.R)
+    torch.cuda.synchronize()
+    _check_tables(db, teams, ot, kv_pairs)
+
+
+def test_build_tables_duplicate_keys():
+    # exact duplicate rows: zero distances and ties everywhere, so every
+    # choice is made by the tie rules (lowest token index, earliest
+    # representative)
+    wl = datagen.WORKLOADS["qwen8k"].with_(name="dups", N=2048, P=1024, R=16, Hq=2, Hkv=1)
+    b = datagen.generate(wl)
+    b.K[:, :, 512:1024] = b.K[:, :, 0:512]
+    b.K[:, :, 1024 + 3::7] = b.K[:, :, 1024:1025]
+    log("[gpu] build tables with duplicate keys")
+    db = dev_batch(b)
+    ot = oracle_teams(b, [(0, 0)])
+    teams = sp.build_teams(db.K, db.V, wl.P, wl.R)
+    torch.cuda.synchronize()
+    _check_tables(db, teams, ot, [(0, 0)])
