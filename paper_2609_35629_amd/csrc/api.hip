@@ -229,18 +229,19 @@ santapp_status santapp_build_teams(const void* K, const void* V, int B, int Hkv,
         return fail(SANTAPP_ENOMEM, "device allocation failed: %s", hipGetErrorString(e));
     }
     const char* what = "team build";
-    e = launch_build_parents(K, dtype, static_cast<int>(BH), N, d, parent_size, reps_per_parent,
+    bool packed = false;
+    e = launch_build_parents(K, V, dtype, static_cast<int>(BH), N, d, parent_size, reps_per_parent,
                              t->M, mind, owner, t->team_begin, t->team_size, t->log_n,
-                             t->rep_token, t->perm, s);
-    if (e == hipSuccess) {
+                             t->rep_token, t->perm, t->packed_K, t->packed_V, t->reps, &packed, s);
+    if (e == hipSuccess && !packed) {
         what = "packing K";
         e = launch_gather_rows(K, t->packed_K, t->perm, static_cast<int>(BH), N, N, row, s);
     }
-    if (e == hipSuccess) {
+    if (e == hipSuccess && !packed) {
         what = "packing V";
         e = launch_gather_rows(V, t->packed_V, t->perm, static_cast<int>(BH), N, N, row, s);
     }
-    if (e == hipSuccess) {
+    if (e == hipSuccess && !packed) {
         what = "gathering representatives";
         e = launch_gather_rows(K, t->reps, t->rep_token, static_cast<int>(BH), t->M, N, row, s);
     }

@@ -240,6 +240,11 @@ struct RegRow<bf16_t, D> {
 #pragma unroll
         for (int k = 0; k < 4; ++k) asm volatile("" : "+v"(w[j0 / 2 + k]));
     }
+    __device__ __forceinline__ void store(bf16_t* row) const {
+        uint4* p = reinterpret_cast<uint4*>(row);
+#pragma unroll
+        for (int k = 0; k < kWords / 4; ++k) p[k] = make_uint4(w[4 * k], w[4 * k + 1], w[4 * k + 2], w[4 * k + 3]);
+    }
 };
 
 template <int D>
@@ -265,6 +270,11 @@ struct RegRow<float, D> {
     __device__ __forceinline__ void opaque8(int j0) {
 #pragma unroll
         for (int k = 0; k < 8; ++k) asm volatile("" : "+v"(w[j0 + k]));
+    }
+    __device__ __forceinline__ void store(float* row) const {
+        float4* p = reinterpret_cast<float4*>(row);
+#pragma unroll
+        for (int k = 0; k < kWords / 4; ++k) p[k] = make_float4(w[4 * k], w[4 * k + 1], w[4 * k + 2], w[4 * k + 3]);
     }
 };
 
@@ -307,12 +317,16 @@ __device__ __forceinline__ ArgVal reg_block_arg(ArgVal x, ArgVal* s_red, int nw)
 
 // Thread t owns members t + k * blockDim.x, k < MPT, and is launched with
 // max(D, ceil(members / MPT) rounded up to a wave) threads.  Two members per
-// thread let one LDS read of the representative serve two distances.
+// thread let one LDS read of the representative serve two distances.  The
+// kernel also writes the parent's rows of the packed copies: each member's
+// key from its registers and its value row, at its packed position, and the
+// representative key of each of its teams.
 template <typename T, int D, int MPT>
 __global__ __launch_bounds__(kRegThreads) void k_build_parent_regs(
-    const T* __restrict__ K, int N, int P, int R, int M, int* __restrict__ team_begin,
-    int* __restrict__ team_size, double* __restrict__ log_n, int* __restrict__ rep_token,
-    int* __restrict__ perm) {
+    const T* __restrict__ K, const T* __restrict__ V, int N, int P, int R, int M,
+    int* __restrict__ team_begin, int* __restrict__ team_size, double* __restrict__ log_n,
+    int* __restrict__ rep_token, int* __restrict__ perm, T* __restrict__ packed_K,
+    T* __restrict__ packed_V, T* __restrict__ reps) {
 #pragma clang fp contract(off)
     __shared__ __align__(16) double s_vec[2][D];  // the mean, then each new representative
     __shared__ __align__(16) float s_tile[kWave][D];  // one wave's rows, for the mean
@@ -499,6 +513,9 @@ __global__ __launch_bounds__(kRegThreads) void k_build_parent_regs(
     // representative, slot and wave
     int* pperm = perm + static_cast<size_t>(bh) * N + start;
     const uint64_t lt = lanemask_lt();
+    int pos[MPT];
+#pragma unroll
+    for (int k = 0; k < MPT; ++k) pos[k] = 0;
     for (int ub = 0; ub < r; ub += kRankBlock) {
         const int nb = min(kRankBlock, r - ub);
         int rank_in_wave[MPT];
@@ -517,14 +534,36 @@ __global__ __launch_bounds__(kRegThreads) void k_build_parent_regs(
         for (int k = 0; k < MPT; ++k) {
             const int ok = member[k] ? o[k] : -1;
             if (ok >= ub && ok < ub + nb) {
-                int pos = s_off[ok] + rank_in_wave[k];
+                int ps = s_off[ok] + rank_in_wave[k];
                 for (int kk = 0; kk < k; ++kk)
-                    for (int v = 0; v < nw; ++v) pos += s_wcnt[kk][v][ok - ub];
-                for (int v = 0; v < w; ++v) pos += s_wcnt[k][v][ok - ub];
-                pperm[pos] = start + tid + k * nt;
+                    for (int v = 0; v < nw; ++v) ps += s_wcnt[kk][v][ok - ub];
+                for (int v = 0; v < w; ++v) ps += s_wcnt[k][v][ok - ub];
+                pperm[ps] = start + tid + k * nt;
+                pos[k] = ps;
             }
         }
         __syncthreads();
+    }
+
+    // packed copies: key rows from registers, value rows copied, and each
+    // team's representative key (its member's row, re-read from memory)
+    constexpr int kChunks = D * static_cast<int>(sizeof(T)) / 16;  // 16-byte chunks per row
+    const size_t prow0 = static_cast<size_t>(bh) * N + start;
+#pragma unroll
+    for (int k = 0; k < MPT; ++k) {
+        if (member[k]) {
+            const size_t prow = prow0 + pos[k];
+            row[k].store(packed_K + prow * D);
+            const uint4* src = reinterpret_cast<const uint4*>(V + (prow0 + tid + k * nt) * D);
+            uint4* dst = reinterpret_cast<uint4*>(packed_V + prow * D);
+#pragma unroll
+            for (int c = 0; c < kChunks; ++c) dst[c] = src[c];
+        }
+    }
+    for (int c = tid; c < r * kChunks; c += nt) {
+        const int u = c / kChunks, q = c - u * kChunks;
+        reinterpret_cast<uint4*>(reps + (tbase + u) * D)[q] =
+            reinterpret_cast<const uint4*>(Kc + static_cast<size_t>(s_reps[u]) * D)[q];
     }
 }
 
@@ -548,10 +587,12 @@ __global__ __launch_bounds__(256) void k_gather_rows(const uint4* __restrict__ s
 
 }  // namespace
 
-hipError_t launch_build_parents(const void* K, santapp_dtype dtype, int BH, int N, int d, int P,
-                                int R, int M, double* mind, int* owner, int* team_begin,
-                                int* team_size, double* log_n, int* rep_token, int* perm,
+hipError_t launch_build_parents(const void* K, const void* V, santapp_dtype dtype, int BH, int N,
+                                int d, int P, int R, int M, double* mind, int* owner,
+                                int* team_begin, int* team_size, double* log_n, int* rep_token,
+                                int* perm, void* packed_K, void* packed_V, void* reps, bool* packed,
                                 hipStream_t s) {
+    *packed = false;
     const dim3 grid((N + P - 1) / P, BH);
     // register-resident kernel where a parent fits 2 kRegThreads members and
     // a row 64 registers (two members per thread above kRegThreads); the
@@ -561,15 +602,15 @@ hipError_t launch_build_parents(const void* K, santapp_dtype dtype, int BH, int 
     if (members <= 2 * kRegThreads && R <= kMaxReps) {
         const int mpt = members > kRegThreads ? 2 : 1;
         const int threads = std::max(d, ((members + mpt - 1) / mpt + kWave - 1) / kWave * kWave);
-#define SANTAPP_REGS(TT, DD)                                                                        \
-    do {                                                                                           \
-        if (mpt == 1)                                                                              \
-            k_build_parent_regs<TT, DD, 1><<<grid, threads, 0, s>>>(                               \
-                static_cast<const TT*>(K), N, P, R, M, team_begin, team_size, log_n, rep_token, perm); \
-        else                                                                                       \
-            k_build_parent_regs<TT, DD, 2><<<grid, threads, 0, s>>>(                               \
-                static_cast<const TT*>(K), N, P, R, M, team_begin, team_size, log_n, rep_token, perm); \
-        return hipGetLastError();                                                                  \
+#define SANTAPP_REGS(TT, DD)                                                                       \
+    do {                                                                                          \
+        auto kern = mpt == 1 ? k_build_parent_regs<TT, DD, 1> : k_build_parent_regs<TT, DD, 2>;  \
+        kern<<<grid, threads, 0, s>>>(static_cast<const TT*>(K), static_cast<const TT*>(V), N, P, R, \
+                                      M, team_begin, team_size, log_n, rep_token, perm,           \
+                                      static_cast<TT*>(packed_K), static_cast<TT*>(packed_V),    \
+                                      static_cast<TT*>(reps));                                    \
+        *packed = true;                                                                           \
+        return hipGetLastError();                                                                 \
     } while (0)
         if (dtype == SANTAPP_BF16 && d == 128) SANTAPP_REGS(bf16_t, 128);
         if (dtype == SANTAPP_BF16 && d == 64) SANTAPP_REGS(bf16_t, 64);

@@ -93,9 +93,13 @@ DecodeLayout dense_layout(int B, int Hq, int Hkv, int N, int T, int d);
 __host__ __device__ inline int chunk_count(int rows) { return (rows + kChunkRows - 1) / kChunkRows; }
 __host__ __device__ inline int dense_count(int rows) { return (rows + kDenseRows - 1) / kDenseRows; }
 
-hipError_t launch_build_parents(const void* K, santapp_dtype dtype, int BH, int N, int d, int P,
-                                int R, int M, double* mind, int* owner, int* team_begin,
-                                int* team_size, double* log_n, int* rep_token, int* perm,
+// Team table of every parent.  Where the register-resident kernel runs it
+// also writes the packed copies (packed_K, packed_V, reps) and sets *packed;
+// otherwise the caller gathers them from perm and rep_token.
+hipError_t launch_build_parents(const void* K, const void* V, santapp_dtype dtype, int BH, int N,
+                                int d, int P, int R, int M, double* mind, int* owner,
+                                int* team_begin, int* team_size, double* log_n, int* rep_token,
+                                int* perm, void* packed_K, void* packed_V, void* reps, bool* packed,
                                 hipStream_t s);
 
 hipError_t launch_gather_rows(const void* src, void* dst, const int* index, int BH, int rows_out,
