@@ -56,7 +56,7 @@ def lib():
                                          ctypes.c_int, _i, _i, _i]
         L.oracle_build_teams.restype = ctypes.c_int
         L.oracle_decode_head.argtypes = (
-            [_d, ctypes.c_int, _d, _d, ctypes.c_int, _i, _i, _i, ctypes.c_int,
+            [_d, ctypes.c_int, _d, _d, ctypes.c_int, _i, _i, _i, _d, ctypes.c_int,
              _d, _d, ctypes.c_int, ctypes.c_int, ctypes.c_uint64, ctypes.c_uint64,
              ctypes.c_uint64, ctypes.c_uint64, ctypes.c_double, ctypes.c_double,
              _d, _d, _d, _d, _d, _d, _i, _d, _d])
@@ -64,6 +64,8 @@ def lib():
         L.oracle_dense_head.argtypes = [_d, ctypes.c_int, _d, _d, ctypes.c_int, _d, _d,
                                         ctypes.c_int, ctypes.c_double, _d, _d, _d, _d]
         L.oracle_dense_head.restype = ctypes.c_int
+        L.oracle_team_means.argtypes = [_d, ctypes.c_int, _i, _i, ctypes.c_int, _d]
+        L.oracle_team_means.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -162,7 +164,10 @@ class HeadResult:
 
 
 def decode_head(q, K, V, teams: Teams, sK, sV, Kbudget: int, seed: int, step: int,
-                b: int, h: int, scale: float, ref_shift: float = float("nan")) -> HeadResult:
+                b: int, h: int, scale: float, ref_shift: float = float("nan"),
+                route_keys: Optional[np.ndarray] = None) -> HeadResult:
+    """``route_keys [M, d]``: the keys the teams are routed by (default: the
+    representative keys; the team means for the centroid-guided variant)."""
     q = _f64(q)
     K = _f64(K)
     V = _f64(V)
@@ -183,8 +188,14 @@ def decode_head(q, K, V, teams: Teams, sK, sV, Kbudget: int, seed: int, step: in
     members = np.ascontiguousarray(teams.members, np.int32)
     tptr = np.ascontiguousarray(teams.team_ptr, np.int32)
     reps = np.ascontiguousarray(teams.rep_token, np.int32)
+    rk = None
+    if route_keys is not None:
+        rk = _f64(route_keys)
+        if rk.shape != (M, d):
+            raise ValueError("route_keys must be [M, d]")
     ns = lib().oracle_decode_head(
-        _pd(q), d, _pd(K), _pd(V), K.shape[0], _pi(members), _pi(tptr), _pi(reps), M,
+        _pd(q), d, _pd(K), _pd(V), K.shape[0], _pi(members), _pi(tptr), _pi(reps),
+        _pd(rk) if rk is not None else None, M,
         _pd(sK), _pd(sV), T, int(Kbudget), seed, step, b, h, float(scale), float(ref_shift),
         _pd(out), _pd(U), _pd(Z), _pd(sh), _pd(phi), _pd(Y), _pi(sel), _pd(c), _pd(tau))
     if ns < 0:
@@ -218,7 +229,7 @@ class StepResult:
 
 
 def decode(q, K, V, sK, sV, teams, Kbudget: int, seed: int, step: int, scale: float,
-           heads: Optional[List[tuple]] = None) -> StepResult:
+           heads: Optional[List[tuple]] = None, route_keys=None) -> StepResult:
     """Alg. 1 for every (b, h) (or only the listed ``heads`` pairs).
 
     ``q [B,Hq,d]``, ``K,V [B,Hkv,N,d]``, ``sK,sV [B,Hkv,T,d]`` hold exact
@@ -237,7 +248,8 @@ def decode(q, K, V, sK, sV, teams, Kbudget: int, seed: int, step: int, scale: fl
         if (b, kv) not in cache:
             cache = {(b, kv): (_f64(K[b, kv]), _f64(V[b, kv]), _f64(sK[b, kv]), _f64(sV[b, kv]))}
         Kb, Vb, sKb, sVb = cache[(b, kv)]
-        r = decode_head(q[b, h], Kb, Vb, teams[b][kv], sKb, sVb, Kbudget, seed, step, b, h, scale)
+        r = decode_head(q[b, h], Kb, Vb, teams[b][kv], sKb, sVb, Kbudget, seed, step, b, h, scale,
+                        route_keys=None if route_keys is None else route_keys[b][kv])
         out[b, h] = r.out
         res[b][h] = r
     return StepResult(out, res)
@@ -258,6 +270,92 @@ def dense(q, K, V, sK, sV, scale: float, heads: Optional[List[tuple]] = None) ->
 # --------------------------------------------------------------------------
 # Logical KV-access counter (eq. qwen-logical-access)
 # --------------------------------------------------------------------------
+# --------------------------------------------------------------------------
+# Routing keys of the centroid-guided variant and the KL routing diagnostic
+# (section "Attention-distribution diagnostic", appendix "Dense-trajectory KL
+# and task-variant evaluation", eq. diagnostic-kl)
+# --------------------------------------------------------------------------
+def team_means(K: np.ndarray, teams: Teams) -> np.ndarray:
+    """``[M, d]`` arithmetic mean of each team's keys (fp64; per dimension the
+    members are summed in team order, then divided by n_g)."""
+    K = _f64(K)
+    d = K.shape[1]
+    out = np.empty((teams.M, d))
+    members = np.ascontiguousarray(teams.members, np.int32)
+    tptr = np.ascontiguousarray(teams.team_ptr, np.int32)
+    if lib().oracle_team_means(_pd(K), d, _pi(members), _pi(tptr), teams.M, _pd(out)) != 0:
+        raise ValueError("oracle_team_means rejected its arguments")
+    return out
+
+
+_BF16_MAX = float(np.array([0x7F7F0000], np.uint32).view(np.float32)[0])
+_BF16_OVERFLOW = _BF16_MAX + 2.0 ** (127 - 8)  # halfway to the next binade: rounds to inf
+
+
+def round_to_bf16(x) -> np.ndarray:
+    """Each fp64 value rounded to the nearest bf16 value, ties to an even
+    significand (round-to-nearest-even), returned as fp64 values.
+
+    The nearest bf16 lies within one bf16 step of the bf16 truncation of the
+    value's nearest fp32; of those three candidates the nearest is taken (the
+    distances are exact: each candidate is within a factor of two of x)."""
+    x = _f64(x)
+    with np.errstate(invalid="ignore", over="ignore"):
+        f = x.astype(np.float32).view(np.uint32).astype(np.int64)
+        t = f & 0xFFFF0000
+        cand = np.stack([t - 0x10000, t, t + 0x10000]) & 0xFFFFFFFF
+        cv = cand.astype(np.uint32).view(np.float32).astype(np.float64)
+    dist = np.where(np.isfinite(cv), np.abs(cv - x[None]), np.inf)
+    best = np.argmin(dist, axis=0)
+    bd = np.take_along_axis(dist, best[None], 0)[0]
+    tied = (dist == bd[None]) & np.isfinite(dist)
+    even = ((cand >> 16) & 1) == 0
+    # among tied candidates prefer the even one (at most two can tie)
+    pick = np.where(tied.sum(0) > 1, np.argmax(tied & even, axis=0), best)
+    out = np.take_along_axis(cv, pick[None], 0)[0]
+    out = np.where(np.abs(x) >= _BF16_OVERFLOW, np.copysign(np.inf, x), out)
+    out = np.where(np.isnan(x), np.nan, out)
+    return np.where(x == 0, x, out)
+
+
+def routing_keys(K: np.ndarray, teams: Teams, kind: str, dtype: str) -> np.ndarray:
+    """``[M, d]`` keys the teams are routed by: ``"representative"`` (the
+    representative's key) or ``"centroid"`` (the team mean, stored in the
+    cache's element type: rounded to nearest-even bf16, or to fp32)."""
+    K = _f64(K)
+    if kind == "representative":
+        return K[teams.rep_token]
+    if kind != "centroid":
+        raise ValueError(kind)
+    m = team_means(K, teams)
+    if dtype == "bf16":
+        return round_to_bf16(m)
+    return m.astype(np.float32).astype(np.float64)
+
+
+def _logsumexp(v: np.ndarray) -> float:
+    mx = np.max(v)
+    return float(mx + np.log(np.sum(np.exp(v - mx))))
+
+
+def routing_kl(q, K, teams: Teams, route_keys, scale: float) -> float:
+    """eq. diagnostic-kl for one query head: KL(p || q) in nats, with p the
+    dense attention over the N prompt tokens and q_i = P(g(i)) / n_g(i), where
+    P is the softmax over teams of log n_g + scale q . key_g."""
+    q = _f64(q)
+    K = _f64(K)
+    s = scale * (K @ q)
+    logp = s - _logsumexp(s)
+    n = teams.sizes.astype(np.float64)
+    phi = np.log(n) + scale * (_f64(route_keys) @ q)
+    logP = phi - _logsumexp(phi)
+    group = np.empty(K.shape[0], np.int64)
+    for g in range(teams.M):
+        group[teams.members[teams.team_ptr[g]:teams.team_ptr[g + 1]]] = g
+    logq = logP[group] - np.log(n[group])
+    return float(np.sum(np.exp(logp) * (logp - logq)))
+
+
 def union_rows(teams: Teams, selections) -> int:
     """Prompt rows read for one KV head: the union of the selected teams of
     the query heads sharing it (teams are disjoint, so sizes add)."""

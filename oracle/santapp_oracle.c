@@ -209,6 +209,9 @@ int oracle_build_teams(const double* K, int N, int d, int P, int R,
 /* and Z_hat are returned in that shifted scale and *shift_out = m, so that  */
 /* the unshifted sums are U_hat * e^m and Z_hat * e^m.                       */
 /*                                                                           */
+/* route_keys [M, d] (NULL: the representative keys K[rep_token[g]]) gives   */
+/* the key each team is routed by: the centroid-guided variant routes by    */
+/* the team mean (section "Attention-distribution diagnostic").              */
 /* Optional outputs (NULL to skip): phi[M], Y[M]; sel[M] receives the        */
 /* selected team ids in ascending order and c_sel[M] their corrections;      */
 /* *tau_out is -inf when every team is selected.  Returns |S|, or -1.        */
@@ -226,7 +229,8 @@ static int rank_cmp(const void* a, const void* b)
 
 int oracle_decode_head(const double* q, int d,
                        const double* K, const double* V, int N,
-                       const int* members, const int* team_ptr, const int* rep_token, int M,
+                       const int* members, const int* team_ptr, const int* rep_token,
+                       const double* route_keys, int M,
                        const double* sK, const double* sV, int T,
                        int Kbudget, uint64_t seed, uint64_t step, uint64_t b, uint64_t h,
                        double scale, double ref_shift,
@@ -250,7 +254,8 @@ int oracle_decode_head(const double* q, int d,
         for (int g = 0; g < M; ++g) { c[g] = 1.0; in_S[g] = 1; ph[g] = NAN; yy[g] = NAN; }
     } else {
         for (int g = 0; g < M; ++g) {
-            const double* l = K + (size_t)rep_token[g] * d;
+            /* routing key: the representative's key, or route_keys[g] when given */
+            const double* l = route_keys ? route_keys + (size_t)g * d : K + (size_t)rep_token[g] * d;
             double dot = 0.0;
             for (int j = 0; j < d; ++j) dot = dot + q[j] * l[j];
             int n_g = team_ptr[g + 1] - team_ptr[g];
@@ -374,5 +379,27 @@ int oracle_dense_head(const double* q, int d, const double* K, const double* V, 
     *Z = z;
     *shift_out = m;
     free(s);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Team means (the routing keys of the centroid-guided variant, section      */
+/* "Attention-distribution diagnostic": the arithmetic mean of the group's  */
+/* keys).  Per team and dimension the members' values are summed in team    */
+/* order (ascending token index) and divided by n_g.  out: [M, d].          */
+/* ------------------------------------------------------------------------ */
+int oracle_team_means(const double* K, int d, const int* members, const int* team_ptr, int M,
+                      double* out)
+{
+    if (d < 1 || M < 1) return -1;
+    for (int g = 0; g < M; ++g) {
+        int n = team_ptr[g + 1] - team_ptr[g];
+        if (n < 1) return -1;
+        for (int j = 0; j < d; ++j) {
+            double s = 0.0;
+            for (int t = team_ptr[g]; t < team_ptr[g + 1]; ++t) s = s + K[(size_t)members[t] * d + j];
+            out[(size_t)g * d + j] = s / (double)n;
+        }
+    }
     return 0;
 }
