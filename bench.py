@@ -47,10 +47,36 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="budget of the oracle CPU-baseline sample (0 disables it)")
     p.add_argument("--no-dense", action="store_true")
+    p.add_argument("--kl-table", action="store_true",
+                   help="print the routing KL diagnostic of several groupings of the workload and exit")
     p.add_argument("--calibrate-copy", action="store_true",
                    help="only run a plain 256 MiB device-to-device copy five times (the reference "
                         "kernel for scaling the FETCH_SIZE / WRITE_SIZE counters) and exit")
     return p.parse_args()
+
+
+def kl_table(wl, db):
+    """Mean KL(p || q) in nats (eq. diagnostic-kl) over every (sequence, query
+    head) of the workload, for teams and for centroid-guided sampling over
+    contiguous groups (one team of B tokens per parent, routed by its mean),
+    the groupings the paper's routing table compares (there with k-means
+    groups on recorded model states)."""
+    import paper_2609_35629_amd as sp
+    variants = [("teams P=16 R=4 (representative keys)", 16, 4, "representative"),
+                ("teams P=16 R=4 (team means)", 16, 4, "centroid"),
+                ("centroid-guided B=4 (contiguous)", 4, 1, "centroid"),
+                ("centroid-guided B=16 (contiguous)", 16, 1, "centroid"),
+                (f"teams P={wl.P} R={wl.R} (representative keys)", wl.P, wl.R, "representative"),
+                (f"teams P={wl.P} R={wl.R} (team means)", wl.P, wl.R, "centroid")]
+    rows = []
+    for name, P, R, kind in variants:
+        t = sp.build_teams(db["K"], db["V"], P, R)
+        sp.set_route_keys(t, kind)
+        kl = sp.routing_kl(t, db["q"], scale=wl.scale)
+        rows.append({"variant": name, "P": P, "R": R, "M": t.M, "route_keys": kind,
+                     "mean_kl_nats": round(float(kl.mean().item()), 4)})
+        t.close()
+    print(json.dumps({"workload": wl.name, "N": wl.N, "B": wl.B, "Hq": wl.Hq, "kl_table": rows}))
 
 
 def main():
@@ -82,6 +108,9 @@ def main():
     print(f"[bench] workload={wl.name} B={wl.B} N={wl.N} K={wl.K} T={wl.T}", file=sys.stderr, flush=True)
     batch = datagen.generate(wl)
     db = upload(batch)
+    if args.kl_table:
+        kl_table(wl, db)
+        return
     teams = sp.build_teams(db["K"], db["V"], wl.P, wl.R)
     M = teams.M
     ws = sp.decode_workspace(teams, wl.Hq, wl.T, wl.K)
@@ -183,6 +212,14 @@ def main():
         prep_us.append((time.perf_counter() - t0) * 1e6)
         extra.close()
 
+    # routing diagnostic (eq. diagnostic-kl) of this table on the step's
+    # queries, routed by the representative keys and by the team means
+    routing_kl = {}
+    for kind in ("representative", "centroid"):
+        sp.set_route_keys(teams, kind)
+        routing_kl[kind] = round(float(sp.routing_kl(teams, db["q"], scale=wl.scale).mean().item()), 4)
+    sp.set_route_keys(teams, "representative")
+
     cpu = None
     if args.cpu_seconds > 0:
         cpu = cpu_baseline(wl, batch, args.cpu_seconds)
@@ -207,6 +244,7 @@ def main():
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic},
         "prep_us": round(float(np.median(prep_us)), 1),
+        "routing_kl_nats": routing_kl,
         "step_gbs": round(float(np.mean(step_bytes) / value / 1e3), 1),
         "step_hbm_frac": round(float(np.mean(step_bytes) / value / 1e3) / HBM_PEAK_GBS, 4),
         "step_bytes_mean": int(np.mean(step_bytes)),

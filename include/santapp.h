@@ -16,6 +16,9 @@
  *                         eq. method-estimate, GQA sharing of the reads.
  *   santapp_dense_decode  eq. method-attention over the whole current cache
  *                         (the dense baseline).
+ *   santapp_teams_set_route_keys, santapp_routing_kl
+ *                         section "Attention-distribution diagnostic":
+ *                         centroid routing keys and eq. diagnostic-kl.
  *
  * Conventions
  *   - Every tensor argument is a DEVICE pointer owned by the caller unless
@@ -66,7 +69,9 @@ typedef struct {
     int M;                   /* teams per (b, kv); identical for all (b, kv) */
     const void* packed_K;    /* [B,Hkv,N,d] prompt keys in team order        */
     const void* packed_V;    /* [B,Hkv,N,d] prompt values in team order      */
-    const void* reps;        /* [B,Hkv,M,d] representative key of each team  */
+    const void* reps;        /* [B,Hkv,M,d] routing key of each team (its    */
+                             /* representative's key unless changed by       */
+                             /* santapp_teams_set_route_keys)                */
     const int* team_begin;   /* [B,Hkv,M] first packed row of each team      */
     const int* team_size;    /* [B,Hkv,M] n_g                                */
     const double* log_n;     /* [B,Hkv,M] log n_g (fp64)                     */
@@ -97,6 +102,27 @@ typedef struct {
 santapp_status santapp_build_teams(const void* K, const void* V, int B, int Hkv, int N, int d,
                                    santapp_dtype dtype, int parent_size, int reps_per_parent,
                                    void* stream, santapp_teams** out);
+
+/*
+ * Keys the teams are routed by (the table's `reps`; section
+ * "Attention-distribution diagnostic" and its appendix, which compare
+ * routing by an actual representative key with centroid-guided sampling):
+ *   SANTAPP_ROUTE_REPRESENTATIVE  each team's representative key (the state
+ *                                 santapp_build_teams leaves);
+ *   SANTAPP_ROUTE_CENTROID        the arithmetic mean of the team's keys: per
+ *                                 dimension the members' values summed in fp64
+ *                                 in team order (ascending token index),
+ *                                 divided by n_g, rounded to the table's
+ *                                 element type (nearest, ties to even).
+ * With contiguous parents of B tokens and one representative each
+ * (parent_size = B, reps_per_parent = 1) the centroid keys give the paper's
+ * centroid-guided sampling over contiguous groups.  Decoding with a table
+ * uses whichever keys it holds; the team partition is unchanged.  Enqueued
+ * on `stream`; never allocates.
+ */
+typedef enum { SANTAPP_ROUTE_REPRESENTATIVE = 0, SANTAPP_ROUTE_CENTROID = 1 } santapp_route_key;
+
+santapp_status santapp_teams_set_route_keys(santapp_teams* teams, santapp_route_key kind, void* stream);
 
 /* Fill *desc with the table's sizes and device pointers. */
 santapp_status santapp_teams_info(const santapp_teams* teams, santapp_teams_desc* desc);
@@ -180,6 +206,21 @@ santapp_status santapp_dense_decode(const float* q, const void* K, const void* V
                                     int N, int d, santapp_dtype dtype, const void* suffix_K,
                                     const void* suffix_V, int T, int Hq, double scale, float* out,
                                     void* workspace, size_t ws_bytes, void* stream);
+
+/* Workspace for santapp_routing_kl (bytes, host-only query). */
+santapp_status santapp_routing_kl_workspace_bytes(const santapp_teams* teams, int Hq, size_t* bytes);
+
+/*
+ * Routing diagnostic of eq. diagnostic-kl for every sequence b and query head
+ * h: KL(p || q) in nats, with p the dense softmax attention over the N prompt
+ * tokens (the suffix excluded) and q_i = P(g(i)) / n_g(i), where P is the
+ * softmax over the teams of log n_g + scale q . key_g with the table's
+ * current routing keys (no sampling).  Scores, sums and logarithms in fp64.
+ * q: [B,Hq,d] fp32; kl: [B,Hq] fp64 (device).  scale 0 means 1/sqrt(d).
+ * Never allocates; the workspace needs no initialisation.
+ */
+santapp_status santapp_routing_kl(const santapp_teams* teams, const float* q, int Hq, double scale,
+                                  double* kl, void* workspace, size_t ws_bytes, void* stream);
 
 /* Message of the last failed call on this thread ("" if none). */
 const char* santapp_last_error(void);

@@ -128,6 +128,35 @@ def build_teams(K: torch.Tensor, V: torch.Tensor, parent_size: int, reps_per_par
     return Teams(h, K.dtype)
 
 
+def set_route_keys(teams: Teams, kind: str, stream=None) -> None:
+    """Route the teams by ``"representative"`` keys (the default after
+    :func:`build_teams`) or by ``"centroid"`` keys (team means)."""
+    code = {"representative": _lib.ROUTE_REPRESENTATIVE, "centroid": _lib.ROUTE_CENTROID}[kind]
+    check(_lib.load().santapp_teams_set_route_keys(teams.handle, code, _stream(stream)))
+
+
+def routing_kl_workspace(teams: Teams, Hq: int) -> torch.Tensor:
+    n = ctypes.c_size_t()
+    check(_lib.load().santapp_routing_kl_workspace_bytes(teams.handle, Hq, ctypes.byref(n)))
+    return torch.empty(max(n.value, 1), dtype=torch.uint8, device="cuda")
+
+
+def routing_kl(teams: Teams, q: torch.Tensor, scale: float = 0.0, out: Optional[torch.Tensor] = None,
+               workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """KL(p || q) per (sequence, query head) in nats, ``[B, Hq]`` fp64 (eq.
+    diagnostic-kl with the table's current routing keys)."""
+    _need(q, "q", dtype=torch.float32)
+    B, Hq, d = q.shape
+    if out is None:
+        out = torch.empty((B, Hq), dtype=torch.float64, device="cuda")
+    _need(out, "out", shape=(B, Hq), dtype=torch.float64)
+    if workspace is None:
+        workspace = routing_kl_workspace(teams, Hq)
+    check(_lib.load().santapp_routing_kl(teams.handle, _ptr(q), Hq, float(scale), _ptr(out), _ptr(workspace),
+                                         workspace.numel(), _stream(stream)))
+    return out
+
+
 def budget_to_K(S: int, P: int, R: int, M: int) -> int:
     k = ctypes.c_int()
     check(_lib.load().santapp_budget_to_K(S, P, R, M, ctypes.byref(k)))

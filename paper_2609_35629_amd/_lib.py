@@ -18,7 +18,10 @@ EXPORTS = [
     "santapp_build_teams", "santapp_teams_info", "santapp_teams_destroy", "santapp_budget_to_K",
     "santapp_decode_workspace_bytes", "santapp_workspace_zero", "santapp_decode",
     "santapp_dense_workspace_bytes", "santapp_dense_decode", "santapp_last_error",
+    "santapp_teams_set_route_keys", "santapp_routing_kl_workspace_bytes", "santapp_routing_kl",
 ]
+
+ROUTE_REPRESENTATIVE, ROUTE_CENTROID = 0, 1
 
 
 class TeamsDesc(ctypes.Structure):
@@ -72,6 +75,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     L.santapp_dense_workspace_bytes.argtypes = [i, i, i, i, i, i, ctypes.POINTER(sz)]
     L.santapp_dense_decode.argtypes = [vp, vp, vp, i, i, i, i, i, vp, vp, i, i, ctypes.c_double,
                                        vp, vp, sz, vp]
+    L.santapp_teams_set_route_keys.argtypes = [vp, i, vp]
+    L.santapp_routing_kl_workspace_bytes.argtypes = [vp, i, ctypes.POINTER(sz)]
+    L.santapp_routing_kl.argtypes = [vp, vp, i, ctypes.c_double, vp, vp, sz, vp]
     L.santapp_last_error.argtypes = []
     L.santapp_last_error.restype = ctypes.c_char_p
     for name in EXPORTS:

@@ -305,6 +305,96 @@ santapp_status santapp_teams_info(const santapp_teams* t, santapp_teams_desc* d)
 
 void santapp_teams_destroy(santapp_teams* t) { free_teams(t); }
 
+santapp_status santapp_teams_set_route_keys(santapp_teams* t, santapp_route_key kind, void* stream) {
+    if (!t) return fail(SANTAPP_EINVAL, "teams is NULL");
+    if (kind != SANTAPP_ROUTE_REPRESENTATIVE && kind != SANTAPP_ROUTE_CENTROID)
+        return fail(SANTAPP_EINVAL, "unknown routing key kind %d", static_cast<int>(kind));
+    const hipError_t e = launch_route_keys(t->packed_K, t->team_begin, t->team_size, t->rep_token, t->perm,
+                                           t->B * t->Hkv, t->N, t->M, t->d, t->dtype,
+                                           kind == SANTAPP_ROUTE_CENTROID, t->reps, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? ok() : hip_fail(e, "routing keys");
+}
+
+namespace {
+
+// KL workspace: phi, Y (unused by the diagnostic, written by the routing
+// kernel) and the per-team sums, each [B, Hq, M].
+struct KlLayout {
+    size_t phi, Y, part, total;
+};
+
+KlLayout kl_layout(int B, int Hq, int M) {
+    const size_t n = static_cast<size_t>(B) * Hq * M;
+    KlLayout L;
+    L.phi = 0;
+    L.Y = align_up(L.phi + n * sizeof(double));
+    L.part = align_up(L.Y + n * sizeof(double));
+    L.total = align_up(L.part + n * kl_part_bytes());
+    return L;
+}
+
+}  // namespace
+
+santapp_status santapp_routing_kl_workspace_bytes(const santapp_teams* t, int Hq, size_t* bytes) {
+    if (!t || !bytes) return fail(SANTAPP_EINVAL, "NULL argument");
+    if (Hq < 1 || Hq % t->Hkv != 0) return fail(SANTAPP_EINVAL, "Hq must be a positive multiple of Hkv");
+    *bytes = kl_layout(t->B, Hq, t->M).total;
+    return ok();
+}
+
+santapp_status santapp_routing_kl(const santapp_teams* t, const float* q, int Hq, double scale, double* kl,
+                                  void* workspace, size_t ws_bytes, void* stream) {
+    if (!t) return fail(SANTAPP_EINVAL, "teams is NULL");
+    if (!q || !kl) return fail(SANTAPP_EINVAL, "q and kl must be device pointers");
+    if (Hq < 1 || Hq % t->Hkv != 0) return fail(SANTAPP_EINVAL, "Hq (%d) must be a positive multiple of Hkv (%d)", Hq, t->Hkv);
+    if (Hq / t->Hkv > kMaxGroup) return fail(SANTAPP_ELIMIT, "%d query heads per KV head exceed %d", Hq / t->Hkv, kMaxGroup);
+    if (!(scale >= 0.0) || !isfinite(scale)) return fail(SANTAPP_EINVAL, "scale must be finite and >= 0");
+    if (scale == 0.0) scale = 1.0 / sqrt(static_cast<double>(t->d));
+    const KlLayout L = kl_layout(t->B, Hq, t->M);
+    if (!workspace || ws_bytes < L.total)
+        return fail(SANTAPP_EWORKSPACE, "workspace of %zu bytes needed (got %zu)", L.total, ws_bytes);
+    if (!aligned16(q) || !aligned16(kl) || !aligned16(workspace))
+        return fail(SANTAPP_EINVAL, "q, kl and workspace must be 16-byte aligned");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    char* ws = static_cast<char*>(workspace);
+    double* phi = reinterpret_cast<double*>(ws + L.phi);
+    RouteArgs R{};
+    R.reps = t->reps;
+    R.team_size = t->team_size;
+    R.log_n = t->log_n;
+    R.team_begin = t->team_begin;
+    R.q = q;
+    R.B = t->B;
+    R.Hkv = t->Hkv;
+    R.Hq = Hq;
+    R.G = Hq / t->Hkv;
+    R.d = t->d;
+    R.M = t->M;
+    R.dtype = t->dtype;
+    R.scale = scale;
+    hipError_t e = launch_route_phi(R, phi, reinterpret_cast<double*>(ws + L.Y), s);
+    if (e != hipSuccess) return hip_fail(e, "routing kernel");
+    KlArgs A{};
+    A.packed_K = t->packed_K;
+    A.team_begin = t->team_begin;
+    A.team_size = t->team_size;
+    A.log_n = t->log_n;
+    A.q = q;
+    A.phi = phi;
+    A.part = ws + L.part;
+    A.kl = kl;
+    A.B = t->B;
+    A.Hkv = t->Hkv;
+    A.Hq = Hq;
+    A.N = t->N;
+    A.M = t->M;
+    A.d = t->d;
+    A.dtype = t->dtype;
+    A.scale = scale;
+    e = launch_routing_kl(A, s);
+    return e == hipSuccess ? ok() : hip_fail(e, "KL kernels");
+}
+
 santapp_status santapp_workspace_zero(void* ws, size_t bytes, void* stream) {
     if (bytes == 0) return ok();
     if (!ws) return fail(SANTAPP_EINVAL, "workspace is NULL");

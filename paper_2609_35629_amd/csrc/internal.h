@@ -124,6 +124,34 @@ struct RouteArgs {
 // (k_select): two launches on the stream.
 hipError_t launch_route_select(const RouteArgs& a, hipStream_t s);
 
+// Routing logits only (k_route): phi and Y for every (b, h, team).
+hipError_t launch_route_phi(const RouteArgs& a, double* phi, double* Y, hipStream_t s);
+
+// Routing keys of a table: the team means (centroid) or the representatives'
+// keys, written to reps [BH, M, d].
+hipError_t launch_route_keys(const void* packed_K, const int* team_begin, const int* team_size,
+                             const int* rep_token, const int* perm, int BH, int N, int M, int d,
+                             santapp_dtype dtype, bool centroid, void* reps, hipStream_t s);
+
+struct KlArgs {
+    const void* packed_K;    // [BH, N, d]
+    const int* team_begin;   // [BH, M]
+    const int* team_size;    // [BH, M]
+    const double* log_n;     // [BH, M]
+    const float* q;          // [B, Hq, d]
+    const double* phi;       // [B, Hq, M] routing logits
+    void* part;              // [B, Hq, M] per-team sums (kl_part_bytes() each)
+    double* kl;              // [B, Hq]
+    int B, Hkv, Hq, N, M, d;
+    santapp_dtype dtype;
+    double scale;
+};
+
+size_t kl_part_bytes();
+
+// Per-team sums over the prompt rows, then KL(p || q) per query head.
+hipError_t launch_routing_kl(const KlArgs& a, hipStream_t s);
+
 struct AttendArgs {
     const void* K;    // [BH, N, d] packed (sampled path) or original (dense path)
     const void* V;

@@ -804,7 +804,36 @@ hipError_t route_t(const RouteArgs& a, hipStream_t s) {
     }
 }
 
+template <typename T, int D>
+hipError_t route_phi_d(const RouteArgs& a, double* phi, double* Y, hipStream_t s) {
+    const dim3 grid((a.M + kRouteTeams - 1) / kRouteTeams, a.B * a.Hkv);
+#define SANTAPP_PHI(GG)                                                                             \
+    case GG:                                                                                        \
+        k_route<T, D, GG><<<grid, kRouteThreads, 0, s>>>(static_cast<const T*>(a.reps), a.log_n, a.q, \
+                                                         a.M, a.Hkv, a.Hq, a.scale, a.seed, a.step,   \
+                                                         phi, Y);                                     \
+        break
+    switch (a.G) {
+        SANTAPP_PHI(1); SANTAPP_PHI(2); SANTAPP_PHI(3); SANTAPP_PHI(4);
+        SANTAPP_PHI(5); SANTAPP_PHI(6); SANTAPP_PHI(7); SANTAPP_PHI(8);
+        default: return hipErrorInvalidValue;
+    }
+#undef SANTAPP_PHI
+    return hipGetLastError();
+}
+
 }  // namespace
+
+hipError_t launch_route_phi(const RouteArgs& a, double* phi, double* Y, hipStream_t s) {
+    if (a.dtype == SANTAPP_BF16) {
+        if (a.d == 128) return route_phi_d<bf16_t, 128>(a, phi, Y, s);
+        if (a.d == 64) return route_phi_d<bf16_t, 64>(a, phi, Y, s);
+    } else {
+        if (a.d == 128) return route_phi_d<float, 128>(a, phi, Y, s);
+        if (a.d == 64) return route_phi_d<float, 64>(a, phi, Y, s);
+    }
+    return hipErrorInvalidValue;
+}
 
 hipError_t launch_route_select(const RouteArgs& a, hipStream_t s) {
     return a.dtype == SANTAPP_BF16 ? route_t<bf16_t>(a, s) : route_t<float>(a, s);
