@@ -281,3 +281,46 @@ def test_build_tables_duplicate_keys():
     teams = sp.build_teams(db.K, db.V, wl.P, wl.R)
     torch.cuda.synchronize()
     _check_tables(db, teams, ot, [(0, 0)])
+
+
+def test_limiting_case_sampling_law():
+    # Every key its own team (P = R = 1): phi_g = scale q . k_g, so a budget
+    # of one team is drawn from softmax(phi), the dense attention p over the
+    # prompt (the limiting case of the routing law).  The GPU's picks over
+    # 4000 steps (fresh Philox noise per step) are tested against p per query
+    # head with a chi-square test (tokens expected fewer than 5 times pooled).
+    from scipy.stats import chi2
+
+    wl = datagen.WORKLOADS["limit"].with_(K=1)
+    log("[gpu] limiting case: sampling law over 4000 steps")
+    b = datagen.generate(wl)
+    db = dev_batch(b)
+    teams = sp.build_teams(db.K, db.V, wl.P, wl.R)
+    assert teams.M == wl.N
+    ws = sp.decode_workspace(teams, wl.Hq, wl.T, 1)
+    dbg = sp.DebugOut(wl.B, wl.Hq, wl.Hkv, teams.M, 1)
+    steps = 4000
+    picks = torch.empty((steps, wl.Hq), dtype=torch.int32, device="cuda")
+    for t in range(steps):
+        sp.decode(teams, db.q, db.sK, db.sV, 1, seed=7, step=t, scale=wl.scale, workspace=ws, debug=dbg)
+        picks[t] = dbg.sel[0, :, 0]
+    torch.cuda.synchronize()
+    picks = picks.cpu().numpy()
+    # team g is token g here: one-token parents in token order
+    pvals = []
+    for h in range(wl.Hq):
+        kv = h // wl.G
+        s = wl.scale * (b.f64(b.K[0, kv]) @ b.q[0, h].astype(np.float64))
+        p = np.exp(s - s.max())
+        p /= p.sum()
+        counts = np.bincount(picks[:, h], minlength=wl.N).astype(np.float64)
+        e = steps * p
+        big = e >= 5
+        obs = np.concatenate([counts[big], [counts[~big].sum()]])
+        exp = np.concatenate([e[big], [e[~big].sum()]])
+        keep = exp > 0
+        stat = float(np.sum((obs[keep] - exp[keep]) ** 2 / exp[keep]))
+        dof = int(keep.sum()) - 1
+        pvals.append(float(chi2.sf(stat, dof)) if dof > 0 else 1.0)
+    log(f"[gpu]   chi-square p-values: min {min(pvals):.3g}, median {np.median(pvals):.3g}")
+    assert min(pvals) > 1e-5, pvals
