@@ -131,6 +131,8 @@ DecodeLayout decode_layout(int B, int Hq, int Hkv, int T, int d, int M, int Kp, 
     L.Y = take(BQ * M * sizeof(double));
     L.lc = take(BQ * M * sizeof(float));
     L.lpos = take(BQ * M * sizeof(unsigned short));
+    L.sbits = take(BQ * kSelWords * sizeof(uint64_t));
+    L.hunits = take(BQ * sizeof(int));
     L.hdr = take(BH * sizeof(PlanHeader));
     L.chunk = take(BH * L.max_chunks * sizeof(Chunk));
     L.ulogc = take(BH * M * kLogcStride * sizeof(float));

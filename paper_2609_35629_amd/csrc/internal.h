@@ -12,6 +12,7 @@ namespace santapp {
 constexpr int kMaxHeadDim = 256;   // LDS vector in the team builder
 constexpr int kMaxReps = 1024;     // representatives per parent
 constexpr int kMaxTeams = 8192;    // teams per (b, kv) the sampler handles
+constexpr int kSelWords = kMaxTeams / 64;  // 64-team selection words per query head
 constexpr int kMaxGroup = 8;       // query heads per KV head (8-bit head masks)
 constexpr int kLogcStride = 8;     // floats per union team in the read plan
 constexpr int kChunkRows = 64;     // rows per sampled attention unit (two 32-row steps of one wave)
@@ -83,6 +84,7 @@ struct DecodeLayout {
     int max_chunks = 0, max_hunits = 0;
     size_t phi = 0, Y = 0, lc = 0, lpos = 0, hdr = 0, chunk = 0, ulogc = 0, po = 0,
            pml = 0, total = 0;
+    size_t sbits = 0, hunits = 0;  // per query head: selection words, unit count (M > 2048)
 };
 
 // cap: host table with cap[x] = most chunks any x distinct teams of one

@@ -425,14 +425,278 @@ __global__ __launch_bounds__(kRouteThreads) void k_route(
     }
 }
 
-template <int G, int PL>
+// ---------------------------------------------------------------------------
+// One query head per workgroup, for team counts past the register path of
+// k_select (M > 32 x 64): the same selection as k_select's head waves (tau,
+// the selected teams with ties to the lower index, log c and each selected
+// team's first position in the head's list), with the workgroup's 512 threads
+// sharing the head's keys (kHeadKeys each).  Results go to the workspace:
+// selection bits in team order (kSelWords words per head), log c and
+// positions (lc, lpos) and the head's unit count; k_select<G, 0, true> then
+// builds the plan.
+constexpr int kHeadKeys = kMaxTeams / kSelectThreads;
+
+template <bool kMax>
+__device__ __forceinline__ uint64_t block_ext64(uint64_t v, uint64_t* s_red) {
+    v = kMax ? wave_max64(v) : wave_min64(v);
+    if (lane_id() == 0) s_red[wave_id()] = v;
+    __syncthreads();
+    uint64_t r = s_red[0];
+    for (int w = 1; w < kSelectWaves; ++w) r = kMax ? max(r, s_red[w]) : min(r, s_red[w]);
+    __syncthreads();
+    return r;
+}
+
+template <bool kOr>
+__device__ __forceinline__ uint64_t block_bits64(uint64_t v, uint64_t* s_red) {
+    v = kOr ? wave_or64(v) : wave_and64(v);
+    if (lane_id() == 0) s_red[wave_id()] = v;
+    __syncthreads();
+    uint64_t r = s_red[0];
+    for (int w = 1; w < kSelectWaves; ++w) r = kOr ? (r | s_red[w]) : (r & s_red[w]);
+    __syncthreads();
+    return r;
+}
+
+template <int G>
+__global__ __launch_bounds__(kSelectThreads) void k_select_head(
+    const double* __restrict__ phi, const double* __restrict__ Y, const int* __restrict__ team_size,
+    int M, int Hkv, int Hq, int Kp, float* __restrict__ lc, unsigned short* __restrict__ lpos,
+    uint64_t* __restrict__ sbits, int* __restrict__ hunits, int* __restrict__ dbg_sel,
+    float* __restrict__ dbg_logc, double* __restrict__ dbg_tau) {
+    __shared__ __align__(16) uint32_t s_hist[256];
+    __shared__ uint64_t s_red[kSelectWaves];
+    __shared__ uint64_t s_cand[kWave];
+    __shared__ int s_ncand;
+    __shared__ int s_bc[3];  // a histogram's bin, the count above it, its count
+    __shared__ uint64_t s_sel[kSelWords];
+    __shared__ uint64_t s_tie[kSelWords];
+    __shared__ __align__(16) int s_w[3 * kSelectWaves];
+
+    const int bq = blockIdx.x;  // b * Hq + query head
+    const int b = bq / Hq, hq = bq - b * Hq;
+    const size_t tb0 = (static_cast<size_t>(b) * Hkv + hq / G) * M;
+    const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
+    const double* y = Y + static_cast<size_t>(bq) * M;
+    const double* ph = phi + static_cast<size_t>(bq) * M;
+    const int nwords = (M + kWave - 1) / kWave;
+
+    // key j of this thread is team j * 512 + tid (word 8 j + w of the bits)
+    uint64_t k[kHeadKeys];
+#pragma unroll
+    for (int j = 0; j < kHeadKeys; ++j) {
+        const int g = j * kSelectThreads + tid;
+        k[j] = g < M ? order_key(y[g]) : 0;
+    }
+    auto valid = [&](int j) { return j * kSelectThreads + tid < M; };
+
+    // tau's key: rank Kp (0-based, descending) among the M keys
+    uint64_t kmin = ~0ull, kmax = 0;
+#pragma unroll
+    for (int j = 0; j < kHeadKeys; ++j) {
+        if (valid(j)) {
+            kmin = min(kmin, k[j]);
+            kmax = max(kmax, k[j]);
+        }
+    }
+    kmin = block_ext64<false>(kmin, s_red);
+    kmax = block_ext64<true>(kmax, s_red);
+    const double ymin = key_value(kmin);
+    const double range = key_value(kmax) - ymin;
+    int want = Kp;
+    uint64_t tkey = kmin;
+    if (range > 0.0) {  // uniform; else every key is equal
+        const double fs = (static_cast<double>(1 << kFineBits) - 0.001) / range;
+        int fine[kHeadKeys];
+#pragma unroll
+        for (int j = 0; j < kHeadKeys; ++j)
+            fine[j] = valid(j) ? min((1 << kFineBits) - 1, static_cast<int>((key_value(k[j]) - ymin) * fs)) : -1;
+        // a 256-bin histogram of the (selected) keys' bins, and the bin that
+        // holds rank `want`
+        auto hist_pass = [&](auto bin_of) {
+            if (tid < 64) reinterpret_cast<uint4*>(s_hist)[tid] = make_uint4(0, 0, 0, 0);
+            __syncthreads();
+#pragma unroll
+            for (int j = 0; j < kHeadKeys; ++j) {
+                const int bn = bin_of(j);
+                if (bn >= 0) atomicAdd(&s_hist[bn], 1u);
+            }
+            __syncthreads();
+            if (w == 0) {
+                int above, cnt;
+                const int bin = hist_select(s_hist, want, above, cnt);
+                if (lane == 0) {
+                    s_bc[0] = bin;
+                    s_bc[1] = above;
+                    s_bc[2] = cnt;
+                }
+            }
+            __syncthreads();
+            const int bin = s_bc[0];
+            want -= s_bc[1];
+            const int cnt = s_bc[2];
+            __syncthreads();  // s_bc and s_hist are reused
+            return make_int2(bin, cnt);
+        };
+        // at most 64 keys left: gather them and rank them directly
+        auto rank_direct = [&](auto in) {
+            if (tid == 0) s_ncand = 0;
+            __syncthreads();
+#pragma unroll
+            for (int j = 0; j < kHeadKeys; ++j)
+                if (in(j)) s_cand[atomicAdd(&s_ncand, 1)] = k[j];
+            __syncthreads();
+            const int n = s_ncand;
+            if (w == 0) {
+                const uint64_t mine = s_cand[min(lane, n - 1)];
+                int gt = 0, ge = 0;
+                for (int t = 0; t < n; ++t) {
+                    const uint64_t o = readlane(mine, t);
+                    gt += o > mine ? 1 : 0;
+                    ge += o >= mine ? 1 : 0;
+                }
+                const bool owner = lane < n && gt <= want && want < ge;
+                const uint64_t r = readlane(mine, __ffsll(static_cast<unsigned long long>(__ballot(owner))) - 1);
+                if (lane == 0) s_red[0] = r;
+            }
+            __syncthreads();
+            const uint64_t r = s_red[0];
+            __syncthreads();
+            return r;
+        };
+        const int2 p0 = hist_pass([&](int j) { return fine[j] >= 0 ? fine[j] >> 8 : -1; });
+        const int top = p0.x;
+        if (p0.y <= kWave) {
+            tkey = rank_direct([&](int j) { return fine[j] >= 0 && (fine[j] >> 8) == top; });
+        } else {
+            const int2 p1 = hist_pass([&](int j) { return fine[j] >= 0 && (fine[j] >> 8) == top ? fine[j] & 255 : -1; });
+            const int target = (top << 8) | p1.x;
+            auto in_bucket = [&](int j) { return fine[j] == target; };
+            if (p1.y <= kWave) {
+                tkey = rank_direct(in_bucket);
+            } else {
+                // many keys in one fine bucket: exact radix over their 64-bit keys
+                uint64_t kand = ~0ull, kor = 0;
+#pragma unroll
+                for (int j = 0; j < kHeadKeys; ++j) {
+                    if (in_bucket(j)) {
+                        kand &= k[j];
+                        kor |= k[j];
+                    }
+                }
+                const uint64_t all_and = block_bits64<false>(kand, s_red);
+                const uint64_t all_or = block_bits64<true>(kor, s_red);
+                const uint64_t diff = all_or & ~all_and;
+                const int topbit = diff ? 63 - __clzll(static_cast<long long>(diff)) : 7;
+                int sh = topbit >= 7 ? topbit - 7 : 0;
+                uint64_t prefix = 0, pmask = 0;
+                if (sh + 8 < 64) {
+                    pmask = ~0ull << (sh + 8);
+                    prefix = all_and & pmask;
+                }
+                for (;;) {  // uniform
+                    const int2 pr = hist_pass([&](int j) {
+                        return in_bucket(j) && (k[j] & pmask) == prefix ? static_cast<int>((k[j] >> sh) & 255) : -1;
+                    });
+                    prefix |= static_cast<uint64_t>(pr.x) << sh;
+                    pmask |= 0xffull << sh;
+                    if (pr.y == 1 || sh == 0) {
+                        // one key, or equal keys: any key with the prefix
+#pragma unroll
+                        for (int j = 0; j < kHeadKeys; ++j)
+                            if (in_bucket(j) && (k[j] & pmask) == prefix) s_red[0] = k[j];
+                        __syncthreads();
+                        tkey = s_red[0];
+                        __syncthreads();
+                        break;
+                    }
+                    sh = sh >= 8 ? sh - 8 : 0;  // the last digit may overlap bits fixed before
+                }
+            }
+        }
+    }
+    const double tau = key_value(tkey);
+
+    // the keys above tau's, and the first need_ties keys equal to it in
+    // team order
+    int above = 0;
+#pragma unroll
+    for (int j = 0; j < kHeadKeys; ++j) above += (valid(j) && k[j] > tkey) ? 1 : 0;
+    {
+        const int x[1] = {above};
+        int ex[1], tot[1];
+        block_scan<1>(x, ex, tot, s_w);
+        above = tot[0];
+    }
+    const int need_ties = Kp - above;
+#pragma unroll
+    for (int j = 0; j < kHeadKeys; ++j) {
+        const bool v = valid(j);
+        const uint64_t sb = __ballot(v && k[j] > tkey);
+        const uint64_t tb = __ballot(v && k[j] == tkey);
+        if (lane == 0 && j * kSelectWaves + w < kSelWords) {
+            s_sel[j * kSelectWaves + w] = sb;
+            s_tie[j * kSelectWaves + w] = tb;
+        }
+    }
+    __syncthreads();
+    if (need_ties > 0) {  // uniform; exactly equal perturbed scores
+        const int tc = tid < nwords ? static_cast<int>(__popcll(s_tie[tid])) : 0;
+        const int x[1] = {tc};
+        int ex[1], tot[1];
+        block_scan<1>(x, ex, tot, s_w);
+        if (tid < nwords && ex[0] < need_ties) {
+            uint64_t t = s_tie[tid];
+            for (int left = need_ties - ex[0]; left > 0 && t; --left) {
+                const uint64_t lowest = t & (~t + 1);
+                s_sel[tid] |= lowest;
+                t ^= lowest;
+            }
+        }
+        __syncthreads();
+    }
+
+    // thread t < nwords takes word t (teams 64 t ..): its selected teams'
+    // log c and first positions in the head's list, in team order
+    const uint64_t word = tid < nwords ? s_sel[tid] : 0;
+    int nunits = 0;
+    for (uint64_t t = word; t; t &= t - 1) nunits += chunk_count(team_size[tb0 + tid * kWave + __ffsll(static_cast<unsigned long long>(t)) - 1]);
+    const int x[2] = {static_cast<int>(__popcll(word)), nunits};
+    int ex[2], tot[2];
+    block_scan<2>(x, ex, tot, s_w);
+    int rank = ex[0], pos = ex[1];
+    for (uint64_t t = word; t; t &= t - 1) {
+        const int g = tid * kWave + __ffsll(static_cast<unsigned long long>(t)) - 1;
+        const float v = log_inclusion(static_cast<float>(ph[g] - tau));
+        lc[static_cast<size_t>(bq) * M + g] = v;
+        lpos[static_cast<size_t>(bq) * M + g] = static_cast<unsigned short>(pos);
+        if (dbg_sel) dbg_sel[static_cast<size_t>(bq) * Kp + rank] = g;
+        if (dbg_logc) dbg_logc[static_cast<size_t>(bq) * Kp + rank] = v;
+        ++rank;
+        pos += chunk_count(team_size[tb0 + g]);
+    }
+    if (tid < nwords) sbits[static_cast<size_t>(bq) * kSelWords + tid] = word;
+    if (tid == 0) {
+        hunits[bq] = tot[1];
+        if (dbg_tau) dbg_tau[bq] = tau;
+    }
+}
+
+// FROM_HEADS (PL = 0 only): the heads' selections, corrections, positions
+// and unit counts come from k_select_head (sbits, hunits), and only the read
+// plan is built here.
+// HTPT (FROM_HEADS only): teams per thread and plan pass.  16 covers 8192
+// teams in one pass; the host takes it only when no pass can hold more
+// union teams than the records (G K <= kSelectRecs).
+template <int G, int PL, bool FROM_HEADS = false, int HTPT = 4>
 __global__ __launch_bounds__(kSelectThreads) void k_select(
     const double* __restrict__ phi, const double* __restrict__ Y, const int* __restrict__ team_begin,
     const int* __restrict__ team_size, int M, int Hkv, int Hq, int Kp, int T_suf, int max_chunks,
     float* __restrict__ lc, unsigned short* __restrict__ lpos, PlanHeader* __restrict__ hdr,
     Chunk* __restrict__ chunks, float* __restrict__ ulogc, int* __restrict__ dbg_sel,
     float* __restrict__ dbg_logc, double* __restrict__ dbg_tau, int* __restrict__ dbg_uteams,
-    int* __restrict__ dbg_urows) {
+    int* __restrict__ dbg_urows, const uint64_t* __restrict__ sbits, const int* __restrict__ hunits) {
+    static_assert(!FROM_HEADS || PL == 0, "the plan from the heads' results reads global tables");
     // Team sizes and starts, and per (head, team) log c and the team's
     // first position in the head's list of units: in LDS up to
     // kSelectLdsTeams teams, else sizes and starts are read from the table
@@ -465,6 +729,18 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
         else return lpos[(hq0 + h) * M + g];
     };
 
+    auto size_of = [&](int g) { return kLds ? s_size[g] : team_size[tb0 + g]; };
+    auto begin_of = [&](int g) { return kLds ? s_begin[g] : team_begin[tb0 + g]; };
+    if constexpr (FROM_HEADS) {
+        // the heads' selection bits (team order) and unit counts
+        const int nwords = (M + kWave - 1) / kWave;
+        for (int i = tid; i < G * nwords; i += kSelectThreads) {
+            const int h = i / nwords, wd = i - h * nwords;
+            s_bits[h][wd] = sbits[(hq0 + h) * kSelWords + wd];
+        }
+        if (tid < G) s_hunits[tid] = hunits[hq0 + tid];
+        __syncthreads();
+    } else {
     // loads first: each head wave's perturbed scores, then the team table
     // (into LDS once the heads have found tau, so that its load overlaps
     // the search: the search waits only for the earlier loads)
@@ -483,8 +759,6 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
             bg[k] = team_begin[tb0 + g];
         }
     }
-    auto size_of = [&](int g) { return kLds ? s_size[g] : team_size[tb0 + g]; };
-    auto begin_of = [&](int g) { return kLds ? s_begin[g] : team_begin[tb0 + g]; };
 
     const int nj = ks.count();
     uint64_t tkey = 0;
@@ -598,6 +872,7 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
         }
     }
     __syncthreads();
+    }  // !FROM_HEADS
 
     // ---- union of the heads' selections in ascending team order -------------
     // One pass per kPass teams (all of them when the team table is in LDS),
@@ -618,9 +893,12 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
         }
         return hm;
     };
-    constexpr int TPT = kLds ? PL / 8 : 1;  // teams per thread and pass (M <= 512 TPT with LDS tables)
+    // teams per thread and pass: M <= 512 TPT with LDS tables; HTPT with the
+    // heads' results
+    constexpr int TPT = kLds ? PL / 8 : (FROM_HEADS ? HTPT : 1);
     constexpr int kPass = kSelectThreads * TPT;
-    static_assert(kPass <= kSelectRecs, "a pass's union teams fit the LDS records");
+    static_assert(kPass <= kSelectRecs || (FROM_HEADS && HTPT * kSelectThreads == kMaxTeams),
+                  "a pass's union teams fit the LDS records (single pass: G K <= kSelectRecs, checked on the host)");
     Chunk* const cb = chunks + static_cast<size_t>(bh) * max_chunks;
     int run_u = 0, run_rows = 0, run_c = 0;
     for (int base = 0; base < M; base += kPass) {
@@ -651,7 +929,7 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
                 float4* L = reinterpret_cast<float4*>(ulogc + (tb0 + run_u + slot) * kLogcStride);
                 L[0] = make_float4(lv[0], lv[1], lv[2], lv[3]);
                 L[1] = make_float4(lv[4], lv[5], lv[6], lv[7]);
-                s_rec[slot] = make_int2(ust, g);
+                if (slot < kSelectRecs) s_rec[slot] = make_int2(ust, g);
                 if (table)
                     for (int c = 0; c < nck[k]; ++c) s_u2t[ust + c] = static_cast<unsigned short>(slot);
                 ++slot;
@@ -768,14 +1046,28 @@ hipError_t route_g(const RouteArgs& a, hipStream_t s) {
             phi, Y, a.team_begin, a.team_size, a.M, a.Hkv, a.Hq, a.Kp, a.T, L.max_chunks, lc,   \
             reinterpret_cast<unsigned short*>(a.ws + L.lpos), hdr, ch, ulogc, d ? d->sel : nullptr, \
             d ? d->logc : nullptr, d ? d->tau : nullptr, d ? d->union_teams : nullptr,            \
-            d ? d->union_rows : nullptr);                                                         \
+            d ? d->union_rows : nullptr, nullptr, nullptr);                                       \
     } while (0)
-    if (a.M <= 8 * kWave)
+    if (a.M <= 8 * kWave) {
         SANTAPP_SEL(8);
-    else if (a.M <= 32 * kWave)
+    } else if (a.M <= 32 * kWave) {
         SANTAPP_SEL(32);
-    else
-        SANTAPP_SEL(0);
+    } else {
+        // one workgroup per query head for the selection, then the plan
+        uint64_t* sbits = reinterpret_cast<uint64_t*>(a.ws + L.sbits);
+        int* hunits = reinterpret_cast<int*>(a.ws + L.hunits);
+        unsigned short* lpos = reinterpret_cast<unsigned short*>(a.ws + L.lpos);
+        k_select_head<G><<<a.B * a.Hq, kSelectThreads, 0, s>>>(
+            phi, Y, a.team_size, a.M, a.Hkv, a.Hq, a.Kp, lc, lpos, sbits, hunits, d ? d->sel : nullptr,
+            d ? d->logc : nullptr, d ? d->tau : nullptr);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        auto plan = static_cast<long long>(G) * a.Kp <= kSelectRecs ? k_select<G, 0, true, 16> : k_select<G, 0, true, 4>;
+        plan<<<a.B * a.Hkv, kSelectThreads, 0, s>>>(
+            phi, Y, a.team_begin, a.team_size, a.M, a.Hkv, a.Hq, a.Kp, a.T, L.max_chunks, lc, lpos, hdr, ch,
+            ulogc, nullptr, nullptr, nullptr, d ? d->union_teams : nullptr, d ? d->union_rows : nullptr,
+            sbits, hunits);
+    }
 #undef SANTAPP_SEL
     return hipGetLastError();
 }
