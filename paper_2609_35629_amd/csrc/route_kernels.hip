@@ -19,6 +19,10 @@
 //           the exactly attended suffix.  Each (sequence, KV head) pair owns a
 //           fixed region of the unit list, so the plan needs no global
 //           atomics.
+// k_select_head  past 2048 teams per KV head: the head waves' part of
+//           k_select by one workgroup per query head (the head's scores no
+//           longer fit one wave's registers); k_select then only builds the
+//           plan from the heads' results.
 #include <math.h>
 
 #include <atomic>
