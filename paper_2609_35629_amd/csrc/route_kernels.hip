@@ -139,8 +139,7 @@ __device__ __forceinline__ void block_scan(const int (&x)[NV], int (&ex)[NV], in
 }
 
 // The perturbed scores of one head as order-preserving keys, with each key's
-// fine value bucket.  PL > 0 keeps element i = j * 64 + lane in register j
-// (M <= 64 PL); PL == 0 re-reads them from global memory on every pass.
+// fine value bucket: element i = j * 64 + lane in register j (M <= 64 PL).
 template <int PL>
 struct KeySet {
     // phi stays in registers only for small PL; larger sets re-read it for
@@ -182,29 +181,6 @@ struct KeySet {
             fine[j] = min((1 << kFineBits) - 1, static_cast<int>((key_value(k[j]) - ymin) * fs));
     }
     __device__ __forceinline__ int fine_of(int j, double, double) const { return fine[j]; }
-};
-
-template <>
-struct KeySet<0> {
-    static constexpr bool kPhiRegs = false;
-    const double* y;
-    const double* p;
-    int M;
-    __device__ __forceinline__ void init(const double* yy, const double* pp, int MM) {
-        y = yy;
-        p = pp;
-        M = MM;
-    }
-    __device__ __forceinline__ int count() const { return (M + kWave - 1) / kWave; }
-    __device__ __forceinline__ bool valid(int j) const { return j * kWave + lane_id() < M; }
-    __device__ __forceinline__ uint64_t key(int j) const {
-        return order_key(y[min(j * kWave + lane_id(), M - 1)]);
-    }
-    __device__ __forceinline__ double phi(int j) const { return p[min(j * kWave + lane_id(), M - 1)]; }
-    __device__ __forceinline__ void set_fine(double, double) {}
-    __device__ __forceinline__ int fine_of(int j, double ymin, double fs) const {
-        return min((1 << kFineBits) - 1, static_cast<int>((key_value(key(j)) - ymin) * fs));
-    }
 };
 
 // Rank `want` (0-based, descending) among the lane bins of one LDS histogram:
@@ -700,7 +676,7 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
     Chunk* __restrict__ chunks, float* __restrict__ ulogc, int* __restrict__ dbg_sel,
     float* __restrict__ dbg_logc, double* __restrict__ dbg_tau, int* __restrict__ dbg_uteams,
     int* __restrict__ dbg_urows, const uint64_t* __restrict__ sbits, const int* __restrict__ hunits) {
-    static_assert(!FROM_HEADS || PL == 0, "the plan from the heads' results reads global tables");
+    static_assert(FROM_HEADS == (PL == 0), "head waves hold their keys in registers; PL = 0 only builds the plan");
     // Team sizes and starts, and per (head, team) log c and the team's
     // first position in the head's list of units: in LDS up to
     // kSelectLdsTeams teams, else sizes and starts are read from the table
