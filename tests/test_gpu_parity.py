@@ -324,3 +324,15 @@ def test_limiting_case_sampling_law():
         pvals.append(float(chi2.sf(stat, dof)) if dof > 0 else 1.0)
     log(f"[gpu]   chi-square p-values: min {min(pvals):.3g}, median {np.median(pvals):.3g}")
     assert min(pvals) > 1e-5, pvals
+
+
+@pytest.mark.parametrize("name,kw", [
+    # bf16 rows of 64 values (the d = 64 attention kernels), 8 query heads per
+    # KV head (the largest group), a ragged suffix
+    ("bf16-d64-g8", dict(d=64, N=4096, P=512, R=8, Hq=16, Hkv=2, K=10, T=33)),
+    # 8 query heads per KV head at d = 128, one KV head, budget past half the teams
+    ("bf16-d128-g8", dict(N=4096, P=256, R=8, Hq=8, Hkv=1, K=70, T=5)),
+])
+def test_head_dims_and_groups(name, kw):
+    wl = datagen.WORKLOADS["qwen8k"].with_(name=name, **kw)
+    _run(wl, steps=(0, 3))
