@@ -221,8 +221,11 @@ santapp_status santapp_build_teams(const void* K, const void* V, int B, int Hkv,
     alloc(reinterpret_cast<void**>(&t->log_n), BH * M * sizeof(double));
     alloc(reinterpret_cast<void**>(&t->rep_token), BH * M * sizeof(int));
     alloc(reinterpret_cast<void**>(&t->perm), BH * N * sizeof(int));
-    alloc(reinterpret_cast<void**>(&mind), BH * N * sizeof(double));
-    alloc(reinterpret_cast<void**>(&owner), BH * N * sizeof(int));
+    if (!build_packs_in_place(N, d, dtype, parent_size, reps_per_parent)) {
+        // running minimum and owner per token, for the general build kernel
+        alloc(reinterpret_cast<void**>(&mind), BH * N * sizeof(double));
+        alloc(reinterpret_cast<void**>(&owner), BH * N * sizeof(int));
+    }
     if (e != hipSuccess) {
         release(mind);
         release(owner);

@@ -587,6 +587,12 @@ __global__ __launch_bounds__(256) void k_gather_rows(const uint4* __restrict__ s
 
 }  // namespace
 
+bool build_packs_in_place(int N, int d, santapp_dtype dtype, int P, int R) {
+    const int members = std::min(P, N);
+    return members <= 2 * kRegThreads && R <= kMaxReps &&
+           ((dtype == SANTAPP_BF16 && (d == 128 || d == 64)) || (dtype == SANTAPP_FP32 && d == 64));
+}
+
 hipError_t launch_build_parents(const void* K, const void* V, santapp_dtype dtype, int BH, int N,
                                 int d, int P, int R, int M, double* mind, int* owner,
                                 int* team_begin, int* team_size, double* log_n, int* rep_token,
@@ -599,7 +605,7 @@ hipError_t launch_build_parents(const void* K, const void* V, santapp_dtype dtyp
     // general kernel otherwise.  At least one thread per dimension: they sum
     // the parent mean.
     const int members = std::min(P, N);
-    if (members <= 2 * kRegThreads && R <= kMaxReps) {
+    if (build_packs_in_place(N, d, dtype, P, R)) {
         const int mpt = members > kRegThreads ? 2 : 1;
         const int threads = std::max(d, ((members + mpt - 1) / mpt + kWave - 1) / kWave * kWave);
 #define SANTAPP_REGS(TT, DD)                                                                       \

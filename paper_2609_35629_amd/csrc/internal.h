@@ -95,6 +95,10 @@ DecodeLayout dense_layout(int B, int Hq, int Hkv, int N, int T, int d);
 __host__ __device__ inline int chunk_count(int rows) { return (rows + kChunkRows - 1) / kChunkRows; }
 __host__ __device__ inline int dense_count(int rows) { return (rows + kDenseRows - 1) / kDenseRows; }
 
+// Whether launch_build_parents takes the register-resident kernel (which
+// needs no per-token scratch and writes the packed copies itself).
+bool build_packs_in_place(int N, int d, santapp_dtype dtype, int P, int R);
+
 // Team table of every parent.  Where the register-resident kernel runs it
 // also writes the packed copies (packed_K, packed_V, reps) and sets *packed;
 // otherwise the caller gathers them from perm and rep_token.

@@ -678,9 +678,10 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(
     int* __restrict__ dbg_urows, const uint64_t* __restrict__ sbits, const int* __restrict__ hunits) {
     static_assert(FROM_HEADS == (PL == 0), "head waves hold their keys in registers; PL = 0 only builds the plan");
     // Team sizes and starts, and per (head, team) log c and the team's
-    // first position in the head's list of units: in LDS up to
-    // kSelectLdsTeams teams, else sizes and starts are read from the table
-    // and the per-head values go to the workspace.
+    // first position in the head's list of units: in LDS when the heads'
+    // keys are in registers (up to 2048 teams); with the heads' results
+    // (FROM_HEADS) sizes and starts come from the table and the per-head
+    // values from the workspace.
     constexpr bool kLds = PL > 0;
     extern __shared__ int s_dyn[];  // kLds: [M] sizes, [M] starts, [G][M] floats, [G][M] ushorts
     __shared__ __align__(16) uint32_t s_hist[kSelectWaves][256];
