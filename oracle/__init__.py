@@ -66,6 +66,13 @@ def lib():
         L.oracle_dense_head.restype = ctypes.c_int
         L.oracle_team_means.argtypes = [_d, ctypes.c_int, _i, _i, ctypes.c_int, _d]
         L.oracle_team_means.restype = ctypes.c_int
+        L.oracle_build_teams_parents.argtypes = [_d, ctypes.c_int, ctypes.c_int, _i, _i, ctypes.c_int,
+                                                 ctypes.c_int, _i, _i, _i]
+        L.oracle_build_teams_parents.restype = ctypes.c_int
+        L.oracle_kmeans.argtypes = [_d, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                    ctypes.c_int, ctypes.c_int, ctypes.c_double, ctypes.c_int,
+                                    ctypes.c_uint64, _d, _i, _i, _d]
+        L.oracle_kmeans.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -140,6 +147,82 @@ def build_teams(K: np.ndarray, P: int, R: int) -> Teams:
     if M < 0:
         raise ValueError("oracle_build_teams rejected its arguments")
     return Teams(members, team_ptr[:M + 1].copy(), rep_token[:M].copy())
+
+
+def build_teams_from_labels(K: np.ndarray, labels: np.ndarray, R: int) -> Teams:
+    """Teams of any parent partition given as one label per token: parent u
+    is ``{i : labels[i] == u}``, parents in ascending label order, empty ones
+    omitted (Alg. "Global minibatch k-means parent partition", last step),
+    then Alg. "Build actual-key teams from a parent partition" per parent."""
+    K = _f64(K)
+    N, d = K.shape
+    labels = np.asarray(labels)
+    if labels.shape != (N,) or labels.min() < 0:
+        raise ValueError("labels must be [N] and non-negative")
+    order = np.argsort(labels, kind="stable").astype(np.int32)
+    counts = np.bincount(labels, minlength=int(labels.max()) + 1)
+    pptr = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    members = np.empty(N, np.int32)
+    team_ptr = np.empty(N + 1, np.int32)
+    rep_token = np.empty(N, np.int32)
+    M = lib().oracle_build_teams_parents(_pd(K), N, d, _pi(order), _pi(pptr), len(counts), R,
+                                         _pi(members), _pi(team_ptr), _pi(rep_token))
+    if M < 0:
+        raise ValueError("oracle_build_teams_parents rejected its arguments")
+    return Teams(members, team_ptr[:M + 1].copy(), rep_token[:M].copy())
+
+
+# --------------------------------------------------------------------------
+# K-means parents (Alg. "Global minibatch k-means parent partition")
+# --------------------------------------------------------------------------
+@dataclasses.dataclass
+class KMeansSettings:
+    """theta of the paper's reported runs (minibatch 4096, at most 100
+    iterations, 10-minibatch no-improvement rule, reassignment ratio 0.01,
+    default seeding sample) and the seed xi = 0."""
+    batch: int = 4096
+    max_iter: int = 100
+    max_no_improvement: int = 10
+    reassignment_ratio: float = 0.01
+    init_size: int = 0
+    seed: int = 0
+
+
+def kmeans_parent_count(N: int, P: int) -> int:
+    """M_parent = min(N, max(2, floor(N / P))) (N >= 2)."""
+    if N < 2 or P < 1:
+        raise ValueError("k-means parents need N >= 2 and P >= 1")
+    return min(N, max(2, N // P))
+
+
+@dataclasses.dataclass
+class KMeansResult:
+    labels: np.ndarray        # [N] nearest final center of every token
+    centers: np.ndarray       # [M, d] final centers
+    init_centers: np.ndarray  # [M, d] the seeding result
+    steps: int                # minibatch steps run
+
+
+def kmeans(X: np.ndarray, M: int, theta: KMeansSettings = KMeansSettings()) -> KMeansResult:
+    X = _f64(X)
+    N, d = X.shape
+    centers = np.empty((M, d))
+    init = np.empty((M, d))
+    labels = np.empty(N, np.int32)
+    steps = np.zeros(1, np.int32)
+    rc = lib().oracle_kmeans(_pd(X), N, d, M, theta.batch, theta.max_iter, theta.max_no_improvement,
+                             float(theta.reassignment_ratio), theta.init_size, int(theta.seed),
+                             _pd(centers), _pi(labels), _pi(steps), _pd(init))
+    if rc != 0:
+        raise ValueError("oracle_kmeans rejected its arguments")
+    return KMeansResult(labels, centers, init, int(steps[0]))
+
+
+def kmeans_parents(K: np.ndarray, P: int, theta: KMeansSettings = KMeansSettings()) -> KMeansResult:
+    """Parents of one KV head's prompt keys ``[N, d]``: k-means with
+    M_parent centers; ``labels`` define the parents."""
+    K = _f64(K)
+    return kmeans(K, kmeans_parent_count(K.shape[0], P), theta)
 
 
 def build_all(K: np.ndarray, P: int, R: int) -> List[List[Teams]]:
