@@ -19,6 +19,10 @@
  *   santapp_teams_set_route_keys, santapp_routing_kl
  *                         section "Attention-distribution diagnostic":
  *                         centroid routing keys and eq. diagnostic-kl.
+ *   santapp_kmeans_parents  Alg. "Global minibatch k-means parent partition"
+ *                         with the settings stated after it.
+ *   santapp_build_teams_from_labels  Alg. "Build actual-key teams from a
+ *                         parent partition" for any parent partition.
  *
  * Conventions
  *   - Every tensor argument is a DEVICE pointer owned by the caller unless
@@ -77,6 +81,8 @@ typedef struct {
     const double* log_n;     /* [B,Hkv,M] log n_g (fp64)                     */
     const int* rep_token;    /* [B,Hkv,M] original token index of l_g        */
     const int* perm;         /* [B,Hkv,N] packed row -> original token index */
+    const int* team_count;   /* [B,Hkv] real teams of each (b, kv); teams    */
+                             /* g >= team_count are absent (see below)       */
 } santapp_teams_desc;
 
 /*
@@ -102,6 +108,64 @@ typedef struct {
 santapp_status santapp_build_teams(const void* K, const void* V, int B, int Hkv, int N, int d,
                                    santapp_dtype dtype, int parent_size, int reps_per_parent,
                                    void* stream, santapp_teams** out);
+
+/*
+ * Minibatch k-means settings theta (the paper's reported runs: batch 4096,
+ * max_iter 100, max_no_improvement 10, reassignment_ratio 0.01, init_size 0,
+ * seed 0).
+ */
+typedef struct {
+    int batch_size;             /* points per minibatch, drawn with replacement  */
+    int max_iter;               /* steps = floor(max_iter * N / batch_size)      */
+    int max_no_improvement;     /* stop after this many steps without a new      */
+                                /* minimum of the smoothed batch inertia (0: no) */
+    double reassignment_ratio;  /* in [0, 1): centers with a cumulative count    */
+                                /* below ratio * the largest move to a batch     */
+                                /* point                                         */
+    int init_size;              /* seeding sample; 0: 3 * batch_size (at least   */
+                                /* 3 M, at most N)                               */
+    uint64_t seed;              /* xi                                            */
+} santapp_kmeans_settings;
+
+/*
+ * K-means parents of one layer (Alg. "Global minibatch k-means parent
+ * partition"): for every (b, kv), M = min(N, max(2, floor(N / parent_size)))
+ * centers fitted to the post-RoPE keys by greedy k-means++ seeding and
+ * minibatch steps with cumulative-count updates, then labels[b,kv,i] = the
+ * nearest center of token i (ties: lowest index).  Every (b, kv) pair uses
+ * the same random draws (Philox4x64-10, key (seed, 1)); distances are fp64 on
+ * the exact key values.
+ *
+ * K:      [B,Hkv,N,d] keys (device, not modified).
+ * labels: [B,Hkv,N] int32 output (device, caller-owned).
+ * num_parents (host, may be NULL): receives M.
+ * steps (host [B*Hkv], may be NULL): minibatch steps each pair ran.
+ * Limits: N >= 2, d in {64, 128}, M <= 1024 (else SANTAPP_ELIMIT).
+ * Allocates scratch device memory; synchronises `stream` before returning.
+ */
+santapp_status santapp_kmeans_parents(const void* K, int B, int Hkv, int N, int d, santapp_dtype dtype,
+                                      int parent_size, const santapp_kmeans_settings* theta, int* labels,
+                                      int* num_parents, int* steps, void* stream);
+
+/*
+ * Team table of label-defined parents: parent u of (b, kv) is
+ * {i : labels[b,kv,i] == u}; parents are taken in ascending label order,
+ * empty ones omitted, and each is split into teams as in
+ * santapp_build_teams (representatives, assignment, ties, member order).
+ * labels: [B,Hkv,N] int32 in [0, num_labels) (device; else SANTAPP_EINVAL).
+ * The pairs' team counts differ in general: the table's M is the largest,
+ * and the teams g >= team_count[b,kv] of a pair are absent: no rows
+ * (team_size 0, team_begin N), rep_token 0 and log_n = -1e300, a finite
+ * stand-in for log 0 that keeps every routing score finite.  Decoding never
+ * samples an absent team while its pair has more than K real teams; when it
+ * has at most K, every real team is taken with correction 1 and absent ones
+ * add nothing.  The table's parent_size is 0.
+ * Limits: d in {64, 128}; num_labels <= 1024; R <= 1024.
+ * Allocates device memory; synchronises `stream` before returning.
+ */
+santapp_status santapp_build_teams_from_labels(const void* K, const void* V, int B, int Hkv, int N, int d,
+                                               santapp_dtype dtype, const int* labels, int num_labels,
+                                               int reps_per_parent, void* stream, santapp_teams** out);
 
 /*
  * Keys the teams are routed by (the table's `reps`; section

@@ -82,6 +82,9 @@ class Teams:
     def perm(self) -> torch.Tensor:
         return self._view(self.desc.perm, (self.B, self.Hkv, self.N), torch.int32)
 
+    def team_count(self) -> torch.Tensor:
+        return self._view(self.desc.team_count, (self.B, self.Hkv), torch.int32)
+
     def packed_K(self) -> torch.Tensor:
         return self._view(self.desc.packed_K, (self.B, self.Hkv, self.N, self.d), self.torch_dtype)
 
@@ -125,6 +128,39 @@ def build_teams(K: torch.Tensor, V: torch.Tensor, parent_size: int, reps_per_par
     check(_lib.load().santapp_build_teams(_ptr(K), _ptr(V), B, Hkv, N, d, _dtype_code(K),
                                           parent_size, reps_per_parent, _stream(stream),
                                           ctypes.byref(h)))
+    return Teams(h, K.dtype)
+
+
+def kmeans_parents(K: torch.Tensor, parent_size: int, batch_size: int = 4096, max_iter: int = 100,
+                   max_no_improvement: int = 10, reassignment_ratio: float = 0.01, init_size: int = 0,
+                   seed: int = 0, stream=None):
+    """K-means parent labels ``[B, Hkv, N]`` (int32) of prompt keys ``K``;
+    returns ``(labels, num_parents, steps)`` with the minibatch steps each
+    (b, kv) pair ran."""
+    _need(K, "K")
+    B, Hkv, N, d = K.shape
+    labels = torch.empty((B, Hkv, N), dtype=torch.int32, device=K.device)
+    th = _lib.KMeansSettings(batch_size, max_iter, max_no_improvement, float(reassignment_ratio), init_size,
+                             seed)
+    mp = ctypes.c_int()
+    steps = (ctypes.c_int * (B * Hkv))()
+    check(_lib.load().santapp_kmeans_parents(_ptr(K), B, Hkv, N, d, _dtype_code(K), parent_size,
+                                             ctypes.byref(th), _ptr(labels), ctypes.byref(mp), steps,
+                                             _stream(stream)))
+    return labels, mp.value, list(steps)
+
+
+def build_teams_from_labels(K: torch.Tensor, V: torch.Tensor, labels: torch.Tensor, num_labels: int,
+                            reps_per_parent: int, stream=None) -> Teams:
+    """Team table of the parents ``{i : labels[b, kv, i] == u}``."""
+    _need(K, "K")
+    _need(V, "V", shape=K.shape, dtype=K.dtype)
+    B, Hkv, N, d = K.shape
+    _need(labels, "labels", shape=(B, Hkv, N), dtype=torch.int32)
+    h = ctypes.c_void_p()
+    check(_lib.load().santapp_build_teams_from_labels(_ptr(K), _ptr(V), B, Hkv, N, d, _dtype_code(K),
+                                                      _ptr(labels), num_labels, reps_per_parent,
+                                                      _stream(stream), ctypes.byref(h)))
     return Teams(h, K.dtype)
 
 

@@ -19,6 +19,7 @@ EXPORTS = [
     "santapp_decode_workspace_bytes", "santapp_workspace_zero", "santapp_decode",
     "santapp_dense_workspace_bytes", "santapp_dense_decode", "santapp_last_error",
     "santapp_teams_set_route_keys", "santapp_routing_kl_workspace_bytes", "santapp_routing_kl",
+    "santapp_kmeans_parents", "santapp_build_teams_from_labels",
 ]
 
 ROUTE_REPRESENTATIVE, ROUTE_CENTROID = 0, 1
@@ -32,6 +33,14 @@ class TeamsDesc(ctypes.Structure):
         ("packed_K", ctypes.c_void_p), ("packed_V", ctypes.c_void_p), ("reps", ctypes.c_void_p),
         ("team_begin", ctypes.c_void_p), ("team_size", ctypes.c_void_p),
         ("log_n", ctypes.c_void_p), ("rep_token", ctypes.c_void_p), ("perm", ctypes.c_void_p),
+        ("team_count", ctypes.c_void_p),
+    ]
+
+
+class KMeansSettings(ctypes.Structure):
+    _fields_ = [
+        ("batch_size", ctypes.c_int), ("max_iter", ctypes.c_int), ("max_no_improvement", ctypes.c_int),
+        ("reassignment_ratio", ctypes.c_double), ("init_size", ctypes.c_int), ("seed", ctypes.c_uint64),
     ]
 
 
@@ -65,6 +74,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     vp, i, u64, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_uint64, ctypes.c_size_t
     L.santapp_build_teams.argtypes = [vp, vp, i, i, i, i, i, i, i, vp, ctypes.POINTER(vp)]
     L.santapp_teams_info.argtypes = [vp, ctypes.POINTER(TeamsDesc)]
+    L.santapp_kmeans_parents.argtypes = [vp, i, i, i, i, i, i, ctypes.POINTER(KMeansSettings), vp,
+                                         ctypes.POINTER(i), ctypes.POINTER(i), vp]
+    L.santapp_build_teams_from_labels.argtypes = [vp, vp, i, i, i, i, i, vp, i, i, vp, ctypes.POINTER(vp)]
     L.santapp_teams_destroy.argtypes = [vp]
     L.santapp_teams_destroy.restype = None
     L.santapp_budget_to_K.argtypes = [i, i, i, i, ctypes.POINTER(i)]

@@ -24,6 +24,7 @@ struct santapp_teams {
     double* log_n;
     int* rep_token;
     int* perm;
+    int* team_count;  // [B*Hkv] teams of each pair (M for contiguous parents)
     // cap[x]: the most attention chunks any x distinct teams of one (b, kv)
     // need (sum of their x largest chunk counts, maximum over (b, kv))
     std::vector<int> cap;
@@ -107,8 +108,11 @@ void free_teams(santapp_teams* t) {
     release(t->log_n);
     release(t->rep_token);
     release(t->perm);
+    release(t->team_count);
     delete t;
 }
+
+santapp_status finish_table(santapp_teams* t, santapp_teams** out);
 
 }  // namespace
 
@@ -221,6 +225,7 @@ santapp_status santapp_build_teams(const void* K, const void* V, int B, int Hkv,
     alloc(reinterpret_cast<void**>(&t->log_n), BH * M * sizeof(double));
     alloc(reinterpret_cast<void**>(&t->rep_token), BH * M * sizeof(int));
     alloc(reinterpret_cast<void**>(&t->perm), BH * N * sizeof(int));
+    alloc(reinterpret_cast<void**>(&t->team_count), BH * sizeof(int));
     if (!build_packs_in_place(N, d, dtype, parent_size, reps_per_parent)) {
         // running minimum and owner per token, for the general build kernel
         alloc(reinterpret_cast<void**>(&mind), BH * N * sizeof(double));
@@ -256,15 +261,29 @@ santapp_status santapp_build_teams(const void* K, const void* V, int B, int Hkv,
     }
     release(mind);
     release(owner);
-    std::vector<int> sizes;
     if (e == hipSuccess) {
-        what = "team size copy";
-        sizes.resize(BH * t->M);
-        e = hipMemcpy(sizes.data(), t->team_size, sizes.size() * sizeof(int), hipMemcpyDeviceToHost);
+        what = "team counts";
+        const std::vector<int> counts(BH, t->M);
+        e = hipMemcpy(t->team_count, counts.data(), BH * sizeof(int), hipMemcpyHostToDevice);
     }
     if (e != hipSuccess) {
         free_teams(t);
         return hip_fail(e, what);
+    }
+    return finish_table(t, out);
+}
+
+namespace {
+
+// Chunk capacities and the device's compute units of a built table; frees it
+// on failure.
+santapp_status finish_table(santapp_teams* t, santapp_teams** out) {
+    const size_t BH = static_cast<size_t>(t->B) * t->Hkv;
+    std::vector<int> sizes(BH * t->M);
+    const hipError_t e = hipMemcpy(sizes.data(), t->team_size, sizes.size() * sizeof(int), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) {
+        free_teams(t);
+        return hip_fail(e, "team size copy");
     }
     int dev = 0;
     t->cus = 0;
@@ -287,6 +306,211 @@ santapp_status santapp_build_teams(const void* K, const void* V, int B, int Hkv,
     return ok();
 }
 
+}  // namespace
+
+santapp_status santapp_kmeans_parents(const void* K, int B, int Hkv, int N, int d, santapp_dtype dtype,
+                                      int parent_size, const santapp_kmeans_settings* theta, int* labels,
+                                      int* num_parents, int* steps, void* stream) {
+    if (!K || !labels || !theta) return fail(SANTAPP_EINVAL, "K, labels and theta must not be NULL");
+    if (!aligned16(K) || !aligned16(labels)) return fail(SANTAPP_EINVAL, "K and labels must be 16-byte aligned");
+    if (B < 1 || Hkv < 1 || N < 2) return fail(SANTAPP_EINVAL, "B, Hkv must be >= 1 and N >= 2");
+    if (parent_size < 1) return fail(SANTAPP_EINVAL, "parent_size must be >= 1");
+    if (theta->batch_size < 1 || theta->max_iter < 0 || theta->max_no_improvement < 0 ||
+        theta->init_size < 0 || !(theta->reassignment_ratio >= 0.0 && theta->reassignment_ratio < 1.0))
+        return fail(SANTAPP_EINVAL, "invalid k-means settings");
+    if (!dtype_ok(dtype)) return fail(SANTAPP_EDTYPE, "unsupported dtype %d", static_cast<int>(dtype));
+    if (d != 64 && d != 128) return fail(SANTAPP_ELIMIT, "head dim %d not supported (64 or 128)", d);
+    const int M = std::min(N, std::max(2, N / parent_size));
+    if (M > kKmMaxCenters) return fail(SANTAPP_ELIMIT, "%d k-means parents exceed %d", M, kKmMaxCenters);
+    const size_t BH = static_cast<size_t>(B) * Hkv;
+    if (BH * static_cast<size_t>(N) > static_cast<size_t>(0x7fffffff))
+        return fail(SANTAPP_ELIMIT, "B*Hkv*N exceeds 2^31");
+    const long long steps_total = static_cast<long long>(theta->max_iter) * N / theta->batch_size;
+    if (steps_total > 0x7fffffff) return fail(SANTAPP_ELIMIT, "too many minibatch steps");
+    int s0 = theta->init_size > 0 ? theta->init_size : 3 * theta->batch_size;
+    if (s0 < M) s0 = 3 * M;
+    if (s0 > N) s0 = N;
+    const KmLayout L = kmeans_layout(static_cast<int>(BH), N, d, M, theta->batch_size, s0);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    char* ws = nullptr;
+    hipError_t e = hipMalloc(reinterpret_cast<void**>(&ws), L.total);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(SANTAPP_ENOMEM, "k-means scratch (%zu bytes): %s", L.total, hipGetErrorString(e));
+    }
+    const char* what = "k-means seeding";
+    e = launch_kmeans_seed(K, dtype, static_cast<int>(BH), N, d, L, ws, theta->seed, s);
+    const double alpha = std::min(1.0, 2.0 * theta->batch_size / (static_cast<double>(N) + 1.0));
+    std::vector<KmState> st(BH);
+    // minibatch steps in groups; stopped pairs skip the rest, and the loop
+    // ends once every pair has stopped
+    constexpr int kGroup = 16;
+    for (long long first = 0; e == hipSuccess && first < steps_total; first += kGroup) {
+        const int count = static_cast<int>(std::min<long long>(kGroup, steps_total - first));
+        what = "k-means steps";
+        e = launch_kmeans_steps(K, dtype, static_cast<int>(BH), N, d, L, ws, theta->batch_size,
+                                static_cast<int>(first), count, alpha, theta->reassignment_ratio,
+                                theta->max_no_improvement, theta->seed, s);
+        if (e == hipSuccess && theta->max_no_improvement > 0) {
+            what = "k-means state";
+            e = hipMemcpyAsync(st.data(), ws + L.state, BH * sizeof(KmState), hipMemcpyDeviceToHost, s);
+            if (e == hipSuccess) e = hipStreamSynchronize(s);
+            if (e == hipSuccess &&
+                std::all_of(st.begin(), st.end(), [](const KmState& x) { return x.stop != 0; }))
+                break;
+        }
+    }
+    if (e == hipSuccess) {
+        what = "k-means labels";
+        e = launch_kmeans_labels(K, dtype, static_cast<int>(BH), N, d, L, ws, labels, s);
+    }
+    if (e == hipSuccess) {
+        what = "k-means state";
+        e = hipMemcpyAsync(st.data(), ws + L.state, BH * sizeof(KmState), hipMemcpyDeviceToHost, s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+    }
+    release(ws);
+    if (e != hipSuccess) return hip_fail(e, what);
+    if (num_parents) *num_parents = M;
+    if (steps)
+        for (size_t i = 0; i < BH; ++i) steps[i] = st[i].steps;
+    return ok();
+}
+
+santapp_status santapp_build_teams_from_labels(const void* K, const void* V, int B, int Hkv, int N, int d,
+                                               santapp_dtype dtype, const int* labels, int num_labels,
+                                               int reps_per_parent, void* stream, santapp_teams** out) {
+    if (!out) return fail(SANTAPP_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (!K || !V || !labels) return fail(SANTAPP_EINVAL, "K, V and labels must be device pointers");
+    if (!aligned16(K) || !aligned16(V) || !aligned16(labels))
+        return fail(SANTAPP_EINVAL, "K, V and labels must be 16-byte aligned");
+    if (B < 1 || Hkv < 1 || N < 1) return fail(SANTAPP_EINVAL, "B, Hkv, N must be >= 1");
+    if (num_labels < 1) return fail(SANTAPP_EINVAL, "num_labels must be >= 1");
+    if (reps_per_parent < 1) return fail(SANTAPP_EINVAL, "reps_per_parent must be >= 1");
+    if (!dtype_ok(dtype)) return fail(SANTAPP_EDTYPE, "unsupported dtype %d", static_cast<int>(dtype));
+    if (d != 64 && d != 128) return fail(SANTAPP_ELIMIT, "head dim %d not supported (64 or 128)", d);
+    if (num_labels > kMaxLabels) return fail(SANTAPP_ELIMIT, "num_labels %d exceeds %d", num_labels, kMaxLabels);
+    if (reps_per_parent > kMaxReps)
+        return fail(SANTAPP_ELIMIT, "reps_per_parent %d exceeds %d", reps_per_parent, kMaxReps);
+    const size_t BH = static_cast<size_t>(B) * Hkv;
+    if (BH * static_cast<size_t>(N) > static_cast<size_t>(0x7fffffff))
+        return fail(SANTAPP_ELIMIT, "B*Hkv*N exceeds 2^31");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const size_t esz = elem_size(dtype);
+    const size_t row = static_cast<size_t>(d) * esz;
+    const int Mp = num_labels;
+
+    // parent lists, then the team counts that size the table
+    int *members = nullptr, *pbeg = nullptr, *toff = nullptr, *tcount = nullptr, *bad = nullptr;
+    double* mind = nullptr;
+    int* owner = nullptr;
+    hipError_t e = hipSuccess;
+    auto alloc = [&](void** p, size_t bytes) {
+        if (e == hipSuccess) e = hipMalloc(p, bytes);
+    };
+    auto cleanup = [&]() {
+        release(members);
+        release(pbeg);
+        release(toff);
+        release(tcount);
+        release(bad);
+        release(mind);
+        release(owner);
+    };
+    alloc(reinterpret_cast<void**>(&members), BH * N * sizeof(int));
+    alloc(reinterpret_cast<void**>(&pbeg), BH * (Mp + 1) * sizeof(int));
+    alloc(reinterpret_cast<void**>(&toff), BH * (Mp + 1) * sizeof(int));
+    alloc(reinterpret_cast<void**>(&tcount), BH * sizeof(int));
+    alloc(reinterpret_cast<void**>(&bad), sizeof(int));
+    alloc(reinterpret_cast<void**>(&mind), BH * N * sizeof(double));
+    alloc(reinterpret_cast<void**>(&owner), BH * N * sizeof(int));
+    if (e != hipSuccess) {
+        cleanup();
+        (void)hipGetLastError();
+        return fail(SANTAPP_ENOMEM, "device allocation failed: %s", hipGetErrorString(e));
+    }
+    const char* what = "parent lists";
+    e = hipMemsetAsync(bad, 0, sizeof(int), s);
+    if (e == hipSuccess)
+        e = launch_parent_lists(labels, static_cast<int>(BH), N, Mp, reps_per_parent, members, pbeg, toff,
+                                tcount, bad, s);
+    std::vector<int> counts(BH);
+    int flag = 0;
+    if (e == hipSuccess) e = hipMemcpyAsync(counts.data(), tcount, BH * sizeof(int), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(&flag, bad, sizeof(int), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) {
+        cleanup();
+        return hip_fail(e, what);
+    }
+    if (flag) {
+        cleanup();
+        return fail(SANTAPP_EINVAL, "a label lies outside [0, %d)", Mp);
+    }
+    const int M = *std::max_element(counts.begin(), counts.end());
+
+    santapp_teams* t = new santapp_teams();
+    t->B = B;
+    t->Hkv = Hkv;
+    t->N = N;
+    t->d = d;
+    t->dtype = dtype;
+    t->P = 0;
+    t->R = reps_per_parent;
+    t->M = M;
+    alloc(&t->packed_K, BH * N * row);
+    alloc(&t->packed_V, BH * N * row);
+    alloc(&t->reps, BH * M * row);
+    alloc(reinterpret_cast<void**>(&t->team_begin), BH * M * sizeof(int));
+    alloc(reinterpret_cast<void**>(&t->team_size), BH * M * sizeof(int));
+    alloc(reinterpret_cast<void**>(&t->log_n), BH * M * sizeof(double));
+    alloc(reinterpret_cast<void**>(&t->rep_token), BH * M * sizeof(int));
+    alloc(reinterpret_cast<void**>(&t->perm), BH * N * sizeof(int));
+    alloc(reinterpret_cast<void**>(&t->team_count), BH * sizeof(int));
+    if (e != hipSuccess) {
+        cleanup();
+        free_teams(t);
+        (void)hipGetLastError();
+        return fail(SANTAPP_ENOMEM, "device allocation failed: %s", hipGetErrorString(e));
+    }
+    what = "team counts";
+    e = hipMemcpyAsync(t->team_count, tcount, BH * sizeof(int), hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess) {
+        what = "absent teams";
+        e = launch_pad_teams(tcount, static_cast<int>(BH), M, N, t->team_begin, t->team_size, t->log_n,
+                             t->rep_token, s);
+    }
+    if (e == hipSuccess) {
+        what = "team build";
+        e = launch_build_parent_lists(K, dtype, static_cast<int>(BH), N, d, Mp, reps_per_parent, M, members,
+                                      pbeg, toff, mind, owner, t->team_begin, t->team_size, t->log_n,
+                                      t->rep_token, t->perm, s);
+    }
+    if (e == hipSuccess) {
+        what = "packing K";
+        e = launch_gather_rows(K, t->packed_K, t->perm, static_cast<int>(BH), N, N, row, s);
+    }
+    if (e == hipSuccess) {
+        what = "packing V";
+        e = launch_gather_rows(V, t->packed_V, t->perm, static_cast<int>(BH), N, N, row, s);
+    }
+    if (e == hipSuccess) {
+        what = "gathering representatives";
+        e = launch_gather_rows(K, t->reps, t->rep_token, static_cast<int>(BH), M, N, row, s);
+    }
+    if (e == hipSuccess) {
+        what = "team build sync";
+        e = hipStreamSynchronize(s);
+    }
+    cleanup();
+    if (e != hipSuccess) {
+        free_teams(t);
+        return hip_fail(e, what);
+    }
+    return finish_table(t, out);
+}
+
 santapp_status santapp_teams_info(const santapp_teams* t, santapp_teams_desc* d) {
     if (!t || !d) return fail(SANTAPP_EINVAL, "NULL argument");
     d->B = t->B;
@@ -305,6 +529,7 @@ santapp_status santapp_teams_info(const santapp_teams* t, santapp_teams_desc* d)
     d->log_n = t->log_n;
     d->rep_token = t->rep_token;
     d->perm = t->perm;
+    d->team_count = t->team_count;
     return ok();
 }
 

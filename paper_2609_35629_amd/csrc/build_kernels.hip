@@ -64,11 +64,14 @@ __device__ double sqdist_to(const T* __restrict__ row, const double* __restrict_
     return acc;
 }
 
-template <typename T>
+// LIST: the parent's members are the token indices mem[0 .. n) (ascending)
+// of a label-defined partition; otherwise the contiguous span [pP, pP + n).
+template <typename T, bool LIST>
 __global__ __launch_bounds__(kBuildThreads) void k_build_parent(
     const T* __restrict__ K, int N, int d, int P, int R, int M, double* __restrict__ mind_all,
     int* __restrict__ owner_all, int* __restrict__ team_begin, int* __restrict__ team_size,
-    double* __restrict__ log_n, int* __restrict__ rep_token, int* __restrict__ perm) {
+    double* __restrict__ log_n, int* __restrict__ rep_token, int* __restrict__ perm,
+    const int* __restrict__ members, const int* __restrict__ pbeg, const int* __restrict__ toff, int Mp) {
 #pragma clang fp contract(off)
     __shared__ double s_vec[kMaxHeadDim];
     __shared__ ArgVal s_red[kBuildWaves];
@@ -80,18 +83,30 @@ __global__ __launch_bounds__(kBuildThreads) void k_build_parent(
     const int p = blockIdx.x;
     const int bh = blockIdx.y;
     const int tid = threadIdx.x;
-    const int start = p * P;
-    const int n = min(P, N - start);
+    int start, n, team0;
+    if constexpr (LIST) {
+        start = pbeg[static_cast<size_t>(bh) * (Mp + 1) + p];
+        n = pbeg[static_cast<size_t>(bh) * (Mp + 1) + p + 1] - start;
+        team0 = toff[static_cast<size_t>(bh) * (Mp + 1) + p];
+        if (n == 0) return;  // empty parents are omitted (uniform over the workgroup)
+    } else {
+        start = p * P;
+        n = min(P, N - start);
+        team0 = p * min(R, P);  // every earlier parent is full-size
+    }
     const int r = min(R, n);
-    const int team0 = p * min(R, P);  // every earlier parent is full-size
-    const T* Kc = K + (static_cast<size_t>(bh) * N + start) * d;
+    const int* mem = LIST ? members + static_cast<size_t>(bh) * N + start : nullptr;
+    // token of member i, and its key row
+    auto tok = [&](int i) { return LIST ? mem[i] : start + i; };
+    const T* Kb = K + static_cast<size_t>(bh) * N * d;
+    auto row = [&](int i) { return Kb + static_cast<size_t>(tok(i)) * d; };
     double* mind = mind_all + static_cast<size_t>(bh) * N + start;
     int* owner = owner_all + static_cast<size_t>(bh) * N + start;
 
     // parent mean, summed over members in token order
     for (int j = tid; j < d; j += kBuildThreads) {
         double s = 0.0;
-        for (int i = 0; i < n; ++i) s = s + static_cast<double>(load_elem(Kc, static_cast<size_t>(i) * d + j));
+        for (int i = 0; i < n; ++i) s = s + static_cast<double>(load_elem(row(i), j));
         s_vec[j] = s / static_cast<double>(n);
     }
     __syncthreads();
@@ -99,7 +114,7 @@ __global__ __launch_bounds__(kBuildThreads) void k_build_parent(
     // first representative: the member nearest the mean
     ArgVal best{INFINITY, 0x7fffffff};
     for (int i = tid; i < n; i += kBuildThreads) {
-        ArgVal c{sqdist_to(Kc + static_cast<size_t>(i) * d, s_vec, d), i};
+        ArgVal c{sqdist_to(row(i), s_vec, d), i};
         best = pick_min(best, c);
     }
     best = block_arg<false>(best, s_red);
@@ -109,14 +124,13 @@ __global__ __launch_bounds__(kBuildThreads) void k_build_parent(
 
     for (int u = 0; u < r; ++u) {
         if (tid == 0) s_reps[u] = rep;
-        for (int j = tid; j < d; j += kBuildThreads)
-            s_vec[j] = static_cast<double>(load_elem(Kc, static_cast<size_t>(rep) * d + j));
+        for (int j = tid; j < d; j += kBuildThreads) s_vec[j] = static_cast<double>(load_elem(row(rep), j));
         __syncthreads();
         // fold the new representative into the running minimum; a chosen
         // representative gets -1 so that it is never chosen again
         ArgVal far{-INFINITY, 0x7fffffff};
         for (int i = tid; i < n; i += kBuildThreads) {
-            double m, dd = sqdist_to(Kc + static_cast<size_t>(i) * d, s_vec, d);
+            double m, dd = sqdist_to(row(i), s_vec, d);
             int o;
             if (u == 0) {
                 m = dd;
@@ -163,7 +177,7 @@ __global__ __launch_bounds__(kBuildThreads) void k_build_parent(
         team_begin[tbase + u] = start + s_off[u];
         team_size[tbase + u] = s_cnt[u];
         log_n[tbase + u] = log(static_cast<double>(s_cnt[u]));
-        rep_token[tbase + u] = start + s_reps[u];
+        rep_token[tbase + u] = tok(s_reps[u]);
     }
 
     // packed position of each member: team offset + rank among the team's
@@ -184,7 +198,7 @@ __global__ __launch_bounds__(kBuildThreads) void k_build_parent(
         if (i < n) {
             int pos = s_off[o] + rank_in_wave;
             for (int v = 0; v < w; ++v) pos += s_wcnt[v][o];
-            pperm[pos] = start + i;
+            pperm[pos] = tok(i);
         }
         __syncthreads();
         for (int u = tid; u < r; u += kBuildThreads) {
@@ -624,13 +638,29 @@ hipError_t launch_build_parents(const void* K, const void* V, santapp_dtype dtyp
 #undef SANTAPP_REGS
     }
     if (dtype == SANTAPP_BF16)
-        k_build_parent<bf16_t><<<grid, kBuildThreads, 0, s>>>(
+        k_build_parent<bf16_t, false><<<grid, kBuildThreads, 0, s>>>(
             static_cast<const bf16_t*>(K), N, d, P, R, M, mind, owner, team_begin, team_size,
-            log_n, rep_token, perm);
+            log_n, rep_token, perm, nullptr, nullptr, nullptr, 0);
     else
-        k_build_parent<float><<<grid, kBuildThreads, 0, s>>>(
+        k_build_parent<float, false><<<grid, kBuildThreads, 0, s>>>(
             static_cast<const float*>(K), N, d, P, R, M, mind, owner, team_begin, team_size,
-            log_n, rep_token, perm);
+            log_n, rep_token, perm, nullptr, nullptr, nullptr, 0);
+    return hipGetLastError();
+}
+
+hipError_t launch_build_parent_lists(const void* K, santapp_dtype dtype, int BH, int N, int d, int Mp,
+                                     int R, int M, const int* members, const int* pbeg, const int* toff,
+                                     double* mind, int* owner, int* team_begin, int* team_size,
+                                     double* log_n, int* rep_token, int* perm, hipStream_t s) {
+    const dim3 grid(Mp, BH);
+    if (dtype == SANTAPP_BF16)
+        k_build_parent<bf16_t, true><<<grid, kBuildThreads, 0, s>>>(
+            static_cast<const bf16_t*>(K), N, d, 0, R, M, mind, owner, team_begin, team_size, log_n,
+            rep_token, perm, members, pbeg, toff, Mp);
+    else
+        k_build_parent<float, true><<<grid, kBuildThreads, 0, s>>>(
+            static_cast<const float*>(K), N, d, 0, R, M, mind, owner, team_begin, team_size, log_n,
+            rep_token, perm, members, pbeg, toff, Mp);
     return hipGetLastError();
 }
 

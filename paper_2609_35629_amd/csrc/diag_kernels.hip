@@ -56,7 +56,8 @@ __global__ __launch_bounds__(D) void k_team_centroid(const T* __restrict__ packe
         for (int k = 0; k < 8; ++k) s = s + static_cast<double>(v[k]);
     }
     for (; i < n; ++i) s = s + static_cast<double>(load_elem(col, static_cast<size_t>(i) * D));
-    store_mean(reps + t * D + j, s / static_cast<double>(n));
+    // an absent team (no rows) keeps a zero key; its log n excludes it
+    store_mean(reps + t * D + j, n > 0 ? s / static_cast<double>(n) : 0.0);
 }
 
 // The representative's key: its packed row is found among the team's rows

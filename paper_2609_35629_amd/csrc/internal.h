@@ -19,6 +19,15 @@ constexpr int kChunkRows = 64;     // rows per sampled attention unit (two 32-ro
 constexpr int kDenseRows = 128;    // rows per dense attention unit
 constexpr int kAttendWavesPerCU = 8; // resident attention waves per compute unit
 constexpr int kMergeThreads = 256;   // threads of a merge workgroup
+constexpr int kKmMaxCenters = 1024;  // k-means parents per (b, kv)
+constexpr int kKmMaxTrials = 8;      // seeding candidates per round: 2 + floor(ln 1024)
+constexpr int kMaxLabels = 1024;     // parents of a label-defined partition
+// log n of an absent team (tables whose (b, kv) pairs have different team
+// counts pad the shorter ones): a finite stand-in for log 0, far below every
+// real routing score, so that no score is infinite and sampling never takes
+// such a team while its pair has more than K real ones
+constexpr double kAbsentLogN = -1e300;
+constexpr double kAbsentBelow = -1e299;  // routing scores below this are absent teams
 
 // Attention work unit: up to kChunkRows consecutive rows of one union team of
 // the packed cache, or of the suffix (slot < 0); the dense path cuts its rows
@@ -110,6 +119,51 @@ hipError_t launch_build_parents(const void* K, const void* V, santapp_dtype dtyp
 
 hipError_t launch_gather_rows(const void* src, void* dst, const int* index, int BH, int rows_out,
                               int rows_in, size_t row_bytes, hipStream_t s);
+
+// Team table of label-defined parents: parent u of pair bh has the members
+// members[bh N + pbeg[bh (Mp+1) + u] ..] (token order) and its first team is
+// toff[bh (Mp+1) + u]; team_begin is a position in that member order.
+hipError_t launch_build_parent_lists(const void* K, santapp_dtype dtype, int BH, int N, int d, int Mp,
+                                     int R, int M, const int* members, const int* pbeg, const int* toff,
+                                     double* mind, int* owner, int* team_begin, int* team_size,
+                                     double* log_n, int* rep_token, int* perm, hipStream_t s);
+
+// k-means state of one (b, kv): smoothed batch inertia and its minimum, the
+// count of steps without a new minimum, the stop flag and the steps run.
+struct KmState {
+    double ewa, ewa_min;
+    int no_imp, stop, steps, pad;
+};
+
+// Scratch of santapp_kmeans_parents (byte offsets into one buffer).
+struct KmLayout {
+    int M = 0, s0 = 0, L = 0, nkpp = 0, nasg = 0;
+    size_t samp = 0, cand = 0, D2 = 0, Dt = 0, part = 0, cent = 0, w = 0, state = 0, bpart = 0,
+           bcnt = 0, binert = 0, total = 0;
+};
+KmLayout kmeans_layout(int BH, int N, int d, int M, int batch, int s0);
+
+// Seeding (every round), then `count` minibatch steps from step `first`,
+// then the final labels [BH, N].
+hipError_t launch_kmeans_seed(const void* K, santapp_dtype dtype, int BH, int N, int d,
+                              const KmLayout& L, char* ws, uint64_t seed, hipStream_t s);
+hipError_t launch_kmeans_steps(const void* K, santapp_dtype dtype, int BH, int N, int d,
+                               const KmLayout& L, char* ws, int batch, int first, int count,
+                               double alpha, double ratio, int max_no_improvement, uint64_t seed,
+                               hipStream_t s);
+hipError_t launch_kmeans_labels(const void* K, santapp_dtype dtype, int BH, int N, int d,
+                                const KmLayout& L, char* ws, int* labels, hipStream_t s);
+
+// Members of each parent in token order, parent offsets pbeg [BH, Mp+1],
+// team offsets toff [BH, Mp+1], team counts [BH]; *bad is set (never
+// cleared) when a label lies outside [0, Mp).
+hipError_t launch_parent_lists(const int* labels, int BH, int N, int Mp, int R, int* members, int* pbeg,
+                               int* toff, int* team_count, int* bad, hipStream_t s);
+
+// Absent teams g >= team_count[bh] of every pair: size 0, begin N,
+// log n = kAbsentLogN, representative token 0.
+hipError_t launch_pad_teams(const int* team_count, int BH, int M, int N, int* team_begin, int* team_size,
+                            double* log_n, int* rep_token, hipStream_t s);
 
 struct RouteArgs {
     const void* reps;       // [BH, M, d]

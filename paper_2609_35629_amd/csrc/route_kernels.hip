@@ -93,6 +93,12 @@ struct RepChunk<float, 4> {
     }
 };
 
+// Value-histogram bucket of a key in [0, 2^kFineBits): keys below the range
+// (absent teams) land in bucket 0.
+__device__ __forceinline__ int fine_bucket(double y, double ymin, double fs) {
+    return static_cast<int>(fmin(static_cast<double>((1 << kFineBits) - 1), fmax(0.0, (y - ymin) * fs)));
+}
+
 // log c for c = 1 - exp(-exp(x)) in fp32 (eq. method-inclusion).  x >= -37
 // for a selected team (its perturbed score beats tau and a Gumbel draw is at
 // most 53 log 2), so e^x stays a normal fp32.  For e^x < 1/16 a four-term
@@ -178,7 +184,7 @@ struct KeySet {
     __device__ __forceinline__ void set_fine(double ymin, double fs) {
 #pragma unroll
         for (int j = 0; j < PL; ++j)
-            fine[j] = min((1 << kFineBits) - 1, static_cast<int>((key_value(k[j]) - ymin) * fs));
+            fine[j] = fine_bucket(key_value(k[j]), ymin, fs);
     }
     __device__ __forceinline__ int fine_of(int j, double, double) const { return fine[j]; }
 };
@@ -228,16 +234,22 @@ template <int PL>
 __device__ uint64_t select_key(KeySet<PL>& ks, int want, uint32_t* hist, uint64_t* cand) {
     const int lane = lane_id();
     const int nj = ks.count();
-    uint64_t kmin = ~0ull, kmax = 0;
+    // the histogram spans the real teams' keys (absent teams, far below,
+    // fall into bucket 0) unless those are all equal
+    const uint64_t kreal = order_key(kAbsentBelow);
+    uint64_t kmin = ~0ull, kmax = 0, rmin = ~0ull;
 #pragma unroll
     for (int j = 0; j < nj; ++j) {
         if (ks.valid(j)) {
             kmin = min(kmin, ks.key(j));
             kmax = max(kmax, ks.key(j));
+            if (ks.key(j) >= kreal) rmin = min(rmin, ks.key(j));
         }
     }
     kmin = wave_min64(kmin);
     kmax = wave_max64(kmax);
+    rmin = wave_min64(rmin);
+    if (rmin < kmax) kmin = rmin;
     const double ymin = key_value(kmin);
     const double range = key_value(kmax) - ymin;
     if (!(range > 0.0)) return kmin;  // every key equal
@@ -471,16 +483,21 @@ __global__ __launch_bounds__(kSelectThreads) void k_select_head(
     auto valid = [&](int j) { return j * kSelectThreads + tid < M; };
 
     // tau's key: rank Kp (0-based, descending) among the M keys
-    uint64_t kmin = ~0ull, kmax = 0;
+    // histogram range: the real teams' keys unless those are all equal
+    const uint64_t kreal = order_key(kAbsentBelow);
+    uint64_t kmin = ~0ull, kmax = 0, rmin = ~0ull;
 #pragma unroll
     for (int j = 0; j < kHeadKeys; ++j) {
         if (valid(j)) {
             kmin = min(kmin, k[j]);
             kmax = max(kmax, k[j]);
+            if (k[j] >= kreal) rmin = min(rmin, k[j]);
         }
     }
     kmin = block_ext64<false>(kmin, s_red);
     kmax = block_ext64<true>(kmax, s_red);
+    rmin = block_ext64<false>(rmin, s_red);
+    if (rmin < kmax) kmin = rmin;
     const double ymin = key_value(kmin);
     const double range = key_value(kmax) - ymin;
     int want = Kp;
@@ -490,7 +507,7 @@ __global__ __launch_bounds__(kSelectThreads) void k_select_head(
         int fine[kHeadKeys];
 #pragma unroll
         for (int j = 0; j < kHeadKeys; ++j)
-            fine[j] = valid(j) ? min((1 << kFineBits) - 1, static_cast<int>((key_value(k[j]) - ymin) * fs)) : -1;
+            fine[j] = valid(j) ? fine_bucket(key_value(k[j]), ymin, fs) : -1;
         // a 256-bin histogram of the (selected) keys' bins, and the bin that
         // holds rank `want`
         auto hist_pass = [&](auto bin_of) {
