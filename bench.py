@@ -47,12 +47,28 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="budget of the oracle CPU-baseline sample (0 disables it)")
     p.add_argument("--no-dense", action="store_true")
+    p.add_argument("--parents", choices=("contiguous", "kmeans"), default="contiguous",
+                   help="parent partition of the team table (Alg. contiguous / minibatch k-means)")
     p.add_argument("--kl-table", action="store_true",
                    help="print the routing KL diagnostic of several groupings of the workload and exit")
     p.add_argument("--calibrate-copy", action="store_true",
                    help="only run a plain 256 MiB device-to-device copy five times (the reference "
                         "kernel for scaling the FETCH_SIZE / WRITE_SIZE counters) and exit")
     return p.parse_args()
+
+
+def make_table(wl, db, parents, P=None, R=None):
+    """Team table of the workload's keys: contiguous parents, or minibatch
+    k-means parents with the paper's settings (batch 4096, at most 100
+    iterations, 10-step no-improvement rule, reassignment ratio 0.01, seed 0).
+    Returns (table, minibatch steps per (b, kv) or None)."""
+    import paper_2609_35629_amd as sp
+    P = wl.P if P is None else P
+    R = wl.R if R is None else R
+    if parents == "contiguous":
+        return sp.build_teams(db["K"], db["V"], P, R), None
+    labels, mp, steps = sp.kmeans_parents(db["K"], P)
+    return sp.build_teams_from_labels(db["K"], db["V"], labels, mp, R), steps
 
 
 def kl_table(wl, db):
@@ -68,9 +84,17 @@ def kl_table(wl, db):
                 ("centroid-guided B=16 (contiguous)", 16, 1, "centroid"),
                 (f"teams P={wl.P} R={wl.R} (representative keys)", wl.P, wl.R, "representative"),
                 (f"teams P={wl.P} R={wl.R} (team means)", wl.P, wl.R, "centroid")]
+    variants = [v + ("contiguous",) for v in variants]
+    # k-means parents (the paper's main policy), and centroid-guided sampling
+    # over k-means groups where their count stays within the k-means limit
+    variants.append((f"teams P={wl.P} R={wl.R}, k-means parents (representative keys)", wl.P, wl.R,
+                     "representative", "kmeans"))
+    for Bg in (16, 32):
+        if wl.N // Bg <= 1024:
+            variants.append((f"centroid-guided B={Bg} (k-means groups)", Bg, 1, "centroid", "kmeans"))
     rows = []
-    for name, P, R, kind in variants:
-        t = sp.build_teams(db["K"], db["V"], P, R)
+    for name, P, R, kind, parents in variants:
+        t, _ = make_table(wl, db, parents, P, R)
         sp.set_route_keys(t, kind)
         kl = sp.routing_kl(t, db["q"], scale=wl.scale)
         rows.append({"variant": name, "P": P, "R": R, "M": t.M, "route_keys": kind,
@@ -111,7 +135,7 @@ def main():
     if args.kl_table:
         kl_table(wl, db)
         return
-    teams = sp.build_teams(db["K"], db["V"], wl.P, wl.R)
+    teams, km_steps = make_table(wl, db, args.parents)
     M = teams.M
     ws = sp.decode_workspace(teams, wl.Hq, wl.T, wl.K)
     out = torch.empty((wl.B, wl.Hq, wl.d), dtype=torch.float32, device="cuda")
@@ -198,17 +222,18 @@ def main():
     # copy-calibrated), for the workload they were measured on, while the
     # kernel's sources are unchanged since
     traffic = None
-    if wl.name == "qwen32k" and wl.K == 32 and wl.B == 1 and not args.no_evict:
+    if wl.name == "qwen32k" and wl.K == 32 and wl.B == 1 and not args.no_evict and args.parents == "contiguous":
         traffic = measured_traffic()
 
     # preparation per prompt, excluded from the step as in the paper: host
-    # time of santapp_build_teams (device allocations, team build, packed
-    # copies; the call returns once its kernels are done), median of three
+    # time of the table build (k-means when chosen, device allocations, team
+    # build, packed copies; the calls return once their kernels are done),
+    # median of three
     prep_us = []
     for _ in range(3):
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        extra = sp.build_teams(db["K"], db["V"], wl.P, wl.R)
+        extra, _ = make_table(wl, db, args.parents)
         prep_us.append((time.perf_counter() - t0) * 1e6)
         extra.close()
 
@@ -221,7 +246,7 @@ def main():
     sp.set_route_keys(teams, "representative")
 
     cpu = None
-    if args.cpu_seconds > 0:
+    if args.cpu_seconds > 0 and args.parents == "contiguous":
         cpu = cpu_baseline(wl, batch, args.cpu_seconds)
 
     res = {
@@ -239,7 +264,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{wl.name}: Qwen2.5-7B-shaped layer, {wl.N}-token prompt, B={wl.B}",
                    "B": wl.B, "Hq": wl.Hq, "Hkv": wl.Hkv, "d": wl.d, "N": wl.N, "T": wl.T,
-                   "P": wl.P, "R": wl.R, "M": M, "K": wl.K, "evict_1GiB": not args.no_evict},
+                   "P": wl.P, "R": wl.R, "M": M, "K": wl.K, "parents": args.parents,
+                   "evict_1GiB": not args.no_evict},
         "roofline": {"bound": "hbm", "kernel": "k_attend_mfma<128, false>", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic},
@@ -256,6 +282,8 @@ def main():
                           "merge": round(float(np.mean(stages_us[:, 2])), 3)},
         "wall_s_sparse_loop": round(t_wall1 - t_wall0, 3),
     }
+    if km_steps is not None:
+        res["kmeans_steps"] = km_steps
     if dense_us is not None:
         d = float(np.mean(dense_us))
         res["dense_us"] = round(d, 3)

@@ -21,6 +21,10 @@ namespace {
 
 constexpr int kBuildThreads = 256;
 constexpr int kBuildWaves = kBuildThreads / kWave;
+// label-defined parents hold about N / M members each (k-means: about P),
+// one workgroup per parent: four times the threads for fewer rounds per
+// member sweep
+constexpr int kListBuildThreads = 1024;
 
 // (value, index) reductions with ties broken toward the lower index.
 struct ArgVal {
@@ -36,7 +40,7 @@ __device__ __forceinline__ ArgVal pick_max(ArgVal a, ArgVal b) {
     return (b.v > a.v || (b.v == a.v && b.i < a.i)) ? b : a;
 }
 
-template <bool kMax>
+template <bool kMax, int W = kBuildWaves>
 __device__ ArgVal block_arg(ArgVal x, ArgVal* s_red) {
     for (int off = kWave / 2; off > 0; off >>= 1) {
         ArgVal y;
@@ -47,38 +51,59 @@ __device__ ArgVal block_arg(ArgVal x, ArgVal* s_red) {
     if (lane_id() == 0) s_red[wave_id()] = x;
     __syncthreads();
     ArgVal r = s_red[0];
-    for (int w = 1; w < kBuildWaves; ++w) r = kMax ? pick_max(r, s_red[w]) : pick_min(r, s_red[w]);
+    for (int w = 1; w < W; ++w) r = kMax ? pick_max(r, s_red[w]) : pick_min(r, s_red[w]);
     __syncthreads();
     return r;
 }
 
-// |k_i - c|^2 with c held in LDS as fp64, summed in dimension order.
+// |k_i - c|^2 with c held in LDS as fp64, summed in dimension order; the row
+// is read 16 bytes at a time (rows are 16-byte aligned, d a multiple of 8).
 template <typename T>
 __device__ double sqdist_to(const T* __restrict__ row, const double* __restrict__ c, int d) {
 #pragma clang fp contract(off)
     double acc = 0.0;
-    for (int j = 0; j < d; ++j) {
-        const double t = static_cast<double>(load_elem(row, j)) - c[j];
-        acc = acc + t * t;
+    constexpr int kPer = 16 / static_cast<int>(sizeof(T));
+    for (int j = 0; j < d; j += kPer) {
+        const uint4 w = *reinterpret_cast<const uint4*>(row + j);
+        float v[kPer];
+        if constexpr (sizeof(T) == 2) {
+            const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                v[2 * q] = bf16lo(ws[q]);
+                v[2 * q + 1] = bf16hi(ws[q]);
+            }
+        } else {
+            v[0] = __uint_as_float(w.x);
+            v[1] = __uint_as_float(w.y);
+            v[2] = __uint_as_float(w.z);
+            v[3] = __uint_as_float(w.w);
+        }
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) {
+            const double t = static_cast<double>(v[q]) - c[j + q];
+            acc = acc + t * t;
+        }
     }
     return acc;
 }
 
-// LIST: the parent's members are the token indices mem[0 .. n) (ascending)
+// NT threads per workgroup.  LIST: the parent's members are the token
+// indices mem[0 .. n) (ascending)
 // of a label-defined partition; otherwise the contiguous span [pP, pP + n).
-template <typename T, bool LIST>
-__global__ __launch_bounds__(kBuildThreads) void k_build_parent(
+template <typename T, bool LIST, int NT>
+__global__ __launch_bounds__(NT) void k_build_parent(
     const T* __restrict__ K, int N, int d, int P, int R, int M, double* __restrict__ mind_all,
     int* __restrict__ owner_all, int* __restrict__ team_begin, int* __restrict__ team_size,
     double* __restrict__ log_n, int* __restrict__ rep_token, int* __restrict__ perm,
     const int* __restrict__ members, const int* __restrict__ pbeg, const int* __restrict__ toff, int Mp) {
 #pragma clang fp contract(off)
     __shared__ double s_vec[kMaxHeadDim];
-    __shared__ ArgVal s_red[kBuildWaves];
+    __shared__ ArgVal s_red[(NT / kWave)];
     __shared__ int s_reps[kMaxReps];
     __shared__ int s_cnt[kMaxReps];
     __shared__ int s_off[kMaxReps];
-    __shared__ int s_wcnt[kBuildWaves][kMaxReps];
+    __shared__ int s_wcnt[(NT / kWave)][kMaxReps];
 
     const int p = blockIdx.x;
     const int bh = blockIdx.y;
@@ -104,7 +129,7 @@ __global__ __launch_bounds__(kBuildThreads) void k_build_parent(
     int* owner = owner_all + static_cast<size_t>(bh) * N + start;
 
     // parent mean, summed over members in token order
-    for (int j = tid; j < d; j += kBuildThreads) {
+    for (int j = tid; j < d; j += NT) {
         double s = 0.0;
         for (int i = 0; i < n; ++i) s = s + static_cast<double>(load_elem(row(i), j));
         s_vec[j] = s / static_cast<double>(n);
@@ -113,23 +138,23 @@ __global__ __launch_bounds__(kBuildThreads) void k_build_parent(
 
     // first representative: the member nearest the mean
     ArgVal best{INFINITY, 0x7fffffff};
-    for (int i = tid; i < n; i += kBuildThreads) {
+    for (int i = tid; i < n; i += NT) {
         ArgVal c{sqdist_to(row(i), s_vec, d), i};
         best = pick_min(best, c);
     }
-    best = block_arg<false>(best, s_red);
+    best = block_arg<false, NT / kWave>(best, s_red);
     // a reduction without a winner (NaN keys) falls back to member 0, so
     // that every index stays inside the parent
     int rep = best.i < n ? best.i : 0;
 
     for (int u = 0; u < r; ++u) {
         if (tid == 0) s_reps[u] = rep;
-        for (int j = tid; j < d; j += kBuildThreads) s_vec[j] = static_cast<double>(load_elem(row(rep), j));
+        for (int j = tid; j < d; j += NT) s_vec[j] = static_cast<double>(load_elem(row(rep), j));
         __syncthreads();
         // fold the new representative into the running minimum; a chosen
         // representative gets -1 so that it is never chosen again
         ArgVal far{-INFINITY, 0x7fffffff};
-        for (int i = tid; i < n; i += kBuildThreads) {
+        for (int i = tid; i < n; i += NT) {
             double m, dd = sqdist_to(row(i), s_vec, d);
             int o;
             if (u == 0) {
@@ -152,7 +177,7 @@ __global__ __launch_bounds__(kBuildThreads) void k_build_parent(
             far = pick_max(far, ArgVal{m, i});
         }
         if (u + 1 < r) {
-            far = block_arg<true>(far, s_red);
+            far = block_arg<true, NT / kWave>(far, s_red);
             rep = far.i < n ? far.i : 0;
         } else {
             __syncthreads();
@@ -160,9 +185,9 @@ __global__ __launch_bounds__(kBuildThreads) void k_build_parent(
     }
 
     // team sizes and offsets inside the parent
-    for (int u = tid; u < r; u += kBuildThreads) s_cnt[u] = 0;
+    for (int u = tid; u < r; u += NT) s_cnt[u] = 0;
     __syncthreads();
-    for (int i = tid; i < n; i += kBuildThreads) atomicAdd(&s_cnt[owner[i]], 1);
+    for (int i = tid; i < n; i += NT) atomicAdd(&s_cnt[owner[i]], 1);
     __syncthreads();
     if (tid == 0) {
         int acc = 0;
@@ -173,7 +198,7 @@ __global__ __launch_bounds__(kBuildThreads) void k_build_parent(
     }
     __syncthreads();
     const size_t tbase = static_cast<size_t>(bh) * M + team0;
-    for (int u = tid; u < r; u += kBuildThreads) {
+    for (int u = tid; u < r; u += NT) {
         team_begin[tbase + u] = start + s_off[u];
         team_size[tbase + u] = s_cnt[u];
         log_n[tbase + u] = log(static_cast<double>(s_cnt[u]));
@@ -185,7 +210,7 @@ __global__ __launch_bounds__(kBuildThreads) void k_build_parent(
     int* pperm = perm + static_cast<size_t>(bh) * N + start;
     const int w = wave_id();
     const uint64_t lt = lanemask_lt();
-    for (int base = 0; base < n; base += kBuildThreads) {
+    for (int base = 0; base < n; base += NT) {
         const int i = base + tid;
         const int o = (i < n) ? owner[i] : -1;
         int rank_in_wave = 0;
@@ -201,9 +226,9 @@ __global__ __launch_bounds__(kBuildThreads) void k_build_parent(
             pperm[pos] = tok(i);
         }
         __syncthreads();
-        for (int u = tid; u < r; u += kBuildThreads) {
+        for (int u = tid; u < r; u += NT) {
             int add = 0;
-            for (int v = 0; v < kBuildWaves; ++v) add += s_wcnt[v][u];
+            for (int v = 0; v < (NT / kWave); ++v) add += s_wcnt[v][u];
             s_off[u] += add;
         }
         __syncthreads();
@@ -638,11 +663,11 @@ hipError_t launch_build_parents(const void* K, const void* V, santapp_dtype dtyp
 #undef SANTAPP_REGS
     }
     if (dtype == SANTAPP_BF16)
-        k_build_parent<bf16_t, false><<<grid, kBuildThreads, 0, s>>>(
+        k_build_parent<bf16_t, false, kBuildThreads><<<grid, kBuildThreads, 0, s>>>(
             static_cast<const bf16_t*>(K), N, d, P, R, M, mind, owner, team_begin, team_size,
             log_n, rep_token, perm, nullptr, nullptr, nullptr, 0);
     else
-        k_build_parent<float, false><<<grid, kBuildThreads, 0, s>>>(
+        k_build_parent<float, false, kBuildThreads><<<grid, kBuildThreads, 0, s>>>(
             static_cast<const float*>(K), N, d, P, R, M, mind, owner, team_begin, team_size,
             log_n, rep_token, perm, nullptr, nullptr, nullptr, 0);
     return hipGetLastError();
@@ -654,11 +679,11 @@ hipError_t launch_build_parent_lists(const void* K, santapp_dtype dtype, int BH,
                                      double* log_n, int* rep_token, int* perm, hipStream_t s) {
     const dim3 grid(Mp, BH);
     if (dtype == SANTAPP_BF16)
-        k_build_parent<bf16_t, true><<<grid, kBuildThreads, 0, s>>>(
+        k_build_parent<bf16_t, true, kListBuildThreads><<<grid, kListBuildThreads, 0, s>>>(
             static_cast<const bf16_t*>(K), N, d, 0, R, M, mind, owner, team_begin, team_size, log_n,
             rep_token, perm, members, pbeg, toff, Mp);
     else
-        k_build_parent<float, true><<<grid, kBuildThreads, 0, s>>>(
+        k_build_parent<float, true, kListBuildThreads><<<grid, kListBuildThreads, 0, s>>>(
             static_cast<const float*>(K), N, d, 0, R, M, mind, owner, team_begin, team_size, log_n,
             rep_token, perm, members, pbeg, toff, Mp);
     return hipGetLastError();

@@ -68,6 +68,25 @@ __device__ __forceinline__ double draw_unit(uint64_t w) {
     return static_cast<double>(w >> 11) * 0x1.0p-53;
 }
 
+// 16 bytes of a key row as floats (8 bf16 or 4 fp32 values, in order).
+__device__ __forceinline__ void load_row16(const bf16_t* p, float (&v)[8]) {
+    const uint4 w = *reinterpret_cast<const uint4*>(p);
+    const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        v[2 * q] = bf16lo(ws[q]);
+        v[2 * q + 1] = bf16hi(ws[q]);
+    }
+}
+
+__device__ __forceinline__ void load_row16(const float* p, float (&v)[4]) {
+    const uint4 w = *reinterpret_cast<const uint4*>(p);
+    v[0] = __uint_as_float(w.x);
+    v[1] = __uint_as_float(w.y);
+    v[2] = __uint_as_float(w.z);
+    v[3] = __uint_as_float(w.w);
+}
+
 // Per-workgroup sum of one value per thread: waves by xor shuffles, then the
 // wave totals in wave order.
 template <int W>
@@ -115,14 +134,19 @@ __global__ __launch_bounds__(kKppThreads) void k_kpp_dist(
     double acc[kKmMaxTrials];
 #pragma unroll
     for (int t = 0; t < kKmMaxTrials; ++t) acc[t] = 0.0;
-#pragma unroll 4
-    for (int k = 0; k < D; ++k) {
-        const double xv = static_cast<double>(load_elem(x, k));
+    constexpr int kPer = 16 / static_cast<int>(sizeof(T));
+#pragma unroll 2
+    for (int k0 = 0; k0 < D; k0 += kPer) {
+        float xv[kPer];
+        load_row16(x + k0, xv);
 #pragma unroll
-        for (int t = 0; t < kKmMaxTrials; ++t) {
-            if (t < nc) {
-                const double e = xv - s_cand[t][k];
-                acc[t] = acc[t] + e * e;
+        for (int q = 0; q < kPer; ++q) {
+#pragma unroll
+            for (int t = 0; t < kKmMaxTrials; ++t) {
+                if (t < nc) {
+                    const double e = static_cast<double>(xv[q]) - s_cand[t][k0 + q];
+                    acc[t] = acc[t] + e * e;
+                }
             }
         }
     }
@@ -154,10 +178,12 @@ __global__ __launch_bounds__(kPickThreads) void k_kpp_pick(
     const int bh = blockIdx.x, tid = threadIdx.x;
     const int nc = c == 0 ? 1 : L;
     const T* X = K + static_cast<size_t>(bh) * N * D;
-    if (tid < nc) {
+    if (wave_id() < nc) {  // wave t sums trial t's workgroup partials
+        const int t = wave_id();
         double p = 0.0;
-        for (int b = 0; b < nblk; ++b) p = p + part[(static_cast<size_t>(bh) * nblk + b) * L + tid];
-        s_pot[tid] = p;
+        for (int b = lane_id(); b < nblk; b += kWave) p = p + part[(static_cast<size_t>(bh) * nblk + b) * L + t];
+        for (int off = kWave / 2; off > 0; off >>= 1) p = p + __shfl_xor(p, off);
+        if (lane_id() == 0) s_pot[t] = p;
     }
     if (tid < kKmMaxTrials) s_first[tid] = s0 - 1;
     __syncthreads();
@@ -236,7 +262,7 @@ __global__ __launch_bounds__(kAsgThreads) void k_km_assign(
     const double* __restrict__ cent, const KmState* __restrict__ state, int* __restrict__ labels,
     double* __restrict__ bpart, int* __restrict__ bcnt, double* __restrict__ binert) {
 #pragma clang fp contract(off)
-    __shared__ double s_x[kAsgPts][D + 1];
+    __shared__ float s_x[kAsgPts][D + 1];  // exact key values
     __shared__ double s_c[kAsgCen][D + 1];
     __shared__ int s_tok[kAsgPts];
     __shared__ int s_lab[kAsgPts];
@@ -257,7 +283,7 @@ __global__ __launch_bounds__(kAsgThreads) void k_km_assign(
     for (int e = tid; e < kAsgPts * D; e += kAsgThreads) {
         const int p = e / D, k = e % D;
         const int tok = s_tok[p];
-        s_x[p][k] = tok >= 0 ? static_cast<double>(load_elem(X + static_cast<size_t>(tok) * D, k)) : 0.0;
+        s_x[p][k] = tok >= 0 ? load_elem(X + static_cast<size_t>(tok) * D, k) : 0.f;
     }
     const int pg = tid >> 4, cg = tid & 15;
     double bd[4];
@@ -283,7 +309,7 @@ __global__ __launch_bounds__(kAsgThreads) void k_km_assign(
         for (int k = 0; k < D; ++k) {
             double xv[4], cv[2];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) xv[i] = s_x[4 * pg + i][k];
+            for (int i = 0; i < 4; ++i) xv[i] = static_cast<double>(s_x[4 * pg + i][k]);
 #pragma unroll
             for (int e = 0; e < 2; ++e) cv[e] = s_c[2 * cg + e][k];
 #pragma unroll
@@ -369,7 +395,7 @@ __global__ __launch_bounds__(kAsgThreads) void k_km_assign(
                 cur = u;
                 acc = 0.0;
             }
-            acc = acc + s_x[p][tid];
+            acc = acc + static_cast<double>(s_x[p][tid]);
         }
         if (cur >= 0) bpart[(blk * M + cur) * D + tid] = acc;
     }
@@ -382,14 +408,26 @@ __global__ __launch_bounds__(D) void k_km_update(int M, int nblk, const double* 
 #pragma clang fp contract(off)
     const int u = blockIdx.x, bh = blockIdx.y, k = threadIdx.x;
     if (state[bh].stop) return;
+    // eight workgroups' counts and partial sums loaded together (a partial
+    // of a center the workgroup did not see is stale and not added), then
+    // added in workgroup order
     double S = 0.0;
     int n = 0;
-    for (int b = 0; b < nblk; ++b) {
-        const size_t blk = static_cast<size_t>(bh) * nblk + b;
-        const int c = bcnt[blk * M + u];
-        if (c) {
-            S = S + bpart[(blk * M + u) * D + k];
-            n += c;
+    for (int b0 = 0; b0 < nblk; b0 += 8) {
+        int c[8];
+        double v[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const size_t blk = static_cast<size_t>(bh) * nblk + min(b0 + q, nblk - 1);
+            c[q] = b0 + q < nblk ? bcnt[blk * M + u] : 0;
+            v[q] = bpart[(blk * M + u) * D + k];
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            if (c[q]) {
+                S = S + v[q];
+                n += c[q];
+            }
         }
     }
     if (n == 0) return;  // uniform over the workgroup
@@ -444,7 +482,14 @@ __global__ __launch_bounds__(256) void k_km_control(
     }
     if (tid == 0) {
         double I = 0.0;
-        for (int b = 0; b < nblk; ++b) I = I + binert[static_cast<size_t>(bh) * nblk + b];
+        for (int b0 = 0; b0 < nblk; b0 += 8) {
+            double v[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) v[q] = binert[static_cast<size_t>(bh) * nblk + min(b0 + q, nblk - 1)];
+#pragma unroll
+            for (int q = 0; q < 8; ++q)
+                if (b0 + q < nblk) I = I + v[q];
+        }
         I = I / static_cast<double>(batch);
         KmState s = *st;
         s.ewa = step == 0 ? I : s.ewa * (1.0 - alpha) + I * alpha;
