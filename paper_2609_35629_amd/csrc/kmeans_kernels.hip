@@ -121,9 +121,18 @@ __global__ __launch_bounds__(kKppThreads) void k_kpp_dist(
     const int bh = blockIdx.y, tid = threadIdx.x;
     const int nc = c == 0 ? 1 : L;
     const T* X = K + static_cast<size_t>(bh) * N * D;
-    for (int e = tid; e < nc * D; e += kKppThreads) {
-        const int t = e / D, k = e % D;
-        s_cand[t][k] = static_cast<double>(load_elem(X + static_cast<size_t>(samp[cand[bh * L + t]]) * D, k));
+    __shared__ int s_ctok[kKmMaxTrials];
+    if (tid < nc) s_ctok[tid] = samp[cand[bh * L + tid]];
+    __syncthreads();
+    {
+        constexpr int kPer = 16 / static_cast<int>(sizeof(T));
+        for (int e = tid; e < nc * (D / kPer); e += kKppThreads) {
+            const int t = e / (D / kPer), k0 = (e % (D / kPer)) * kPer;
+            float v[kPer];
+            load_row16(X + static_cast<size_t>(s_ctok[t]) * D + k0, v);
+#pragma unroll
+            for (int r = 0; r < kPer; ++r) s_cand[t][k0 + r] = static_cast<double>(v[r]);
+        }
     }
     __syncthreads();
     const int j = blockIdx.x * kKppThreads + tid;
@@ -175,6 +184,7 @@ __global__ __launch_bounds__(kPickThreads) void k_kpp_pick(
     __shared__ double s_tot[kPickThreads / kWave];
     __shared__ int s_best;
     __shared__ int s_first[kKmMaxTrials];
+    __shared__ double s_u[kKmMaxTrials];
     const int bh = blockIdx.x, tid = threadIdx.x;
     const int nc = c == 0 ? 1 : L;
     const T* X = K + static_cast<size_t>(bh) * N * D;
@@ -230,10 +240,11 @@ __global__ __launch_bounds__(kPickThreads) void k_kpp_pick(
         total = total + s_tot[w];
     }
     const double pre = wpre + exc;
+    if (tid < L) s_u[tid] = draw_unit(km_word(seed, static_cast<uint64_t>(tid), 2, static_cast<uint64_t>(c + 1)));
+    __syncthreads();
     double target[kKmMaxTrials];
 #pragma unroll
-    for (int t = 0; t < kKmMaxTrials; ++t)
-        target[t] = t < L ? draw_unit(km_word(seed, static_cast<uint64_t>(t), 2, static_cast<uint64_t>(c + 1))) * total : 0.0;
+    for (int t = 0; t < kKmMaxTrials; ++t) target[t] = t < L ? s_u[t] * total : 0.0;
     int found[kKmMaxTrials];
 #pragma unroll
     for (int t = 0; t < kKmMaxTrials; ++t) found[t] = s0;
@@ -280,10 +291,27 @@ __global__ __launch_bounds__(kAsgThreads) void k_km_assign(
         s_tok[tid] = tok;
     }
     __syncthreads();
-    for (int e = tid; e < kAsgPts * D; e += kAsgThreads) {
-        const int p = e / D, k = e % D;
-        const int tok = s_tok[p];
-        s_x[p][k] = tok >= 0 ? load_elem(X + static_cast<size_t>(tok) * D, k) : 0.f;
+    // point rows, 16 bytes per load: every load of a thread is independent
+    {
+        constexpr int kPer = 16 / static_cast<int>(sizeof(T));
+        constexpr int kChunks = kAsgPts * D / kPer;
+        static_assert(kChunks % kAsgThreads == 0, "whole 16-byte chunks per thread");
+        float v[kChunks / kAsgThreads][kPer];
+#pragma unroll
+        for (int q = 0; q < kChunks / kAsgThreads; ++q) {
+            const int e = q * kAsgThreads + tid;
+            const int p = e / (D / kPer), k0 = (e % (D / kPer)) * kPer;
+            const int tok = s_tok[p];
+            load_row16(X + static_cast<size_t>(tok >= 0 ? tok : 0) * D + k0, v[q]);
+        }
+#pragma unroll
+        for (int q = 0; q < kChunks / kAsgThreads; ++q) {
+            const int e = q * kAsgThreads + tid;
+            const int p = e / (D / kPer), k0 = (e % (D / kPer)) * kPer;
+            const bool ok = s_tok[p] >= 0;
+#pragma unroll
+            for (int r = 0; r < kPer; ++r) s_x[p][k0 + r] = ok ? v[q][r] : 0.f;
+        }
     }
     const int pg = tid >> 4, cg = tid & 15;
     double bd[4];
