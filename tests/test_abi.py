@@ -89,3 +89,32 @@ def test_host_argument_checks():
                                   fake, fake, 1 << 30, None) == _lib.EINVAL
     assert L.santapp_dense_decode(fake, fake, fake, 1, 4, 100, 128, 0, None, None, 5, 28, 0.0,
                                   fake, fake, 1 << 30, None) == _lib.EINVAL  # T > 0, no suffix
+
+
+def test_kmeans_and_label_table_argument_checks():
+    """Host-side checks of the k-means and label-table entry points (no GPU
+    call is reached)."""
+    L = _lib.load()
+    fake = ctypes.c_void_p(1 << 20)
+    th = _lib.KMeansSettings(4096, 100, 10, 0.01, 0, 0)
+    mp = ctypes.c_int()
+    args = lambda K, N, d, P, t: (K, 1, 4, N, d, 0, P, ctypes.byref(t), fake, ctypes.byref(mp), None, None)
+    assert L.santapp_kmeans_parents(*args(None, 4096, 128, 1024, th)) == _lib.EINVAL
+    assert L.santapp_kmeans_parents(*args(fake, 1, 128, 1024, th)) == _lib.EINVAL      # N >= 2
+    assert L.santapp_kmeans_parents(*args(fake, 4096, 96, 1024, th)) == _lib.ELIMIT    # head dim
+    assert L.santapp_kmeans_parents(*args(fake, 4096, 128, 1, th)) == _lib.ELIMIT      # 4096 centers
+    assert b"1024" in L.santapp_last_error()
+    bad = _lib.KMeansSettings(4096, 100, 10, 1.0, 0, 0)                                # ratio in [0, 1)
+    assert L.santapp_kmeans_parents(*args(fake, 4096, 128, 1024, bad)) == _lib.EINVAL
+    bad = _lib.KMeansSettings(0, 100, 10, 0.01, 0, 0)                                  # empty batch
+    assert L.santapp_kmeans_parents(*args(fake, 4096, 128, 1024, bad)) == _lib.EINVAL
+    h = ctypes.c_void_p()
+    assert L.santapp_build_teams_from_labels(fake, fake, 1, 1, 64, 64, 0, None, 4, 2, None,
+                                             ctypes.byref(h)) == _lib.EINVAL
+    assert L.santapp_build_teams_from_labels(fake, fake, 1, 1, 64, 64, 0, fake, 2000, 2, None,
+                                             ctypes.byref(h)) == _lib.ELIMIT
+    assert L.santapp_build_teams_from_labels(fake, fake, 1, 1, 64, 64, 0, ctypes.c_void_p((1 << 20) + 4), 4, 2,
+                                             None, ctypes.byref(h)) == _lib.EINVAL
+    assert b"aligned" in L.santapp_last_error()
+    assert L.santapp_build_teams_from_labels(fake, fake, 1, 1, 64, 64, 0, fake, 4, 0, None,
+                                             ctypes.byref(h)) == _lib.EINVAL
