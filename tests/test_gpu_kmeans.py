@@ -166,3 +166,31 @@ def test_decode_with_kmeans_tables(Kb):
                 assert gap <= 1e-6 * max(1.0, abs(r.tau)), (h, real, r.sel)
         if tc[0, kv] <= Kb:  # every real team taken: the exact attention
             assert len(r.sel) == tc[0, kv]
+
+
+def test_kmeans_full_size_headline_layer():
+    """The 32768-token layer the benchmark times (4 KV heads, d = 128, bf16,
+    P = 1024, the paper's settings): labels, steps run and the team table of
+    two of the pairs against the oracle, element by element."""
+    wl = datagen.WORKLOADS["qwen32k"]
+    b = datagen.generate(wl)
+    db = dev_batch(b)
+    log("[gpu] kmeans full size qwen32k")
+    labels, mp, steps = sp.kmeans_parents(db.K, wl.P)
+    teams = sp.build_teams_from_labels(db.K, db.V, labels, mp, wl.R)
+    torch.cuda.synchronize()
+    lab = labels.cpu().numpy()
+    perm, tb, ts, rt = (teams.perm().cpu().numpy(), teams.team_begin().cpu().numpy(),
+                        teams.team_size().cpu().numpy(), teams.rep_token().cpu().numpy())
+    tc = teams.team_count().cpu().numpy()
+    for kv in (0, 3):
+        r = oracle.kmeans_parents(b.f64(b.K[0, kv]), wl.P)
+        log(f"[gpu]   kv={kv} steps gpu={steps[kv]} oracle={r.steps}")
+        assert steps[kv] == r.steps
+        np.testing.assert_array_equal(lab[0, kv], r.labels)
+        t = oracle.build_teams_from_labels(b.f64(b.K[0, kv]), r.labels, wl.R)
+        assert tc[0, kv] == t.M
+        np.testing.assert_array_equal(perm[0, kv], t.members)
+        np.testing.assert_array_equal(tb[0, kv, :t.M], t.team_ptr[:-1])
+        np.testing.assert_array_equal(ts[0, kv, :t.M], t.sizes)
+        np.testing.assert_array_equal(rt[0, kv, :t.M], t.rep_token)
