@@ -236,20 +236,25 @@ __device__ uint64_t select_key(KeySet<PL>& ks, int want, uint32_t* hist, uint64_
     const int nj = ks.count();
     // the histogram spans the real teams' keys (absent teams, far below,
     // fall into bucket 0) unless those are all equal
-    const uint64_t kreal = order_key(kAbsentBelow);
-    uint64_t kmin = ~0ull, kmax = 0, rmin = ~0ull;
+    uint64_t kmin = ~0ull, kmax = 0;
 #pragma unroll
     for (int j = 0; j < nj; ++j) {
         if (ks.valid(j)) {
             kmin = min(kmin, ks.key(j));
             kmax = max(kmax, ks.key(j));
-            if (ks.key(j) >= kreal) rmin = min(rmin, ks.key(j));
         }
     }
     kmin = wave_min64(kmin);
     kmax = wave_max64(kmax);
-    rmin = wave_min64(rmin);
-    if (rmin < kmax) kmin = rmin;
+    const uint64_t kreal = order_key(kAbsentBelow);
+    if (kmin < kreal) {  // wave-uniform: only tables with absent teams
+        uint64_t rmin = ~0ull;
+#pragma unroll
+        for (int j = 0; j < nj; ++j)
+            if (ks.valid(j) && ks.key(j) >= kreal) rmin = min(rmin, ks.key(j));
+        rmin = wave_min64(rmin);
+        if (rmin < kmax) kmin = rmin;
+    }
     const double ymin = key_value(kmin);
     const double range = key_value(kmax) - ymin;
     if (!(range > 0.0)) return kmin;  // every key equal
@@ -484,20 +489,25 @@ __global__ __launch_bounds__(kSelectThreads) void k_select_head(
 
     // tau's key: rank Kp (0-based, descending) among the M keys
     // histogram range: the real teams' keys unless those are all equal
-    const uint64_t kreal = order_key(kAbsentBelow);
-    uint64_t kmin = ~0ull, kmax = 0, rmin = ~0ull;
+    uint64_t kmin = ~0ull, kmax = 0;
 #pragma unroll
     for (int j = 0; j < kHeadKeys; ++j) {
         if (valid(j)) {
             kmin = min(kmin, k[j]);
             kmax = max(kmax, k[j]);
-            if (k[j] >= kreal) rmin = min(rmin, k[j]);
         }
     }
     kmin = block_ext64<false>(kmin, s_red);
     kmax = block_ext64<true>(kmax, s_red);
-    rmin = block_ext64<false>(rmin, s_red);
-    if (rmin < kmax) kmin = rmin;
+    const uint64_t kreal = order_key(kAbsentBelow);
+    if (kmin < kreal) {  // uniform: only tables with absent teams
+        uint64_t rmin = ~0ull;
+#pragma unroll
+        for (int j = 0; j < kHeadKeys; ++j)
+            if (valid(j) && k[j] >= kreal) rmin = min(rmin, k[j]);
+        rmin = block_ext64<false>(rmin, s_red);
+        if (rmin < kmax) kmin = rmin;
+    }
     const double ymin = key_value(kmin);
     const double range = key_value(kmax) - ymin;
     int want = Kp;
