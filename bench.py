@@ -347,7 +347,7 @@ def measured_traffic():
     if len(vals) != 3:
         return None
     csrc = os.path.join(ROOT, "paper_2609_35629_amd", "csrc")
-    src = b"".join(open(os.path.join(csrc, f), "rb").read() for f in ("attend_kernels.hip", "common.h", "internal.h"))
+    src = b"".join(open(os.path.join(csrc, f), "rb").read() for f in ("decode_kernels.hip", "common.h", "internal.h"))
     if hashlib.sha256(src).hexdigest() != vals["sources_sha256"]:
         return None
     return int(vals["read_bytes_per_launch"]) + int(vals["write_bytes_per_launch"])

@@ -37,7 +37,8 @@
  *     after the failing step and santapp_last_error() returns a message for
  *     the calling thread.  No call aborts the process.
  *   - santapp_decode and santapp_dense_decode never allocate: the caller
- *     provides a workspace of the queried size.
+ *     provides a workspace of the queried size, zeroed once before its
+ *     first use.
  */
 #ifndef SANTAPP_H
 #define SANTAPP_H
@@ -204,11 +205,11 @@ santapp_status santapp_budget_to_K(int S, int P, int R, int M, int* K);
 /* Optional diagnostic outputs of santapp_decode (device pointers; each may be
  * NULL).  The arrays are written only when the step samples (K < M).
  * events[0..3], when non-NULL, are hipEvent_t handles created by the caller:
- * events[0] is recorded on `stream` before the routing/sampling kernels,
- * events[1] and events[2] are stamped by the attention kernel's launch at
- * that kernel's start and end (its execution time, without the dispatch gap
- * before it), and events[3] is recorded after the merge kernel, so that
- * hipEventElapsedTime gives the time of each stage. */
+ * events[0] is recorded on `stream` before the step's launches, events[1]
+ * and events[2] are stamped by the attention launch at that kernel's start
+ * and end (its execution time, without the dispatch gap before it; in the
+ * one-launch mode that kernel also samples), and events[3] is recorded after
+ * the step, so that hipEventElapsedTime gives the time of each stage. */
 typedef struct {
     double* phi;      /* [B,Hq,M] routing logits log n_g + scale q.l_g          */
     double* Y;        /* [B,Hq,M] perturbed routing scores phi_g + G_g          */
@@ -222,10 +223,14 @@ typedef struct {
 
 /*
  * Workspace for santapp_decode with these sizes (bytes, host-only query).
- * It holds the step's routing scores, read plan and partial results; every
- * entry a call reads is written earlier in the same call, so it needs no
- * initialisation.  Calls that share a workspace must not overlap in time (use
- * one workspace per stream).
+ * It holds the step's samples, read plan and partial results, and one
+ * counter triple per (b, kv) pair through which the workgroups of a step hand
+ * work to each other.  A workspace must be zeroed once before its first use
+ * (santapp_workspace_zero); every completed call leaves its counters at zero,
+ * and every other entry a call reads is written earlier in the same call.
+ * Calls that share a workspace must not overlap in time (use one workspace
+ * per stream).  The size depends on the compute units of the device the
+ * table was built on.
  */
 santapp_status santapp_decode_workspace_bytes(const santapp_teams* teams, int Hq, int T, int K,
                                               size_t* bytes);
@@ -239,8 +244,13 @@ santapp_status santapp_workspace_zero(void* ws, size_t bytes, void* stream);
  * one layer (query head h reads KV head h / (Hq / Hkv)).
  *
  * q:        [B,Hq,d] fp32 post-RoPE queries.
- * suffix_K, suffix_V: [B,Hkv,T,d] generated rows attended exactly (same dtype
- *           as the table; may be NULL when T == 0).
+ * suffix_K, suffix_V: the generated rows attended exactly (section "Cache
+ *           state and budget": empty on the first sparse call, one row more
+ *           per generated token); same dtype as the table; may be NULL when
+ *           T == 0.  Row t < T of pair p = b Hkv + kv starts at element
+ *           (p suffix_stride + t) d, so a caller can append rows in place to a
+ *           buffer [B,Hkv,capacity,d] (suffix_stride = capacity); 0 means T
+ *           (a dense [B,Hkv,T,d] tensor).  suffix_stride < T is EINVAL.
  * K:        teams to sample per query head (>= 1).  K >= M selects every team
  *           with correction 1 (dense attention over the cache).
  * seed, step: Gumbel noise of team g for head h of sequence b is word g % 4 of
@@ -250,10 +260,14 @@ santapp_status santapp_workspace_zero(void* ws, size_t bytes, void* stream);
  * out:      [B,Hq,d] fp32 estimate U^ / Z^.
  * Routing logits, the perturbed scores, the selection and tau are computed in
  * fp64; attention scores and the online softmax in fp32.
+ * A step runs as three launches (sampling, attention, merge); for bf16
+ * tables, setting the environment variable SANTAPP_DECODE_LAUNCH=fused before
+ * the first call of a process runs all three phases in one launch, in which
+ * the phases hand work to each other through the workspace counters.
  * Never allocates and never synchronises.
  */
 santapp_status santapp_decode(const santapp_teams* teams, const float* q, const void* suffix_K,
-                              const void* suffix_V, int T, int Hq, int K, uint64_t seed,
+                              const void* suffix_V, int T, int suffix_stride, int Hq, int K, uint64_t seed,
                               uint64_t step, double scale, float* out, void* workspace,
                               size_t ws_bytes, const santapp_decode_debug* dbg, void* stream);
 
@@ -263,13 +277,15 @@ santapp_status santapp_dense_workspace_bytes(int B, int Hq, int Hkv, int N, int 
 
 /*
  * Dense softmax attention over K, V [B,Hkv,N,d] followed by the suffix rows
- * [B,Hkv,T,d] (eq. method-attention), with the same GQA mapping, dtypes and
- * scale convention as santapp_decode.  Never allocates or synchronises.
+ * (eq. method-attention), with the same GQA mapping, suffix layout, dtypes
+ * and scale convention as santapp_decode.  The workspace follows the same
+ * rules (zeroed before first use; its counters are left zero).  Never
+ * allocates or synchronises.
  */
 santapp_status santapp_dense_decode(const float* q, const void* K, const void* V, int B, int Hkv,
                                     int N, int d, santapp_dtype dtype, const void* suffix_K,
-                                    const void* suffix_V, int T, int Hq, double scale, float* out,
-                                    void* workspace, size_t ws_bytes, void* stream);
+                                    const void* suffix_V, int T, int suffix_stride, int Hq, double scale,
+                                    float* out, void* workspace, size_t ws_bytes, void* stream);
 
 /* Workspace for santapp_routing_kl (bytes, host-only query). */
 santapp_status santapp_routing_kl_workspace_bytes(const santapp_teams* teams, int Hq, size_t* bytes);

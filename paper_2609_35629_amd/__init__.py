@@ -258,19 +258,35 @@ class DebugOut:
         return d
 
 
+def _suffix(suffix_K, suffix_V, B, Hkv, d, dtype, T=None):
+    """Validate a suffix buffer ``[B, Hkv, capacity, d]`` of which the first
+    ``T`` rows per (b, kv) are attended (all of them when ``T`` is None);
+    returns ``(T, stride)``."""
+    if suffix_K is None:
+        if T:
+            raise SantappError(_lib.EINVAL, "suffix rows requested without a suffix buffer")
+        return 0, 0
+    cap = suffix_K.shape[2]
+    _need(suffix_K, "suffix_K", shape=(B, Hkv, cap, d), dtype=dtype)
+    _need(suffix_V, "suffix_V", shape=suffix_K.shape, dtype=dtype)
+    T = cap if T is None else int(T)
+    if T < 0 or T > cap:
+        raise SantappError(_lib.EINVAL, f"T={T} outside the suffix buffer's {cap} rows")
+    return T, cap
+
+
 def decode(teams: Teams, q: torch.Tensor, suffix_K: Optional[torch.Tensor],
            suffix_V: Optional[torch.Tensor], K: int, seed: int = 0, step: int = 0,
            scale: float = 0.0, out: Optional[torch.Tensor] = None,
            workspace: Optional[torch.Tensor] = None, debug: Optional[DebugOut] = None,
-           stream=None) -> torch.Tensor:
-    """One SANTA++ decode step: ``q [B, Hq, d]`` fp32 -> ``out [B, Hq, d]`` fp32."""
+           stream=None, T: Optional[int] = None) -> torch.Tensor:
+    """One SANTA++ decode step: ``q [B, Hq, d]`` fp32 -> ``out [B, Hq, d]`` fp32.
+
+    ``suffix_K``/``suffix_V`` ``[B, Hkv, capacity, d]`` hold the generated
+    rows; the first ``T`` of each (b, kv) are attended (default: all)."""
     B, Hq, d = q.shape
     _need(q, "q", shape=(teams.B, Hq, teams.d), dtype=torch.float32)
-    T = 0
-    if suffix_K is not None:
-        T = suffix_K.shape[2]
-        _need(suffix_K, "suffix_K", shape=(teams.B, teams.Hkv, T, teams.d), dtype=teams.torch_dtype)
-        _need(suffix_V, "suffix_V", shape=suffix_K.shape, dtype=teams.torch_dtype)
+    T, stride = _suffix(suffix_K, suffix_V, teams.B, teams.Hkv, teams.d, teams.torch_dtype, T)
     if out is None:
         out = torch.empty((B, Hq, d), dtype=torch.float32, device=q.device)
     _need(out, "out", shape=(B, Hq, d), dtype=torch.float32)
@@ -278,7 +294,7 @@ def decode(teams: Teams, q: torch.Tensor, suffix_K: Optional[torch.Tensor],
         workspace = decode_workspace(teams, Hq, T, K)
     dbg = ctypes.byref(debug.struct()) if debug is not None else None
     check(_lib.load().santapp_decode(
-        teams.handle, _ptr(q), _ptr(suffix_K), _ptr(suffix_V), T, Hq, K,
+        teams.handle, _ptr(q), _ptr(suffix_K), _ptr(suffix_V), T, stride, Hq, K,
         ctypes.c_uint64(seed), ctypes.c_uint64(step), float(scale), _ptr(out), _ptr(workspace),
         workspace.numel(), dbg, _stream(stream)))
     return out
@@ -287,23 +303,21 @@ def decode(teams: Teams, q: torch.Tensor, suffix_K: Optional[torch.Tensor],
 def dense_decode(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor,
                  suffix_K: Optional[torch.Tensor], suffix_V: Optional[torch.Tensor],
                  scale: float = 0.0, out: Optional[torch.Tensor] = None,
-                 workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    """Dense attention over K, V ``[B, Hkv, N, d]`` plus the suffix rows."""
+                 workspace: Optional[torch.Tensor] = None, stream=None,
+                 T: Optional[int] = None) -> torch.Tensor:
+    """Dense attention over K, V ``[B, Hkv, N, d]`` plus the first ``T`` suffix
+    rows of ``[B, Hkv, capacity, d]`` (default: all)."""
     B, Hq, d = q.shape
     _need(q, "q", dtype=torch.float32)
     _need(K, "K")
     _need(V, "V", shape=K.shape, dtype=K.dtype)
     _, Hkv, N, _ = K.shape
-    T = 0
-    if suffix_K is not None:
-        T = suffix_K.shape[2]
-        _need(suffix_K, "suffix_K", shape=(B, Hkv, T, d), dtype=K.dtype)
-        _need(suffix_V, "suffix_V", shape=suffix_K.shape, dtype=K.dtype)
+    T, stride = _suffix(suffix_K, suffix_V, B, Hkv, d, K.dtype, T)
     if out is None:
         out = torch.empty((B, Hq, d), dtype=torch.float32, device=q.device)
     if workspace is None:
         workspace = dense_workspace(B, Hq, Hkv, N, T, d)
     check(_lib.load().santapp_dense_decode(
         _ptr(q), _ptr(K), _ptr(V), B, Hkv, N, d, _dtype_code(K), _ptr(suffix_K), _ptr(suffix_V),
-        T, Hq, float(scale), _ptr(out), _ptr(workspace), workspace.numel(), _stream(stream)))
+        T, stride, Hq, float(scale), _ptr(out), _ptr(workspace), workspace.numel(), _stream(stream)))
     return out

@@ -82,10 +82,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     L.santapp_budget_to_K.argtypes = [i, i, i, i, ctypes.POINTER(i)]
     L.santapp_decode_workspace_bytes.argtypes = [vp, i, i, i, ctypes.POINTER(sz)]
     L.santapp_workspace_zero.argtypes = [vp, sz, vp]
-    L.santapp_decode.argtypes = [vp, vp, vp, vp, i, i, i, u64, u64, ctypes.c_double, vp, vp, sz,
+    L.santapp_decode.argtypes = [vp, vp, vp, vp, i, i, i, i, u64, u64, ctypes.c_double, vp, vp, sz,
                                  ctypes.POINTER(DecodeDebug), vp]
     L.santapp_dense_workspace_bytes.argtypes = [i, i, i, i, i, i, ctypes.POINTER(sz)]
-    L.santapp_dense_decode.argtypes = [vp, vp, vp, i, i, i, i, i, vp, vp, i, i, ctypes.c_double,
+    L.santapp_dense_decode.argtypes = [vp, vp, vp, i, i, i, i, i, vp, vp, i, i, i, ctypes.c_double,
                                        vp, vp, sz, vp]
     L.santapp_teams_set_route_keys.argtypes = [vp, i, vp]
     L.santapp_routing_kl_workspace_bytes.argtypes = [vp, i, ctypes.POINTER(sz)]

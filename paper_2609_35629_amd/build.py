@@ -13,7 +13,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 OBJDIR = os.path.join(ROOT, "_build", "santapp")
 LIB = os.path.join(PKG, "libsantapp.so")
-SOURCES = ["api.hip", "build_kernels.hip", "route_kernels.hip", "attend_kernels.hip", "diag_kernels.hip",
+SOURCES = ["api.hip", "build_kernels.hip", "route_kernels.hip", "decode_kernels.hip", "diag_kernels.hip",
            "kmeans_kernels.hip"]
 
 ARCH = os.environ.get("SANTAPP_ARCH", "gfx950")

@@ -3,6 +3,8 @@
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
 
 #include <algorithm>
 #include <atomic>
@@ -59,6 +61,8 @@ size_t elem_size(santapp_dtype dt) { return dt == SANTAPP_BF16 ? 2 : 4; }
 bool dtype_ok(santapp_dtype dt) { return dt == SANTAPP_BF16 || dt == SANTAPP_FP32; }
 
 size_t align_up(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+constexpr int kWaves8 = santapp::kDecodeThreads / 64;  // waves of a decode workgroup
 
 // Device buffers are read and written with 16-byte vector accesses.
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
@@ -118,46 +122,55 @@ santapp_status finish_table(santapp_teams* t, santapp_teams** out);
 
 namespace santapp {
 
-DecodeLayout decode_layout(int B, int Hq, int Hkv, int T, int d, int M, int Kp, const int* cap) {
+int decode_wgs(int cus, long long BH, long long units_per_pair) {
+    if (cus < 1) cus = 8;
+    long long want = (BH * units_per_pair + kWaves8 - 1) / kWaves8;  // a unit per wave
+    want = std::max<long long>(want, std::min<long long>(BH, cus));   // every pair a workgroup
+    want = std::min<long long>(want, cus);
+    if (cus % 8 == 0) want = std::min<long long>(cus, (want + 7) / 8 * 8);
+    return static_cast<int>(std::max<long long>(want, 1));
+}
+
+namespace {
+
+struct Carver {
+    size_t off = 0;
+    size_t take(size_t bytes) {
+        const size_t at = off;
+        off = align_up(off + bytes);
+        return at;
+    }
+};
+
+}  // namespace
+
+DecodeLayout decode_layout(int B, int Hq, int Hkv, int T, int d, int M, int Kp, const int* cap, int cus) {
     DecodeLayout L;
     const size_t BH = static_cast<size_t>(B) * Hkv, BQ = static_cast<size_t>(B) * Hq;
     const int G = Hq / Hkv;
     const long long xs = std::min<long long>(M, static_cast<long long>(G) * Kp);
-    L.max_chunks = cap[xs] + chunk_count(T);
-    L.max_hunits = cap[std::min(M, Kp)] + chunk_count(T);
-    size_t off = 0;
-    auto take = [&](size_t bytes) {
-        const size_t at = off;
-        off = align_up(off + bytes);
-        return at;
-    };
-    L.phi = take(BQ * M * sizeof(double));
-    L.Y = take(BQ * M * sizeof(double));
-    L.lc = take(BQ * M * sizeof(float));
-    L.lpos = take(BQ * M * sizeof(unsigned short));
-    L.sbits = take(BQ * kSelWords * sizeof(uint64_t));
-    L.hunits = take(BQ * sizeof(int));
-    L.hdr = take(BH * sizeof(PlanHeader));
-    L.chunk = take(BH * L.max_chunks * sizeof(Chunk));
-    L.ulogc = take(BH * M * kLogcStride * sizeof(float));
-    L.po = take(BQ * L.max_hunits * d * sizeof(float));
-    L.pml = take(BQ * L.max_hunits * 2 * sizeof(float));
-    L.total = off;
+    L.nwg = decode_wgs(cus, static_cast<long long>(BH), chunk_count(T) + static_cast<long long>(std::max(1, cap[xs])));
+    L.maxwp = BH <= static_cast<size_t>(L.nwg) ? static_cast<int>((L.nwg + BH - 1) / BH) : 1;
+    L.swords = (M + 63) / 64;
+    Carver c;
+    L.ctr = c.take((BH + BH * G) * sizeof(int));
+    L.sbits = c.take(BQ * L.swords * sizeof(uint64_t));
+    L.lc = c.take(BQ * M * sizeof(float));
+    L.part = c.take(BH * L.maxwp * G * state_stride(d) * sizeof(float));
+    L.total = c.off;
     return L;
 }
 
-DecodeLayout dense_layout(int B, int Hq, int Hkv, int N, int T, int d) {
+DecodeLayout dense_layout(int B, int Hq, int Hkv, int N, int T, int d, int cus) {
     DecodeLayout L;
-    const size_t BQ = static_cast<size_t>(B) * Hq;
-    (void)Hkv;
-    L.max_chunks = dense_count(N) + dense_count(T);
-    L.max_hunits = L.max_chunks;  // every head reads every unit
-    size_t off = 0;
-    L.po = off;
-    off = align_up(off + BQ * L.max_chunks * d * sizeof(float));
-    L.pml = off;
-    off = align_up(off + BQ * L.max_chunks * 2 * sizeof(float));
-    L.total = off;
+    const size_t BH = static_cast<size_t>(B) * Hkv;
+    const int G = Hq / Hkv;
+    L.nwg = decode_wgs(cus, static_cast<long long>(BH), chunk_count(N) + static_cast<long long>(chunk_count(T)));
+    L.maxwp = BH <= static_cast<size_t>(L.nwg) ? static_cast<int>((L.nwg + BH - 1) / BH) : 1;
+    Carver c;
+    L.ctr = c.take((BH + BH * G) * sizeof(int));
+    L.part = c.take(BH * L.maxwp * G * state_stride(d) * sizeof(float));
+    L.total = c.off;
     return L;
 }
 
@@ -590,9 +603,7 @@ santapp_status santapp_routing_kl(const santapp_teams* t, const float* q, int Hq
     double* phi = reinterpret_cast<double*>(ws + L.phi);
     RouteArgs R{};
     R.reps = t->reps;
-    R.team_size = t->team_size;
     R.log_n = t->log_n;
-    R.team_begin = t->team_begin;
     R.q = q;
     R.B = t->B;
     R.Hkv = t->Hkv;
@@ -638,8 +649,8 @@ santapp_status santapp_decode_workspace_bytes(const santapp_teams* t, int Hq, in
     if (Hq < 1 || Hq % t->Hkv != 0) return fail(SANTAPP_EINVAL, "Hq must be a positive multiple of Hkv");
     if (T < 0 || K < 1) return fail(SANTAPP_EINVAL, "T must be >= 0 and K >= 1");
     const int Kp = std::min(K, t->M);
-    *bytes = Kp == t->M ? dense_layout(t->B, Hq, t->Hkv, t->N, T, t->d).total
-                        : decode_layout(t->B, Hq, t->Hkv, T, t->d, t->M, Kp, t->cap.data()).total;
+    *bytes = Kp == t->M ? dense_layout(t->B, Hq, t->Hkv, t->N, T, t->d, t->cus).total
+                        : decode_layout(t->B, Hq, t->Hkv, T, t->d, t->M, Kp, t->cap.data(), t->cus).total;
     return ok();
 }
 
@@ -648,12 +659,36 @@ santapp_status santapp_dense_workspace_bytes(int B, int Hq, int Hkv, int N, int 
     if (!bytes) return fail(SANTAPP_EINVAL, "NULL argument");
     if (B < 1 || Hkv < 1 || Hq < 1 || Hq % Hkv != 0 || N < 0 || T < 0 || N + T < 1 || d < 1)
         return fail(SANTAPP_EINVAL, "invalid sizes");
-    *bytes = dense_layout(B, Hq, Hkv, N, T, d).total;
+    *bytes = dense_layout(B, Hq, Hkv, N, T, d, device_cus()).total;
     return ok();
 }
 
+namespace {
+
+// Launch mode of a bf16 step: the sampling, attention and merge launches,
+// unless SANTAPP_DECODE_LAUNCH=fused asks for all of them in one launch
+// (read once per process).
+bool fused_wanted() {
+    static const bool fused = [] {
+        const char* e = getenv("SANTAPP_DECODE_LAUNCH");
+        return e != nullptr && strcmp(e, "fused") == 0;
+    }();
+    return fused;
+}
+
+santapp_status check_suffix(const void* sK, const void* sV, int T, int& stride) {
+    if (T < 0) return fail(SANTAPP_EINVAL, "T must be >= 0");
+    if (stride == 0) stride = T;
+    if (stride < T) return fail(SANTAPP_EINVAL, "suffix_stride (%d) is smaller than T (%d)", stride, T);
+    if (T > 0 && (!sK || !sV)) return fail(SANTAPP_EINVAL, "suffix K/V are NULL with T > 0");
+    if (T > 0 && (!aligned16(sK) || !aligned16(sV))) return fail(SANTAPP_EINVAL, "suffix K/V must be 16-byte aligned");
+    return SANTAPP_OK;
+}
+
+}  // namespace
+
 santapp_status santapp_decode(const santapp_teams* t, const float* q, const void* suffix_K,
-                              const void* suffix_V, int T, int Hq, int K, uint64_t seed,
+                              const void* suffix_V, int T, int suffix_stride, int Hq, int K, uint64_t seed,
                               uint64_t step, double scale, float* out, void* workspace,
                               size_t ws_bytes, const santapp_decode_debug* dbg, void* stream) {
     if (!t) return fail(SANTAPP_EINVAL, "teams is NULL");
@@ -661,29 +696,32 @@ santapp_status santapp_decode(const santapp_teams* t, const float* q, const void
     if (Hq < 1 || Hq % t->Hkv != 0) return fail(SANTAPP_EINVAL, "Hq (%d) must be a positive multiple of Hkv (%d)", Hq, t->Hkv);
     const int G = Hq / t->Hkv;
     if (G > kMaxGroup) return fail(SANTAPP_ELIMIT, "%d query heads per KV head exceed %d", G, kMaxGroup);
-    if (static_cast<long long>(t->B) * t->Hkv > kMaxPairs)
-        return fail(SANTAPP_ELIMIT, "B * Hkv = %lld exceeds %d", static_cast<long long>(t->B) * t->Hkv, kMaxPairs);
-    if (T < 0) return fail(SANTAPP_EINVAL, "T must be >= 0");
-    if (T > 0 && (!suffix_K || !suffix_V)) return fail(SANTAPP_EINVAL, "suffix K/V are NULL with T > 0");
-    if (!aligned16(q) || !aligned16(out) || !aligned16(workspace) || (T > 0 && (!aligned16(suffix_K) || !aligned16(suffix_V))))
-        return fail(SANTAPP_EINVAL, "q, out, suffix K/V and workspace must be 16-byte aligned");
+    if (santapp_status st = check_suffix(suffix_K, suffix_V, T, suffix_stride)) return st;
+    if (!aligned16(q) || !aligned16(out) || !aligned16(workspace))
+        return fail(SANTAPP_EINVAL, "q, out and workspace must be 16-byte aligned");
     if (K < 1) return fail(SANTAPP_EINVAL, "K must be >= 1 (got %d)", K);
     if (!(scale >= 0.0) || !isfinite(scale)) return fail(SANTAPP_EINVAL, "scale must be finite and >= 0");
     if (scale == 0.0) scale = 1.0 / sqrt(static_cast<double>(t->d));
     const int Kp = std::min(K, t->M);
-    const DecodeLayout L = Kp == t->M ? dense_layout(t->B, Hq, t->Hkv, t->N, T, t->d)
-                                      : decode_layout(t->B, Hq, t->Hkv, T, t->d, t->M, Kp, t->cap.data());
+    const bool dense = Kp == t->M;
+    if (!dense && t->M > kMaxTeams) return fail(SANTAPP_ELIMIT, "%d teams per KV head exceed %d", t->M, kMaxTeams);
+    const DecodeLayout L = dense ? dense_layout(t->B, Hq, t->Hkv, t->N, T, t->d, t->cus)
+                                 : decode_layout(t->B, Hq, t->Hkv, T, t->d, t->M, Kp, t->cap.data(), t->cus);
     if (!workspace || ws_bytes < L.total)
         return fail(SANTAPP_EWORKSPACE, "workspace of %zu bytes needed (got %zu)", L.total, ws_bytes);
     hipStream_t s = static_cast<hipStream_t>(stream);
-    char* ws = static_cast<char*>(workspace);
 
-    AttendArgs A{};
+    DecodeArgs A{};
+    A.reps = t->reps;
+    A.log_n = t->log_n;
+    A.team_begin = t->team_begin;
+    A.team_size = t->team_size;
     A.K = t->packed_K;
     A.V = t->packed_V;
     A.sK = suffix_K;
     A.sV = suffix_V;
     A.q = q;
+    A.out = out;
     A.B = t->B;
     A.Hkv = t->Hkv;
     A.Hq = Hq;
@@ -691,18 +729,31 @@ santapp_status santapp_decode(const santapp_teams* t, const float* q, const void
     A.d = t->d;
     A.N = t->N;
     A.T = T;
+    A.sstride = suffix_stride;
     A.M = t->M;
-    A.max_chunks = L.max_chunks;
-    A.max_hunits = L.max_hunits;
-    A.grid_waves = t->cus > 0 ? t->cus * kAttendWavesPerCU : 0;
-    A.cus = t->cus;
+    A.Kp = Kp;
     A.dtype = t->dtype;
-    A.scale = static_cast<float>(scale);
-    A.ws = ws;
-    A.lay = &L;
-    A.part_o = reinterpret_cast<float*>(ws + L.po);
-    A.part_ml = reinterpret_cast<float*>(ws + L.pml);
-    A.out = out;
+    A.dense = dense;
+    A.scale = scale;
+    A.scale_log2 = static_cast<float>(scale * 1.4426950408889634);
+    A.seed = seed;
+    A.step = step;
+    A.lay = L;
+    A.ws = static_cast<char*>(workspace);
+    if (dbg) {
+        A.dbg_phi = dbg->phi;
+        A.dbg_Y = dbg->Y;
+        A.dbg_sel = dbg->sel;
+        A.dbg_logc = dbg->logc;
+        A.dbg_tau = dbg->tau;
+        A.dbg_uteams = dbg->union_teams;
+        A.dbg_urows = dbg->union_rows;
+        // events 1 and 2 are stamped by the attention launch itself, at the
+        // kernel's start and end
+        A.ev_start = static_cast<hipEvent_t>(dbg->events[1]);
+        A.ev_stop = static_cast<hipEvent_t>(dbg->events[2]);
+    }
+    A.fused = t->dtype == SANTAPP_BF16 && fused_wanted() && L.nwg % 8 == 0;
 
     hipError_t e;
     auto mark = [&](int i) -> hipError_t {
@@ -710,86 +761,38 @@ santapp_status santapp_decode(const santapp_teams* t, const float* q, const void
         return hipSuccess;
     };
     if ((e = mark(0)) != hipSuccess) return hip_fail(e, "event record");
-    if (L.max_hunits > kMaxHeadUnits)
-        return fail(SANTAPP_ELIMIT, "a head would read %d units (at most %d)", L.max_hunits, kMaxHeadUnits);
-    if (Kp == t->M) {
-        // every team selected with correction 1: dense attention over the cache
-        A.dense = true;
-    } else {
-        if (t->M > kMaxTeams)
-            return fail(SANTAPP_ELIMIT, "%d teams per KV head exceed %d", t->M, kMaxTeams);
-        RouteArgs R{};
-        R.reps = t->reps;
-        R.team_size = t->team_size;
-        R.log_n = t->log_n;
-        R.team_begin = t->team_begin;
-        R.q = q;
-        R.B = t->B;
-        R.Hkv = t->Hkv;
-        R.Hq = Hq;
-        R.G = G;
-        R.d = t->d;
-        R.M = t->M;
-        R.Kp = Kp;
-        R.T = T;
-        R.dtype = t->dtype;
-        R.scale = scale;
-        R.seed = seed;
-        R.step = step;
-        R.lay = &L;
-        R.ws = ws;
-        R.dbg = dbg;
-        if ((e = launch_route_select(R, s)) != hipSuccess) return hip_fail(e, "routing and sampling kernel");
-        if (dbg && dbg->phi &&
-            (e = hipMemcpyAsync(dbg->phi, ws + L.phi, sizeof(double) * t->B * Hq * t->M,
-                                hipMemcpyDeviceToDevice, s)) != hipSuccess)
-            return hip_fail(e, "debug copy");
-        if (dbg && dbg->Y &&
-            (e = hipMemcpyAsync(dbg->Y, ws + L.Y, sizeof(double) * t->B * Hq * t->M,
-                                hipMemcpyDeviceToDevice, s)) != hipSuccess)
-            return hip_fail(e, "debug copy");
-        A.dense = false;
-    }
-    // events 1 and 2 are stamped by the attention kernel's launch itself,
-    // at the kernel's start and end
-    if (dbg) {
-        A.ev_start = static_cast<hipEvent_t>(dbg->events[1]);
-        A.ev_stop = static_cast<hipEvent_t>(dbg->events[2]);
-    }
-    if ((e = launch_attend(A, s)) != hipSuccess) return hip_fail(e, "attention kernel");
-    if ((e = launch_merge(A, s)) != hipSuccess) return hip_fail(e, "merge kernel");
+    if ((e = launch_decode(A, s)) != hipSuccess) return hip_fail(e, "decode kernels");
     if ((e = mark(3)) != hipSuccess) return hip_fail(e, "event record");
     return ok();
 }
 
 santapp_status santapp_dense_decode(const float* q, const void* K, const void* V, int B, int Hkv,
                                     int N, int d, santapp_dtype dtype, const void* suffix_K,
-                                    const void* suffix_V, int T, int Hq, double scale, float* out,
-                                    void* workspace, size_t ws_bytes, void* stream) {
+                                    const void* suffix_V, int T, int suffix_stride, int Hq, double scale,
+                                    float* out, void* workspace, size_t ws_bytes, void* stream) {
     if (!q || !out) return fail(SANTAPP_EINVAL, "q and out must be device pointers");
     if (B < 1 || Hkv < 1 || N < 0 || T < 0 || N + T < 1)
         return fail(SANTAPP_EINVAL, "invalid sizes");
     if (N > 0 && (!K || !V)) return fail(SANTAPP_EINVAL, "K and V are NULL with N > 0");
-    if (T > 0 && (!suffix_K || !suffix_V)) return fail(SANTAPP_EINVAL, "suffix K/V are NULL with T > 0");
-    if (!aligned16(q) || !aligned16(out) || !aligned16(workspace) || (N > 0 && (!aligned16(K) || !aligned16(V))) ||
-        (T > 0 && (!aligned16(suffix_K) || !aligned16(suffix_V))))
-        return fail(SANTAPP_EINVAL, "q, out, K/V, suffix K/V and workspace must be 16-byte aligned");
+    if (santapp_status st = check_suffix(suffix_K, suffix_V, T, suffix_stride)) return st;
+    if (!aligned16(q) || !aligned16(out) || !aligned16(workspace) || (N > 0 && (!aligned16(K) || !aligned16(V))))
+        return fail(SANTAPP_EINVAL, "q, out, K/V and workspace must be 16-byte aligned");
     if (Hq < 1 || Hq % Hkv != 0) return fail(SANTAPP_EINVAL, "Hq must be a positive multiple of Hkv");
     if (Hq / Hkv > kMaxGroup) return fail(SANTAPP_ELIMIT, "more than %d query heads per KV head", kMaxGroup);
     if (!dtype_ok(dtype)) return fail(SANTAPP_EDTYPE, "unsupported dtype %d", static_cast<int>(dtype));
     if (d != 64 && d != 128) return fail(SANTAPP_ELIMIT, "head dim %d not supported (64 or 128)", d);
     if (!(scale >= 0.0) || !isfinite(scale)) return fail(SANTAPP_EINVAL, "scale must be finite and >= 0");
     if (scale == 0.0) scale = 1.0 / sqrt(static_cast<double>(d));
-    const DecodeLayout L = dense_layout(B, Hq, Hkv, N, T, d);
+    const DecodeLayout L = dense_layout(B, Hq, Hkv, N, T, d, device_cus());
     if (!workspace || ws_bytes < L.total)
         return fail(SANTAPP_EWORKSPACE, "workspace of %zu bytes needed (got %zu)", L.total, ws_bytes);
-    char* ws = static_cast<char*>(workspace);
-    AttendArgs A{};
+    DecodeArgs A{};
     A.K = K;
     A.V = V;
     A.sK = suffix_K;
     A.sV = suffix_V;
     A.q = q;
+    A.out = out;
     A.B = B;
     A.Hkv = Hkv;
     A.Hq = Hq;
@@ -797,24 +800,18 @@ santapp_status santapp_dense_decode(const float* q, const void* K, const void* V
     A.d = d;
     A.N = N;
     A.T = T;
+    A.sstride = suffix_stride;
     A.M = 0;
-    A.max_chunks = L.max_chunks;
-    A.max_hunits = L.max_hunits;
-    A.cus = device_cus();
-    A.grid_waves = A.cus * kAttendWavesPerCU;
+    A.Kp = 0;
     A.dtype = dtype;
-    A.scale = static_cast<float>(scale);
     A.dense = true;
-    A.ws = ws;
-    A.lay = &L;
-    A.part_o = reinterpret_cast<float*>(ws + L.po);
-    A.part_ml = reinterpret_cast<float*>(ws + L.pml);
-    A.out = out;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e;
-    if ((e = launch_attend(A, s)) != hipSuccess) return hip_fail(e, "attention kernel");
-    if ((e = launch_merge(A, s)) != hipSuccess) return hip_fail(e, "merge kernel");
-    return ok();
+    A.scale = scale;
+    A.scale_log2 = static_cast<float>(scale * 1.4426950408889634);
+    A.lay = L;
+    A.ws = static_cast<char*>(workspace);
+    A.fused = dtype == SANTAPP_BF16 && fused_wanted() && L.nwg % 8 == 0;
+    const hipError_t e = launch_decode(A, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? ok() : hip_fail(e, "dense decode kernels");
 }
 
 }  // extern "C"

@@ -65,6 +65,58 @@ __device__ __forceinline__ float load_elem<float>(const float* p, size_t i) {
     return p[i];
 }
 
+// A lane's DPL consecutive elements of a routing-key row (16 lanes per
+// row), widened to fp32 exactly.
+template <typename T, int DPL>
+struct RepChunk;
+
+template <>
+struct RepChunk<bf16_t, 8> {
+    using raw = uint4;
+    static __device__ __forceinline__ raw load(const bf16_t* p) { return load_stream(p); }
+    static __device__ __forceinline__ float get(const raw& r, int e) {
+        const uint32_t w = (e < 2) ? r.x : (e < 4) ? r.y : (e < 6) ? r.z : r.w;
+        return (e & 1) ? bf16hi(w) : bf16lo(w);
+    }
+};
+
+template <>
+struct RepChunk<bf16_t, 4> {
+    using raw = uint2;
+    static __device__ __forceinline__ raw load(const bf16_t* p) { return load_stream8(p); }
+    static __device__ __forceinline__ float get(const raw& r, int e) {
+        const uint32_t w = (e < 2) ? r.x : r.y;
+        return (e & 1) ? bf16hi(w) : bf16lo(w);
+    }
+};
+
+template <>
+struct RepChunk<float, 8> {
+    struct raw {
+        float4 a, b;
+    };
+    static __device__ __forceinline__ raw load(const float* p) {
+        raw r;
+        r.a = load_stream_f(p);
+        r.b = load_stream_f(p + 4);
+        return r;
+    }
+    static __device__ __forceinline__ float get(const raw& r, int e) {
+        const float4& v = (e < 4) ? r.a : r.b;
+        const int k = e & 3;
+        return k == 0 ? v.x : k == 1 ? v.y : k == 2 ? v.z : v.w;
+    }
+};
+
+template <>
+struct RepChunk<float, 4> {
+    using raw = float4;
+    static __device__ __forceinline__ raw load(const float* p) { return load_stream_f(p); }
+    static __device__ __forceinline__ float get(const raw& r, int e) {
+        return e == 0 ? r.x : e == 1 ? r.y : e == 2 ? r.z : r.w;
+    }
+};
+
 // ---------------------------------------------------------------------------
 // Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11).  One round maps
 // (x0,x1,x2,x3) to (hi(M1 x2)^x1^k0, lo(M1 x2), hi(M0 x0)^x3^k1, lo(M0 x0));

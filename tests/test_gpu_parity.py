@@ -152,7 +152,7 @@ def test_plan_beyond_unit_table():
     teams, res = _run(wl, steps=(0,))
     assert teams.M == 8
     cmp, dbg, so = res[0]
-    assert int(dbg.union_rows.sum().item()) > 4096 * 64
+    assert int(dbg.union_rows.sum().item()) > 4096 * 32  # more units than the plan's LDS table
 
 
 def test_short_last_parent_and_odd_groups():
