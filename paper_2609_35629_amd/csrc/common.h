@@ -126,6 +126,16 @@ struct u64x4 {
     uint64_t v[4];
 };
 
+// The 128-bit product of two 64-bit words from four independent 32 x 32-bit
+// partial products (each one multiply-add on the vector ALU).
+__device__ __forceinline__ void mul64_wide(uint64_t a, uint64_t b, uint64_t& lo, uint64_t& hi) {
+    const uint64_t a0 = a & 0xffffffffull, a1 = a >> 32, b0 = b & 0xffffffffull, b1 = b >> 32;
+    const uint64_t p00 = a0 * b0, p01 = a0 * b1, p10 = a1 * b0, p11 = a1 * b1;
+    const uint64_t mid = (p00 >> 32) + (p01 & 0xffffffffull) + (p10 & 0xffffffffull);
+    lo = (mid << 32) | (p00 & 0xffffffffull);
+    hi = p11 + (p01 >> 32) + (p10 >> 32) + (mid >> 32);
+}
+
 __device__ __forceinline__ u64x4 philox4x64_10(uint64_t c0, uint64_t c1, uint64_t c2, uint64_t c3,
                                                uint64_t k0, uint64_t k1) {
     const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
@@ -139,8 +149,9 @@ __device__ __forceinline__ u64x4 philox4x64_10(uint64_t c0, uint64_t c1, uint64_
             k0 += W0;
             k1 += W1;
         }
-        const uint64_t lo0 = M0 * c0, hi0 = __umul64hi(M0, c0);
-        const uint64_t lo1 = M1 * c2, hi1 = __umul64hi(M1, c2);
+        uint64_t lo0, hi0, lo1, hi1;
+        mul64_wide(M0, c0, lo0, hi0);
+        mul64_wide(M1, c2, lo1, hi1);
         const uint64_t n0 = hi1 ^ c1 ^ k0;
         const uint64_t n2 = hi0 ^ c3 ^ k1;
         c0 = n0;

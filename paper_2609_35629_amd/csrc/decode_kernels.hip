@@ -45,6 +45,7 @@
 #include <math.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include <hip/hip_ext.h>
 
@@ -437,14 +438,14 @@ __device__ uint64_t select_rank_key(const uint64_t (&k)[HK], int M, int want, Se
 
 // The common case of select_rank_key: one value histogram of 256 bins over
 // [min Y, max Y] and a direct ranking of the keys in the bin that holds rank
-// `want`, in three workgroup barriers.  Tables with absent teams and bins of
-// more than 64 keys take the general path.
+// `want`, in three workgroup barriers.  The caller has cleared S.hist and
+// S.ncand before an earlier barrier.  Returns the key and, through `above`,
+// the count of keys strictly greater than it.  Tables with absent teams and
+// bins of more than 64 keys take the general path (above = -1).
 template <int HK>
-__device__ uint64_t select_rank_key_fast(const uint64_t (&k)[HK], int M, int want, SelScratch& S) {
+__device__ uint64_t select_rank_key_fast(const uint64_t (&k)[HK], int M, int want, SelScratch& S, int& above) {
     const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
     auto valid = [&](int j) { return j * kThreads + tid < M; };
-    if (tid < 64) reinterpret_cast<uint4*>(S.hist)[tid] = make_uint4(0, 0, 0, 0);
-    if (tid == 0) S.ncand = 0;
     uint64_t kmin = ~0ull, kmax = 0;
 #pragma unroll
     for (int j = 0; j < HK; ++j) {
@@ -467,11 +468,17 @@ __device__ uint64_t select_rank_key_fast(const uint64_t (&k)[HK], int M, int wan
         kmin = min(kmin, S.red[v]);
         kmax = max(kmax, S.cand[v]);
     }
-    __syncthreads();  // red / cand are reused
-    if (kmin < order_key(kAbsentBelow)) return select_rank_key<HK>(k, M, want, S);  // uniform
+    above = -1;
+    if (kmin < order_key(kAbsentBelow)) {  // uniform
+        __syncthreads();                   // red / cand are reused
+        return select_rank_key<HK>(k, M, want, S);
+    }
     const double ymin = key_value(kmin);
     const double range = key_value(kmax) - ymin;
-    if (!(range > 0.0)) return kmin;  // uniform: every key equal
+    if (!(range > 0.0)) {  // uniform: every key equal
+        above = 0;
+        return kmin;
+    }
     const double fs = 255.999 / range;
     int bin[HK];
 #pragma unroll
@@ -479,15 +486,15 @@ __device__ uint64_t select_rank_key_fast(const uint64_t (&k)[HK], int M, int wan
         bin[j] = valid(j) ? static_cast<int>(fmin(255.0, (key_value(k[j]) - ymin) * fs)) : -1;
         if (bin[j] >= 0) atomicAdd(&S.hist[bin[j]], 1u);
     }
-    __syncthreads();
+    __syncthreads();  // also orders the reads of red / cand above before the writes of cand below
     // every wave finds the same bin (no broadcast needed)
-    int above, cnt;
-    const int sb = hist_select(S.hist, want, above, cnt);
+    int hi_cnt, cnt;
+    const int sb = hist_select(S.hist, want, hi_cnt, cnt);
     if (cnt > kWave) {  // uniform
         __syncthreads();
         return select_rank_key<HK>(k, M, want, S);
     }
-    const int rest = want - above;
+    const int rest = want - hi_cnt;
 #pragma unroll
     for (int j = 0; j < HK; ++j)
         if (bin[j] == sb) S.cand[atomicAdd(&S.ncand, 1)] = k[j];
@@ -502,7 +509,9 @@ __device__ uint64_t select_rank_key_fast(const uint64_t (&k)[HK], int M, int wan
         ge += o >= mine ? 1 : 0;
     }
     const bool owner = lane < n && gt <= rest && rest < ge;
-    return readlane(mine, __ffsll(static_cast<unsigned long long>(__ballot(owner))) - 1);
+    const int src = __ffsll(static_cast<unsigned long long>(__ballot(owner))) - 1;
+    above = hi_cnt + readlane(gt, src);
+    return readlane(mine, src);
 }
 
 // Workspace views of a step.
@@ -555,73 +564,56 @@ template <typename T, int D, int HK, bool FUSED>
 __device__ void sample_head(const DecodeArgs& a, const Views& v, int p, int j, char* t0, char* t1, char* misc) {
     using RL = RepLanes<T, D>;
     constexpr int EPL = RL::EPL, LPL = RL::LPL;
-    constexpr int kMaxM = HK * kThreads;
-    constexpr int RB = HK > 1 ? 4 : 8;  // rounds of 64 teams whose loads fly together
     double* const s_dot = reinterpret_cast<double*>(t0);
     uint64_t* const s_word = reinterpret_cast<uint64_t*>(t1);
     SelScratch& S = *reinterpret_cast<SelScratch*>(misc);
     const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
-    const int M = a.M, G = a.G, Kp = a.Kp;
-    const int b = p / a.Hkv, kv = p - b * a.Hkv, hq = kv * G + j;
+    const int M = a.M, Kp = a.Kp;
+    const int b = p / a.Hkv, kv = p - b * a.Hkv, hq = kv * a.G + j;
     const size_t bq = static_cast<size_t>(b) * a.Hq + hq;
     const size_t tb0 = static_cast<size_t>(p) * M;
     const T* reps = static_cast<const T*>(a.reps);
-    const int grp = tid >> 3, sub = tid & 7;  // team of a round, lane of the team
-    const int nrounds = (M + 63) / 64;
-
-    // the routing keys' loads go out first (8 lanes per key, 64 keys per
-    // round), then this thread's log n, the query dims, the Philox words
-    auto load_batch = [&](uint4 (&raw)[RB][LPL], int r0) {
-#pragma unroll
-        for (int rr = 0; rr < RB; ++rr) {
-            const int g = min((r0 + rr) * 64 + grp, M - 1);
-            const uint4* src = reinterpret_cast<const uint4*>(reps + (tb0 + g) * D + sub * EPL);
-#pragma unroll
-            for (int l = 0; l < LPL; ++l) raw[rr][l] = load_stream(src + l);
-        }
-    };
-    uint4 ra[RB][LPL];
-    double la[RB];
-    auto load_ln = [&](double (&ln)[RB], int r0) {
-#pragma unroll
-        for (int rr = 0; rr < RB; ++rr) ln[rr] = a.log_n[tb0 + min((r0 + rr) * 64 + grp, M - 1)];
-    };
-    load_batch(ra, 0);
-    load_ln(la, 0);
-    float qf[EPL];
-    {
-        const float* qrow = a.q + bq * D + sub * EPL;
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) qf[e] = qrow[e];
-    }
-    // while the loads fly: the Philox words (the block at counter
-    // (g / 4, h, b, step), key (seed, 0), holds the words of teams
-    // 4 (g / 4) .. + 3), then the Gumbel variate of each of this thread's
-    // teams
     const int nblk = (M + 3) / 4;
-    for (int bi = tid; bi < nblk; bi += kThreads) {
+
+    // the select scratch starts empty (read only after the barriers below)
+    if (tid < 64) reinterpret_cast<uint4*>(S.hist)[tid] = make_uint4(0, 0, 0, 0);
+    if (tid == 0) S.ncand = 0;
+
+    // The Philox block at counter (g / 4, h, b, step), key (seed, 0), holds
+    // the words of teams 4 (g / 4) .. + 3.
+    auto philox_words = [&](int bi) {
         const u64x4 r = philox4x64_10(static_cast<uint64_t>(bi), static_cast<uint64_t>(hq), static_cast<uint64_t>(b),
                                       a.step, a.seed, 0);
 #pragma unroll
         for (int e = 0; e < 4; ++e)
             if (4 * bi + e < M) s_word[4 * bi + e] = r.v[e];
-    }
-    __syncthreads();
-    double gum[HK];
+    };
+    // phi_g = log n_g + scale q.l_g for the team of octet `grp` in each
+    // round (8 lanes per routing key, `per` keys per round): the dot product
+    // in fp64 (exact products; two partial sums per lane, then the octet's
+    // sum), stored by the octet's first lane
+    auto query_dims = [&](int sub, double (&qd)[EPL]) {
+        const float* qrow = a.q + bq * D + sub * EPL;
 #pragma unroll
-    for (int jj = 0; jj < HK; ++jj) {
-        const int g = jj * kThreads + tid;
-        gum[jj] = g < M ? gumbel_of_word(s_word[g]) : 0.0;
-    }
-    double qd[EPL];
-#pragma unroll
-    for (int e = 0; e < EPL; ++e) qd[e] = static_cast<double>(qf[e]);
-    // phi_g = log n_g + scale q.l_g: the dot product in fp64 (exact
-    // products; two partial sums per lane, then the octet's sum)
-    auto logits = [&](const uint4 (&raw)[RB][LPL], const double (&ln)[RB], int r0) {
+        for (int e = 0; e < EPL; ++e) qd[e] = static_cast<double>(qrow[e]);
+    };
+    auto load_batch = [&](auto& raw, auto& ln, int grp, int sub, int per, int r0) {
+        constexpr int RB = sizeof(ln) / sizeof(double);
 #pragma unroll
         for (int rr = 0; rr < RB; ++rr) {
-            if (r0 + rr < nrounds) {  // uniform
+            const int g = min((r0 + rr) * per + grp, M - 1);
+            const uint4* src = reinterpret_cast<const uint4*>(reps + (tb0 + g) * D + sub * EPL);
+#pragma unroll
+            for (int l = 0; l < LPL; ++l) raw[rr][l] = load_stream(src + l);
+            ln[rr] = a.log_n[tb0 + g];
+        }
+    };
+    auto logits_batch = [&](const auto& raw, const auto& ln, const double (&qd)[EPL], int grp, int sub, int per,
+                            int r0) {
+        constexpr int RB = sizeof(ln) / sizeof(double);
+#pragma unroll
+        for (int rr = 0; rr < RB; ++rr) {
+            if ((r0 + rr) * per < M) {  // uniform
                 double acc0 = 0.0, acc1 = 0.0;
 #pragma unroll
                 for (int e = 0; e < EPL; e += 2) {
@@ -629,7 +621,7 @@ __device__ void sample_head(const DecodeArgs& a, const Views& v, int p, int j, c
                     acc1 = fma(qd[e + 1], static_cast<double>(RL::elem(raw[rr], e + 1)), acc1);
                 }
                 const double acc = row8_sum(acc0 + acc1);
-                const int g = (r0 + rr) * 64 + grp;
+                const int g = (r0 + rr) * per + grp;
                 if (sub == 0 && g < M) {
                     const double ph = ln[rr] + a.scale * acc;
                     s_dot[g] = ph;
@@ -639,63 +631,88 @@ __device__ void sample_head(const DecodeArgs& a, const Views& v, int p, int j, c
         }
     };
     if constexpr (HK == 1) {
-        logits(ra, la, 0);  // M <= 512: one batch covers every team
+        // M <= 512: two waves draw the Philox words while the other six
+        // compute the logits, 48 teams per round, every round's loads in
+        // flight together (two batches for fp32 keys)
+        constexpr int kPhiloxThreads = 2 * kWave;
+        constexpr int kPer = (kThreads - kPhiloxThreads) / 8;
+        constexpr int kRounds = (kThreads + kPer - 1) / kPer;
+        constexpr int kBatch = LPL <= 2 ? kRounds : 24 / LPL;
+        if (tid < kPhiloxThreads) {
+            for (int bi = tid; bi < nblk; bi += kPhiloxThreads) philox_words(bi);
+        } else {
+            const int lt = tid - kPhiloxThreads, grp = lt >> 3, sub = lt & 7;
+            const int rounds = (M + kPer - 1) / kPer;
+            uint4 raw[kBatch][LPL];
+            double ln[kBatch], qd[EPL];
+            load_batch(raw, ln, grp, sub, kPer, 0);
+            query_dims(sub, qd);
+            logits_batch(raw, ln, qd, grp, sub, kPer, 0);
+            for (int r0 = kBatch; r0 < rounds; r0 += kBatch) {
+                load_batch(raw, ln, grp, sub, kPer, r0);
+                logits_batch(raw, ln, qd, grp, sub, kPer, r0);
+            }
+        }
     } else {
-        // two batches in flight: the next one loads while this one computes
-        uint4 rb[RB][LPL];
-        double lb[RB];
-        for (int r0 = 0; r0 < nrounds; r0 += 2 * RB) {
-            if (r0 + RB < nrounds) {
-                load_batch(rb, r0 + RB);
-                load_ln(lb, r0 + RB);
-            }
-            logits(ra, la, r0);
-            if (r0 + 2 * RB < nrounds) {
-                load_batch(ra, r0 + 2 * RB);
-                load_ln(la, r0 + 2 * RB);
-            }
-            if (r0 + RB < nrounds) logits(rb, lb, r0 + RB);
+        // every thread: the Philox words while the first keys load, then the
+        // logits with two batches of four rounds in flight
+        constexpr int RB = 4;
+        const int grp = tid >> 3, sub = tid & 7, per = kThreads / 8;
+        const int rounds = (M + per - 1) / per;
+        uint4 ra[RB][LPL], rb[RB][LPL];
+        double la[RB], lb[RB], qd[EPL];
+        load_batch(ra, la, grp, sub, per, 0);
+        query_dims(sub, qd);
+        for (int bi = tid; bi < nblk; bi += kThreads) philox_words(bi);
+        for (int r0 = 0; r0 < rounds; r0 += 2 * RB) {
+            if (r0 + RB < rounds) load_batch(rb, lb, grp, sub, per, r0 + RB);
+            logits_batch(ra, la, qd, grp, sub, per, r0);
+            if (r0 + 2 * RB < rounds) load_batch(ra, la, grp, sub, per, r0 + 2 * RB);
+            if (r0 + RB < rounds) logits_batch(rb, lb, qd, grp, sub, per, r0 + RB);
         }
     }
     __syncthreads();
 
-    // the perturbed score as an order-preserving key: key j of this thread
-    // is team j * kThreads + tid
+    // the perturbed score Y_g = phi_g + G_g as an order-preserving key: key
+    // jj of this thread is team jj * kThreads + tid
+    auto valid = [&](int jj) { return jj * kThreads + tid < M; };
+    double phi[HK];
     uint64_t k[HK];
 #pragma unroll
     for (int jj = 0; jj < HK; ++jj) {
         const int g = jj * kThreads + tid;
+        phi[jj] = 0.0;
         k[jj] = 0;
         if (g < M) {
-            const double y = s_dot[g] + gum[jj];
+            phi[jj] = s_dot[g];
+            const double y = phi[jj] + gumbel_of_word(s_word[g]);
             k[jj] = order_key(y);
             if (a.dbg_Y) a.dbg_Y[bq * M + g] = y;
         }
     }
-    auto valid = [&](int jj) { return jj * kThreads + tid < M; };
 
     // tau: the key of rank Kp (0-based, descending)
-    const uint64_t tkey = select_rank_key_fast<HK>(k, M, Kp, S);
+    int above;
+    const uint64_t tkey = select_rank_key_fast<HK>(k, M, Kp, S, above);
     const double tau = key_value(tkey);
-
-    // the sample: the keys above tau's, and the first need_ties keys equal to
-    // it in team order (exactly equal perturbed scores)
-    int above = 0;
+    if (above < 0) {  // uniform: the general select does not count
+        int x[1] = {0};
 #pragma unroll
-    for (int jj = 0; jj < HK; ++jj) above += (valid(jj) && k[jj] > tkey) ? 1 : 0;
-    {
-        const int x[1] = {above};
+        for (int jj = 0; jj < HK; ++jj) x[0] += (valid(jj) && k[jj] > tkey) ? 1 : 0;
         int ex[1], tot[1];
         block_scan<1>(x, ex, tot, S.w);
         above = tot[0];
     }
+
+    // the sample: the keys above tau's, and the first need_ties keys equal to
+    // it in team order (exactly equal perturbed scores)
     const int need_ties = Kp - above;
     const int nwords = (M + kWave - 1) / kWave;
 #pragma unroll
     for (int jj = 0; jj < HK; ++jj) {
         const bool vj = valid(jj);
         const uint64_t sb = __ballot(vj && k[jj] > tkey);
-        const uint64_t tb = __ballot(vj && k[jj] == tkey);
+        const uint64_t tb = need_ties > 0 ? __ballot(vj && k[jj] == tkey) : 0;
         if (lane == 0 && jj * kWaves + w < kSelWords) {
             S.sel[jj * kWaves + w] = sb;
             S.tie[jj * kWaves + w] = tb;
@@ -718,31 +735,34 @@ __device__ void sample_head(const DecodeArgs& a, const Views& v, int p, int j, c
         __syncthreads();
     }
 
-    // thread t < nwords publishes word t (teams 64 t ..) and its sampled
-    // teams' log c (and, for the diagnostics, their ranks in the head's
-    // ascending sample)
-    const uint64_t word = tid < nwords ? S.sel[tid] : 0;
-    int rank = 0;
-    if (a.dbg_sel || a.dbg_logc) {  // uniform
-        const int x[1] = {static_cast<int>(__popcll(word))};
-        int ex[1], tot[1];
-        block_scan<1>(x, ex, tot, S.w);
-        rank = ex[0];
-    }
-    for (uint64_t t = word; t; t &= t - 1) {
-        const int g = tid * kWave + __ffsll(static_cast<unsigned long long>(t)) - 1;
-        const float lcv = log_inclusion(static_cast<float>(s_dot[g] - tau));
-        if (FUSED)
-            store_f32_coherent(v.lc + bq * M + g, lcv);
-        else
-            v.lc[bq * M + g] = lcv;
-        if (rank < Kp) {  // always: exactly Kp teams are sampled
-            if (a.dbg_sel) a.dbg_sel[bq * Kp + rank] = g;
-            if (a.dbg_logc) a.dbg_logc[bq * Kp + rank] = lcv;
+    // log c of every sampled team, by the thread that holds its key (and,
+    // for the diagnostics, its rank in the head's ascending sample); thread
+    // t < nwords publishes sample word t (teams 64 t ..)
+    const bool ranks = a.dbg_sel || a.dbg_logc;
+#pragma unroll
+    for (int jj = 0; jj < HK; ++jj) {
+        const int g = jj * kThreads + tid;
+        const int wd = jj * kWaves + w;
+        const bool taken = valid(jj) && (k[jj] > tkey || (need_ties > 0 && k[jj] == tkey &&
+                                                          ((S.sel[wd] >> lane) & 1ull)));
+        if (taken) {
+            const float lcv = log_inclusion(static_cast<float>(phi[jj] - tau));
+            if (FUSED)
+                store_f32_coherent(v.lc + bq * M + g, lcv);
+            else
+                v.lc[bq * M + g] = lcv;
+            if (ranks) {
+                int rank = static_cast<int>(__popcll(S.sel[wd] & ((1ull << lane) - 1ull)));
+                for (int x = 0; x < wd; ++x) rank += static_cast<int>(__popcll(S.sel[x]));
+                if (rank < Kp) {  // always: exactly Kp teams are sampled
+                    if (a.dbg_sel) a.dbg_sel[bq * Kp + rank] = g;
+                    if (a.dbg_logc) a.dbg_logc[bq * Kp + rank] = lcv;
+                }
+            }
         }
-        ++rank;
     }
     if (tid < nwords) {
+        const uint64_t word = S.sel[tid];
         if (FUSED)
             store_u64_coherent(v.sbits + bq * a.lay.swords + tid, word);
         else
