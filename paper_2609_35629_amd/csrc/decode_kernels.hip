@@ -557,8 +557,8 @@ struct RepLanes {
 
 // ---------------------------------------------------------------------------
 // Phase A: query head j of pair p.  LDS: the head's routing logits (HK *
-// kThreads doubles, in the first value-tile set), its Philox words (in the
-// second) and the select scratch.
+// kThreads doubles, in the first value-tile set), its Philox words or Gumbel
+// variates (in the second) and the select scratch.
 // ---------------------------------------------------------------------------
 template <typename T, int D, int HK, bool FUSED>
 __device__ void sample_head(const DecodeArgs& a, const Views& v, int p, int j, char* t0, char* t1, char* misc) {
@@ -587,6 +587,15 @@ __device__ void sample_head(const DecodeArgs& a, const Views& v, int p, int j, c
 #pragma unroll
         for (int e = 0; e < 4; ++e)
             if (4 * bi + e < M) s_word[4 * bi + e] = r.v[e];
+    };
+    // the same block's four Gumbel variates, stored in place of its words
+    auto philox_gumbels = [&](int bi) {
+        const u64x4 r = philox4x64_10(static_cast<uint64_t>(bi), static_cast<uint64_t>(hq), static_cast<uint64_t>(b),
+                                      a.step, a.seed, 0);
+        double* const s_gum = reinterpret_cast<double*>(s_word);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            if (4 * bi + e < M) s_gum[4 * bi + e] = gumbel_of_word(r.v[e]);
     };
     // phi_g = log n_g + scale q.l_g for the team of octet `grp` in each
     // round (8 lanes per routing key, `per` keys per round): the dot product
@@ -631,15 +640,16 @@ __device__ void sample_head(const DecodeArgs& a, const Views& v, int p, int j, c
         }
     };
     if constexpr (HK == 1) {
-        // M <= 512: two waves draw the Philox words while the other six
-        // compute the logits, 48 teams per round, every round's loads in
-        // flight together (two batches for fp32 keys)
+        // M <= 512: two waves draw the Philox words and turn them into
+        // Gumbel variates while the other six compute the logits, 48 teams
+        // per round, every round's loads in flight together (two batches for
+        // fp32 keys)
         constexpr int kPhiloxThreads = 2 * kWave;
         constexpr int kPer = (kThreads - kPhiloxThreads) / 8;
         constexpr int kRounds = (kThreads + kPer - 1) / kPer;
         constexpr int kBatch = LPL <= 2 ? kRounds : 24 / LPL;
         if (tid < kPhiloxThreads) {
-            for (int bi = tid; bi < nblk; bi += kPhiloxThreads) philox_words(bi);
+            for (int bi = tid; bi < nblk; bi += kPhiloxThreads) philox_gumbels(bi);
         } else {
             const int lt = tid - kPhiloxThreads, grp = lt >> 3, sub = lt & 7;
             const int rounds = (M + kPer - 1) / kPer;
@@ -685,7 +695,8 @@ __device__ void sample_head(const DecodeArgs& a, const Views& v, int p, int j, c
         k[jj] = 0;
         if (g < M) {
             phi[jj] = s_dot[g];
-            const double y = phi[jj] + gumbel_of_word(s_word[g]);
+            const double gm = HK == 1 ? reinterpret_cast<const double*>(s_word)[g] : gumbel_of_word(s_word[g]);
+            const double y = phi[jj] + gm;
             k[jj] = order_key(y);
             if (a.dbg_Y) a.dbg_Y[bq * M + g] = y;
         }
