@@ -1472,24 +1472,39 @@ __device__ void merge_head(const DecodeArgs& a, const float* part_p, int p, int 
     constexpr int NSL = kThreads / NQ;
     const int tid = threadIdx.x, G = a.G;
     const int sl = tid / NQ, dq = tid - sl * NQ;
+    // this thread's states w = sl, sl + NSL, ...: KL of them loaded together
+    // (one memory round trip per KL), then folded in
+    constexpr int KL = 8;
     float mx = kNeg, L = 0.f;
     float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
     bool nan = false;
-#pragma unroll 4
-    for (int w = sl; w < nwp; w += NSL) {
-        const float* st = part_p + (static_cast<size_t>(w) * G + h) * SS;
-        const float2 ml = COHERENT ? load_f2_coherent(st + D) : *reinterpret_cast<const float2*>(st + D);
-        const float4 x = COHERENT ? load_f4_coherent(st + 4 * dq) : reinterpret_cast<const float4*>(st)[dq];
-        nan = nan || ml.x != ml.x;
-        if (ml.x > kEmpty) {
-            const float mn = fmaxf(mx, ml.x);
-            const float sa = fast_exp2(mx - mn), sb = fast_exp2(ml.x - mn);
-            L = L * sa + ml.y * sb;
-            o.x = o.x * sa + x.x * sb;
-            o.y = o.y * sa + x.y * sb;
-            o.z = o.z * sa + x.z * sb;
-            o.w = o.w * sa + x.w * sb;
-            mx = mn;
+    for (int w0 = sl; w0 < nwp; w0 += NSL * KL) {
+        float2 ml[KL];
+        float4 x[KL];
+#pragma unroll
+        for (int k = 0; k < KL; ++k) {
+            const int w = w0 + k * NSL;
+            ml[k] = make_float2(kNeg, 0.f);
+            x[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (w < nwp) {
+                const float* st = part_p + (static_cast<size_t>(w) * G + h) * SS;
+                ml[k] = COHERENT ? load_f2_coherent(st + D) : *reinterpret_cast<const float2*>(st + D);
+                x[k] = COHERENT ? load_f4_coherent(st + 4 * dq) : reinterpret_cast<const float4*>(st)[dq];
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < KL; ++k) {
+            nan = nan || ml[k].x != ml[k].x;
+            if (ml[k].x > kEmpty) {
+                const float mn = fmaxf(mx, ml[k].x);
+                const float sa = fast_exp2(mx - mn), sb = fast_exp2(ml[k].x - mn);
+                L = L * sa + ml[k].y * sb;
+                o.x = o.x * sa + x[k].x * sb;
+                o.y = o.y * sa + x[k].y * sb;
+                o.z = o.z * sa + x[k].z * sb;
+                o.w = o.w * sa + x[k].w * sb;
+                mx = mn;
+            }
         }
     }
     if (nan) mx = __builtin_nanf("");
