@@ -1066,21 +1066,28 @@ __device__ __forceinline__ float* wave_state(char* lds, int wv, int h, int D) {
     return reinterpret_cast<float*>(lds) + (static_cast<size_t>(wv) * kMaxGroup + h) * state_stride(D);
 }
 
-// The pair's units as the waves see them: the suffix units, then each pass
-// of the plan (a workgroup-wide step) with its units.  `run(lo, hi, unit)`
-// walks the wave's units u in [lo, hi), u == gwp (mod waves of the pair),
-// with unit(u) giving each one.
+// The pair's units as the waves see them: the suffix units and each pass of
+// the plan (a workgroup-wide step) with its units.  `run(lo, hi, unit, rev)`
+// walks the wave's units u in [lo, hi), u == s (mod waves of the pair), with
+// unit(u) giving each one; s is the wave's index among the pair's waves, or
+// that index counted from the last wave when `rev`.  The sampled path hands
+// the suffix units to the pair's last waves, which the union units reach
+// last, and runs them while the samples are drawn (one launch) or after the
+// plan (the samples are there when the attention launch starts): a
+// workgroup's plan passes wait for all its waves, so suffix rows read first
+// would hold them up.
 template <typename T, bool DENSE, bool FUSED, int PT, typename Run>
 __device__ __forceinline__ bool walk_units(const DecodeArgs& a, const Views& v, int p, int iw, char* plan_lds,
                                            Run&& run) {
     PlanLds& P = *reinterpret_cast<PlanLds*>(plan_lds);
     const int nsuf = (a.T + kUnitRows - 1) / kUnitRows;
     auto by_index = [&](int u) { return index_unit<T>(a, p, nsuf, u); };
-    run(0, nsuf, by_index);
     if (DENSE) {
-        run(nsuf, nsuf + (a.N + kUnitRows - 1) / kUnitRows, by_index);
+        run(0, nsuf, by_index, false);
+        run(nsuf, nsuf + (a.N + kUnitRows - 1) / kUnitRows, by_index, false);
         return true;
     }
+    if (FUSED) run(0, nsuf, by_index, true);
     const int tid = threadIdx.x, M = a.M;
     const size_t tb0 = static_cast<size_t>(p) * M;
     int sz[PT], bg[PT];
@@ -1100,13 +1107,14 @@ __device__ __forceinline__ bool walk_units(const DecodeArgs& a, const Views& v, 
         for (int base = 0; base < M; base += kThreads * PT) {
             if (base > 0) fetch(base);
             const int3 t = plan_pass<PT, FUSED>(a, v, p, base, sz, bg, P);
-            run(run_u, run_u + t.y, [&](int u) { return plan_unit<T>(a, P, p, u - run_u, t.x, t.y); });
+            run(run_u, run_u + t.y, [&](int u) { return plan_unit<T>(a, P, p, u - run_u, t.x, t.y); }, false);
             run_u += t.y;
             run_teams += t.x;
             run_rows += t.z;
             if (base + kThreads * PT < M) __syncthreads();  // the records are rewritten by the next pass
         }
     }
+    if (!FUSED) run(0, nsuf, by_index, true);
     if (iw == 0 && tid == 0) {
         if (a.dbg_uteams) a.dbg_uteams[p] = run_teams;
         if (a.dbg_urows) a.dbg_urows[p] = run_rows;
@@ -1205,8 +1213,9 @@ __device__ void attend_mfma(const DecodeArgs& a, const Views& v, int p, int iw, 
     // other buffers and computes while those fly; the two buffer sets
     // alternate between two inlined copies of the step, so that each copy
     // names its registers statically.
-    auto run = [&](int lo_u, int hi_u, auto&& unit) {
-        int u = lo_u + (((gwp - lo_u) % NW) + NW) % NW;
+    auto run = [&](int lo_u, int hi_u, auto&& unit, bool rev) {
+        const int gs = rev ? NW - 1 - gwp : gwp;
+        int u = lo_u + (((gs - lo_u) % NW) + NW) % NW;
         if (u >= hi_u) return;  // uniform
         Unit<bf16_t> cur = unit(u);
         float ccr = corrections(cur);
@@ -1359,8 +1368,9 @@ __device__ void attend_f32(const DecodeArgs& a, const Views& v, int p, int iw, i
 #pragma unroll
         for (int e = 0; e < VPL; ++e) acc[h][e] = 0.f;
 
-    auto run = [&](int lo_u, int hi_u, auto&& unit) {
-        for (int u = lo_u + (((gwp - lo_u) % NW) + NW) % NW; u < hi_u; u += NW) {
+    auto run = [&](int lo_u, int hi_u, auto&& unit, bool rev) {
+        const int gs = rev ? NW - 1 - gwp : gwp;
+        for (int u = lo_u + (((gs - lo_u) % NW) + NW) % NW; u < hi_u; u += NW) {
             const Unit<float> U = unit(u);
             float bias[4];
             bool on[4];
