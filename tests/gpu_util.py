@@ -77,32 +77,72 @@ class Compare:
     rel_l2: np.ndarray      # per compared head
     max_phi_rel: float
     max_tau_abs: float
+    equal: np.ndarray = None        # per compared head: same team set as the oracle
+    max_logc_abs: float = 0.0       # |log c_gpu - log c_oracle| over heads with equal sets
+    max_tau_rel_equal: float = 0.0  # |tau_gpu - tau_oracle| / max(1, |tau|) over the same heads
+
+    @property
+    def rel_l2_equal(self) -> np.ndarray:
+        """rel-L2 of the heads whose selection equals the oracle's (the
+        fixed-selection comparison of the appendix "Kernel evaluation
+        protocol")."""
+        return self.rel_l2[self.equal] if self.equal is not None else self.rel_l2
+
+    def assert_selection_bar(self):
+        """At least 99.9% of the instances select the oracle's team set (so
+        every one of fewer than 1000), and every mismatch is a near-tie of
+        the oracle's K-th and (K+1)-th perturbed scores."""
+        assert not self.unexcused, self.unexcused
+        assert self.sel_equal + self.excused == self.heads
+        assert self.sel_equal >= int(np.ceil(0.999 * self.heads)), (self.sel_equal, self.heads)
 
 
 def compare_step(wl: datagen.Workload, Kb: int, out_gpu: np.ndarray, dbg: Optional[sp.DebugOut],
                  step_or: oracle.StepResult, pairs, sampled: bool) -> Compare:
-    G = wl.G
-    rel, unexc = [], []
+    rel, unexc, equal = [], [], []
     eq = exc = 0
-    max_phi = max_tau = 0.0
+    max_phi = max_tau = max_lc = max_tau_eq = 0.0
     if sampled:
         sel = dbg.sel.cpu().numpy()
         phi = dbg.phi.cpu().numpy()
         tau = dbg.tau.cpu().numpy()
+        logc = dbg.logc.cpu().numpy()
     for (bi, h) in pairs:
         r = step_or.heads[bi][h]
         rel.append(oracle.rel_l2(out_gpu[bi, h], r.out))
         if not sampled:
+            equal.append(True)
             continue
         max_phi = max(max_phi, float(np.max(np.abs(phi[bi, h] - r.phi) / np.maximum(1.0, np.abs(r.phi)))))
         max_tau = max(max_tau, abs(float(tau[bi, h]) - r.tau))
-        if np.array_equal(np.sort(sel[bi, h]), r.sel):
+        if np.array_equal(sel[bi, h], r.sel):  # both ascending
             eq += 1
+            equal.append(True)
+            max_lc = max(max_lc, float(np.max(np.abs(logc[bi, h].astype(np.float64) - np.log(r.c)))))
+            max_tau_eq = max(max_tau_eq, abs(float(tau[bi, h]) - r.tau) / max(1.0, abs(r.tau)))
         else:
+            equal.append(False)
             ys = np.sort(r.Y)[::-1]
             gap = ys[Kb - 1] - ys[Kb]
             if gap <= 1e-6 * max(1.0, abs(r.tau)):
                 exc += 1
             else:
                 unexc.append((bi, h, gap))
-    return Compare(len(pairs), eq, exc, unexc, np.array(rel), max_phi, max_tau)
+    return Compare(len(pairs), eq, exc, unexc, np.array(rel), max_phi, max_tau, np.array(equal, bool), max_lc,
+                   max_tau_eq)
+
+
+def union_stats(teams_or, sels, G: int):
+    """Per (b, kv): the number of distinct teams the pair's G query heads
+    selected and their prompt rows (eq. qwen-logical-access's u), from
+    selections sels[b][h] (ascending team ids)."""
+    B = len(sels)
+    Hkv = len(sels[0]) // G
+    ut = np.zeros((B, Hkv), np.int64)
+    ur = np.zeros((B, Hkv), np.int64)
+    for b in range(B):
+        for kv in range(Hkv):
+            hs = [sels[b][h] for h in range(kv * G, (kv + 1) * G)]
+            ut[b, kv] = len(set(int(g) for s in hs for g in s))
+            ur[b, kv] = oracle.union_rows(teams_or[b][kv], hs)
+    return ut, ur
