@@ -44,6 +44,9 @@ def parse():
     p.add_argument("--K", type=int, default=None, help="teams per query head (default: workload's)")
     p.add_argument("--B", type=int, default=None)
     p.add_argument("--no-evict", action="store_true", help="keep the last-level cache warm")
+    p.add_argument("--check-steps", type=int, default=-1,
+                   help="timed steps checked against the oracle afterwards (-1: as many as fit in "
+                        "about 20 s of oracle time, 0: none)")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="budget of the oracle CPU-baseline sample (0 disables it)")
     p.add_argument("--no-dense", action="store_true")
@@ -194,13 +197,15 @@ def main():
 
     # bytes each timed step read: the union rows of every (b, kv) (replayed
     # with the diagnostics on; same seed and step give the same selection)
-    row_bytes = 2 * wl.d * 2
+    row_bytes = 2 * wl.d * (2 if wl.dtype == datagen.BF16 else 4)
     union_rows = np.zeros(args.steps)
+    replays = []
     for i in range(args.steps):
         dbg = sp.DebugOut(wl.B, wl.Hq, wl.Hkv, M, wl.K)
         run_sparse(args.warmup + i, dbg)
         torch.cuda.synchronize()
         union_rows[i] = dbg.union_rows.sum().item()
+        replays.append((out.cpu().numpy(), dbg.sel.cpu().numpy()))
     sampled = wl.K < M
     BH = wl.B * wl.Hkv
     rep_bytes = BH * M * wl.d * 2 if sampled else 0
@@ -245,9 +250,20 @@ def main():
         routing_kl[kind] = round(float(sp.routing_kl(teams, db["q"], scale=wl.scale).mean().item()), 4)
     sp.set_route_keys(teams, "representative")
 
+    # the timed steps against the oracle (test infrastructure, outside the
+    # timed region): output rel-L2 per head and team-set agreement
+    check = None
+    host = None
+    if args.parents == "contiguous" and (args.check_steps != 0 or args.cpu_seconds > 0):
+        host = HostOracle(wl, batch)
+    if host is not None and args.check_steps != 0:
+        check = host.check(replays, args.warmup, args.check_steps, sampled=wl.K < M)
+
     cpu = None
-    if args.cpu_seconds > 0 and args.parents == "contiguous":
-        cpu = cpu_baseline(wl, batch, args.cpu_seconds)
+    if host is not None and args.cpu_seconds > 0:
+        cpu = host.time_steps(args.cpu_seconds)
+
+    ceiling = hbm_read_ceiling(evict)
 
     res = {
         "metric": "SANTA++ decode-attn us/step/layer + achieved HBM GB/s, 32K ctx, 32 teams",
@@ -266,13 +282,16 @@ def main():
                    "B": wl.B, "Hq": wl.Hq, "Hkv": wl.Hkv, "d": wl.d, "N": wl.N, "T": wl.T,
                    "P": wl.P, "R": wl.R, "M": M, "K": wl.K, "parents": args.parents,
                    "evict_1GiB": not args.no_evict},
-        "roofline": {"bound": "hbm", "kernel": "k_attend_mfma<128, false>", "achieved": round(achieved, 1),
+        "roofline": {"bound": "hbm", "kernel": attend_kernel_name(wl, M), "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic},
+        "hbm_read_ceiling": ceiling,
         "prep_us": round(float(np.median(prep_us)), 1),
         "routing_kl_nats": routing_kl,
         "step_gbs": round(float(np.mean(step_bytes) / value / 1e3), 1),
         "step_hbm_frac": round(float(np.mean(step_bytes) / value / 1e3) / HBM_PEAK_GBS, 4),
+        "step_frac_of_measured_ceiling": round(float(np.mean(step_bytes) / value / 1e3) / ceiling["read_gbs"], 4),
+        "attend_frac_of_measured_ceiling": round(achieved / ceiling["read_gbs"], 4),
         "step_bytes_mean": int(np.mean(step_bytes)),
         "union_rows_mean": float(np.mean(union_rows)),
         "read_fraction": round(read_fraction, 4),
@@ -289,6 +308,8 @@ def main():
         res["dense_us"] = round(d, 3)
         res["dense_gbs"] = round(dense_bytes / d / 1e3, 1)
         res["speedup_vs_dense"] = round(d / value, 3)
+    if check is not None:
+        res.update(check)
     if cpu is not None:
         res["cpu_baseline"] = cpu
     print(json.dumps(res), flush=True)
@@ -334,11 +355,11 @@ class HipEvents:
 
 def measured_traffic():
     """Read + write bytes per launch of the sparse attention kernel from
-    profiles/traffic_k_attend_qwen32k_K32.md, or None when the kernel's
+    profiles/traffic_k_decode_attend_qwen32k_K32.md, or None when the kernel's
     sources no longer hash to the value recorded there."""
     import hashlib
     import re
-    path = os.path.join(ROOT, "profiles", "traffic_k_attend_qwen32k_K32.md")
+    path = os.path.join(ROOT, "profiles", "traffic_k_decode_attend_qwen32k_K32.md")
     try:
         text = open(path).read()
     except OSError:
@@ -385,30 +406,159 @@ def upload(batch):
             "sK": dev(batch.sK) if T else None, "sV": dev(batch.sV) if T else None}
 
 
-def cpu_baseline(wl, batch, budget_s):
-    """The oracle (test infrastructure) on the host: whole decode steps (all
-    query heads), as many as fit in the time budget; team construction is
-    excluded, as for the GPU."""
-    import numpy as np
+def attend_kernel_name(wl, M):
+    """The launch the stage events bracket: the attention kernel of the split
+    launch, or the single kernel of the fused one (template arguments: row
+    type, head dimension, teams per sampler thread, launch mode, dense)."""
+    dt = "bf16_t" if wl.dtype == "bf16" else "float"
+    mode = "kFused" if os.environ.get("SANTAPP_DECODE_LAUNCH") == "fused" and wl.dtype == "bf16" else "kAttend"
+    hk = 1 if M <= 512 else (4 if M <= 2048 else 16)
+    return f"k_decode<{dt}, {wl.d}, {hk}, {mode}, false>"
 
-    import oracle
-    Kf = batch.f32(batch.K)
-    teams = oracle.build_all(Kf, wl.P, wl.R)
-    Vf = batch.f32(batch.V)
-    sKf = batch.f32(batch.sK)
-    sVf = batch.f32(batch.sV)
-    steps = 0
-    t0 = time.perf_counter()
-    while True:
-        oracle.decode(batch.q, Kf, Vf, sKf, sVf, teams, wl.K, wl.seed, steps, wl.scale)
-        steps += 1
-        if time.perf_counter() - t0 > budget_s:
-            break
-    el = time.perf_counter() - t0
-    return {"value": round(el / steps * 1e6, 1), "unit": "us/step/layer", "cores": 1,
-            "kind": "oracle",
-            "sample": f"{steps} full decode steps ({wl.B}x{wl.Hq} heads each) of the same workload, "
-                      f"fp64 C oracle, one thread, team build excluded"}
+
+def hbm_read_ceiling(buf):
+    """Measured streaming rates of this GPU over the 1 GiB buffer: a plain
+    read of all of it (the package's streaming-read probe, best of five
+    launches at each of four grid sizes) and a 512 MiB device copy (read +
+    write, best of five)."""
+    import torch
+    from paper_2609_35629_amd import build as pkg_build
+    probe = ctypes.CDLL(pkg_build.PROBE_LIB)
+    probe.santapp_probe_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int,
+                                         ctypes.c_void_p]
+    probe.santapp_probe_read.restype = ctypes.c_int
+    sink = torch.zeros(4, dtype=torch.int32, device="cuda")
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    nbytes = buf.numel() * buf.element_size()
+
+    def best_of(fn, reps=5):
+        fn()
+        best = None
+        for _ in range(reps):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1)
+            best = ms if best is None else min(best, ms)
+        return best
+
+    def read(grid):
+        rc = probe.santapp_probe_read(ctypes.c_void_p(buf.data_ptr()), nbytes, ctypes.c_void_p(sink.data_ptr()),
+                                      grid, stream)
+        if rc != 0:
+            raise RuntimeError(f"streaming-read probe failed ({rc})")
+
+    grids = (256, 512, 1024, 2048)
+    read_ms = {g: best_of(lambda: read(g)) for g in grids}
+    g_best = min(read_ms, key=read_ms.get)
+    half = buf.numel() // 2
+    src, dst = buf[:half], buf[half:]
+    copy_ms = best_of(lambda: dst.copy_(src))
+    return {"read_gbs": round(nbytes / (read_ms[g_best] * 1e-3) / 1e9, 1),
+            "copy_gbs": round(2 * half * buf.element_size() / (copy_ms * 1e-3) / 1e9, 1),
+            "read_grid": g_best,
+            "method": "1 GiB streaming read (16-byte non-temporal loads, 512-thread workgroups, best grid of "
+                      "256/512/1024/2048, best of 5) and a 512 MiB torch device copy (read + write, best of 5)"}
+
+
+class HostOracle:
+    """The oracle (test infrastructure) on the host, over the same batch:
+    team tables built once, inputs widened to fp64 once."""
+
+    def __init__(self, wl, batch):
+        import oracle
+        self.oracle = oracle
+        self.wl = wl
+        self.batch = batch
+        self.teams = oracle.build_all(batch.f64(batch.K), wl.P, wl.R)
+        self.x64 = [batch.f64(x) for x in (batch.K, batch.V, batch.sK, batch.sV)]
+
+    def _head(self, b, h, step):
+        wl = self.wl
+        kv = h // wl.G
+        K, V, sK, sV = self.x64
+        return self.oracle.decode_head(self.batch.q[b, h], K[b, kv], V[b, kv], self.teams[b][kv], sK[b, kv],
+                                       sV[b, kv], wl.K, wl.seed, step, b, h, wl.scale)
+
+    def step(self, step, pool=None):
+        wl = self.wl
+        heads = [(b, h) for b in range(wl.B) for h in range(wl.Hq)]
+        if pool is None:
+            return [self._head(b, h, step) for (b, h) in heads]
+        return list(pool.map(lambda bh: self._head(bh[0], bh[1], step), heads))
+
+    def check(self, replays, first_step, max_steps, sampled):
+        """rel-L2 of every head of the replayed timed steps and the share of
+        (query, head) instances whose team set equals the oracle's."""
+        import numpy as np
+        wl = self.wl
+        n = len(replays)
+        if max_steps < 0:
+            t0 = time.perf_counter()
+            self.step(first_step)
+            per = max(time.perf_counter() - t0, 1e-3)
+            max_steps = max(1, min(n, int(20.0 / per)))
+        n = min(n, max_steps)
+        rel, equal, total = [], 0, 0
+        for i in range(n):
+            out, sel = replays[i]
+            res = self.step(first_step + i)
+            for j, r in enumerate(res):
+                b, h = divmod(j, wl.Hq)
+                rel.append(self.oracle.rel_l2(out[b, h], r.out))
+                if sampled:
+                    total += 1
+                    equal += int(np.array_equal(sel[b, h], r.sel))
+        rel = np.array(rel)
+        outd = {"rel_l2_vs_oracle": {"max": float(f"{rel.max():.3e}"), "mean": float(f"{rel.mean():.3e}"),
+                                     "heads": int(rel.size), "steps": n}}
+        if sampled:
+            outd["team_set_agreement"] = {"equal": equal, "instances": total,
+                                          "fraction": round(equal / max(total, 1), 6)}
+        return outd
+
+    def time_steps(self, budget_s):
+        """Whole decode steps (all query heads) on the host cores: one thread,
+        then a thread per core over the (b, h) heads (the C oracle runs with
+        the GIL released); each figure is the median of five repetitions of
+        a fixed number of steps, sized so that the whole leg takes about
+        budget_s seconds."""
+        import statistics
+        from concurrent.futures import ThreadPoolExecutor
+        try:
+            nproc = len(os.sched_getaffinity(0))
+        except AttributeError:
+            nproc = os.cpu_count() or 1
+        threads = max(1, min(nproc, 16))
+        t0 = time.perf_counter()
+        self.step(0)
+        per = max(time.perf_counter() - t0, 1e-4)
+        k = max(1, int(budget_s / 2 / 5 / per))  # steps per single-thread repetition
+
+        def reps(pool):
+            times = []
+            s = 0
+            for _ in range(5):
+                t = time.perf_counter()
+                for _ in range(k):
+                    self.step(s, pool)
+                    s += 1
+                times.append((time.perf_counter() - t) / k)
+            return statistics.median(times)
+
+        single = reps(None)
+        with ThreadPoolExecutor(max_workers=threads) as pool:
+            multi = reps(pool)
+        wl = self.wl
+        return {"value": round(multi * 1e6, 1), "unit": "us/step/layer", "cores": threads, "kind": "oracle",
+                "single_thread_us": round(single * 1e6, 1), "multi_thread_us": round(multi * 1e6, 1),
+                "nproc": nproc,
+                "sample": f"median of 5 repetitions of {k} full decode steps ({wl.B}x{wl.Hq} heads each) of "
+                          f"the same workload, fp64 C oracle, team build and input widening excluded; "
+                          f"multi-thread: {threads} threads over the (b, h) heads"}
 
 
 if __name__ == "__main__":

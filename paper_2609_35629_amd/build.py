@@ -13,6 +13,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 OBJDIR = os.path.join(ROOT, "_build", "santapp")
 LIB = os.path.join(PKG, "libsantapp.so")
+PROBE_LIB = os.path.join(PKG, "libsantapp_probe.so")  # streaming-read probe (measurement only)
 SOURCES = ["api.hip", "build_kernels.hip", "route_kernels.hip", "decode_kernels.hip", "diag_kernels.hip",
            "kmeans_kernels.hip"]
 
@@ -41,17 +42,24 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every kernel file and link ``libsantapp.so`` next to this file."""
-    os.makedirs(OBJDIR, exist_ok=True)
-    with concurrent.futures.ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        objs = list(ex.map(_compile, SOURCES))
-    tmp = LIB + ".tmp"
+def _link(objs, out):
+    tmp = out + ".tmp"
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, out)
+
+
+def build(verbose: bool = False) -> str:
+    """Compile every kernel file and link ``libsantapp.so`` (and the
+    streaming-read probe ``libsantapp_probe.so``) next to this file."""
+    os.makedirs(OBJDIR, exist_ok=True)
+    with concurrent.futures.ThreadPoolExecutor(max_workers=len(SOURCES) + 1) as ex:
+        objs = list(ex.map(_compile, SOURCES + ["probe.hip"]))
+    _link(objs[-1:], PROBE_LIB)
+    objs = objs[:-1]
+    _link(objs, LIB)
     if verbose:
         print(f"built {LIB}", file=sys.stderr)
     return LIB
