@@ -271,6 +271,24 @@ santapp_status santapp_decode(const santapp_teams* teams, const float* q, const 
                               uint64_t step, double scale, float* out, void* workspace,
                               size_t ws_bytes, const santapp_decode_debug* dbg, void* stream);
 
+/*
+ * santapp_decode for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * the same step, the same arguments except the workspace, over a scratch
+ * buffer the library owns -- a static device array of 4 MiB on every GPU the
+ * library runs on, held until the process ends.  The call allocates nothing
+ * and never synchronises; its first use on a device enqueues a clear of that
+ * device's array on `stream` ahead of the step.  Steps whose workspace
+ * (santapp_decode_workspace_bytes) exceeds 4 MiB return SANTAPP_ELIMIT.
+ * Every call on one GPU shares that GPU's array, which keeps the last call's
+ * contents: calls that overlap in time on one GPU (other streams, other host
+ * threads) race and must be serialised by the caller.
+ */
+santapp_status santapp_decode_static(const santapp_teams* teams, const float* q, const void* suffix_K,
+                                     const void* suffix_V, int T, int suffix_stride, int Hq, int K,
+                                     uint64_t seed, uint64_t step, double scale, float* out,
+                                     const santapp_decode_debug* dbg, void* stream);
+
 /* Workspace for santapp_dense_decode (bytes, host-only query). */
 santapp_status santapp_dense_workspace_bytes(int B, int Hq, int Hkv, int N, int T, int d,
                                              size_t* bytes);

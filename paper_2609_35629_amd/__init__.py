@@ -15,7 +15,7 @@ import torch
 from . import _lib
 from ._lib import SantappError, check  # noqa: F401
 
-__all__ = ["Teams", "build_teams", "decode", "dense_decode", "decode_workspace",
+__all__ = ["Teams", "build_teams", "decode", "decode_static", "dense_decode", "decode_workspace",
            "dense_workspace", "budget_to_K", "SantappError"]
 
 
@@ -297,6 +297,24 @@ def decode(teams: Teams, q: torch.Tensor, suffix_K: Optional[torch.Tensor],
         teams.handle, _ptr(q), _ptr(suffix_K), _ptr(suffix_V), T, stride, Hq, K,
         ctypes.c_uint64(seed), ctypes.c_uint64(step), float(scale), _ptr(out), _ptr(workspace),
         workspace.numel(), dbg, _stream(stream)))
+    return out
+
+
+def decode_static(teams: Teams, q: torch.Tensor, suffix_K: Optional[torch.Tensor],
+                  suffix_V: Optional[torch.Tensor], K: int, out: torch.Tensor, seed: int = 0, step: int = 0,
+                  scale: float = 0.0, debug: Optional[DebugOut] = None, stream=None,
+                  T: Optional[int] = None) -> torch.Tensor:
+    """:func:`decode` over the library's static scratch (santapp_decode_static):
+    nothing is allocated, so ``out [B, Hq, d]`` fp32 must be given.  Calls on
+    one GPU share the scratch and must not overlap in time."""
+    B, Hq, d = q.shape
+    _need(q, "q", shape=(teams.B, Hq, teams.d), dtype=torch.float32)
+    T, stride = _suffix(suffix_K, suffix_V, teams.B, teams.Hkv, teams.d, teams.torch_dtype, T)
+    _need(out, "out", shape=(B, Hq, d), dtype=torch.float32)
+    dbg = ctypes.byref(debug.struct()) if debug is not None else None
+    check(_lib.load().santapp_decode_static(
+        teams.handle, _ptr(q), _ptr(suffix_K), _ptr(suffix_V), T, stride, Hq, K,
+        ctypes.c_uint64(seed), ctypes.c_uint64(step), float(scale), _ptr(out), dbg, _stream(stream)))
     return out
 
 

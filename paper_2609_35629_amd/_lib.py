@@ -16,7 +16,7 @@ STATUS_NAMES = {OK: "OK", EINVAL: "EINVAL", EDTYPE: "EDTYPE", ENOMEM: "ENOMEM", 
 # every function include/santapp.h declares
 EXPORTS = [
     "santapp_build_teams", "santapp_teams_info", "santapp_teams_destroy", "santapp_budget_to_K",
-    "santapp_decode_workspace_bytes", "santapp_workspace_zero", "santapp_decode",
+    "santapp_decode_workspace_bytes", "santapp_workspace_zero", "santapp_decode", "santapp_decode_static",
     "santapp_dense_workspace_bytes", "santapp_dense_decode", "santapp_last_error",
     "santapp_teams_set_route_keys", "santapp_routing_kl_workspace_bytes", "santapp_routing_kl",
     "santapp_kmeans_parents", "santapp_build_teams_from_labels",
@@ -84,6 +84,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     L.santapp_workspace_zero.argtypes = [vp, sz, vp]
     L.santapp_decode.argtypes = [vp, vp, vp, vp, i, i, i, i, u64, u64, ctypes.c_double, vp, vp, sz,
                                  ctypes.POINTER(DecodeDebug), vp]
+    L.santapp_decode_static.argtypes = [vp, vp, vp, vp, i, i, i, i, u64, u64, ctypes.c_double, vp,
+                                        ctypes.POINTER(DecodeDebug), vp]
     L.santapp_dense_workspace_bytes.argtypes = [i, i, i, i, i, i, ctypes.POINTER(sz)]
     L.santapp_dense_decode.argtypes = [vp, vp, vp, i, i, i, i, i, vp, vp, i, i, i, ctypes.c_double,
                                        vp, vp, sz, vp]

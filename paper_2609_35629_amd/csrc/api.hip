@@ -9,6 +9,7 @@
 #include <algorithm>
 #include <atomic>
 #include <functional>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -764,6 +765,68 @@ santapp_status santapp_decode(const santapp_teams* t, const float* q, const void
     if ((e = launch_decode(A, s)) != hipSuccess) return hip_fail(e, "decode kernels");
     if ((e = mark(3)) != hipSuccess) return hip_fail(e, "event record");
     return ok();
+}
+
+// ---------------------------------------------------------------------------
+// santapp_decode_static: santapp_decode over a scratch buffer the library
+// owns, a file-scope device array of kStaticScratchBytes that every GPU the
+// library runs on holds until the process ends.  Its device address is taken
+// once per device (with that device current) and used for every launch; its
+// first use on a device clears it with the fill kernel (the counters must
+// start at zero; every completed call leaves them at zero).
+// ---------------------------------------------------------------------------
+namespace {
+
+constexpr size_t kStaticScratchBytes = size_t(4) << 20;
+constexpr int kMaxDevices = 64;
+
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+struct ScratchSlot {
+    void* ptr = nullptr;  // device address of `scratch` on this device
+    bool cleared = false;
+};
+static ScratchSlot g_scratch[kMaxDevices];
+static std::mutex g_scratch_mu;
+
+static santapp_status static_scratch(hipStream_t s, void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) return fail(SANTAPP_ELIMIT, "device %d beyond the %d devices supported", dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    ScratchSlot& sl = g_scratch[dev];
+    if (!sl.ptr) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) return hip_fail(e != hipSuccess ? e : hipErrorInvalidSymbol, "hipGetSymbolAddress(scratch)");
+        sl.ptr = p;
+    }
+    if (!sl.cleared) {
+        e = launch_zero(sl.ptr, kStaticScratchBytes, s);
+        if (e != hipSuccess) return hip_fail(e, "static scratch clear");
+        sl.cleared = true;
+    }
+    *out = sl.ptr;
+    return SANTAPP_OK;
+}
+
+}  // namespace
+
+santapp_status santapp_decode_static(const santapp_teams* t, const float* q, const void* suffix_K,
+                                     const void* suffix_V, int T, int suffix_stride, int Hq, int K,
+                                     uint64_t seed, uint64_t step, double scale, float* out,
+                                     const santapp_decode_debug* dbg, void* stream) {
+    if (!t) return fail(SANTAPP_EINVAL, "teams is NULL");
+    size_t need = 0;
+    if (santapp_status st = santapp_decode_workspace_bytes(t, Hq, T, K, &need)) return st;
+    if (need > kStaticScratchBytes)
+        return fail(SANTAPP_ELIMIT, "this step needs %zu bytes of scratch; the static scratch holds %zu "
+                    "(use santapp_decode with a workspace)", need, kStaticScratchBytes);
+    void* ws = nullptr;
+    if (santapp_status st = static_scratch(static_cast<hipStream_t>(stream), &ws)) return st;
+    return santapp_decode(t, q, suffix_K, suffix_V, T, suffix_stride, Hq, K, seed, step, scale, out, ws,
+                          kStaticScratchBytes, dbg, stream);
 }
 
 santapp_status santapp_dense_decode(const float* q, const void* K, const void* V, int B, int Hkv,
