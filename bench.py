@@ -47,6 +47,8 @@ def parse():
     p.add_argument("--check-steps", type=int, default=-1,
                    help="timed steps checked against the oracle afterwards (-1: as many as fit in "
                         "about 20 s of oracle time, 0: none)")
+    p.add_argument("--loop-steps", type=int, default=64,
+                   help="steps of the two-layer decode loop timed as the suffix grows (0: skip)")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="budget of the oracle CPU-baseline sample (0 disables it)")
     p.add_argument("--no-dense", action="store_true")
@@ -264,6 +266,9 @@ def main():
         cpu = host.time_steps(args.cpu_seconds)
 
     ceiling = hbm_read_ceiling(evict)
+    loop = None
+    if args.loop_steps > 0 and args.parents == "contiguous":
+        loop = loop_timing(wl, args.loop_steps, 2, evict, hev, args.no_evict)
 
     res = {
         "metric": "SANTA++ decode-attn us/step/layer + achieved HBM GB/s, 32K ctx, 32 teams",
@@ -310,6 +315,8 @@ def main():
         res["speedup_vs_dense"] = round(d / value, 3)
     if check is not None:
         res.update(check)
+    if loop is not None:
+        res["decode_loop"] = loop
     if cpu is not None:
         res["cpu_baseline"] = cpu
     print(json.dumps(res), flush=True)
@@ -404,6 +411,54 @@ def upload(batch):
     T = batch.wl.T
     return {"q": torch.from_numpy(batch.q).cuda(), "K": dev(batch.K), "V": dev(batch.V),
             "sK": dev(batch.sK) if T else None, "sV": dev(batch.sV) if T else None}
+
+
+def loop_timing(wl, steps, layers, evict, hev, no_evict):
+    """A two-layer decode loop at the workload's shape: every layer starts
+    with an empty suffix and appends one generated row per (b, kv) and step.
+    Each layer's attention call is timed on its own (events on the stream,
+    the 1 GiB eviction between steps); reported as the mean over the layers
+    and the steps of each quarter of the loop, sampled and dense."""
+    import numpy as np
+    import torch
+
+    import datagen
+    from paper_2609_35629_amd.decode_loop import DecodeLoop
+    trace = datagen.decode_trace(wl, layers, steps)
+    dev = lambda a: upload_rows(a, wl.dtype)
+    prompts = [(dev(b.K), dev(b.V)) for b, _ in trace]
+    rows = [(dev(b.sK), dev(b.sV)) for b, _ in trace]
+    qdev = [torch.from_numpy(qs).cuda() for _, qs in trace]
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    out = {"layers": layers, "steps": steps, "workload": f"{wl.name} shape, T = 0 .. {steps - 1}"}
+    q4 = max(1, steps // 4)
+    for dense in (False, True):
+        loop = DecodeLoop(prompts, steps, wl.Hq, wl.K, wl.P, wl.R, seed=wl.seed, dense=dense)
+        ev = [[(hev.make(), hev.make()) for _ in range(layers)] for _ in range(steps)]
+        torch.cuda.synchronize()
+        for t in range(steps):
+            if not no_evict:
+                evict.add_(1.0)
+            for li, layer in enumerate(loop.layers):
+                hev.record(ev[t][li][0], stream)
+                layer.attend(qdev[li][t], loop.seed + li, t, wl.scale)
+                hev.record(ev[t][li][1], stream)
+                layer.append(rows[li][0][:, :, t], rows[li][1][:, :, t])
+        torch.cuda.synchronize()
+        us = np.array([[hev.us(a, b) for a, b in ev[t]] for t in range(steps)]).mean(axis=1)
+        key = "dense_us_per_layer_step" if dense else "us_per_layer_step"
+        out[key] = {f"T{lo}-{min(lo + q4, steps) - 1}": round(float(us[lo:lo + q4].mean()), 2)
+                    for lo in range(0, steps, q4)}
+        loop.close()
+    return out
+
+
+def upload_rows(a, dtype):
+    import numpy as np
+    import torch
+    if dtype == "bf16":
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
 
 
 def attend_kernel_name(wl, M):

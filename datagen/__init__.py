@@ -197,6 +197,27 @@ def generate(wl: Workload, keep_labels: bool = False) -> Batch:
     return Batch(wl, q, K, V, sK, sV, focus, labels_all)
 
 
+def decode_trace(wl: Workload, layers: int, steps: int):
+    """Inputs of a synthetic multi-layer decode loop of ``steps`` steps.
+
+    Layer l is a batch drawn like ``wl`` from its own data seeds, with
+    ``T = steps`` suffix rows: row t of each (b, kv) is the key/value the
+    loop generates at step t (drawn like the prompt's keys and values, from
+    the layer's clusters).  Step t's queries are the batch's queries plus
+    N(0, 0.25^2) drift per coordinate, from a generator seeded by the layer.
+    Returns a list of (batch, queries [steps, B, Hq, d] fp32), one per layer.
+    """
+    out = []
+    for layer in range(layers):
+        wl_l = wl.with_(name=f"{wl.name}-layer{layer}", T=steps,
+                        data_seeds=tuple(s + 7919 * (layer + 1) for s in wl.data_seeds))
+        b = generate(wl_l)
+        rng = np.random.default_rng([layer, 104729])
+        qs = (b.q[None].astype(np.float64) + 0.25 * rng.standard_normal((steps,) + b.q.shape)).astype(np.float32)
+        out.append((b, qs))
+    return out
+
+
 def get(name: str, **overrides) -> Batch:
     wl = WORKLOADS[name]
     if overrides:
