@@ -45,8 +45,8 @@ def parse():
     p.add_argument("--B", type=int, default=None)
     p.add_argument("--no-evict", action="store_true", help="keep the last-level cache warm")
     p.add_argument("--check-steps", type=int, default=-1,
-                   help="timed steps checked against the oracle afterwards (-1: as many as fit in "
-                        "about 20 s of oracle time, 0: none)")
+                   help="timed steps the cpu_baseline leg checks against the oracle afterwards (-1: as "
+                        "many as fit in about 20 s of oracle time, 0: none)")
     p.add_argument("--loop-steps", type=int, default=64,
                    help="steps of the two-layer decode loop timed as the suffix grows (0: skip)")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
@@ -210,7 +210,7 @@ def main():
         replays.append((out.cpu().numpy(), dbg.sel.cpu().numpy()))
     sampled = wl.K < M
     BH = wl.B * wl.Hkv
-    rep_bytes = BH * M * wl.d * 2 if sampled else 0
+    rep_bytes = BH * M * wl.d * (2 if wl.dtype == datagen.BF16 else 4) if sampled else 0
     suffix_bytes = BH * wl.T * row_bytes
     small_bytes = wl.B * wl.Hq * wl.d * 4 * 2  # q in, out
     if not sampled:
@@ -252,17 +252,15 @@ def main():
         routing_kl[kind] = round(float(sp.routing_kl(teams, db["q"], scale=wl.scale).mean().item()), 4)
     sp.set_route_keys(teams, "representative")
 
-    # the timed steps against the oracle (test infrastructure, outside the
-    # timed region): output rel-L2 per head and team-set agreement
-    check = None
-    host = None
-    if args.parents == "contiguous" and (args.check_steps != 0 or args.cpu_seconds > 0):
+    # the cpu_baseline leg: the oracle (test infrastructure) on the host
+    # cores, outside the timed region -- timed over whole decode steps, and
+    # the checker of the replayed timed steps (output rel-L2 per head and
+    # team-set agreement)
+    check = cpu = None
+    if args.cpu_seconds > 0 and args.parents == "contiguous":
         host = HostOracle(wl, batch)
-    if host is not None and args.check_steps != 0:
-        check = host.check(replays, args.warmup, args.check_steps, sampled=wl.K < M)
-
-    cpu = None
-    if host is not None and args.cpu_seconds > 0:
+        if args.check_steps != 0:
+            check = host.check(replays, args.warmup, args.check_steps, sampled=wl.K < M)
         cpu = host.time_steps(args.cpu_seconds)
 
     ceiling = hbm_read_ceiling(evict)
