@@ -1070,12 +1070,11 @@ __device__ __forceinline__ float* wave_state(char* lds, int wv, int h, int D) {
 // the plan (a workgroup-wide step) with its units.  `run(lo, hi, unit, rev)`
 // walks the wave's units u in [lo, hi), u == s (mod waves of the pair), with
 // unit(u) giving each one; s is the wave's index among the pair's waves, or
-// that index counted from the last wave when `rev`.  The sampled path hands
-// the suffix units to the pair's last waves, which the union units reach
-// last, and runs them while the samples are drawn (one launch) or after the
-// plan (the samples are there when the attention launch starts): a
-// workgroup's plan passes wait for all its waves, so suffix rows read first
-// would hold them up.
+// that index counted from the last wave when `rev`.  In the single launch the
+// suffix units go to the pair's last waves while the samples are drawn; in
+// the split launch (the samples are there when it starts) they join the
+// first plan pass's units, so that they neither hold up a workgroup's plan
+// (its passes wait for all its waves) nor follow a wave's union units.
 template <typename T, bool DENSE, bool FUSED, int PT, typename Run>
 __device__ __forceinline__ bool walk_units(const DecodeArgs& a, const Views& v, int p, int iw, char* plan_lds,
                                            Run&& run) {
@@ -1107,14 +1106,18 @@ __device__ __forceinline__ bool walk_units(const DecodeArgs& a, const Views& v, 
         for (int base = 0; base < M; base += kThreads * PT) {
             if (base > 0) fetch(base);
             const int3 t = plan_pass<PT, FUSED>(a, v, p, base, sz, bg, P);
-            run(run_u, run_u + t.y, [&](int u) { return plan_unit<T>(a, P, p, u - run_u, t.x, t.y); }, false);
+            // the split launch reads the suffix units in the first pass's run
+            // (units 0 .. nsuf - 1), so that no wave reads them after its
+            // union units
+            const int lo = (!FUSED && base == 0) ? 0 : run_u, first = run_u;
+            run(lo, run_u + t.y,
+                [&](int u) { return u < first ? by_index(u) : plan_unit<T>(a, P, p, u - first, t.x, t.y); }, false);
             run_u += t.y;
             run_teams += t.x;
             run_rows += t.z;
             if (base + kThreads * PT < M) __syncthreads();  // the records are rewritten by the next pass
         }
     }
-    if (!FUSED) run(0, nsuf, by_index, true);
     if (iw == 0 && tid == 0) {
         if (a.dbg_uteams) a.dbg_uteams[p] = run_teams;
         if (a.dbg_urows) a.dbg_urows[p] = run_rows;
