@@ -601,10 +601,23 @@ __device__ void sample_head(const DecodeArgs& a, const Views& v, int p, int j, c
     // round (8 lanes per routing key, `per` keys per round): the dot product
     // in fp64 (exact products; two partial sums per lane, then the octet's
     // sum), stored by the octet's first lane
-    auto query_dims = [&](int sub, double (&qd)[EPL]) {
+    // the query dims are loaded before the routing keys and widened after
+    // them, so that the first round waits only for its own loads (the
+    // hardware counts loads in issue order)
+    auto query_load = [&](int sub, float (&qf)[EPL]) {
         const float* qrow = a.q + bq * D + sub * EPL;
 #pragma unroll
-        for (int e = 0; e < EPL; ++e) qd[e] = static_cast<double>(qrow[e]);
+        for (int e = 0; e < EPL; e += 4) {
+            const float4 x = *reinterpret_cast<const float4*>(qrow + e);
+            qf[e] = x.x;
+            qf[e + 1] = x.y;
+            qf[e + 2] = x.z;
+            qf[e + 3] = x.w;
+        }
+    };
+    auto query_dims = [&](const float (&qf)[EPL], double (&qd)[EPL]) {
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) qd[e] = static_cast<double>(qf[e]);
     };
     auto load_batch = [&](auto& raw, auto& ln, int grp, int sub, int per, int r0) {
         constexpr int RB = sizeof(ln) / sizeof(double);
@@ -616,6 +629,10 @@ __device__ void sample_head(const DecodeArgs& a, const Views& v, int p, int j, c
             for (int l = 0; l < LPL; ++l) raw[rr][l] = load_stream(src + l);
             ln[rr] = a.log_n[tb0 + g];
         }
+        // keep every load here, in this order (the compiler would otherwise
+        // sink a round's loads into the block that uses them, behind the
+        // waits of the rounds before it)
+        asm volatile("" ::: "memory");
     };
     auto logits_batch = [&](const auto& raw, const auto& ln, const double (&qd)[EPL], int grp, int sub, int per,
                             int r0) {
@@ -655,8 +672,10 @@ __device__ void sample_head(const DecodeArgs& a, const Views& v, int p, int j, c
             const int rounds = (M + kPer - 1) / kPer;
             uint4 raw[kBatch][LPL];
             double ln[kBatch], qd[EPL];
+            float qf[EPL];
+            query_load(sub, qf);
             load_batch(raw, ln, grp, sub, kPer, 0);
-            query_dims(sub, qd);
+            query_dims(qf, qd);
             logits_batch(raw, ln, qd, grp, sub, kPer, 0);
             for (int r0 = kBatch; r0 < rounds; r0 += kBatch) {
                 load_batch(raw, ln, grp, sub, kPer, r0);
@@ -671,8 +690,10 @@ __device__ void sample_head(const DecodeArgs& a, const Views& v, int p, int j, c
         const int rounds = (M + per - 1) / per;
         uint4 ra[RB][LPL], rb[RB][LPL];
         double la[RB], lb[RB], qd[EPL];
+        float qf[EPL];
+        query_load(sub, qf);
         load_batch(ra, la, grp, sub, per, 0);
-        query_dims(sub, qd);
+        query_dims(qf, qd);
         for (int bi = tid; bi < nblk; bi += kThreads) philox_words(bi);
         for (int r0 = 0; r0 < rounds; r0 += 2 * RB) {
             if (r0 + RB < rounds) load_batch(rb, lb, grp, sub, per, r0 + RB);
