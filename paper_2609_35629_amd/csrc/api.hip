@@ -151,7 +151,7 @@ DecodeLayout decode_layout(int B, int Hq, int Hkv, int T, int d, int M, int Kp, 
     const int G = Hq / Hkv;
     const long long xs = std::min<long long>(M, static_cast<long long>(G) * Kp);
     L.nwg = decode_wgs(cus, static_cast<long long>(BH), chunk_count(T) + static_cast<long long>(std::max(1, cap[xs])));
-    L.maxwp = BH <= static_cast<size_t>(L.nwg) ? static_cast<int>((L.nwg + BH - 1) / BH) : 1;
+    L.maxwp = BH <= static_cast<size_t>(L.nwg) ? pair_wgs(0, L.nwg, static_cast<int>(BH)) : 1;
     L.swords = (M + 63) / 64;
     Carver c;
     L.ctr = c.take((BH + BH * G) * sizeof(int));
@@ -167,7 +167,7 @@ DecodeLayout dense_layout(int B, int Hq, int Hkv, int N, int T, int d, int cus) 
     const size_t BH = static_cast<size_t>(B) * Hkv;
     const int G = Hq / Hkv;
     L.nwg = decode_wgs(cus, static_cast<long long>(BH), chunk_count(N) + static_cast<long long>(chunk_count(T)));
-    L.maxwp = BH <= static_cast<size_t>(L.nwg) ? static_cast<int>((L.nwg + BH - 1) / BH) : 1;
+    L.maxwp = BH <= static_cast<size_t>(L.nwg) ? pair_wgs(0, L.nwg, static_cast<int>(BH)) : 1;
     Carver c;
     L.ctr = c.take((BH + BH * G) * sizeof(int));
     L.part = c.take(BH * L.maxwp * G * state_stride(d) * sizeof(float));

@@ -1674,8 +1674,8 @@ __device__ __forceinline__ void attend_all(const DecodeArgs& a, const Views& v, 
             attend_pair<T, D, DENSE, FUSED, 1>(a, v, p, iw, nwp, t0, t1, misc);
     };
     if (BH <= nwg) {
-        const int p = w % BH;
-        one(p, w / BH, (nwg - 1 - p) / BH + 1);
+        const PairSlot sl = pair_slot(w, nwg, BH);
+        one(sl.p, sl.iw, sl.nwp);
     } else {
         for (int p = w; p < BH; p += nwg) one(p, 0, 1);
     }
@@ -1721,7 +1721,7 @@ __global__ __launch_bounds__(kThreads) void k_merge(DecodeArgs a) {
     const Views v = views_of(a);
     const int BH = a.B * a.Hkv, G = a.G, nwg = a.lay.nwg;
     const int p = blockIdx.x / G, h = blockIdx.x - p * G;
-    const int nwp = BH <= nwg ? (nwg - 1 - p % nwg) / BH + 1 : 1;
+    const int nwp = BH <= nwg ? pair_wgs(p, nwg, BH) : 1;
     const float* part_p = v.part + static_cast<size_t>(p) * a.lay.maxwp * G * state_stride(D);
     merge_head<D, false>(a, part_p, p, h, nwp, true, s_acc, s_ml);
 }

@@ -45,6 +45,38 @@ struct DecodeLayout {
     size_t ctr = 0, sbits = 0, lc = 0, part = 0, total = 0;
 };
 
+// Workgroup w of an attention grid of nwg workgroups serving BH (b, kv)
+// pairs (BH <= nwg): its pair p, its index iw among the pair's workgroups and
+// their count nwp.  A launch places workgroup w on XCD w mod 8.  When the
+// grid holds at least one group of eight consecutive workgroups per pair, the
+// groups go to the pairs in turn, so every pair's workgroups span all eight
+// XCDs (each XCD has its own share of the memory bandwidth); otherwise
+// workgroup w serves pair w mod BH.
+struct PairSlot {
+    int p, iw, nwp;
+};
+__host__ __device__ inline PairSlot pair_slot(int w, int nwg, int BH) {
+    const int groups = nwg / 8;
+    PairSlot s;
+    if (nwg % 8 == 0 && groups >= BH) {
+        const int j = w / 8;
+        s.p = j % BH;
+        s.iw = 8 * (j / BH) + w % 8;
+        s.nwp = 8 * ((groups - 1 - s.p) / BH + 1);
+    } else {
+        s.p = w % BH;
+        s.iw = w / BH;
+        s.nwp = (nwg - 1 - s.p) / BH + 1;
+    }
+    return s;
+}
+// The workgroups of pair p (the nwp of its slots).
+__host__ __device__ inline int pair_wgs(int p, int nwg, int BH) {
+    const int groups = nwg / 8;
+    if (nwg % 8 == 0 && groups >= BH) return 8 * ((groups - 1 - p) / BH + 1);
+    return (nwg - 1 - p) / BH + 1;
+}
+
 // Attention workgroups of a step: one per compute unit (a multiple of eight,
 // the XCDs a launch spreads over), fewer when the step has few units.
 int decode_wgs(int cus, long long BH, long long units_per_pair);
