@@ -145,10 +145,70 @@ struct Carver {
 
 }  // namespace
 
-DecodeLayout decode_layout(int B, int Hq, int Hkv, int T, int d, int M, int Kp, const int* cap, int cus) {
+namespace {
+
+// Launch mode asked for by SANTAPP_DECODE_LAUNCH (read once per process):
+// "split" or "fused" take the three-launch kernels (fused: in one launch);
+// anything else takes the single-launch step wherever it applies.
+enum class LaunchMode { kStep, kSplit, kFused };
+
+LaunchMode launch_mode() {
+    static const LaunchMode m = [] {
+        const char* e = getenv("SANTAPP_DECODE_LAUNCH");
+        if (e != nullptr && strcmp(e, "fused") == 0) return LaunchMode::kFused;
+        if (e != nullptr && strcmp(e, "split") == 0) return LaunchMode::kSplit;
+        return LaunchMode::kStep;
+    }();
+    return m;
+}
+
+// The single-launch step's own workspace: epochs, the tagged exchange words
+// (sampled steps) and the tagged partial states.
+void step_regions(DecodeLayout& L, size_t BH, int G, int M, int d, bool dense, size_t& off) {
+    auto take = [&](size_t bytes) {
+        const size_t at = off;
+        off = (off + bytes + 255) & ~static_cast<size_t>(255);
+        return at;
+    };
+    L.epoch = take(BH * sizeof(uint32_t));
+    if (!dense) {
+        L.xk = take(BH * G * static_cast<size_t>(M) * 16);
+        L.xp = take(BH * G * static_cast<size_t>(M) * 8);
+    }
+    L.part = take(BH * L.maxwp * G * static_cast<size_t>(step_state_bytes(d)));
+}
+
+}  // namespace
+
+bool step_mode(santapp_dtype dt, int d, long long BH, int M, int Kp, bool dense, int cus) {
+    if (launch_mode() != LaunchMode::kStep) return false;
+    if (dt != SANTAPP_BF16 || (d != 64 && d != 128) || cus < 8 || BH < 1 || BH > cus) return false;
+    return dense || (M <= kStepMaxTeams && Kp <= kStepMaxKp);
+}
+
+int step_wgs(int cus, long long BH) {
+    if (cus % 8 == 0 && BH * 8 <= cus) {
+        const long long per = std::min<long long>(kStepMaxWgs, 8 * (cus / (8 * BH)));
+        return static_cast<int>(BH * per);
+    }
+    return static_cast<int>(BH * std::min<long long>(kStepMaxWgs, cus / BH));
+}
+
+DecodeLayout decode_layout(int B, int Hq, int Hkv, int T, int d, int M, int Kp, const int* cap, int cus,
+                           santapp_dtype dt) {
     DecodeLayout L;
     const size_t BH = static_cast<size_t>(B) * Hkv, BQ = static_cast<size_t>(B) * Hq;
     const int G = Hq / Hkv;
+    if (step_mode(dt, d, static_cast<long long>(BH), M, Kp, false, cus)) {
+        L.step = true;
+        L.nwg = step_wgs(cus, static_cast<long long>(BH));
+        L.maxwp = pair_wgs(0, L.nwg, static_cast<int>(BH));
+        L.swords = (M + 63) / 64;
+        size_t off = 0;
+        step_regions(L, BH, G, M, d, false, off);
+        L.total = off;
+        return L;
+    }
     const long long xs = std::min<long long>(M, static_cast<long long>(G) * Kp);
     L.nwg = decode_wgs(cus, static_cast<long long>(BH), chunk_count(T) + static_cast<long long>(std::max(1, cap[xs])));
     L.maxwp = BH <= static_cast<size_t>(L.nwg) ? pair_wgs(0, L.nwg, static_cast<int>(BH)) : 1;
@@ -162,10 +222,19 @@ DecodeLayout decode_layout(int B, int Hq, int Hkv, int T, int d, int M, int Kp, 
     return L;
 }
 
-DecodeLayout dense_layout(int B, int Hq, int Hkv, int N, int T, int d, int cus) {
+DecodeLayout dense_layout(int B, int Hq, int Hkv, int N, int T, int d, int cus, santapp_dtype dt) {
     DecodeLayout L;
     const size_t BH = static_cast<size_t>(B) * Hkv;
     const int G = Hq / Hkv;
+    if (step_mode(dt, d, static_cast<long long>(BH), 0, 0, true, cus)) {
+        L.step = true;
+        L.nwg = step_wgs(cus, static_cast<long long>(BH));
+        L.maxwp = pair_wgs(0, L.nwg, static_cast<int>(BH));
+        size_t off = 0;
+        step_regions(L, BH, G, 0, d, true, off);
+        L.total = off;
+        return L;
+    }
     L.nwg = decode_wgs(cus, static_cast<long long>(BH), chunk_count(N) + static_cast<long long>(chunk_count(T)));
     L.maxwp = BH <= static_cast<size_t>(L.nwg) ? pair_wgs(0, L.nwg, static_cast<int>(BH)) : 1;
     Carver c;
@@ -650,8 +719,8 @@ santapp_status santapp_decode_workspace_bytes(const santapp_teams* t, int Hq, in
     if (Hq < 1 || Hq % t->Hkv != 0) return fail(SANTAPP_EINVAL, "Hq must be a positive multiple of Hkv");
     if (T < 0 || K < 1) return fail(SANTAPP_EINVAL, "T must be >= 0 and K >= 1");
     const int Kp = std::min(K, t->M);
-    *bytes = Kp == t->M ? dense_layout(t->B, Hq, t->Hkv, t->N, T, t->d, t->cus).total
-                        : decode_layout(t->B, Hq, t->Hkv, T, t->d, t->M, Kp, t->cap.data(), t->cus).total;
+    *bytes = Kp == t->M ? dense_layout(t->B, Hq, t->Hkv, t->N, T, t->d, t->cus, t->dtype).total
+                        : decode_layout(t->B, Hq, t->Hkv, T, t->d, t->M, Kp, t->cap.data(), t->cus, t->dtype).total;
     return ok();
 }
 
@@ -660,22 +729,16 @@ santapp_status santapp_dense_workspace_bytes(int B, int Hq, int Hkv, int N, int 
     if (!bytes) return fail(SANTAPP_EINVAL, "NULL argument");
     if (B < 1 || Hkv < 1 || Hq < 1 || Hq % Hkv != 0 || N < 0 || T < 0 || N + T < 1 || d < 1)
         return fail(SANTAPP_EINVAL, "invalid sizes");
-    *bytes = dense_layout(B, Hq, Hkv, N, T, d, device_cus()).total;
+    // the larger of the two element types' layouts (the call's type is not an argument)
+    const int cus = device_cus();
+    *bytes = std::max(dense_layout(B, Hq, Hkv, N, T, d, cus, SANTAPP_BF16).total,
+                      dense_layout(B, Hq, Hkv, N, T, d, cus, SANTAPP_FP32).total);
     return ok();
 }
 
 namespace {
 
-// Launch mode of a bf16 step: the sampling, attention and merge launches,
-// unless SANTAPP_DECODE_LAUNCH=fused asks for all of them in one launch
-// (read once per process).
-bool fused_wanted() {
-    static const bool fused = [] {
-        const char* e = getenv("SANTAPP_DECODE_LAUNCH");
-        return e != nullptr && strcmp(e, "fused") == 0;
-    }();
-    return fused;
-}
+bool fused_wanted() { return launch_mode() == LaunchMode::kFused; }
 
 santapp_status check_suffix(const void* sK, const void* sV, int T, int& stride) {
     if (T < 0) return fail(SANTAPP_EINVAL, "T must be >= 0");
@@ -706,8 +769,9 @@ santapp_status santapp_decode(const santapp_teams* t, const float* q, const void
     const int Kp = std::min(K, t->M);
     const bool dense = Kp == t->M;
     if (!dense && t->M > kMaxTeams) return fail(SANTAPP_ELIMIT, "%d teams per KV head exceed %d", t->M, kMaxTeams);
-    const DecodeLayout L = dense ? dense_layout(t->B, Hq, t->Hkv, t->N, T, t->d, t->cus)
-                                 : decode_layout(t->B, Hq, t->Hkv, T, t->d, t->M, Kp, t->cap.data(), t->cus);
+    const DecodeLayout L = dense ? dense_layout(t->B, Hq, t->Hkv, t->N, T, t->d, t->cus, t->dtype)
+                                 : decode_layout(t->B, Hq, t->Hkv, T, t->d, t->M, Kp, t->cap.data(), t->cus,
+                                                 t->dtype);
     if (!workspace || ws_bytes < L.total)
         return fail(SANTAPP_EWORKSPACE, "workspace of %zu bytes needed (got %zu)", L.total, ws_bytes);
     hipStream_t s = static_cast<hipStream_t>(stream);
@@ -846,7 +910,7 @@ santapp_status santapp_dense_decode(const float* q, const void* K, const void* V
     if (d != 64 && d != 128) return fail(SANTAPP_ELIMIT, "head dim %d not supported (64 or 128)", d);
     if (!(scale >= 0.0) || !isfinite(scale)) return fail(SANTAPP_EINVAL, "scale must be finite and >= 0");
     if (scale == 0.0) scale = 1.0 / sqrt(static_cast<double>(d));
-    const DecodeLayout L = dense_layout(B, Hq, Hkv, N, T, d, device_cus());
+    const DecodeLayout L = dense_layout(B, Hq, Hkv, N, T, d, device_cus(), dtype);
     if (!workspace || ws_bytes < L.total)
         return fail(SANTAPP_EWORKSPACE, "workspace of %zu bytes needed (got %zu)", L.total, ws_bytes);
     DecodeArgs A{};

@@ -61,7 +61,7 @@ constexpr int kWaves = kThreads / kWave;
 static_assert(kWaves == 8, "block scans read eight wave totals");
 constexpr int kFineBits = 16;       // value-histogram resolution of the general sampler
 constexpr int kPlanRecs = kThreads; // union teams of one plan pass
-constexpr int kPlanUnits = 4096;    // units of a plan pass resolved through an LDS table
+constexpr int kPlanUnits = 3072;    // units of a plan pass resolved through an LDS table
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNeg = -1.0e30f;    // logit of a row that carries no weight
 constexpr float kEmpty = -1.0e29f;  // states with a maximum below this hold no row
@@ -150,6 +150,37 @@ __device__ __forceinline__ void store_f4_coherent(float* p, float4 v) {
 __device__ __forceinline__ float4 load_f4_coherent(const float* p) {
     const float2 a = load_f2_coherent(p), b = load_f2_coherent(p + 2);
     return make_float4(a.x, a.y, b.x, b.y);
+}
+
+// 16-byte and 8-byte device-coherent accesses through a buffer resource
+// (cache policy sc1: a store writes through to memory, a load never returns a
+// copy cached in this XCD's L2).  The resource is built from a wave-uniform
+// base and covers `bytes` bytes; accesses outside it read zero and store
+// nothing.
+typedef unsigned u32x4v __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2v __attribute__((ext_vector_type(2)));
+constexpr int kCoherentPolicy = 16;  // sc1
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t coherent_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes), 0x00020000);
+}
+__device__ __forceinline__ u32x4v load16_coherent(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<int>(off), 0, kCoherentPolicy);
+}
+__device__ __forceinline__ void store16_coherent(__amdgpu_buffer_rsrc_t r, uint32_t off, u32x4v x) {
+    __builtin_amdgcn_raw_buffer_store_b128(x, r, static_cast<int>(off), 0, kCoherentPolicy);
+}
+__device__ __forceinline__ u32x2v load8_coherent(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b64(r, static_cast<int>(off), 0, kCoherentPolicy);
+}
+__device__ __forceinline__ void store8_coherent(__amdgpu_buffer_rsrc_t r, uint32_t off, u32x2v x) {
+    __builtin_amdgcn_raw_buffer_store_b64(x, r, static_cast<int>(off), 0, kCoherentPolicy);
+}
+__device__ __forceinline__ uint32_t load_u32_coherent(const uint32_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_u32_coherent(uint32_t* p, uint32_t x) {
+    __hip_atomic_store(p, x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Thread 0 polls a counter until it reaches `target` (bounded); returns
@@ -975,29 +1006,12 @@ struct PlanLds {
     int flag[4];
 };
 
-// Pass `base` of pair p's plan: the teams base + t PT + k of thread t (their
-// sizes and begins sz / bg loaded by the caller).  Returns (union teams,
-// units, rows) of the pass; the records are in place on return.
-template <int PT, bool COHERENT>
-__device__ int3 plan_pass(const DecodeArgs& a, const Views& v, int p, int base, const int (&sz)[PT], const int (&bg)[PT],
-                          PlanLds& P) {
-    const int tid = threadIdx.x, G = a.G, M = a.M;
-    const int b = p / a.Hkv, kv = p - b * a.Hkv;
-    const size_t hq0 = static_cast<size_t>(b) * a.Hq + kv * G;
-    // the heads' sample words that hold this thread's teams (PT divides 64)
-    static_assert(64 % PT == 0, "a thread's teams share one sample word");
-    const int g0 = base + tid * PT;
-    int hm[PT];
-#pragma unroll
-    for (int k = 0; k < PT; ++k) hm[k] = 0;
-    if (g0 < M) {
-        for (int h = 0; h < G; ++h) {
-            const uint64_t* wp = v.sbits + (hq0 + h) * a.lay.swords + (g0 >> 6);
-            const uint64_t wd = COHERENT ? load_u64_coherent(wp) : *wp;
-#pragma unroll
-            for (int k = 0; k < PT; ++k) hm[k] |= static_cast<int>((wd >> ((g0 + k) & 63)) & 1ull) << h;
-        }
-    }
+// The records of one plan pass from this thread's teams g0 .. g0 + PT - 1:
+// their head masks hm (cleared here beyond the table), sizes and packed
+// begins.  Returns (union teams, units, rows) of the pass; the records are in
+// place on return.
+template <int PT>
+__device__ int3 plan_records(int g0, int M, int (&hm)[PT], const int (&sz)[PT], const int (&bg)[PT], PlanLds& P) {
     int nck[PT], lf = 0, lnc = 0, lrows = 0;
 #pragma unroll
     for (int k = 0; k < PT; ++k) {
@@ -1024,6 +1038,32 @@ __device__ int3 plan_pass(const DecodeArgs& a, const Views& v, int p, int base, 
     }
     __syncthreads();
     return make_int3(tot[0], tot[1], tot[2]);
+}
+
+// Pass `base` of pair p's plan: the teams base + t PT + k of thread t (their
+// sizes and begins sz / bg loaded by the caller), head masks from the heads'
+// sample words in the workspace.
+template <int PT, bool COHERENT>
+__device__ int3 plan_pass(const DecodeArgs& a, const Views& v, int p, int base, const int (&sz)[PT], const int (&bg)[PT],
+                          PlanLds& P) {
+    const int tid = threadIdx.x, G = a.G, M = a.M;
+    const int b = p / a.Hkv, kv = p - b * a.Hkv;
+    const size_t hq0 = static_cast<size_t>(b) * a.Hq + kv * G;
+    // the heads' sample words that hold this thread's teams (PT divides 64)
+    static_assert(64 % PT == 0, "a thread's teams share one sample word");
+    const int g0 = base + tid * PT;
+    int hm[PT];
+#pragma unroll
+    for (int k = 0; k < PT; ++k) hm[k] = 0;
+    if (g0 < M) {
+        for (int h = 0; h < G; ++h) {
+            const uint64_t* wp = v.sbits + (hq0 + h) * a.lay.swords + (g0 >> 6);
+            const uint64_t wd = COHERENT ? load_u64_coherent(wp) : *wp;
+#pragma unroll
+            for (int k = 0; k < PT; ++k) hm[k] |= static_cast<int>((wd >> ((g0 + k) & 63)) & 1ull) << h;
+        }
+    }
+    return plan_records<PT>(g0, M, hm, sz, bg, P);
 }
 
 // Unit i (0-based within the pass) of a pass with `teams` union teams and
@@ -1147,11 +1187,94 @@ __device__ __forceinline__ bool walk_units(const DecodeArgs& a, const Views& v, 
 }
 
 // ---------------------------------------------------------------------------
+// Single-launch step: the selection of every head of the pair in LDS.
+// ---------------------------------------------------------------------------
+constexpr int kStepSelWords = kStepMaxTeams / 64;
+
+// Head h's sample as 64-team words (bit g % 64 of word g / 64), the count of
+// sampled teams before each word, log c of its sampled teams in team order,
+// and per team the mask of the heads that sampled it; `ok` is cleared when a
+// head's published scores did not all arrive.
+struct StepSel {
+    uint64_t sel[kMaxGroup][kStepSelWords];
+    int pre[kMaxGroup][kStepSelWords];
+    float lc[kMaxGroup][kStepMaxKp];
+    uint32_t hm[kStepMaxTeams / 4];  // byte g % 4 of word g / 4: the heads that sampled team g
+    int ok;
+    int pad[3];
+};
+
+// log c of team g for head h (g sampled by h).
+__device__ __forceinline__ float step_logc(const StepSel& SS, int h, int g) {
+    const int wd = g >> 6;
+    const uint64_t w = SS.sel[h][wd];
+    const int r = SS.pre[h][wd] + static_cast<int>(__popcll(w & ((1ull << (g & 63)) - 1ull)));
+    return SS.lc[h][min(r, kStepMaxKp - 1)];
+}
+
+// The pair's units for the single-launch step: as walk_units in the split
+// launch, with the heads' samples taken from LDS and the first pass's team
+// sizes and begins from the LDS copy s_tab (size, begin per team) made when
+// the step started (later passes read the table in memory).
+template <typename T, bool DENSE, int PT, typename Run>
+__device__ __forceinline__ bool step_walk_units(const DecodeArgs& a, int p, int iw, char* plan_lds, const StepSel* SS,
+                                                const int* s_tab, Run&& run) {
+    PlanLds& P = *reinterpret_cast<PlanLds*>(plan_lds);
+    const int nsuf = (a.T + kUnitRows - 1) / kUnitRows;
+    auto by_index = [&](int u) { return index_unit<T>(a, p, nsuf, u); };
+    if (DENSE) {
+        run(0, nsuf, by_index, false);
+        run(nsuf, nsuf + (a.N + kUnitRows - 1) / kUnitRows, by_index, false);
+        return true;
+    }
+    const int tid = threadIdx.x, M = a.M;
+    const size_t tb0 = static_cast<size_t>(p) * M;
+    int run_u = nsuf, run_teams = 0, run_rows = 0;
+    for (int base = 0; base < M; base += kThreads * PT) {
+        const int g0 = base + tid * PT;
+        int sz[PT], bg[PT], hm[PT];
+#pragma unroll
+        for (int k = 0; k < PT; ++k) {
+            const int g = min(g0 + k, M - 1);
+            if (base == 0) {
+                sz[k] = s_tab[2 * g];
+                bg[k] = s_tab[2 * g + 1];
+            } else {
+                sz[k] = a.team_size[tb0 + g];
+                bg[k] = a.team_begin[tb0 + g];
+            }
+            hm[k] = 0;
+        }
+        if (g0 < M) {
+#pragma unroll
+            for (int k = 0; k < PT; ++k) {
+                const int g = min(g0 + k, M - 1);
+                hm[k] = static_cast<int>((SS->hm[g >> 2] >> (8 * (g & 3))) & 0xffu);
+            }
+        }
+        const int3 t = plan_records<PT>(g0, M, hm, sz, bg, P);
+        // the suffix units come first in the first pass's run
+        const int lo = base == 0 ? 0 : run_u, first = run_u;
+        run(lo, run_u + t.y,
+            [&](int u) { return u < first ? by_index(u) : plan_unit<T>(a, P, p, u - first, t.x, t.y); }, false);
+        run_u += t.y;
+        run_teams += t.x;
+        run_rows += t.z;
+        if (base + kThreads * PT < M) __syncthreads();  // the records are rewritten by the next pass
+    }
+    if (iw == 0 && tid == 0) {
+        if (a.dbg_uteams) a.dbg_uteams[p] = run_teams;
+        if (a.dbg_urows) a.dbg_urows[p] = run_rows;
+    }
+    return SS->ok != 0;
+}
+
+// ---------------------------------------------------------------------------
 // Phase B for bf16 rows.
 // ---------------------------------------------------------------------------
-template <int D, bool DENSE, bool FUSED, int PT>
+template <int D, bool DENSE, bool FUSED, int PT, bool STEP = false>
 __device__ void attend_mfma(const DecodeArgs& a, const Views& v, int p, int iw, int nwp, char* t0, char* t1,
-                            char* misc) {
+                            char* misc, const StepSel* SS = nullptr, const int* s_tab = nullptr) {
     using QKT = QK<bf16_t, D>;
     using VT = VTile<D>;
     constexpr int NF = QKT::KB;         // K fragments per 16-row tile
@@ -1225,8 +1348,12 @@ __device__ void attend_mfma(const DecodeArgs& a, const Views& v, int p, int iw, 
         float cr = 0.f;
         const int h = lane & 7;
         if (!DENSE && U.g >= 0 && ((U.hmask >> h) & 1)) {
-            const float* src = v.lc + (hq0 + h) * a.M + U.g;
-            cr = FUSED ? load_f32_coherent(src) : *src;
+            if constexpr (STEP) {
+                cr = step_logc(*SS, h, U.g);
+            } else {
+                const float* src = v.lc + (hq0 + h) * a.M + U.g;
+                cr = FUSED ? load_f32_coherent(src) : *src;
+            }
         }
         return cr;
     };
@@ -1323,7 +1450,11 @@ __device__ void attend_mfma(const DecodeArgs& a, const Views& v, int p, int iw, 
         __builtin_amdgcn_s_waitcnt(0);
     };
 
-    const bool ok = walk_units<bf16_t, DENSE, FUSED, PT>(a, v, p, iw, plan_lds, run);
+    bool ok;
+    if constexpr (STEP)
+        ok = step_walk_units<bf16_t, DENSE, PT>(a, p, iw, plan_lds, SS, s_tab, run);
+    else
+        ok = walk_units<bf16_t, DENSE, FUSED, PT>(a, v, p, iw, plan_lds, run);
 
     // the wave's state per head, in canonical form, over the (now free) tiles
     char* const lds = t0;
@@ -1512,6 +1643,7 @@ __device__ void merge_head(const DecodeArgs& a, const float* part_p, int p, int 
     float mx = kNeg, L = 0.f;
     float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
     bool nan = false;
+    const __amdgpu_buffer_rsrc_t rs = coherent_rsrc(part_p, static_cast<uint32_t>(nwp) * G * SS * 4u);
     for (int w0 = sl; w0 < nwp; w0 += NSL * KL) {
         float2 ml[KL];
         float4 x[KL];
@@ -1521,9 +1653,18 @@ __device__ void merge_head(const DecodeArgs& a, const float* part_p, int p, int 
             ml[k] = make_float2(kNeg, 0.f);
             x[k] = make_float4(0.f, 0.f, 0.f, 0.f);
             if (w < nwp) {
-                const float* st = part_p + (static_cast<size_t>(w) * G + h) * SS;
-                ml[k] = COHERENT ? load_f2_coherent(st + D) : *reinterpret_cast<const float2*>(st + D);
-                x[k] = COHERENT ? load_f4_coherent(st + 4 * dq) : reinterpret_cast<const float4*>(st)[dq];
+                const uint32_t off = static_cast<uint32_t>((w * G + h) * SS) * 4u;
+                if (COHERENT) {
+                    const u32x2v m2 = load8_coherent(rs, off + 4u * D);
+                    const u32x4v x4 = load16_coherent(rs, off + 16u * dq);
+                    ml[k] = make_float2(__uint_as_float(m2.x), __uint_as_float(m2.y));
+                    x[k] = make_float4(__uint_as_float(x4.x), __uint_as_float(x4.y), __uint_as_float(x4.z),
+                                       __uint_as_float(x4.w));
+                } else {
+                    const float* st = part_p + (static_cast<size_t>(w) * G + h) * SS;
+                    ml[k] = *reinterpret_cast<const float2*>(st + D);
+                    x[k] = reinterpret_cast<const float4*>(st)[dq];
+                }
             }
         }
 #pragma unroll
@@ -1635,6 +1776,691 @@ __device__ void combine_and_merge(const DecodeArgs& a, const Views& v, int p, in
         }
         __syncthreads();  // s_acc / s_ml are reused
     }
+}
+
+// ===========================================================================
+// Single-launch step.  One launch of B Hkv nwp workgroups, nwp per (b, kv)
+// pair, all resident at once (one per compute unit):
+//   1. routing, split over the pair's workgroups: workgroup iw takes the
+//      pair's teams [iw S, iw S + S) and computes, for every query head of the
+//      group, phi_g = log n_g + scale q.l_g in fp64, the head's Gumbel variate
+//      and Y_g = phi_g + G_g; it publishes Y's order key and phi (fp32) as
+//      tagged words;
+//   2. selection, redundantly in every workgroup of the pair (wave h for head
+//      h): the wave reads the head's M keys once all carry this call's tag,
+//      finds tau (the key of rank K) and the sample (ties to the lower team),
+//      and log c of its sampled teams; every workgroup of the pair holds the
+//      same selection, so no further exchange is needed;
+//   3. the read plan (the union of the heads' samples in team order) and the
+//      attention over the workgroup's share of the units, as in the split
+//      launch;
+//   4. each workgroup publishes one tagged state per head; workgroup h of the
+//      pair merges head h once every state of it carries the tag, and the
+//      merger of head 0 advances the pair's epoch.
+// ===========================================================================
+struct StepViews {
+    uint32_t* epoch;  // [BH]
+    uint64_t* xk;     // [BH, G, M, 2] tagged order keys of Y
+    uint64_t* xp;     // [BH, G, M] tagged phi (fp32)
+    float* part;      // [BH, maxwp, G] published states of step_state_bytes(d) each
+};
+
+__device__ __forceinline__ StepViews step_views(const DecodeArgs& a) {
+    StepViews v;
+    v.epoch = reinterpret_cast<uint32_t*>(a.ws + a.lay.epoch);
+    v.xk = reinterpret_cast<uint64_t*>(a.ws + a.lay.xk);
+    v.xp = reinterpret_cast<uint64_t*>(a.ws + a.lay.xp);
+    v.part = reinterpret_cast<float*>(a.ws + a.lay.part);
+    return v;
+}
+
+// Teams of a workgroup's routing slice: a multiple of four (whole Philox
+// blocks), the pair's M teams covered by its nwp workgroups.
+__device__ __forceinline__ int step_slice(int M, int nwp) { return 4 * ((M + 4 * nwp - 1) / (4 * nwp)); }
+
+// Phase 1 for workgroup iw of pair p: the slice's teams in chunks of 64.
+// Octet o (threads 8 o .. 8 o + 7) takes team c0 + o: each lane holds d / 8
+// dims of the routing key (route_issue), every head's dot product is summed
+// over the octet (fp64, exact products), and lane h keeps phi of head h
+// (route_finish); lane h also draws the Gumbel variate of (h, team) while the
+// routing keys load (route_gumbel).
+template <int D>
+struct RouteRegs {
+    static constexpr int LPL = RepLanes<bf16_t, D>::LPL;
+    uint4 raw[LPL];
+    double ln;
+};
+
+template <int D>
+__device__ __forceinline__ RouteRegs<D> route_issue(const DecodeArgs& a, int p, int c0, int nt) {
+    using RL = RepLanes<bf16_t, D>;
+    RouteRegs<D> r;
+    const int o = threadIdx.x >> 3, sub = threadIdx.x & 7;
+    r.ln = 0.0;
+#pragma unroll
+    for (int l = 0; l < RL::LPL; ++l) r.raw[l] = make_uint4(0, 0, 0, 0);
+    if (o < nt) {
+        const size_t g = static_cast<size_t>(p) * a.M + c0 + o;
+        const uint4* src = reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(a.reps) + g * D + sub * RL::EPL);
+#pragma unroll
+        for (int l = 0; l < RL::LPL; ++l) r.raw[l] = load_stream(src + l);
+        r.ln = a.log_n[g];
+    }
+    return r;
+}
+
+// The Gumbel variate of (head sub, team c0 + o) for lane sub < G of octet o
+// (0 elsewhere): word (c0 + o) % 4 of the Philox block at counter
+// ((c0 + o) / 4, h, b, step), key (seed, 0).
+__device__ __forceinline__ double route_gumbel(const DecodeArgs& a, int p, int c0, int nt) {
+    const int G = a.G, b = p / a.Hkv, kv = p - b * a.Hkv;
+    const int o = threadIdx.x >> 3, h = threadIdx.x & 7;
+    if (o >= nt || h >= G) return 0.0;
+    const int g = c0 + o;
+    const u64x4 r = philox4x64_10(static_cast<uint64_t>(g >> 2), static_cast<uint64_t>(kv * G + h),
+                                  static_cast<uint64_t>(b), a.step, a.seed, 0);
+    const int e = g & 3;
+    return gumbel_of_word(e == 0 ? r.v[0] : e == 1 ? r.v[1] : e == 2 ? r.v[2] : r.v[3]);
+}
+
+template <int D>
+__device__ __forceinline__ void route_finish(const DecodeArgs& a, int p, int c0, int nt, uint32_t tag,
+                                             const RouteRegs<D>& r, const double* s_qd, double gum,
+                                             __amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rp) {
+    using RL = RepLanes<bf16_t, D>;
+    constexpr int EPL = RL::EPL;
+    const int G = a.G, M = a.M;
+    const int o = threadIdx.x >> 3, sub = threadIdx.x & 7;
+    if (o >= nt) return;
+    double phi = 0.0;
+#pragma unroll
+    for (int h = 0; h < kMaxGroup; ++h) {
+        if (h < G) {  // uniform
+            const double* qh = s_qd + h * D + sub * EPL;
+            double a0 = 0.0, a1 = 0.0;
+#pragma unroll
+            for (int e = 0; e < EPL; e += 2) {
+                a0 = fma(qh[e], static_cast<double>(RL::elem(r.raw, e)), a0);
+                a1 = fma(qh[e + 1], static_cast<double>(RL::elem(r.raw, e + 1)), a1);
+            }
+            const double sum = row8_sum(a0 + a1);
+            if (sub == h) phi = r.ln + a.scale * sum;
+        }
+    }
+    if (sub < G) {
+        const int g = c0 + o, h = sub;
+        const double y = phi + gum;
+        const uint64_t key = order_key(y);
+        const uint32_t slot = static_cast<uint32_t>(h) * M + g;
+        store16_coherent(rk, slot * 16u, u32x4v{static_cast<uint32_t>(key >> 32), tag, static_cast<uint32_t>(key), tag});
+        store8_coherent(rp, slot * 8u, u32x2v{__float_as_uint(static_cast<float>(phi)), tag});
+        const int b = p / a.Hkv, kv = p - b * a.Hkv;
+        const size_t bq = static_cast<size_t>(b) * a.Hq + kv * G + h;
+        if (a.dbg_phi) a.dbg_phi[bq * M + g] = phi;
+        if (a.dbg_Y) a.dbg_Y[bq * M + g] = y;
+    }
+}
+
+__device__ __forceinline__ double readlane_f64(double v, int l) {
+    const long long b = __double_as_longlong(v);
+    const int lo = __builtin_amdgcn_readlane(static_cast<int>(b & 0xffffffff), l);
+    const int hi = __builtin_amdgcn_readlane(static_cast<int>(b >> 32), l);
+    return __longlong_as_double((static_cast<long long>(hi) << 32) | static_cast<unsigned>(lo));
+}
+
+// Routing of a slice of at most eight teams, in two roles that run at once:
+// waves 0-3 form the dot products (two teams per wave, 32 lanes per team, d /
+// 32 dims of the routing key and of every query head per lane, read directly;
+// a head's sum over the team's lanes in fp64 with exact products), wave 4
+// draws the slice's Gumbel variates (lane 8 t + h for head h of team t).
+// Both land in s_pg (phi [8][8], then the variates [8][8]); route_publish
+// forms Y after the workgroup barrier that follows.
+template <int D>
+__device__ __forceinline__ void route_split(const DecodeArgs& a, int p, int c0, int nt, double* s_pg) {
+    constexpr int EPL = D / 32;  // 4 (d = 128) or 2 (d = 64)
+    static_assert(EPL == 2 || EPL == 4, "two or four dims per lane");
+    const int lane = lane_id(), w = wave_id();
+    const int G = a.G, M = a.M, b = p / a.Hkv, kv = p - b * a.Hkv;
+    if (w < 4) {
+        if (2 * w >= nt) return;  // uniform
+        const int t = 2 * w + (lane >> 5), l = lane & 31;
+        const int g = c0 + min(t, nt - 1);
+        const size_t tg = static_cast<size_t>(p) * M + g;
+        // every load first (heads beyond G read head G - 1's dims)
+        const bf16_t* row = static_cast<const bf16_t*>(a.reps) + tg * D + l * EPL;
+        uint32_t kr[EPL / 2];
+        if constexpr (EPL == 4) {
+            const uint2 x = *reinterpret_cast<const uint2*>(row);
+            kr[0] = x.x;
+            kr[1] = x.y;
+        } else {
+            kr[0] = *reinterpret_cast<const uint32_t*>(row);
+        }
+        const double ln = a.log_n[tg];
+        const float* qg = a.q + (static_cast<size_t>(b) * a.Hq + kv * G) * D + l * EPL;
+        float qv[kMaxGroup][EPL];
+#pragma unroll
+        for (int h = 0; h < kMaxGroup; ++h) {
+            const float* qh = qg + min(h, G - 1) * D;
+            if constexpr (EPL == 4) {
+                const float4 x = *reinterpret_cast<const float4*>(qh);
+                qv[h][0] = x.x;
+                qv[h][1] = x.y;
+                qv[h][2] = x.z;
+                qv[h][3] = x.w;
+            } else {
+                const float2 x = *reinterpret_cast<const float2*>(qh);
+                qv[h][0] = x.x;
+                qv[h][1] = x.y;
+            }
+        }
+        double kd[EPL];
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) kd[e] = static_cast<double>((e & 1) ? bf16hi(kr[e >> 1]) : bf16lo(kr[e >> 1]));
+        const double lnA = readlane_f64(ln, 0), lnB = readlane_f64(ln, 32);
+#pragma unroll
+        for (int h = 0; h < kMaxGroup; ++h) {
+            if (h < G) {  // uniform
+                double part = static_cast<double>(qv[h][0]) * kd[0];
+#pragma unroll
+                for (int e = 1; e < EPL; ++e) part = fma(static_cast<double>(qv[h][e]), kd[e], part);
+                part = row16_sum(part);
+                const double sA = readlane_f64(part, 0) + readlane_f64(part, 16);
+                const double sB = readlane_f64(part, 32) + readlane_f64(part, 48);
+                if (lane == 0) {
+                    s_pg[(2 * w) * 8 + h] = lnA + a.scale * sA;
+                    s_pg[(2 * w + 1) * 8 + h] = lnB + a.scale * sB;
+                }
+            }
+        }
+    } else if (w == 4) {
+        const int t = lane >> 3, h = lane & 7;
+        if (t < nt && h < G) {
+            const int g = c0 + t;
+            const u64x4 r = philox4x64_10(static_cast<uint64_t>(g >> 2), static_cast<uint64_t>(kv * G + h),
+                                          static_cast<uint64_t>(b), a.step, a.seed, 0);
+            const int e = g & 3;
+            s_pg[64 + t * 8 + h] = gumbel_of_word(e == 0 ? r.v[0] : e == 1 ? r.v[1] : e == 2 ? r.v[2] : r.v[3]);
+        }
+    }
+}
+
+// Y = phi + G of the slice's (team, head) items (lane 8 t + h of wave 0),
+// published as tagged words with phi.
+__device__ __forceinline__ void route_publish(const DecodeArgs& a, int p, int c0, int nt, uint32_t tag,
+                                              const double* s_pg, __amdgpu_buffer_rsrc_t rk,
+                                              __amdgpu_buffer_rsrc_t rp) {
+    const int lane = lane_id();
+    const int t = lane >> 3, h = lane & 7;
+    if (wave_id() != 0 || t >= nt || h >= a.G) return;
+    const int G = a.G, M = a.M, b = p / a.Hkv, kv = p - b * a.Hkv;
+    const int g = c0 + t;
+    const double phi = s_pg[t * 8 + h];
+    const double y = phi + s_pg[64 + t * 8 + h];
+    const uint64_t key = order_key(y);
+    const uint32_t slot = static_cast<uint32_t>(h) * M + g;
+    store16_coherent(rk, slot * 16u, u32x4v{static_cast<uint32_t>(key >> 32), tag, static_cast<uint32_t>(key), tag});
+    store8_coherent(rp, slot * 8u, u32x2v{__float_as_uint(static_cast<float>(phi)), tag});
+    const size_t bq = static_cast<size_t>(b) * a.Hq + kv * G + h;
+    if (a.dbg_phi) a.dbg_phi[bq * M + g] = phi;
+    if (a.dbg_Y) a.dbg_Y[bq * M + g] = y;
+}
+
+// LDS of one wave's selection: a 256-bin histogram and up to 64 candidates.
+struct WaveSel {
+    uint32_t hist[256];
+    uint64_t cand[kWave];
+};
+
+// Key of rank `want` (0-based, descending) among the wave's keys (key j of
+// lane l is team 64 j + l; teams >= M do not count), by an exact radix over
+// the 64-bit keys, eight bits at a time from the top; `above` receives the
+// count of keys strictly greater.
+template <int KPL>
+__device__ uint64_t wave_rank_exact(const uint64_t (&k)[KPL], int M, int want, WaveSel& W, int& above) {
+    const int lane = lane_id();
+    uint64_t prefix = 0, pmask = 0;
+    above = 0;
+    int cnt = 0;
+    for (int sh = 56;; sh -= 8) {  // uniform
+        reinterpret_cast<uint4*>(W.hist)[lane] = make_uint4(0, 0, 0, 0);
+        lds_order();
+#pragma unroll
+        for (int j = 0; j < KPL; ++j)
+            if (64 * j + lane < M && (k[j] & pmask) == prefix) atomicAdd(&W.hist[(k[j] >> sh) & 255], 1u);
+        lds_order();
+        int hi;
+        const int dg = hist_select(W.hist, want, hi, cnt);
+        lds_order();
+        want -= hi;
+        above += hi;
+        prefix |= static_cast<uint64_t>(dg) << sh;
+        pmask |= 0xffull << sh;
+        if (cnt == 1 || sh == 0) break;
+    }
+    if (cnt == 1) {  // the one key with this prefix
+        uint64_t r = 0;
+#pragma unroll
+        for (int j = 0; j < KPL; ++j) {
+            const bool m = 64 * j + lane < M && (k[j] & pmask) == prefix;
+            const uint64_t bal = __ballot(m);
+            if (bal) r = readlane(k[j], __ffsll(static_cast<unsigned long long>(bal)) - 1);
+        }
+        return r;
+    }
+    return prefix;  // every bit fixed: equal keys
+}
+
+// Minimum / maximum of a float over the wave (rotations within each 16-lane
+// row, then the four rows' results); wave-uniform.
+template <bool kMin>
+__device__ __forceinline__ float wave_ext_f(float v) {
+    auto op = [](float x, float y) { return kMin ? fminf(x, y) : fmaxf(x, y); };
+    v = op(v, dpp_f32<0x128>(v));
+    v = op(v, dpp_f32<0x124>(v));
+    v = op(v, dpp_f32<0x122>(v));
+    v = op(v, dpp_f32<0x121>(v));
+    const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+    const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+    const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+    const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+    return op(op(r0, r1), op(r2, r3));
+}
+
+// Key of rank `want` among the wave's keys, and the count above it: a value
+// histogram of 256 bins over [min Y, max Y] with Y rounded to fp32 (rounding
+// keeps the order, so a bin above another holds only larger or equal keys),
+// then a direct ranking of the exact keys in the bin that holds rank `want`;
+// the exact radix where that bin holds more than 64 keys, the keys span no
+// finite fp32 range (absent teams) or all are equal.
+template <int KPL>
+__device__ uint64_t wave_rank(const uint64_t (&k)[KPL], int M, int want, WaveSel& W, int& above) {
+    const int lane = lane_id();
+    float y[KPL];
+    float lo = __builtin_inff(), hi = -__builtin_inff();
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) {
+        y[j] = static_cast<float>(key_value(k[j]));
+        if (64 * j + lane < M) {
+            lo = fminf(lo, y[j]);
+            hi = fmaxf(hi, y[j]);
+        }
+    }
+    lo = wave_ext_f<true>(lo);
+    hi = wave_ext_f<false>(hi);
+    const float range = hi - lo;
+    if (!(range > 0.f) || !(range < 3.0e38f)) return wave_rank_exact<KPL>(k, M, want, W, above);
+    const float fs = 255.99f / range;
+    reinterpret_cast<uint4*>(W.hist)[lane] = make_uint4(0, 0, 0, 0);
+    lds_order();
+    int bin[KPL];
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) {
+        bin[j] = 64 * j + lane < M ? static_cast<int>(fminf(255.f, (y[j] - lo) * fs)) : -1;
+        if (bin[j] >= 0) atomicAdd(&W.hist[bin[j]], 1u);
+    }
+    lds_order();
+    int hcnt, cnt;
+    const int sb = hist_select(W.hist, want, hcnt, cnt);
+    lds_order();
+    if (cnt > kWave) return wave_rank_exact<KPL>(k, M, want, W, above);
+    int n = 0;
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) {
+        const bool in = bin[j] == sb;
+        const uint64_t bal = __ballot(in);
+        if (in) W.cand[n + static_cast<int>(__popcll(bal & lanemask_lt()))] = k[j];
+        n += static_cast<int>(__popcll(bal));
+    }
+    lds_order();
+    const int rest = want - hcnt;
+    const uint64_t mine = W.cand[min(lane, n - 1)];
+    int gt = 0, ge = 0;
+    for (int t = 0; t < n; ++t) {
+        const uint64_t o = readlane(mine, t);
+        gt += o > mine ? 1 : 0;
+        ge += o >= mine ? 1 : 0;
+    }
+    const bool owner = lane < n && gt <= rest && rest < ge;
+    const int src = __ffsll(static_cast<unsigned long long>(__ballot(owner))) - 1;
+    above = hcnt + readlane(gt, src);
+    return readlane(mine, src);
+}
+
+// Phase 2 for wave h (a query head of the pair): wait for the head's M
+// published keys and phis, select, and record the sample, its head bit in the
+// team masks and log c in SS.  Returns false when the words did not all
+// arrive within the spin limit.
+template <int KPL>
+__device__ bool step_select(const DecodeArgs& a, const StepViews& v, int p, int iw, uint32_t tag, WaveSel& W,
+                            StepSel& SS) {
+    const int lane = lane_id(), h = wave_id(), G = a.G, M = a.M, Kp = a.Kp;
+    const int b = p / a.Hkv, kv = p - b * a.Hkv;
+    const size_t hb = (static_cast<size_t>(p) * G + h) * M;
+    const __amdgpu_buffer_rsrc_t rk = coherent_rsrc(v.xk + 2 * hb, static_cast<uint32_t>(M) * 16u);
+    const __amdgpu_buffer_rsrc_t rp = coherent_rsrc(v.xp + hb, static_cast<uint32_t>(M) * 8u);
+    uint64_t k[KPL];
+    float ph[KPL];
+    uint32_t pend = 0;
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) {
+        k[j] = 0;
+        ph[j] = 0.f;
+        if (64 * j + lane < M) pend |= 1u << j;
+    }
+    // every key's words and its phi carry this call's tag (at most 16 keys'
+    // loads in flight)
+    constexpr int kBatch = KPL < 16 ? KPL : 16;
+    bool ok = true;
+    for (int it = 0;; ++it) {
+#pragma unroll
+        for (int j0 = 0; j0 < KPL; j0 += kBatch) {
+            u32x4v w[kBatch];
+            u32x2v f[kBatch];
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j) {
+                if ((pend >> (j0 + j)) & 1u) {
+                    const uint32_t g = static_cast<uint32_t>(64 * (j0 + j) + lane);
+                    w[j] = load16_coherent(rk, g * 16u);
+                    f[j] = load8_coherent(rp, g * 8u);
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j) {
+                if (((pend >> (j0 + j)) & 1u) && w[j].y == tag && w[j].w == tag && f[j].y == tag) {
+                    k[j0 + j] = (static_cast<uint64_t>(w[j].x) << 32) | w[j].z;
+                    ph[j0 + j] = __uint_as_float(f[j].x);
+                    pend &= ~(1u << (j0 + j));
+                }
+            }
+        }
+        if (__ballot(pend != 0) == 0) break;  // uniform
+        if (it >= kSpinLimit) {
+            ok = false;
+            break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+    int above;
+    const uint64_t tkey = wave_rank<KPL>(k, M, Kp, W, above);
+    const double tau = key_value(tkey);
+    // the sample: keys above tau, then keys equal to it in team order; log c
+    // of each sampled team (eq. method-inclusion) by the lane that holds it
+    int need = Kp - above;
+    const size_t bq = static_cast<size_t>(b) * a.Hq + kv * G + h;
+    int cum = 0;
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) {
+        const bool vj = 64 * j + lane < M;
+        uint64_t sb = __ballot(vj && k[j] > tkey);
+        if (need > 0) {  // uniform
+            uint64_t tb = __ballot(vj && k[j] == tkey);
+            while (need > 0 && tb) {
+                const uint64_t low = tb & (~tb + 1);
+                sb |= low;
+                tb ^= low;
+                --need;
+            }
+        }
+        if (lane == 0) {
+            SS.sel[h][j] = sb;
+            SS.pre[h][j] = cum;
+        }
+        if ((sb >> lane) & 1ull) {
+            // the team's head bit, and phi - tau staged by rank
+            const int g = 64 * j + lane;
+            atomicOr(&SS.hm[g >> 2], 1u << (h + 8 * (g & 3)));
+            const int rank = cum + static_cast<int>(__popcll(sb & lanemask_lt()));
+            if (rank < kStepMaxKp) {
+                SS.lc[h][rank] = static_cast<float>(static_cast<double>(ph[j]) - tau);
+                if (iw == 0 && a.dbg_sel) a.dbg_sel[bq * Kp + rank] = g;
+            }
+        }
+        cum += static_cast<int>(__popcll(sb));
+    }
+    // log c of the sampled teams, one per lane (eq. method-inclusion)
+    lds_order();
+    for (int r = lane; r < Kp; r += kWave) {
+        const float lcv = log_inclusion(SS.lc[h][r]);
+        SS.lc[h][r] = lcv;
+        if (iw == 0 && a.dbg_logc) a.dbg_logc[bq * Kp + r] = lcv;
+    }
+    if (iw == 0 && lane == 0 && a.dbg_tau) a.dbg_tau[bq] = tau;
+    return ok;
+}
+
+// Sum of a float over the wave (rotations within each 16-lane row, then the
+// four rows' sums); wave-uniform.
+__device__ __forceinline__ float wave_sum_dpp(float v) {
+    v = row16_sum(v);
+    const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+    const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+    const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+    const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+    return (r0 + r1) + (r2 + r3);
+}
+
+// Phase 4.  A published state (one per workgroup and head) is d / 2 + 1
+// 16-byte chunks: chunk c < d / 2 holds (acc[2c], tag, acc[2c + 1], tag), the
+// last (maximum, tag, mass, tag).  Each 8-byte half carries the tag, so a
+// reader that sees the tag in both halves of a chunk has the chunk's values
+// of this call, and no ordering between the chunks is needed.
+//
+// The workgroup combines its waves' states of each head (canonical form in
+// LDS) and publishes them.  Each (head, eighth of the dims) is then merged by
+// one wave of the pair: lane w reads state w (nwp <= 64) -- the eighth's value
+// chunks and the (maximum, mass) chunk -- until all carry the tag, and the
+// states are rescaled to the common maximum by wave sums.  The merger of
+// (head 0, first eighth) advances the pair's epoch once all its states carry
+// the tag (every workgroup of the pair has then read the epoch).
+template <int D>
+__device__ void step_publish_merge(const DecodeArgs& a, const StepViews& v, int p, int iw, int nwp, uint32_t tag,
+                                   char* lds) {
+    constexpr int NC = D / 2 + 1;  // chunks per state
+    constexpr int DW = D / kWaves; // dims per merging wave
+    const int tid = threadIdx.x, G = a.G, lane = lane_id(), wv = wave_id();
+    __syncthreads();
+    char* const part_p = reinterpret_cast<char*>(v.part) + static_cast<size_t>(p) * a.lay.maxwp * G * NC * 16;
+    const __amdgpu_buffer_rsrc_t rs = coherent_rsrc(part_p, static_cast<uint32_t>(a.lay.maxwp) * G * NC * 16u);
+    for (int i = tid; i < G * NC; i += kThreads) {
+        const int h = i / NC, c = i - h * NC;
+        float mx = kNeg;
+        bool nan = false;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) {
+            const float mw = wave_state(lds, w, h, D)[D];
+            nan = nan || mw != mw;
+            mx = fmaxf(mx, mw);
+        }
+        float x0 = 0.f, x1 = 0.f;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) {
+            const float* st = wave_state(lds, w, h, D);
+            const float mw = st[D];
+            const float wt = mw > kEmpty ? fast_exp2(mw - mx) : 0.f;
+            if (c < D / 2) {
+                x0 = fmaf(wt, st[2 * c], x0);
+                x1 = fmaf(wt, st[2 * c + 1], x1);
+            } else {
+                x1 = fmaf(wt, st[D + 1], x1);
+            }
+        }
+        if (c == D / 2) x0 = nan ? __builtin_nanf("") : mx;
+        store16_coherent(rs, static_cast<uint32_t>((iw * G + h) * NC + c) * 16u,
+                         u32x4v{__float_as_uint(x0), tag, __float_as_uint(x1), tag});
+    }
+    // merge tasks: task t = 8 h + c (head h, dims [c D / 8, (c + 1) D / 8)) runs
+    // on workgroup t mod nwp, wave (t / nwp) mod 8, so that the merge of a
+    // pair is spread over many compute units and each poll is small
+    for (int t = iw + wv * nwp; t < kWaves * G; t += kWaves * nwp) {
+        const int h = t / kWaves, c = t % kWaves;
+        const bool live = lane < nwp;
+        const uint32_t base = static_cast<uint32_t>((lane * G + h) * NC) * 16u;
+        float acc[DW], mw = kNeg, lw = 0.f;
+        uint32_t pend = live ? ((1u << (DW / 2 + 1)) - 1u) : 0u;  // bit DW / 2: the (maximum, mass) chunk
+#pragma unroll
+        for (int i = 0; i < DW; ++i) acc[i] = 0.f;
+        bool ok = true;
+        for (int it = 0;; ++it) {
+            u32x4v x[DW / 2 + 1];
+#pragma unroll
+            for (int k = 0; k <= DW / 2; ++k) {
+                const int cc = k < DW / 2 ? c * (DW / 2) + k : D / 2;
+                if ((pend >> k) & 1u) x[k] = load16_coherent(rs, base + 16u * cc);
+            }
+#pragma unroll
+            for (int k = 0; k <= DW / 2; ++k) {
+                if (((pend >> k) & 1u) && x[k].y == tag && x[k].w == tag) {
+                    if (k < DW / 2) {
+                        acc[2 * k] = __uint_as_float(x[k].x);
+                        acc[2 * k + 1] = __uint_as_float(x[k].z);
+                    } else {
+                        mw = __uint_as_float(x[k].x);
+                        lw = __uint_as_float(x[k].z);
+                    }
+                    pend &= ~(1u << k);
+                }
+            }
+            if (__ballot(pend != 0) == 0) break;  // uniform
+            if (it >= kSpinLimit) {
+                ok = false;
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+        const bool bad = !ok || __ballot(mw != mw) != 0;
+        const float m_all = wave_ext_f<false>(live ? mw : kNeg);
+        const float wt = live && mw > kEmpty ? fast_exp2(mw - m_all) : 0.f;
+        const float L = wave_sum_dpp(wt * lw);
+        const float inv = bad ? __builtin_nanf("") : 1.f / L;
+        const int b = p / a.Hkv, kv = p - b * a.Hkv;
+        float* const out = a.out + (static_cast<size_t>(b) * a.Hq + kv * G + h) * D + c * DW;
+        float r[DW];
+#pragma unroll
+        for (int i = 0; i < DW; ++i) r[i] = wave_sum_dpp(wt * acc[i]) * inv;
+        if (lane == 0) {
+#pragma unroll
+            for (int i = 0; i < DW; i += 4) *reinterpret_cast<float4*>(out + i) = make_float4(r[i], r[i + 1], r[i + 2], r[i + 3]);
+            if (t == 0) store_u32_coherent(v.epoch + p, tag);
+        }
+    }
+}
+
+// LDS of the single-launch step.  t0 and t1 hold the value tiles during the
+// attention; before it, t0 holds the widened queries, the Gumbel variates and
+// the waves' select scratch, and t1 the first plan pass's team table.
+template <int D>
+struct StepLds {
+    static constexpr int tiles = kWaves * VTile<D>::kBytes;
+    static constexpr int states = kWaves * kMaxGroup * (D + 4) * 4;
+    static constexpr int merge = 64 + kThreads * 16 + (kThreads / (D / 4)) * 8;
+    static constexpr int qd = kMaxGroup * D * 8;
+    static constexpr int gum = kMaxGroup * 64 * 8;
+    static constexpr int sel = kWaves * static_cast<int>(sizeof(WaveSel));
+    static constexpr int max2(int x, int y) { return x > y ? x : y; }
+    static constexpr int t0 = max2(max2(tiles, states), max2(merge, qd + gum + sel));
+    static constexpr int t1 = max2(tiles, 2 * kStepMaxTeams * 4);
+    static constexpr int plan_off = kWaves * 1024;
+    static constexpr int sel_off = (plan_off + static_cast<int>(sizeof(PlanLds)) + 15) / 16 * 16;
+    static constexpr int misc = sel_off + static_cast<int>(sizeof(StepSel));
+};
+
+template <int D, int KPL, bool DENSE>
+__global__ __launch_bounds__(kThreads, 1) void k_step(DecodeArgs a) {
+    using L = StepLds<D>;
+    static_assert(L::t0 + L::t1 + L::misc <= 160 * 1024, "the step's LDS fits one compute unit");
+    __shared__ __attribute__((aligned(16))) char s_t0[L::t0];
+    __shared__ __attribute__((aligned(16))) char s_t1[L::t1];
+    __shared__ __attribute__((aligned(16))) char s_misc[L::misc];
+    const StepViews v = step_views(a);
+    const PairSlot sl = pair_slot(blockIdx.x, gridDim.x, a.B * a.Hkv);
+    const int p = sl.p, iw = sl.iw, nwp = sl.nwp;
+    // the call's tag (epoch + 1) is formed where it is first needed, so that
+    // the epoch load does not hold up the loads issued after it
+    const uint32_t epoch = load_u32_coherent(v.epoch + p);
+    StepSel* const SS = reinterpret_cast<StepSel*>(s_misc + L::sel_off);
+    int* const s_tab = reinterpret_cast<int*>(s_t1);
+    const int tid = threadIdx.x;
+    // the plan passes take PT teams per thread when the heads' union fits one
+    // pass's records, else one
+    constexpr int PT = KPL >= 8 ? KPL / 8 : 1;
+    const bool wide = !DENSE && static_cast<long long>(a.G) * a.Kp <= kPlanRecs;
+    if constexpr (!DENSE) {
+        const int G = a.G, M = a.M;
+        const int b = p / a.Hkv, kv = p - b * a.Hkv;
+        double* const s_qd = reinterpret_cast<double*>(s_t0);
+        WaveSel* const s_ws = reinterpret_cast<WaveSel*>(s_t0 + L::qd);
+        const int S = step_slice(M, nwp);
+        const int t0 = iw * S, t1 = min(M, t0 + S);
+        const __amdgpu_buffer_rsrc_t rk = coherent_rsrc(v.xk + 2 * static_cast<size_t>(p) * G * M,
+                                                        static_cast<uint32_t>(G) * M * 16u);
+        const __amdgpu_buffer_rsrc_t rp = coherent_rsrc(v.xp + static_cast<size_t>(p) * G * M,
+                                                        static_cast<uint32_t>(G) * M * 8u);
+        // everything the routing needs is requested at once: the slice's
+        // routing keys, the queries and the first plan pass's table
+        const size_t tb0 = static_cast<size_t>(p) * M;
+        const int first = min(M, kThreads * (wide ? PT : 1));
+        int tsz[PT], tbg[PT];
+#pragma unroll
+        for (int i = 0; i < PT; ++i) {
+            const int g = min(tid + i * kThreads, M - 1);
+            tsz[i] = a.team_size[tb0 + g];
+            tbg[i] = a.team_begin[tb0 + g];
+        }
+        const bool by_wave = S <= kWaves;  // uniform: the split routing of at most eight teams
+        RouteRegs<D> rr;
+        double gum = 0.0;
+        if (by_wave) {
+            route_split<D>(a, p, t0, max(0, t1 - t0), s_qd);
+        } else {
+            rr = route_issue<D>(a, p, t0, max(0, min(64, t1 - t0)));
+            constexpr int kQ = kMaxGroup * D / kThreads;
+            float qv[kQ];
+            const float* qg = a.q + (static_cast<size_t>(b) * a.Hq + kv * G) * D;
+#pragma unroll
+            for (int i = 0; i < kQ; ++i) qv[i] = tid + i * kThreads < G * D ? qg[tid + i * kThreads] : 0.f;
+            gum = route_gumbel(a, p, t0, min(64, t1 - t0));
+#pragma unroll
+            for (int i = 0; i < kQ; ++i)
+                if (tid + i * kThreads < G * D) s_qd[tid + i * kThreads] = static_cast<double>(qv[i]);
+        }
+#pragma unroll
+        for (int i = 0; i < PT; ++i) {
+            const int g = tid + i * kThreads;
+            if (g < first) {
+                s_tab[2 * g] = tsz[i];
+                s_tab[2 * g + 1] = tbg[i];
+            }
+        }
+        for (int i = tid; i < (M + 3) / 4; i += kThreads) SS->hm[i] = 0;
+        if (tid == 0) SS->ok = 1;
+        __syncthreads();
+        const uint32_t tag = epoch + 1u;
+        if (by_wave) {
+            route_publish(a, p, t0, max(0, t1 - t0), tag, s_qd, rk, rp);
+        } else {
+            for (int c0 = t0; c0 < t1; c0 += 64) {  // uniform
+                const int nt = min(64, t1 - c0);
+                if (c0 > t0) {
+                    rr = route_issue<D>(a, p, c0, nt);
+                    gum = route_gumbel(a, p, c0, nt);
+                }
+                route_finish<D>(a, p, c0, nt, tag, rr, s_qd, gum, rk, rp);
+            }
+        }
+        if (wave_id() < G) {
+            const bool ok = step_select<KPL>(a, v, p, iw, tag, s_ws[wave_id()], *SS);
+            if (!ok && lane_id() == 0) SS->ok = 0;
+        }
+        __syncthreads();
+    }
+    const uint32_t tag = epoch + 1u;
+    const Views none{};
+    if (wide)
+        attend_mfma<D, DENSE, false, PT, true>(a, none, p, iw, nwp, s_t0, s_t1, s_misc, SS, s_tab);
+    else
+        attend_mfma<D, DENSE, false, 1, true>(a, none, p, iw, nwp, s_t0, s_t1, s_misc, SS, s_tab);
+    step_publish_merge<D>(a, v, p, iw, nwp, tag, s_t0);
 }
 
 template <typename T, int D, int HK>
@@ -1766,8 +2592,23 @@ hipError_t decode_sampled(const DecodeArgs& a, hipStream_t s) {
     return e;
 }
 
+// The single-launch step (bf16): keys per lane of the selecting waves by the
+// team count.
+template <int D>
+hipError_t decode_step(const DecodeArgs& a, hipStream_t s) {
+    const int grid = a.lay.nwg;
+    if (a.dense) return launch_one(a, k_step<D, 2, true>, grid, true, s);
+    if (a.M <= 128) return launch_one(a, k_step<D, 2, false>, grid, true, s);
+    if (a.M <= 512) return launch_one(a, k_step<D, 8, false>, grid, true, s);
+    if (a.M <= kStepMaxTeams) return launch_one(a, k_step<D, 32, false>, grid, true, s);
+    return hipErrorInvalidValue;
+}
+
 template <typename T, int D>
 hipError_t decode_d(const DecodeArgs& a, hipStream_t s) {
+    if constexpr (sizeof(T) == 2) {
+        if (a.lay.step) return decode_step<D>(a, s);
+    }
     if (a.dense) {
         if (a.fused) {
             if constexpr (sizeof(T) == 2)

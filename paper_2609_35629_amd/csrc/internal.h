@@ -17,6 +17,9 @@ constexpr int kMaxGroup = 8;       // query heads per KV head (8-bit head masks)
 constexpr int kLogcStride = 8;     // floats per union team in the read plan
 constexpr int kUnitRows = 32;      // rows per attention unit (one 32-row step of a wave)
 constexpr int kDecodeThreads = 512;  // threads of every decode workgroup (eight waves)
+constexpr int kStepMaxTeams = 2048;  // teams per (b, kv) of the single-launch step
+constexpr int kStepMaxKp = 128;      // sampled teams per head of the single-launch step
+constexpr int kStepMaxWgs = 64;      // workgroups per (b, kv) pair of the single-launch step
 constexpr int kKmMaxCenters = 1024;  // k-means parents per (b, kv)
 constexpr int kKmMaxTrials = 8;      // seeding candidates per round: 2 + floor(ln 1024)
 constexpr int kMaxLabels = 1024;     // parents of a label-defined partition
@@ -40,10 +43,34 @@ __host__ __device__ inline int state_stride(int d) { return d + 4; }
 // the attention grid, maxwp the most attention workgroups one pair can have
 // (the partial states per pair and head) and swords the 64-team sample words
 // per head.
+//
+// The single-launch step (`step`) uses instead: per pair a 32-bit epoch (the
+// calls the pair has completed, modulo 2^32); per (pair, head, team) two
+// tagged 64-bit words holding the perturbed score's order key (`xk`) and one
+// holding phi in fp32 (`xp`); and the tagged partial states.  Every word a
+// call publishes carries the tag epoch + 1, so words left by earlier calls are
+// never taken for this call's; the workspace must be zero before its first
+// use and needs no reset between calls.
 struct DecodeLayout {
     int nwg = 0, maxwp = 0, swords = 0;
+    bool step = false;
     size_t ctr = 0, sbits = 0, lc = 0, part = 0, total = 0;
+    size_t epoch = 0, xk = 0, xp = 0;
 };
+
+// Bytes of one published state of the single-launch step: d / 2 + 1 chunks
+// of 16 bytes, each holding two values and two copies of the call's tag.
+__host__ __device__ inline int step_state_bytes(int d) { return (d / 2 + 1) * 16; }
+
+// Whether a step takes the single-launch kernel: bf16 rows of 64 or 128 dims,
+// at most kStepMaxTeams teams and kStepMaxKp sampled teams (sampled steps), and
+// at most one (b, kv) pair per compute unit; unless SANTAPP_DECODE_LAUNCH asks
+// for the split or fused launches.
+bool step_mode(santapp_dtype dt, int d, long long BH, int M, int Kp, bool dense, int cus);
+// Workgroups of a single-launch step: the same number for every pair, at most
+// kStepMaxWgs, one per compute unit at most; a multiple of eight per pair where
+// the compute units allow it, so that each pair spans all eight XCDs.
+int step_wgs(int cus, long long BH);
 
 // Workgroup w of an attention grid of nwg workgroups serving BH (b, kv)
 // pairs (BH <= nwg): its pair p, its index iw among the pair's workgroups and
@@ -83,8 +110,9 @@ int decode_wgs(int cus, long long BH, long long units_per_pair);
 
 // cap: host table with cap[x] = most units any x distinct teams of one
 // (b, kv) can need (x = 0 .. M).
-DecodeLayout decode_layout(int B, int Hq, int Hkv, int T, int d, int M, int Kp, const int* cap, int cus);
-DecodeLayout dense_layout(int B, int Hq, int Hkv, int N, int T, int d, int cus);
+DecodeLayout decode_layout(int B, int Hq, int Hkv, int T, int d, int M, int Kp, const int* cap, int cus,
+                           santapp_dtype dt);
+DecodeLayout dense_layout(int B, int Hq, int Hkv, int N, int T, int d, int cus, santapp_dtype dt);
 
 __host__ __device__ inline int chunk_count(int rows) { return (rows + kUnitRows - 1) / kUnitRows; }
 
