@@ -1008,10 +1008,13 @@ struct PlanLds {
 
 // The records of one plan pass from this thread's teams g0 .. g0 + PT - 1:
 // their head masks hm (cleared here beyond the table), sizes and packed
-// begins.  Returns (union teams, units, rows) of the pass; the records are in
-// place on return.
+// begins.  Returns (union teams, units, rows) of the pass (rows only when
+// `rows`, else 0); the records are in place on return.  The union teams
+// (< 4096) and units (< 2^20) of the pass are scanned as one packed count.
 template <int PT>
-__device__ int3 plan_records(int g0, int M, int (&hm)[PT], const int (&sz)[PT], const int (&bg)[PT], PlanLds& P) {
+__device__ int3 plan_records(int g0, int M, int (&hm)[PT], const int (&sz)[PT], const int (&bg)[PT], PlanLds& P,
+                             bool rows = true) {
+    const int lane = lane_id(), w = wave_id();
     int nck[PT], lf = 0, lnc = 0, lrows = 0;
 #pragma unroll
     for (int k = 0; k < PT; ++k) {
@@ -1021,11 +1024,27 @@ __device__ int3 plan_records(int g0, int M, int (&hm)[PT], const int (&sz)[PT], 
         lnc += nck[k];
         lrows += hm[k] ? sz[k] : 0;
     }
-    const int x[3] = {lf, lnc, lrows};
-    int ex[3], tot[3];
-    block_scan<3>(x, ex, tot, P.w);
-    const bool table = tot[1] <= kPlanUnits;  // uniform
-    int slot = ex[0], ust = ex[1];
+    // exclusive prefix over the workgroup: wave scans, then the waves' totals
+    const int x0 = lf | (lnc << 12);
+    const int inc0 = wave_incl_scan(x0);
+    const int inc1 = rows ? wave_incl_scan(lrows) : 0;
+    if (lane == kWave - 1) {
+        P.w[w] = inc0;
+        P.w[kWaves + w] = inc1;
+    }
+    __syncthreads();
+    int pre0 = 0, tot0 = 0, tot1 = 0;
+#pragma unroll
+    for (int v = 0; v < kWaves; ++v) {
+        const int y = P.w[v];
+        pre0 += v < w ? y : 0;
+        tot0 += y;
+        tot1 += rows ? P.w[kWaves + v] : 0;
+    }
+    const int ex0 = pre0 + inc0 - x0;
+    const int totf = tot0 & 0xfff, totu = tot0 >> 12;
+    const bool table = totu <= kPlanUnits;  // uniform
+    int slot = ex0 & 0xfff, ust = ex0 >> 12;
 #pragma unroll
     for (int k = 0; k < PT; ++k) {
         if (hm[k]) {
@@ -1037,7 +1056,7 @@ __device__ int3 plan_records(int g0, int M, int (&hm)[PT], const int (&sz)[PT], 
         }
     }
     __syncthreads();
-    return make_int3(tot[0], tot[1], tot[2]);
+    return make_int3(totf, totu, tot1);
 }
 
 // Pass `base` of pair p's plan: the teams base + t PT + k of thread t (their
@@ -1192,9 +1211,10 @@ __device__ __forceinline__ bool walk_units(const DecodeArgs& a, const Views& v, 
 constexpr int kStepSelWords = kStepMaxTeams / 64;
 
 // Head h's sample as 64-team words (bit g % 64 of word g / 64), the count of
-// sampled teams before each word, log c of its sampled teams in team order,
-// and per team the mask of the heads that sampled it; `ok` is cleared when a
-// head's published scores did not all arrive.
+// sampled teams before each word, phi - tau of its sampled teams in team order
+// (log c is formed from it where a unit needs it), and per team the mask of
+// the heads that sampled it; `ok` is cleared when a head's published scores
+// did not all arrive.
 struct StepSel {
     uint64_t sel[kMaxGroup][kStepSelWords];
     int pre[kMaxGroup][kStepSelWords];
@@ -1204,12 +1224,13 @@ struct StepSel {
     int pad[3];
 };
 
-// log c of team g for head h (g sampled by h).
+// log c of team g for head h (g sampled by h), formed where a unit needs it
+// from phi_g - tau.
 __device__ __forceinline__ float step_logc(const StepSel& SS, int h, int g) {
     const int wd = g >> 6;
     const uint64_t w = SS.sel[h][wd];
     const int r = SS.pre[h][wd] + static_cast<int>(__popcll(w & ((1ull << (g & 63)) - 1ull)));
-    return SS.lc[h][min(r, kStepMaxKp - 1)];
+    return log_inclusion(SS.lc[h][min(r, kStepMaxKp - 1)]);
 }
 
 // The pair's units for the single-launch step: as walk_units in the split
@@ -1252,7 +1273,7 @@ __device__ __forceinline__ bool step_walk_units(const DecodeArgs& a, int p, int 
                 hm[k] = static_cast<int>((SS->hm[g >> 2] >> (8 * (g & 3))) & 0xffu);
             }
         }
-        const int3 t = plan_records<PT>(g0, M, hm, sz, bg, P);
+        const int3 t = plan_records<PT>(g0, M, hm, sz, bg, P, a.dbg_urows != nullptr);
         // the suffix units come first in the first pass's run
         const int lo = base == 0 ? 0 : run_u, first = run_u;
         run(lo, run_u + t.y,
@@ -2207,7 +2228,7 @@ __device__ bool step_select(const DecodeArgs& a, const StepViews& v, int p, int 
             SS.pre[h][j] = cum;
         }
         if ((sb >> lane) & 1ull) {
-            // the team's head bit, and phi - tau staged by rank
+            // the team's head bit, and phi - tau by rank
             const int g = 64 * j + lane;
             atomicOr(&SS.hm[g >> 2], 1u << (h + 8 * (g & 3)));
             const int rank = cum + static_cast<int>(__popcll(sb & lanemask_lt()));
@@ -2218,12 +2239,9 @@ __device__ bool step_select(const DecodeArgs& a, const StepViews& v, int p, int 
         }
         cum += static_cast<int>(__popcll(sb));
     }
-    // log c of the sampled teams, one per lane (eq. method-inclusion)
-    lds_order();
-    for (int r = lane; r < Kp; r += kWave) {
-        const float lcv = log_inclusion(SS.lc[h][r]);
-        SS.lc[h][r] = lcv;
-        if (iw == 0 && a.dbg_logc) a.dbg_logc[bq * Kp + r] = lcv;
+    if (iw == 0 && a.dbg_logc) {  // uniform: diagnostics only
+        lds_order();
+        for (int r = lane; r < Kp; r += kWave) a.dbg_logc[bq * Kp + r] = log_inclusion(SS.lc[h][r]);
     }
     if (iw == 0 && lane == 0 && a.dbg_tau) a.dbg_tau[bq] = tau;
     return ok;
@@ -2247,17 +2265,18 @@ __device__ __forceinline__ float wave_sum_dpp(float v) {
 // of this call, and no ordering between the chunks is needed.
 //
 // The workgroup combines its waves' states of each head (canonical form in
-// LDS) and publishes them.  Each (head, eighth of the dims) is then merged by
-// one wave of the pair: lane w reads state w (nwp <= 64) -- the eighth's value
-// chunks and the (maximum, mass) chunk -- until all carry the tag, and the
-// states are rescaled to the common maximum by wave sums.  The merger of
-// (head 0, first eighth) advances the pair's epoch once all its states carry
-// the tag (every workgroup of the pair has then read the epoch).
+// LDS) and publishes them.  Each (head, sixteenth of the dims) is then merged
+// by one wave of the pair: lane w reads state w (nwp <= 64) -- the sixteenth's
+// value chunks and the (maximum, mass) chunk -- until all carry the tag, and
+// the states are rescaled to the common maximum by wave sums.  The merger of
+// (head 0, first sixteenth) advances the pair's epoch once all its states
+// carry the tag (every workgroup of the pair has then read the epoch).
 template <int D>
 __device__ void step_publish_merge(const DecodeArgs& a, const StepViews& v, int p, int iw, int nwp, uint32_t tag,
                                    char* lds) {
     constexpr int NC = D / 2 + 1;  // chunks per state
-    constexpr int DW = D / kWaves; // dims per merging wave
+    constexpr int kParts = 32;     // merge tasks per head
+    constexpr int DW = D / kParts; // dims per merge task
     const int tid = threadIdx.x, G = a.G, lane = lane_id(), wv = wave_id();
     __syncthreads();
     char* const part_p = reinterpret_cast<char*>(v.part) + static_cast<size_t>(p) * a.lay.maxwp * G * NC * 16;
@@ -2289,11 +2308,11 @@ __device__ void step_publish_merge(const DecodeArgs& a, const StepViews& v, int 
         store16_coherent(rs, static_cast<uint32_t>((iw * G + h) * NC + c) * 16u,
                          u32x4v{__float_as_uint(x0), tag, __float_as_uint(x1), tag});
     }
-    // merge tasks: task t = 8 h + c (head h, dims [c D / 8, (c + 1) D / 8)) runs
-    // on workgroup t mod nwp, wave (t / nwp) mod 8, so that the merge of a
-    // pair is spread over many compute units and each poll is small
-    for (int t = iw + wv * nwp; t < kWaves * G; t += kWaves * nwp) {
-        const int h = t / kWaves, c = t % kWaves;
+    // merge tasks: task t = 16 h + c (head h, dims [c D / 16, (c + 1) D / 16))
+    // runs on workgroup t mod nwp, wave (t / nwp) mod 8, so that the merge of
+    // a pair is spread over many compute units and each poll is small
+    for (int t = iw + wv * nwp; t < kParts * G; t += kWaves * nwp) {
+        const int h = t / kParts, c = t % kParts;
         const bool live = lane < nwp;
         const uint32_t base = static_cast<uint32_t>((lane * G + h) * NC) * 16u;
         float acc[DW], mw = kNeg, lw = 0.f;
