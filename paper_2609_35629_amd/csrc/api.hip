@@ -172,8 +172,7 @@ void step_regions(DecodeLayout& L, size_t BH, int G, int M, int d, bool dense, s
     };
     L.epoch = take(BH * sizeof(uint32_t));
     if (!dense) {
-        L.xk = take(BH * G * static_cast<size_t>(M) * 16);
-        L.xp = take(BH * G * static_cast<size_t>(M) * 8);
+        L.xk = take(BH * G * 3 * static_cast<size_t>(M) * 8);
     }
     L.part = take(BH * L.maxwp * G * static_cast<size_t>(step_state_bytes(d)));
 }

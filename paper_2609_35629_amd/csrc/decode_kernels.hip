@@ -1210,28 +1210,33 @@ __device__ __forceinline__ bool walk_units(const DecodeArgs& a, const Views& v, 
 // ---------------------------------------------------------------------------
 constexpr int kStepSelWords = kStepMaxTeams / 64;
 
-// Head h's sample as 64-team words (bit g % 64 of word g / 64), the count of
-// sampled teams before each word, phi - tau of its sampled teams in team order
-// (log c is formed from it where a unit needs it), and per team the mask of
-// the heads that sampled it; `ok` is cleared when a head's published scores
-// did not all arrive.
+// The pair's selection in LDS: per team the mask of the heads that sampled
+// it, and per head tau's order key -- its high half, and either the team
+// whose published low half completes it (tau_g >= 0) or the low half itself
+// (tau_g < 0); `ok` is cleared when a head's published scores did not all
+// arrive.
 struct StepSel {
-    uint64_t sel[kMaxGroup][kStepSelWords];
-    int pre[kMaxGroup][kStepSelWords];
-    float lc[kMaxGroup][kStepMaxKp];
     uint32_t hm[kStepMaxTeams / 4];  // byte g % 4 of word g / 4: the heads that sampled team g
+    uint32_t tau_hi[kMaxGroup];
+    int tau_g[kMaxGroup];
+    uint32_t tau_lo[kMaxGroup];
     int ok;
     int pad[3];
 };
 
-// log c of team g for head h (g sampled by h), formed where a unit needs it
-// from phi_g - tau.
-__device__ __forceinline__ float step_logc(const StepSel& SS, int h, int g) {
-    const int wd = g >> 6;
-    const uint64_t w = SS.sel[h][wd];
-    const int r = SS.pre[h][wd] + static_cast<int>(__popcll(w & ((1ull << (g & 63)) - 1ull)));
-    return log_inclusion(SS.lc[h][min(r, kStepMaxKp - 1)]);
-}
+// Where a unit of the step finds its corrections: the pair's exchange words
+// and the call's tag.
+struct StepCtx {
+    const uint64_t* xk;  // the pair's [G, 3, M] exchange words
+    uint32_t tag;
+};
+
+// The correction of a unit for one lane's head in flight: phi of the unit's
+// team and the low half of tau's key, as loaded (need = 0: no correction).
+struct CorrWords {
+    u32x2v ph, tl;
+    int need, g;
+};
 
 // The pair's units for the single-launch step: as walk_units in the split
 // launch, with the heads' samples taken from LDS and the first pass's team
@@ -1295,7 +1300,8 @@ __device__ __forceinline__ bool step_walk_units(const DecodeArgs& a, int p, int 
 // ---------------------------------------------------------------------------
 template <int D, bool DENSE, bool FUSED, int PT, bool STEP = false>
 __device__ void attend_mfma(const DecodeArgs& a, const Views& v, int p, int iw, int nwp, char* t0, char* t1,
-                            char* misc, const StepSel* SS = nullptr, const int* s_tab = nullptr) {
+                            char* misc, const StepSel* SS = nullptr, const int* s_tab = nullptr,
+                            const StepCtx* sc = nullptr) {
     using QKT = QK<bf16_t, D>;
     using VT = VTile<D>;
     constexpr int NF = QKT::KB;         // K fragments per 16-row tile
@@ -1365,18 +1371,62 @@ __device__ void attend_mfma(const DecodeArgs& a, const Views& v, int p, int iw, 
     // log c of the unit's team for head lane % 8 (0 where that head did not
     // sample it, or for suffix and dense rows); a step spreads the values to
     // the lanes that hold each head's state
+    // In the single-launch step the corrections are read from the exchange
+    // words with the unit's rows (phi of the unit's team and the low half of
+    // tau's key for head lane % 8) and resolved to log c when the unit
+    // computes.
+    const __amdgpu_buffer_rsrc_t rx =
+        coherent_rsrc(STEP && !DENSE ? static_cast<const void*>(sc->xk) : static_cast<const void*>(a.q),
+                      STEP && !DENSE ? static_cast<uint32_t>(a.G) * a.M * 24u : 0u);
     auto corrections = [&](const Unit<bf16_t>& U) {
-        float cr = 0.f;
         const int h = lane & 7;
-        if (!DENSE && U.g >= 0 && ((U.hmask >> h) & 1)) {
-            if constexpr (STEP) {
-                cr = step_logc(*SS, h, U.g);
-            } else {
+        if constexpr (STEP) {
+            CorrWords c;
+            c.need = 0;
+            c.g = max(U.g, 0);
+            c.ph = u32x2v{0u, 0u};
+            c.tl = u32x2v{0u, 0u};
+            if (!DENSE && U.g >= 0 && ((U.hmask >> h) & 1)) {
+                c.need = 1;
+                const uint32_t hb = static_cast<uint32_t>(h) * 24u * a.M;
+                c.ph = load8_coherent(rx, hb + 16u * a.M + 8u * U.g);
+                const int tg = SS->tau_g[h];
+                if (tg >= 0)
+                    c.tl = load8_coherent(rx, hb + 8u * a.M + 8u * tg);
+                else
+                    c.tl = u32x2v{SS->tau_lo[h], sc->tag};
+            }
+            return c;
+        } else {
+            float cr = 0.f;
+            if (!DENSE && U.g >= 0 && ((U.hmask >> h) & 1)) {
                 const float* src = v.lc + (hq0 + h) * a.M + U.g;
                 cr = FUSED ? load_f32_coherent(src) : *src;
             }
+            return cr;
         }
-        return cr;
+    };
+    // log c of a correction in flight (eq. method-inclusion); a word that
+    // does not yet carry the tag is read again
+    auto corr_value = [&](const auto& c) -> float {
+        if constexpr (STEP) {
+            if (!c.need) return 0.f;
+            const int h = lane & 7;
+            u32x2v ph = c.ph, tl = c.tl;
+            if (ph.y != sc->tag || tl.y != sc->tag) {
+                const uint32_t hb = static_cast<uint32_t>(h) * 24u * a.M;
+                const int tg = max(SS->tau_g[h], 0);
+                for (int it = 0; it < kSpinLimit && (ph.y != sc->tag || tl.y != sc->tag); ++it) {
+                    __builtin_amdgcn_s_sleep(1);
+                    if (ph.y != sc->tag) ph = load8_coherent(rx, hb + 16u * a.M + 8u * static_cast<uint32_t>(c.g));
+                    if (tl.y != sc->tag) tl = load8_coherent(rx, hb + 8u * a.M + 8u * tg);
+                }
+            }
+            const double tau = key_value((static_cast<uint64_t>(SS->tau_hi[h]) << 32) | tl.x);
+            return log_inclusion(static_cast<float>(static_cast<double>(__uint_as_float(ph.x)) - tau));
+        } else {
+            return c;
+        }
     };
 
     typename QKT::frag kf0[2][NF], kf1[2][NF];
@@ -1390,7 +1440,7 @@ __device__ void attend_mfma(const DecodeArgs& a, const Views& v, int p, int iw, 
         int u = lo_u + (((gs - lo_u) % NW) + NW) % NW;
         if (u >= hi_u) return;  // uniform
         Unit<bf16_t> cur = unit(u);
-        float ccr = corrections(cur);
+        auto ccr = corrections(cur);
         issue(cur, tile0, kf0, true);
         ensure_q();
         auto step = [&](char* tile, typename QKT::frag(&kf)[2][NF], char* ntile, typename QKT::frag(&nkf)[2][NF]) {
@@ -1402,13 +1452,14 @@ __device__ void attend_mfma(const DecodeArgs& a, const Views& v, int p, int iw, 
             asm volatile("" ::"v"(kf[1][NF - 1].w) : "memory");
             float bias[4];
             bool on[4];
+            const float cv = corr_value(ccr);
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                bias[r] = -__shfl(ccr, hsel + r) * kLog2e;
+                bias[r] = -__shfl(cv, hsel + r) * kLog2e;
                 on[r] = ((cur.hmask >> (hsel + r)) & 1) != 0;
             }
             const Unit<bf16_t> nxt = has_next ? unit(u + NW) : cur;
-            const float ncr = corrections(nxt);
+            const auto ncr = corrections(nxt);
             issue(nxt, ntile, nkf, has_next);
 
             // scores and the online softmax over the step's 32 rows
@@ -1819,10 +1870,12 @@ __device__ void combine_and_merge(const DecodeArgs& a, const Views& v, int p, in
 //      pair merges head h once every state of it carries the tag, and the
 //      merger of head 0 advances the pair's epoch.
 // ===========================================================================
+// The exchange words of pair p, head h: three rows of M tagged 64-bit words
+// (value, tag): the high 32 bits of Y's order key, its low 32 bits, and phi
+// in fp32.
 struct StepViews {
     uint32_t* epoch;  // [BH]
-    uint64_t* xk;     // [BH, G, M, 2] tagged order keys of Y
-    uint64_t* xp;     // [BH, G, M] tagged phi (fp32)
+    uint64_t* xk;     // [BH, G, 3, M] tagged exchange words
     float* part;      // [BH, maxwp, G] published states of step_state_bytes(d) each
 };
 
@@ -1830,9 +1883,19 @@ __device__ __forceinline__ StepViews step_views(const DecodeArgs& a) {
     StepViews v;
     v.epoch = reinterpret_cast<uint32_t*>(a.ws + a.lay.epoch);
     v.xk = reinterpret_cast<uint64_t*>(a.ws + a.lay.xk);
-    v.xp = reinterpret_cast<uint64_t*>(a.ws + a.lay.xp);
     v.part = reinterpret_cast<float*>(a.ws + a.lay.part);
     return v;
+}
+
+// Publish Y (as its order key, high and low 32 bits) and phi of (head h,
+// team g) to the pair's exchange words (rx covers the pair's G * 3 * M words).
+__device__ __forceinline__ void publish_item(__amdgpu_buffer_rsrc_t rx, int M, int h, int g, double phi, double y,
+                                             uint32_t tag) {
+    const uint64_t key = order_key(y);
+    const uint32_t o = (static_cast<uint32_t>(h) * 3u * M + g) * 8u;
+    store8_coherent(rx, o, u32x2v{static_cast<uint32_t>(key >> 32), tag});
+    store8_coherent(rx, o + 8u * M, u32x2v{static_cast<uint32_t>(key), tag});
+    store8_coherent(rx, o + 16u * M, u32x2v{__float_as_uint(static_cast<float>(phi)), tag});
 }
 
 // Teams of a workgroup's routing slice: a multiple of four (whole Philox
@@ -1887,7 +1950,7 @@ __device__ __forceinline__ double route_gumbel(const DecodeArgs& a, int p, int c
 template <int D>
 __device__ __forceinline__ void route_finish(const DecodeArgs& a, int p, int c0, int nt, uint32_t tag,
                                              const RouteRegs<D>& r, const double* s_qd, double gum,
-                                             __amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rp) {
+                                             __amdgpu_buffer_rsrc_t rx) {
     using RL = RepLanes<bf16_t, D>;
     constexpr int EPL = RL::EPL;
     const int G = a.G, M = a.M;
@@ -1911,10 +1974,7 @@ __device__ __forceinline__ void route_finish(const DecodeArgs& a, int p, int c0,
     if (sub < G) {
         const int g = c0 + o, h = sub;
         const double y = phi + gum;
-        const uint64_t key = order_key(y);
-        const uint32_t slot = static_cast<uint32_t>(h) * M + g;
-        store16_coherent(rk, slot * 16u, u32x4v{static_cast<uint32_t>(key >> 32), tag, static_cast<uint32_t>(key), tag});
-        store8_coherent(rp, slot * 8u, u32x2v{__float_as_uint(static_cast<float>(phi)), tag});
+        publish_item(rx, M, h, g, phi, y, tag);
         const int b = p / a.Hkv, kv = p - b * a.Hkv;
         const size_t bq = static_cast<size_t>(b) * a.Hq + kv * G + h;
         if (a.dbg_phi) a.dbg_phi[bq * M + g] = phi;
@@ -2009,8 +2069,7 @@ __device__ __forceinline__ void route_split(const DecodeArgs& a, int p, int c0, 
 // Y = phi + G of the slice's (team, head) items (lane 8 t + h of wave 0),
 // published as tagged words with phi.
 __device__ __forceinline__ void route_publish(const DecodeArgs& a, int p, int c0, int nt, uint32_t tag,
-                                              const double* s_pg, __amdgpu_buffer_rsrc_t rk,
-                                              __amdgpu_buffer_rsrc_t rp) {
+                                              const double* s_pg, __amdgpu_buffer_rsrc_t rx) {
     const int lane = lane_id();
     const int t = lane >> 3, h = lane & 7;
     if (wave_id() != 0 || t >= nt || h >= a.G) return;
@@ -2018,10 +2077,7 @@ __device__ __forceinline__ void route_publish(const DecodeArgs& a, int p, int c0
     const int g = c0 + t;
     const double phi = s_pg[t * 8 + h];
     const double y = phi + s_pg[64 + t * 8 + h];
-    const uint64_t key = order_key(y);
-    const uint32_t slot = static_cast<uint32_t>(h) * M + g;
-    store16_coherent(rk, slot * 16u, u32x4v{static_cast<uint32_t>(key >> 32), tag, static_cast<uint32_t>(key), tag});
-    store8_coherent(rp, slot * 8u, u32x2v{__float_as_uint(static_cast<float>(phi)), tag});
+    publish_item(rx, M, h, g, phi, y, tag);
     const size_t bq = static_cast<size_t>(b) * a.Hq + kv * G + h;
     if (a.dbg_phi) a.dbg_phi[bq * M + g] = phi;
     if (a.dbg_Y) a.dbg_Y[bq * M + g] = y;
@@ -2148,100 +2204,256 @@ __device__ uint64_t wave_rank(const uint64_t (&k)[KPL], int M, int want, WaveSel
     return readlane(mine, src);
 }
 
-// Phase 2 for wave h (a query head of the pair): wait for the head's M
-// published keys and phis, select, and record the sample, its head bit in the
-// team masks and log c in SS.  Returns false when the words did not all
-// arrive within the spin limit.
+// Monotone fp32 value of a 32-bit key (the high half of a double's order
+// key): the double truncated to its 20 high mantissa bits, then rounded.
+__device__ __forceinline__ float key32_value(uint32_t k) {
+    const uint32_t hi = (k >> 31) ? (k & 0x7fffffffu) : ~k;
+    return static_cast<float>(__hiloint2double(static_cast<int>(hi), 0));
+}
+
+// Exact radix select over 32-bit keys (four 8-bit digits from the top), as
+// wave_rank_exact for 64-bit keys.
+template <int KPL>
+__device__ uint32_t wave_rank32_exact(const uint32_t (&k)[KPL], int M, int want, WaveSel& W, int& above) {
+    const int lane = lane_id();
+    uint32_t prefix = 0, pmask = 0;
+    above = 0;
+    int cnt = 0;
+    for (int sh = 24;; sh -= 8) {  // uniform
+        reinterpret_cast<uint4*>(W.hist)[lane] = make_uint4(0, 0, 0, 0);
+        lds_order();
+#pragma unroll
+        for (int j = 0; j < KPL; ++j)
+            if (64 * j + lane < M && (k[j] & pmask) == prefix) atomicAdd(&W.hist[(k[j] >> sh) & 255u], 1u);
+        lds_order();
+        int hi;
+        const int dg = hist_select(W.hist, want, hi, cnt);
+        lds_order();
+        want -= hi;
+        above += hi;
+        prefix |= static_cast<uint32_t>(dg) << sh;
+        pmask |= 0xffu << sh;
+        if (cnt == 1 || sh == 0) break;
+    }
+    if (cnt == 1) {  // the one key with this prefix
+        uint32_t r = 0;
+#pragma unroll
+        for (int j = 0; j < KPL; ++j) {
+            const uint64_t bal = __ballot(64 * j + lane < M && (k[j] & pmask) == prefix);
+            if (bal) r = static_cast<uint32_t>(readlane(static_cast<int>(k[j]), __ffsll(static_cast<unsigned long long>(bal)) - 1));
+        }
+        return r;
+    }
+    return prefix;  // every bit fixed: equal keys
+}
+
+// Key of rank `want` (0-based, descending) among the wave's 32-bit keys and
+// the count strictly above it: a 256-bin value histogram over [min, max] of
+// the keys' fp32 values, then a direct ranking of the keys in the bin that
+// holds rank `want`; the exact radix where that bin holds more than 64 keys
+// or the keys span no finite fp32 range.
+template <int KPL>
+__device__ uint32_t wave_rank32(const uint32_t (&k)[KPL], int M, int want, WaveSel& W, int& above) {
+    const int lane = lane_id();
+    float y[KPL];
+    float lo = __builtin_inff(), hi = -__builtin_inff();
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) {
+        y[j] = key32_value(k[j]);
+        if (64 * j + lane < M) {
+            lo = fminf(lo, y[j]);
+            hi = fmaxf(hi, y[j]);
+        }
+    }
+    lo = wave_ext_f<true>(lo);
+    hi = wave_ext_f<false>(hi);
+    const float range = hi - lo;
+    if (!(range > 0.f) || !(range < 3.0e38f)) return wave_rank32_exact<KPL>(k, M, want, W, above);
+    const float fs = 255.99f / range;
+    reinterpret_cast<uint4*>(W.hist)[lane] = make_uint4(0, 0, 0, 0);
+    lds_order();
+    int bin[KPL];
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) {
+        bin[j] = 64 * j + lane < M ? static_cast<int>(fminf(255.f, (y[j] - lo) * fs)) : -1;
+        if (bin[j] >= 0) atomicAdd(&W.hist[bin[j]], 1u);
+    }
+    lds_order();
+    int hcnt, cnt;
+    const int sb = hist_select(W.hist, want, hcnt, cnt);
+    lds_order();
+    if (cnt > kWave) return wave_rank32_exact<KPL>(k, M, want, W, above);
+    uint32_t* const cand = reinterpret_cast<uint32_t*>(W.cand);
+    int n = 0;
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) {
+        const bool in = bin[j] == sb;
+        const uint64_t bal = __ballot(in);
+        if (in) cand[n + static_cast<int>(__popcll(bal & lanemask_lt()))] = k[j];
+        n += static_cast<int>(__popcll(bal));
+    }
+    lds_order();
+    const int rest = want - hcnt;
+    const uint32_t mine = cand[min(lane, n - 1)];
+    int gt = 0, ge = 0;
+    for (int t = 0; t < n; ++t) {
+        const uint32_t o = static_cast<uint32_t>(readlane(static_cast<int>(mine), t));
+        gt += o > mine ? 1 : 0;
+        ge += o >= mine ? 1 : 0;
+    }
+    const bool owner = lane < n && gt <= rest && rest < ge;
+    const int src = __ffsll(static_cast<unsigned long long>(__ballot(owner))) - 1;
+    above = hcnt + readlane(gt, src);
+    return static_cast<uint32_t>(readlane(static_cast<int>(mine), src));
+}
+
+// Poll `n` rows-of-words loads: lane's words at byte offsets off[j] (for the
+// bits of `pend`) until each carries `tag`; returns false at the spin limit.
+template <int KPL>
+__device__ __forceinline__ bool poll_words(__amdgpu_buffer_rsrc_t r, const uint32_t (&off)[KPL], uint32_t pend,
+                                           uint32_t tag, uint32_t (&val)[KPL]) {
+    constexpr int kBatch = KPL < 16 ? KPL : 16;
+    for (int it = 0;; ++it) {
+#pragma unroll
+        for (int j0 = 0; j0 < KPL; j0 += kBatch) {
+            u32x2v w[kBatch];
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j)
+                if ((pend >> (j0 + j)) & 1u) w[j] = load8_coherent(r, off[j0 + j]);
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j) {
+                if (((pend >> (j0 + j)) & 1u) && w[j].y == tag) {
+                    val[j0 + j] = w[j].x;
+                    pend &= ~(1u << (j0 + j));
+                }
+            }
+        }
+        if (__ballot(pend != 0) == 0) return true;  // uniform
+        if (it >= kSpinLimit) return false;
+        __builtin_amdgcn_s_sleep(1);
+    }
+}
+
+// Phase 2 for wave h (a query head of the pair).  The wave reads the high
+// halves of the head's M keys once all carry the tag and finds the key of
+// rank K among them.  When that high half is unique (the common case) the
+// sample is every key above it, and a second read fetches the low half of
+// tau's key and phi of the sampled teams; otherwise the low halves of all
+// keys are read and the exact 64-bit keys ranked (ties of equal keys to the
+// lower team index).  The sample goes to SS as bit words, head bits of the
+// team masks and phi - tau by rank.  Returns false when a word did not arrive
+// within the spin limit.
 template <int KPL>
 __device__ bool step_select(const DecodeArgs& a, const StepViews& v, int p, int iw, uint32_t tag, WaveSel& W,
                             StepSel& SS) {
     const int lane = lane_id(), h = wave_id(), G = a.G, M = a.M, Kp = a.Kp;
     const int b = p / a.Hkv, kv = p - b * a.Hkv;
-    const size_t hb = (static_cast<size_t>(p) * G + h) * M;
-    const __amdgpu_buffer_rsrc_t rk = coherent_rsrc(v.xk + 2 * hb, static_cast<uint32_t>(M) * 16u);
-    const __amdgpu_buffer_rsrc_t rp = coherent_rsrc(v.xp + hb, static_cast<uint32_t>(M) * 8u);
-    uint64_t k[KPL];
-    float ph[KPL];
-    uint32_t pend = 0;
+    const size_t hb = (static_cast<size_t>(p) * G + h) * 3 * M;
+    const __amdgpu_buffer_rsrc_t rh = coherent_rsrc(v.xk + hb, static_cast<uint32_t>(M) * 24u);
+    const uint32_t row1 = 8u * M, row2 = 16u * M;
+    uint32_t off[KPL], k[KPL], valid = 0;
 #pragma unroll
     for (int j = 0; j < KPL; ++j) {
+        off[j] = static_cast<uint32_t>(64 * j + lane) * 8u;
         k[j] = 0;
-        ph[j] = 0.f;
-        if (64 * j + lane < M) pend |= 1u << j;
+        if (64 * j + lane < M) valid |= 1u << j;
     }
-    // every key's words and its phi carry this call's tag (at most 16 keys'
-    // loads in flight)
-    constexpr int kBatch = KPL < 16 ? KPL : 16;
-    bool ok = true;
-    for (int it = 0;; ++it) {
-#pragma unroll
-        for (int j0 = 0; j0 < KPL; j0 += kBatch) {
-            u32x4v w[kBatch];
-            u32x2v f[kBatch];
-#pragma unroll
-            for (int j = 0; j < kBatch; ++j) {
-                if ((pend >> (j0 + j)) & 1u) {
-                    const uint32_t g = static_cast<uint32_t>(64 * (j0 + j) + lane);
-                    w[j] = load16_coherent(rk, g * 16u);
-                    f[j] = load8_coherent(rp, g * 8u);
-                }
-            }
-#pragma unroll
-            for (int j = 0; j < kBatch; ++j) {
-                if (((pend >> (j0 + j)) & 1u) && w[j].y == tag && w[j].w == tag && f[j].y == tag) {
-                    k[j0 + j] = (static_cast<uint64_t>(w[j].x) << 32) | w[j].z;
-                    ph[j0 + j] = __uint_as_float(f[j].x);
-                    pend &= ~(1u << (j0 + j));
-                }
-            }
-        }
-        if (__ballot(pend != 0) == 0) break;  // uniform
-        if (it >= kSpinLimit) {
-            ok = false;
-            break;
-        }
-        __builtin_amdgcn_s_sleep(1);
-    }
+    bool ok = poll_words<KPL>(rh, off, valid, tag, k);
     int above;
-    const uint64_t tkey = wave_rank<KPL>(k, M, Kp, W, above);
-    const double tau = key_value(tkey);
-    // the sample: keys above tau, then keys equal to it in team order; log c
-    // of each sampled team (eq. method-inclusion) by the lane that holds it
-    int need = Kp - above;
-    const size_t bq = static_cast<size_t>(b) * a.Hq + kv * G + h;
-    int cum = 0;
+    const uint32_t th = wave_rank32<KPL>(k, M, Kp, W, above);
+    int bcnt = 0;
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) bcnt += static_cast<int>(__popcll(__ballot(((valid >> j) & 1u) && k[j] == th)));
+    uint64_t selw[KPL];
+    int tau_g = -1;
+    uint32_t tau_lo = 0;
+    if (bcnt == 1) {  // uniform: the sample is every key whose high half exceeds th
+#pragma unroll
+        for (int j = 0; j < KPL; ++j) {
+            selw[j] = __ballot(((valid >> j) & 1u) && k[j] > th);
+            const uint64_t t = __ballot(((valid >> j) & 1u) && k[j] == th);
+            if (t) tau_g = 64 * j + __ffsll(static_cast<unsigned long long>(t)) - 1;
+        }
+    } else {  // several keys share tau's high half: rank the exact keys
+        uint32_t offl[KPL], lo[KPL];
+#pragma unroll
+        for (int j = 0; j < KPL; ++j) {
+            offl[j] = row1 + off[j];
+            lo[j] = 0;
+        }
+        ok = poll_words<KPL>(rh, offl, valid, tag, lo) && ok;
+        uint64_t k64[KPL];
+#pragma unroll
+        for (int j = 0; j < KPL; ++j) k64[j] = (static_cast<uint64_t>(k[j]) << 32) | lo[j];
+        int above64;
+        const uint64_t tkey = wave_rank<KPL>(k64, M, Kp, W, above64);
+        tau_lo = static_cast<uint32_t>(tkey);
+        int need = Kp - above64;
+#pragma unroll
+        for (int j = 0; j < KPL; ++j) {
+            const bool vj = (valid >> j) & 1u;
+            uint64_t sb = __ballot(vj && k64[j] > tkey);
+            if (need > 0) {  // uniform
+                uint64_t tb = __ballot(vj && k64[j] == tkey);
+                while (need > 0 && tb) {
+                    const uint64_t low = tb & (~tb + 1);
+                    sb |= low;
+                    tb ^= low;
+                    --need;
+                }
+            }
+            selw[j] = sb;
+        }
+    }
+    // tau for the corrections: its high half, and where its low half is
+    if (lane == 0) {
+        SS.tau_hi[h] = th;  // also the high half of the exact path's key (truncation keeps the order)
+        SS.tau_g[h] = tau_g;
+        SS.tau_lo[h] = tau_lo;
+    }
+    // the head's bit in the masks of its sampled teams
 #pragma unroll
     for (int j = 0; j < KPL; ++j) {
-        const bool vj = 64 * j + lane < M;
-        uint64_t sb = __ballot(vj && k[j] > tkey);
-        if (need > 0) {  // uniform
-            uint64_t tb = __ballot(vj && k[j] == tkey);
-            while (need > 0 && tb) {
-                const uint64_t low = tb & (~tb + 1);
-                sb |= low;
-                tb ^= low;
-                --need;
-            }
-        }
-        if (lane == 0) {
-            SS.sel[h][j] = sb;
-            SS.pre[h][j] = cum;
-        }
-        if ((sb >> lane) & 1ull) {
-            // the team's head bit, and phi - tau by rank
+        if ((selw[j] >> lane) & 1ull) {
             const int g = 64 * j + lane;
             atomicOr(&SS.hm[g >> 2], 1u << (h + 8 * (g & 3)));
-            const int rank = cum + static_cast<int>(__popcll(sb & lanemask_lt()));
-            if (rank < kStepMaxKp) {
-                SS.lc[h][rank] = static_cast<float>(static_cast<double>(ph[j]) - tau);
-                if (iw == 0 && a.dbg_sel) a.dbg_sel[bq * Kp + rank] = g;
-            }
         }
-        cum += static_cast<int>(__popcll(sb));
     }
-    if (iw == 0 && a.dbg_logc) {  // uniform: diagnostics only
-        lds_order();
-        for (int r = lane; r < Kp; r += kWave) a.dbg_logc[bq * Kp + r] = log_inclusion(SS.lc[h][r]);
+    // diagnostics (one workgroup of the pair): tau, the sample in ascending
+    // team order and its log c, from the exchange words
+    const size_t bq = static_cast<size_t>(b) * a.Hq + kv * G + h;
+    double tau = 0.0;
+    if (iw == 0 && (a.dbg_tau || a.dbg_sel || a.dbg_logc)) {  // uniform
+        uint32_t tl = tau_lo;
+        if (tau_g >= 0) {
+            uint32_t o1[1] = {row1 + static_cast<uint32_t>(tau_g) * 8u}, v1[1] = {0};
+            ok = poll_words<1>(rh, o1, 1u, tag, v1) && ok;
+            tl = v1[0];
+        }
+        tau = key_value((static_cast<uint64_t>(th) << 32) | tl);
+        uint32_t offp[KPL], ph[KPL], mine = 0;
+#pragma unroll
+        for (int j = 0; j < KPL; ++j) {
+            offp[j] = row2 + off[j];
+            ph[j] = 0;
+            if ((selw[j] >> lane) & 1ull) mine |= 1u << j;
+        }
+        ok = poll_words<KPL>(rh, offp, mine, tag, ph) && ok;
+        int cum = 0;
+#pragma unroll
+        for (int j = 0; j < KPL; ++j) {
+            const uint64_t sb = selw[j];
+            if ((sb >> lane) & 1ull) {
+                const int rank = cum + static_cast<int>(__popcll(sb & lanemask_lt()));
+                if (rank < Kp) {
+                    if (a.dbg_sel) a.dbg_sel[bq * Kp + rank] = 64 * j + lane;
+                    if (a.dbg_logc)
+                        a.dbg_logc[bq * Kp + rank] =
+                            log_inclusion(static_cast<float>(static_cast<double>(__uint_as_float(ph[j])) - tau));
+                }
+            }
+            cum += static_cast<int>(__popcll(sb));
+        }
     }
     if (iw == 0 && lane == 0 && a.dbg_tau) a.dbg_tau[bq] = tau;
     return ok;
@@ -2411,10 +2623,8 @@ __global__ __launch_bounds__(kThreads, 1) void k_step(DecodeArgs a) {
         WaveSel* const s_ws = reinterpret_cast<WaveSel*>(s_t0 + L::qd);
         const int S = step_slice(M, nwp);
         const int t0 = iw * S, t1 = min(M, t0 + S);
-        const __amdgpu_buffer_rsrc_t rk = coherent_rsrc(v.xk + 2 * static_cast<size_t>(p) * G * M,
-                                                        static_cast<uint32_t>(G) * M * 16u);
-        const __amdgpu_buffer_rsrc_t rp = coherent_rsrc(v.xp + static_cast<size_t>(p) * G * M,
-                                                        static_cast<uint32_t>(G) * M * 8u);
+        const __amdgpu_buffer_rsrc_t rx = coherent_rsrc(v.xk + 3 * static_cast<size_t>(p) * G * M,
+                                                        static_cast<uint32_t>(G) * M * 24u);
         // everything the routing needs is requested at once: the slice's
         // routing keys, the queries and the first plan pass's table
         const size_t tb0 = static_cast<size_t>(p) * M;
@@ -2456,7 +2666,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_step(DecodeArgs a) {
         __syncthreads();
         const uint32_t tag = epoch + 1u;
         if (by_wave) {
-            route_publish(a, p, t0, max(0, t1 - t0), tag, s_qd, rk, rp);
+            route_publish(a, p, t0, max(0, t1 - t0), tag, s_qd, rx);
         } else {
             for (int c0 = t0; c0 < t1; c0 += 64) {  // uniform
                 const int nt = min(64, t1 - c0);
@@ -2464,7 +2674,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_step(DecodeArgs a) {
                     rr = route_issue<D>(a, p, c0, nt);
                     gum = route_gumbel(a, p, c0, nt);
                 }
-                route_finish<D>(a, p, c0, nt, tag, rr, s_qd, gum, rk, rp);
+                route_finish<D>(a, p, c0, nt, tag, rr, s_qd, gum, rx);
             }
         }
         if (wave_id() < G) {
@@ -2475,10 +2685,11 @@ __global__ __launch_bounds__(kThreads, 1) void k_step(DecodeArgs a) {
     }
     const uint32_t tag = epoch + 1u;
     const Views none{};
+    const StepCtx ctx{v.xk + 3 * static_cast<size_t>(p) * a.G * a.M, tag};
     if (wide)
-        attend_mfma<D, DENSE, false, PT, true>(a, none, p, iw, nwp, s_t0, s_t1, s_misc, SS, s_tab);
+        attend_mfma<D, DENSE, false, PT, true>(a, none, p, iw, nwp, s_t0, s_t1, s_misc, SS, s_tab, &ctx);
     else
-        attend_mfma<D, DENSE, false, 1, true>(a, none, p, iw, nwp, s_t0, s_t1, s_misc, SS, s_tab);
+        attend_mfma<D, DENSE, false, 1, true>(a, none, p, iw, nwp, s_t0, s_t1, s_misc, SS, s_tab, &ctx);
     step_publish_merge<D>(a, v, p, iw, nwp, tag, s_t0);
 }
 

@@ -45,9 +45,9 @@ __host__ __device__ inline int state_stride(int d) { return d + 4; }
 // per head.
 //
 // The single-launch step (`step`) uses instead: per pair a 32-bit epoch (the
-// calls the pair has completed, modulo 2^32); per (pair, head, team) two
-// tagged 64-bit words holding the perturbed score's order key (`xk`) and one
-// holding phi in fp32 (`xp`); and the tagged partial states.  Every word a
+// calls the pair has completed, modulo 2^32); per (pair, head, team) three
+// tagged 64-bit words (`xk`): the high and the low 32 bits of the perturbed
+// score's order key and phi in fp32; and the tagged partial states.  Every word a
 // call publishes carries the tag epoch + 1, so words left by earlier calls are
 // never taken for this call's; the workspace must be zero before its first
 // use and needs no reset between calls.
@@ -55,7 +55,7 @@ struct DecodeLayout {
     int nwg = 0, maxwp = 0, swords = 0;
     bool step = false;
     size_t ctr = 0, sbits = 0, lc = 0, part = 0, total = 0;
-    size_t epoch = 0, xk = 0, xp = 0;
+    size_t epoch = 0, xk = 0;
 };
 
 // Bytes of one published state of the single-launch step: d / 2 + 1 chunks
