@@ -219,8 +219,14 @@ def main():
     step_bytes = rep_bytes + attend_bytes + small_bytes
     dense_bytes = BH * (wl.N + wl.T) * row_bytes + small_bytes
 
-    attend_us = stages_us[:, 1]
-    achieved = float(np.mean(attend_bytes) / np.mean(attend_us) / 1e3)  # GB/s
+    # the launch the stage events bracket: the single step kernel (every
+    # byte of the step: routing keys, union rows, suffix, q and out) or the
+    # attention launch of the three-launch kernels (union rows and suffix)
+    kernels, _ = sp.decode_launch_info(teams, wl.Hq, wl.T, wl.K)
+    single = kernels == 1 and os.environ.get("SANTAPP_DECODE_LAUNCH") != "fused"
+    kernel_us = stages_us[:, 1]
+    kernel_bytes = step_bytes if single else attend_bytes
+    achieved = float(np.mean(kernel_bytes) / np.mean(kernel_us) / 1e3)  # GB/s
     value = float(np.mean(sparse_us))
     # eq. qwen-logical-access: one key per representative, key + value per row read
     read_fraction = float(np.mean(rep_bytes + attend_bytes) / (BH * (wl.N + wl.T) * row_bytes))
@@ -285,7 +291,7 @@ def main():
                    "B": wl.B, "Hq": wl.Hq, "Hkv": wl.Hkv, "d": wl.d, "N": wl.N, "T": wl.T,
                    "P": wl.P, "R": wl.R, "M": M, "K": wl.K, "parents": args.parents,
                    "evict_1GiB": not args.no_evict},
-        "roofline": {"bound": "hbm", "kernel": attend_kernel_name(wl, M), "achieved": round(achieved, 1),
+        "roofline": {"bound": "hbm", "kernel": attend_kernel_name(wl, M, single), "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic},
         "hbm_read_ceiling": ceiling,
@@ -299,9 +305,12 @@ def main():
         "union_rows_mean": float(np.mean(union_rows)),
         "read_fraction": round(read_fraction, 4),
         "median_us": round(float(np.median(sparse_us)), 3),
-        "stage_us_mean": {"route_select": round(float(np.mean(stages_us[:, 0])), 3),
-                          "attend": round(float(np.mean(stages_us[:, 1])), 3),
-                          "merge": round(float(np.mean(stages_us[:, 2])), 3)},
+        "stage_us_mean": ({"before_kernel": round(float(np.mean(stages_us[:, 0])), 3),
+                           "kernel": round(float(np.mean(stages_us[:, 1])), 3),
+                           "after_kernel": round(float(np.mean(stages_us[:, 2])), 3)} if single else
+                          {"route_select": round(float(np.mean(stages_us[:, 0])), 3),
+                           "attend": round(float(np.mean(stages_us[:, 1])), 3),
+                           "merge": round(float(np.mean(stages_us[:, 2])), 3)}),
         "wall_s_sparse_loop": round(t_wall1 - t_wall0, 3),
     }
     if km_steps is not None:
@@ -360,11 +369,11 @@ class HipEvents:
 
 def measured_traffic():
     """Read + write bytes per launch of the sparse attention kernel from
-    profiles/traffic_k_decode_attend_qwen32k_K32.md, or None when the kernel's
+    profiles/traffic_k_step_qwen32k_K32.md, or None when the kernel's
     sources no longer hash to the value recorded there."""
     import hashlib
     import re
-    path = os.path.join(ROOT, "profiles", "traffic_k_decode_attend_qwen32k_K32.md")
+    path = os.path.join(ROOT, "profiles", "traffic_k_step_qwen32k_K32.md")
     try:
         text = open(path).read()
     except OSError:
@@ -459,10 +468,14 @@ def upload_rows(a, dtype):
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
 
 
-def attend_kernel_name(wl, M):
-    """The launch the stage events bracket: the attention kernel of the split
-    launch, or the single kernel of the fused one (template arguments: row
-    type, head dimension, teams per sampler thread, launch mode, dense)."""
+def attend_kernel_name(wl, M, single):
+    """The launch the stage events bracket: the single step kernel (template
+    arguments: head dimension, keys per lane of the selecting waves, dense),
+    the attention kernel of the split launch, or the single kernel of the
+    fused one (row type, head dimension, teams per sampler thread, launch
+    mode, dense)."""
+    if single:
+        return f"k_step<{wl.d}, {2 if M <= 128 else 8}, {'true' if wl.K >= M else 'false'}>"
     dt = "bf16_t" if wl.dtype == "bf16" else "float"
     mode = "kFused" if os.environ.get("SANTAPP_DECODE_LAUNCH") == "fused" and wl.dtype == "bf16" else "kAttend"
     hk = 1 if M <= 512 else (4 if M <= 2048 else 16)

@@ -223,17 +223,30 @@ typedef struct {
 
 /*
  * Workspace for santapp_decode with these sizes (bytes, host-only query).
- * It holds the step's samples, read plan and partial results, and one
- * counter triple per (b, kv) pair through which the workgroups of a step hand
- * work to each other.  A workspace must be zeroed once before its first use
- * (santapp_workspace_zero); every completed call leaves its counters at zero,
- * and every other entry a call reads is written earlier in the same call.
- * Calls that share a workspace must not overlap in time (use one workspace
- * per stream).  The size depends on the compute units of the device the
- * table was built on.
+ * It holds what the workgroups of a step hand to each other: the perturbed
+ * routing scores, the samples and partial results, with per (b, kv) pair
+ * either a call counter whose value tags every word a call publishes (the
+ * single-launch step) or counters that every completed call leaves at zero
+ * (the three-launch kernels).  A workspace must be zeroed once before its
+ * first use (santapp_workspace_zero) and needs nothing between calls.  Calls
+ * that share a workspace must not overlap in time (use one workspace per
+ * stream).  The size depends on the compute units of the device the table
+ * was built on.
  */
 santapp_status santapp_decode_workspace_bytes(const santapp_teams* teams, int Hq, int T, int K,
                                               size_t* bytes);
+
+/*
+ * How santapp_decode runs a step with these sizes (host-only query): the
+ * kernel launches of one step in *kernels (1 for the single-launch step,
+ * which bf16 tables of at most 512 teams per KV head and budgets of at most
+ * 128 teams take, and for the launches SANTAPP_DECODE_LAUNCH=fused asks for;
+ * 3 otherwise for a sampled step, 2 for a budget that takes every team) and
+ * the workgroups of its main launch in *workgroups.  Errors as
+ * santapp_decode_workspace_bytes.
+ */
+santapp_status santapp_decode_launch_info(const santapp_teams* teams, int Hq, int T, int K, int* kernels,
+                                         int* workgroups);
 
 /* Zero `bytes` bytes of device memory at `ws` on `stream` (a fill kernel,
  * safe inside HIP graph capture). */

@@ -199,6 +199,14 @@ def budget_to_K(S: int, P: int, R: int, M: int) -> int:
     return k.value
 
 
+def decode_launch_info(teams: Teams, Hq: int, T: int, K: int) -> tuple:
+    """(kernel launches of one step, workgroups of its main launch) for these
+    sizes (santapp_decode_launch_info)."""
+    k, w = ctypes.c_int(), ctypes.c_int()
+    check(_lib.load().santapp_decode_launch_info(teams.handle, Hq, T, K, ctypes.byref(k), ctypes.byref(w)))
+    return k.value, w.value
+
+
 def decode_workspace(teams: Teams, Hq: int, T: int, K: int) -> torch.Tensor:
     n = ctypes.c_size_t()
     check(_lib.load().santapp_decode_workspace_bytes(teams.handle, Hq, T, K, ctypes.byref(n)))

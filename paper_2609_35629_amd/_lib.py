@@ -19,7 +19,7 @@ EXPORTS = [
     "santapp_decode_workspace_bytes", "santapp_workspace_zero", "santapp_decode", "santapp_decode_static",
     "santapp_dense_workspace_bytes", "santapp_dense_decode", "santapp_last_error",
     "santapp_teams_set_route_keys", "santapp_routing_kl_workspace_bytes", "santapp_routing_kl",
-    "santapp_kmeans_parents", "santapp_build_teams_from_labels",
+    "santapp_kmeans_parents", "santapp_build_teams_from_labels", "santapp_decode_launch_info",
 ]
 
 ROUTE_REPRESENTATIVE, ROUTE_CENTROID = 0, 1
@@ -82,6 +82,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     L.santapp_budget_to_K.argtypes = [i, i, i, i, ctypes.POINTER(i)]
     L.santapp_decode_workspace_bytes.argtypes = [vp, i, i, i, ctypes.POINTER(sz)]
     L.santapp_workspace_zero.argtypes = [vp, sz, vp]
+    L.santapp_decode_launch_info.argtypes = [vp, i, i, i, ctypes.POINTER(i), ctypes.POINTER(i)]
     L.santapp_decode.argtypes = [vp, vp, vp, vp, i, i, i, i, u64, u64, ctypes.c_double, vp, vp, sz,
                                  ctypes.POINTER(DecodeDebug), vp]
     L.santapp_decode_static.argtypes = [vp, vp, vp, vp, i, i, i, i, u64, u64, ctypes.c_double, vp,

@@ -177,6 +177,8 @@ void step_regions(DecodeLayout& L, size_t BH, int G, int M, int d, bool dense, s
     L.part = take(BH * L.maxwp * G * static_cast<size_t>(step_state_bytes(d)));
 }
 
+bool fused_wanted() { return launch_mode() == LaunchMode::kFused; }
+
 }  // namespace
 
 bool step_mode(santapp_dtype dt, int d, long long BH, int M, int Kp, bool dense, int cus) {
@@ -723,6 +725,22 @@ santapp_status santapp_decode_workspace_bytes(const santapp_teams* t, int Hq, in
     return ok();
 }
 
+santapp_status santapp_decode_launch_info(const santapp_teams* t, int Hq, int T, int K, int* kernels,
+                                         int* workgroups) {
+    if (!t || !kernels || !workgroups) return fail(SANTAPP_EINVAL, "NULL argument");
+    if (Hq < 1 || Hq % t->Hkv != 0) return fail(SANTAPP_EINVAL, "Hq must be a positive multiple of Hkv");
+    if (T < 0 || K < 1) return fail(SANTAPP_EINVAL, "T must be >= 0 and K >= 1");
+    const int Kp = std::min(K, t->M);
+    const bool dense = Kp == t->M;
+    const DecodeLayout L = dense ? dense_layout(t->B, Hq, t->Hkv, t->N, T, t->d, t->cus, t->dtype)
+                                 : decode_layout(t->B, Hq, t->Hkv, T, t->d, t->M, Kp, t->cap.data(), t->cus,
+                                                 t->dtype);
+    const bool fused = !L.step && t->dtype == SANTAPP_BF16 && fused_wanted() && L.nwg % 8 == 0;
+    *kernels = L.step || fused ? 1 : (dense ? 2 : 3);
+    *workgroups = L.nwg;
+    return ok();
+}
+
 santapp_status santapp_dense_workspace_bytes(int B, int Hq, int Hkv, int N, int T, int d,
                                              size_t* bytes) {
     if (!bytes) return fail(SANTAPP_EINVAL, "NULL argument");
@@ -736,8 +754,6 @@ santapp_status santapp_dense_workspace_bytes(int B, int Hq, int Hkv, int N, int 
 }
 
 namespace {
-
-bool fused_wanted() { return launch_mode() == LaunchMode::kFused; }
 
 santapp_status check_suffix(const void* sK, const void* sV, int T, int& stride) {
     if (T < 0) return fail(SANTAPP_EINVAL, "T must be >= 0");

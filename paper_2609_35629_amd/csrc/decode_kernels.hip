@@ -1208,7 +1208,6 @@ __device__ __forceinline__ bool walk_units(const DecodeArgs& a, const Views& v, 
 // ---------------------------------------------------------------------------
 // Single-launch step: the selection of every head of the pair in LDS.
 // ---------------------------------------------------------------------------
-constexpr int kStepSelWords = kStepMaxTeams / 64;
 
 // The pair's selection in LDS: per team the mask of the heads that sampled
 // it, and per head tau's order key -- its high half, and either the team
@@ -2829,8 +2828,7 @@ hipError_t decode_step(const DecodeArgs& a, hipStream_t s) {
     const int grid = a.lay.nwg;
     if (a.dense) return launch_one(a, k_step<D, 2, true>, grid, true, s);
     if (a.M <= 128) return launch_one(a, k_step<D, 2, false>, grid, true, s);
-    if (a.M <= 512) return launch_one(a, k_step<D, 8, false>, grid, true, s);
-    if (a.M <= kStepMaxTeams) return launch_one(a, k_step<D, 32, false>, grid, true, s);
+    if (a.M <= kStepMaxTeams) return launch_one(a, k_step<D, 8, false>, grid, true, s);
     return hipErrorInvalidValue;
 }
 

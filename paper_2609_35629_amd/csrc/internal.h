@@ -17,7 +17,7 @@ constexpr int kMaxGroup = 8;       // query heads per KV head (8-bit head masks)
 constexpr int kLogcStride = 8;     // floats per union team in the read plan
 constexpr int kUnitRows = 32;      // rows per attention unit (one 32-row step of a wave)
 constexpr int kDecodeThreads = 512;  // threads of every decode workgroup (eight waves)
-constexpr int kStepMaxTeams = 2048;  // teams per (b, kv) of the single-launch step
+constexpr int kStepMaxTeams = 512;   // teams per (b, kv) of the single-launch step
 constexpr int kStepMaxKp = 128;      // sampled teams per head of the single-launch step
 constexpr int kStepMaxWgs = 64;      // workgroups per (b, kv) pair of the single-launch step
 constexpr int kKmMaxCenters = 1024;  // k-means parents per (b, kv)
