@@ -1228,6 +1228,7 @@ struct StepSel {
 struct StepCtx {
     const uint64_t* xk;  // the pair's [G, 3, M] exchange words
     uint32_t tag;
+    const float* q;      // the pair's G query rows staged in LDS (sampled steps), else null
 };
 
 // The correction of a unit for one lane's head in flight: phi of the unit's
@@ -1332,7 +1333,11 @@ __device__ void attend_mfma(const DecodeArgs& a, const Views& v, int p, int iw, 
     auto ensure_q = [&]() {
         if (!qready) {  // uniform
             const int h = j16 & 7;
-            qk.load_q(a.q + (hq0 + (h < G ? h : 0)) * D, h < G ? a.scale_log2 : 0.f, c);
+            const int hc = h < G ? h : 0;
+            if constexpr (STEP && !DENSE)
+                qk.load_q(sc->q + hc * D, h < G ? a.scale_log2 : 0.f, c);
+            else
+                qk.load_q(a.q + (hq0 + hc) * D, h < G ? a.scale_log2 : 0.f, c);
             qready = true;
         }
     };
@@ -1346,11 +1351,10 @@ __device__ void attend_mfma(const DecodeArgs& a, const Views& v, int p, int iw, 
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) oacc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    // V copies, then K loads, of unit U into `tile` / kf.  Every step issues
-    // the same loads whether or not a next unit exists (then every lane
-    // fetches the unit's first 16 bytes: one cache line per instruction), so
-    // that the compiler's count of loads in flight, and with it the wait
-    // before each step, is the same on every path.
+    // V copies, then K loads, of unit U into `tile` / kf.  The K loads go
+    // last, so that waiting for them waits for the whole unit.  A stand-in
+    // issue (real = false) has every lane fetch the unit's first 16 bytes:
+    // one cache line per instruction.
     auto issue = [&](const Unit<bf16_t>& U, char* tile, typename QKT::frag(&kf)[2][NF], bool real) {
         const int ls = real ? lane : 0;
 #pragma unroll
@@ -1430,10 +1434,16 @@ __device__ void attend_mfma(const DecodeArgs& a, const Views& v, int p, int iw, 
 
     typename QKT::frag kf0[2][NF], kf1[2][NF];
     // The wave's units u in [lo, hi), u == gwp (mod NW), one 32-row step each.
-    // A step waits for its own data, issues the next unit's loads into the
-    // other buffers and computes while those fly; the two buffer sets
-    // alternate between two inlined copies of the step, so that each copy
-    // names its registers statically.
+    // A unit's corrections go out first, then its rows; its log c is formed
+    // while the rows fly (the wait for the corrections leaves the rows in
+    // flight).  A step waits for its own rows, issues the next unit's loads
+    // into the other buffers and computes while those fly; the two buffer
+    // sets alternate between two inlined copies of the step, so that each
+    // copy names its registers statically.  In the loop every step issues
+    // loads whether or not a next unit exists (then a stand-in issue), so
+    // that the loop's register needs are the same on every path; a wave
+    // with a single unit takes a copy of the step of its own that issues
+    // nothing.
     auto run = [&](int lo_u, int hi_u, auto&& unit, bool rev) {
         const int gs = rev ? NW - 1 - gwp : gwp;
         int u = lo_u + (((gs - lo_u) % NW) + NW) % NW;
@@ -1442,24 +1452,28 @@ __device__ void attend_mfma(const DecodeArgs& a, const Views& v, int p, int iw, 
         auto ccr = corrections(cur);
         issue(cur, tile0, kf0, true);
         ensure_q();
-        auto step = [&](char* tile, typename QKT::frag(&kf)[2][NF], char* ntile, typename QKT::frag(&nkf)[2][NF]) {
-            const bool has_next = u + NW < hi_u;
-            // this step's data first: its K fragments, and with them (issued
-            // before them) its value copies and corrections; nothing later
-            // is in flight yet, so the wait is exact.  Then the next unit
-            // goes out and flies while this one computes.
+        float cv = corr_value(ccr);
+        auto step = [&](char* tile, typename QKT::frag(&kf)[2][NF], char* ntile, typename QKT::frag(&nkf)[2][NF],
+                        auto last) {
+            constexpr bool has_next = !decltype(last)::value;
+            // this step's rows: the K fragments were issued last, so the
+            // wait for them covers the value copies too
             asm volatile("" ::"v"(kf[1][NF - 1].w) : "memory");
             float bias[4];
             bool on[4];
-            const float cv = corr_value(ccr);
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 bias[r] = -__shfl(cv, hsel + r) * kLog2e;
                 on[r] = ((cur.hmask >> (hsel + r)) & 1) != 0;
             }
-            const Unit<bf16_t> nxt = has_next ? unit(u + NW) : cur;
-            const auto ncr = corrections(nxt);
-            issue(nxt, ntile, nkf, has_next);
+            const bool more = has_next && u + NW < hi_u;
+            Unit<bf16_t> nxt = cur;
+            auto ncr = ccr;
+            if constexpr (has_next) {
+                nxt = more ? unit(u + NW) : cur;
+                ncr = corrections(nxt);
+                issue(nxt, ntile, nkf, more);
+            }
 
             // scores and the online softmax over the step's 32 rows
             const f32x4 s0 = qk.scores(kf[0]);
@@ -1506,18 +1520,27 @@ __device__ void attend_mfma(const DecodeArgs& a, const Views& v, int p, int iw, 
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb)
                 oacc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, VT::operand(tile, nb, lane), oacc[nb], 0, 0, 0);
-            if (!has_next) return false;
-            u += NW;
-            cur = nxt;
-            ccr = ncr;
+            if constexpr (has_next) {
+                if (!more) return false;
+                // the next unit's log c: its corrections were issued before
+                // its rows, which stay in flight
+                cv = corr_value(ncr);
+                u += NW;
+                cur = nxt;
+                ccr = ncr;
+            }
             return true;
         };
-        for (;;) {
-            if (!step(tile0, kf0, tile1, kf1)) break;
-            if (!step(tile1, kf1, tile0, kf0)) break;
+        if (u + NW >= hi_u) {  // uniform: a single unit
+            step(tile0, kf0, tile1, kf1, std::true_type{});
+        } else {
+            for (;;) {
+                if (!step(tile0, kf0, tile1, kf1, std::false_type{})) break;
+                if (!step(tile1, kf1, tile0, kf0, std::false_type{})) break;
+            }
         }
-        // the last step issued copies into the other tile: let them land
-        // before the tiles are used again
+        // nothing is left in flight once the last step has waited for its
+        // rows; the drain is kept for the tiles' reuse after the walk
         __builtin_amdgcn_s_waitcnt(0);
     };
 
@@ -2578,7 +2601,9 @@ __device__ void step_publish_merge(const DecodeArgs& a, const StepViews& v, int 
 
 // LDS of the single-launch step.  t0 and t1 hold the value tiles during the
 // attention; before it, t0 holds the widened queries, the Gumbel variates and
-// the waves' select scratch, and t1 the first plan pass's team table.
+// the waves' select scratch, and t1 the first plan pass's team table.  misc
+// holds the probability tiles, the plan records, the selection state and the
+// attention's fp32 copy of the pair's queries.
 template <int D>
 struct StepLds {
     static constexpr int tiles = kWaves * VTile<D>::kBytes;
@@ -2592,7 +2617,8 @@ struct StepLds {
     static constexpr int t1 = max2(tiles, 2 * kStepMaxTeams * 4);
     static constexpr int plan_off = kWaves * 1024;
     static constexpr int sel_off = (plan_off + static_cast<int>(sizeof(PlanLds)) + 15) / 16 * 16;
-    static constexpr int misc = sel_off + static_cast<int>(sizeof(StepSel));
+    static constexpr int q_off = (sel_off + static_cast<int>(sizeof(StepSel)) + 15) / 16 * 16;
+    static constexpr int misc = q_off + kMaxGroup * D * 4;
 };
 
 template <int D, int KPL, bool DENSE>
@@ -2635,6 +2661,15 @@ __global__ __launch_bounds__(kThreads, 1) void k_step(DecodeArgs a) {
             tsz[i] = a.team_size[tb0 + g];
             tbg[i] = a.team_begin[tb0 + g];
         }
+        // the pair's queries: widened for the octet routing, and the
+        // attention's fp32 copy; stored once the routing's loads are out
+        constexpr int kQ = kMaxGroup * D / kThreads;
+        float qv[kQ];
+        {
+            const float* qg = a.q + (static_cast<size_t>(b) * a.Hq + kv * G) * D;
+#pragma unroll
+            for (int i = 0; i < kQ; ++i) qv[i] = tid + i * kThreads < G * D ? qg[tid + i * kThreads] : 0.f;
+        }
         const bool by_wave = S <= kWaves;  // uniform: the split routing of at most eight teams
         RouteRegs<D> rr;
         double gum = 0.0;
@@ -2642,15 +2677,16 @@ __global__ __launch_bounds__(kThreads, 1) void k_step(DecodeArgs a) {
             route_split<D>(a, p, t0, max(0, t1 - t0), s_qd);
         } else {
             rr = route_issue<D>(a, p, t0, max(0, min(64, t1 - t0)));
-            constexpr int kQ = kMaxGroup * D / kThreads;
-            float qv[kQ];
-            const float* qg = a.q + (static_cast<size_t>(b) * a.Hq + kv * G) * D;
-#pragma unroll
-            for (int i = 0; i < kQ; ++i) qv[i] = tid + i * kThreads < G * D ? qg[tid + i * kThreads] : 0.f;
             gum = route_gumbel(a, p, t0, min(64, t1 - t0));
 #pragma unroll
             for (int i = 0; i < kQ; ++i)
                 if (tid + i * kThreads < G * D) s_qd[tid + i * kThreads] = static_cast<double>(qv[i]);
+        }
+        {
+            float* const s_q = reinterpret_cast<float*>(s_misc + L::q_off);
+#pragma unroll
+            for (int i = 0; i < kQ; ++i)
+                if (tid + i * kThreads < G * D) s_q[tid + i * kThreads] = qv[i];
         }
 #pragma unroll
         for (int i = 0; i < PT; ++i) {
@@ -2684,7 +2720,8 @@ __global__ __launch_bounds__(kThreads, 1) void k_step(DecodeArgs a) {
     }
     const uint32_t tag = epoch + 1u;
     const Views none{};
-    const StepCtx ctx{v.xk + 3 * static_cast<size_t>(p) * a.G * a.M, tag};
+    const StepCtx ctx{v.xk + 3 * static_cast<size_t>(p) * a.G * a.M, tag,
+                      DENSE ? nullptr : reinterpret_cast<const float*>(s_misc + L::q_off)};
     if (wide)
         attend_mfma<D, DENSE, false, PT, true>(a, none, p, iw, nwp, s_t0, s_t1, s_misc, SS, s_tab, &ctx);
     else
