@@ -33,15 +33,9 @@ def hipcc() -> str:
     return p
 
 
-# the decode kernels take the single-launch step's hot pointers and shapes as
-# leading scalar arguments, which the dispatch preloads into scalar registers
-# (a kernel whose only argument is a struct preloads nothing)
-FILE_FLAGS = {"decode_kernels.hip": ["-mllvm", "-amdgpu-kernarg-preload-count=7"]}
-
-
 def _compile(src: str) -> str:
     obj = os.path.join(OBJDIR, os.path.splitext(src)[0] + ".o")
-    cmd = [hipcc(), *CFLAGS, *FILE_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [hipcc(), *CFLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{r.stderr}")

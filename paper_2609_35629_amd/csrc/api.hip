@@ -108,7 +108,9 @@ void free_teams(santapp_teams* t) {
     release(t->packed_K);
     release(t->packed_V);
     release(t->reps);
-    release(t->log_n);  // the team table's block (team_begin and team_size point into it)
+    release(t->team_begin);
+    release(t->team_size);
+    release(t->log_n);
     release(t->rep_token);
     release(t->perm);
     release(t->team_count);
@@ -116,19 +118,6 @@ void free_teams(santapp_teams* t) {
 }
 
 santapp_status finish_table(santapp_teams* t, santapp_teams** out);
-
-// The team table as one block: log_n [n] doubles, then team_begin [n] and
-// team_size [n] ints, so that one pointer and n locate all three (the
-// decode step receives the block's base).
-template <typename Alloc>
-void alloc_table(santapp_teams* t, size_t n, Alloc&& alloc) {
-    void* block = nullptr;
-    alloc(&block, n * (sizeof(double) + 2 * sizeof(int)));
-    if (!block) return;
-    t->log_n = static_cast<double*>(block);
-    t->team_begin = reinterpret_cast<int*>(t->log_n + n);
-    t->team_size = t->team_begin + n;
-}
 
 }  // namespace
 
@@ -315,7 +304,9 @@ santapp_status santapp_build_teams(const void* K, const void* V, int B, int Hkv,
     alloc(&t->packed_K, BH * N * row);
     alloc(&t->packed_V, BH * N * row);
     alloc(&t->reps, BH * M * row);
-    alloc_table(t, BH * M, alloc);
+    alloc(reinterpret_cast<void**>(&t->team_begin), BH * M * sizeof(int));
+    alloc(reinterpret_cast<void**>(&t->team_size), BH * M * sizeof(int));
+    alloc(reinterpret_cast<void**>(&t->log_n), BH * M * sizeof(double));
     alloc(reinterpret_cast<void**>(&t->rep_token), BH * M * sizeof(int));
     alloc(reinterpret_cast<void**>(&t->perm), BH * N * sizeof(int));
     alloc(reinterpret_cast<void**>(&t->team_count), BH * sizeof(int));
@@ -555,7 +546,9 @@ santapp_status santapp_build_teams_from_labels(const void* K, const void* V, int
     alloc(&t->packed_K, BH * N * row);
     alloc(&t->packed_V, BH * N * row);
     alloc(&t->reps, BH * M * row);
-    alloc_table(t, BH * M, alloc);
+    alloc(reinterpret_cast<void**>(&t->team_begin), BH * M * sizeof(int));
+    alloc(reinterpret_cast<void**>(&t->team_size), BH * M * sizeof(int));
+    alloc(reinterpret_cast<void**>(&t->log_n), BH * M * sizeof(double));
     alloc(reinterpret_cast<void**>(&t->rep_token), BH * M * sizeof(int));
     alloc(reinterpret_cast<void**>(&t->perm), BH * N * sizeof(int));
     alloc(reinterpret_cast<void**>(&t->team_count), BH * sizeof(int));

@@ -1242,46 +1242,7 @@ struct CorrWords {
 // launch, with the heads' samples taken from LDS and the first pass's team
 // sizes and begins from the LDS copy s_tab (size, begin per team) made when
 // the step started (later passes read the table in memory).
-// The plan of a step's single pass over its M <= 512 teams, a team per
-// thread, without a workgroup scan: each wave sums the packed counts of the
-// teams before its own 64 (lane l reads teams 64 v + l) and scans its own;
-// one barrier then publishes the records.  Returns (union teams, units,
-// rows) as plan_records (rows only when `rows`).
-__device__ __forceinline__ int3 plan_step(int M, const StepSel* SS, const int* s_tab, PlanLds& P, bool rows) {
-    static_assert(kStepMaxTeams == kWaves * kWave, "a team per thread");
-    const int lane = lane_id(), w = wave_id();
-    int before = 0, total = 0, rtotal = 0, own = 0, own_hm = 0, own_sz = 0;
-#pragma unroll
-    for (int v = 0; v < kWaves; ++v) {
-        const int g = kWave * v + lane;
-        const int hm = g < M ? static_cast<int>((SS->hm[g >> 2] >> (8 * (g & 3))) & 0xffu) : 0;
-        const int sz = s_tab[2 * min(g, M - 1)];
-        const int x = hm ? (1 | (chunk_count(sz) << 12)) : 0;
-        before += v < w ? x : 0;
-        total += x;
-        rtotal += hm ? sz : 0;
-        if (v == w) {
-            own = x;
-            own_hm = hm;
-            own_sz = sz;
-        }
-    }
-    before = readlane(wave_incl_scan(before), kWave - 1);
-    total = readlane(wave_incl_scan(total), kWave - 1);
-    rtotal = rows ? readlane(wave_incl_scan(rtotal), kWave - 1) : 0;
-    const int ex = before + wave_incl_scan(own) - own;
-    if (own_hm) {
-        const int g = kWave * w + lane;
-        const int slot = ex & 0xfff, ust = ex >> 12, nck = own >> 12;
-        if (slot < kPlanRecs) P.rec[slot] = make_int4(ust, s_tab[2 * g + 1], own_sz, g | (own_hm << 16));
-        if ((total >> 12) <= kPlanUnits)
-            for (int c = 0; c < nck; ++c) P.u2t[ust + c] = static_cast<unsigned short>(slot);
-    }
-    __syncthreads();
-    return make_int3(total & 0xfff, total >> 12, rtotal);
-}
-
-template <typename T, bool DENSE, typename Run>
+template <typename T, bool DENSE, int PT, typename Run>
 __device__ __forceinline__ bool step_walk_units(const DecodeArgs& a, int p, int iw, char* plan_lds, const StepSel* SS,
                                                 const int* s_tab, Run&& run) {
     PlanLds& P = *reinterpret_cast<PlanLds*>(plan_lds);
@@ -1292,15 +1253,44 @@ __device__ __forceinline__ bool step_walk_units(const DecodeArgs& a, int p, int 
         run(nsuf, nsuf + (a.N + kUnitRows - 1) / kUnitRows, by_index, false);
         return true;
     }
-    // the host takes the step only for M <= kStepMaxTeams: one plan pass
-    if (a.M > kStepMaxTeams) return false;
-    const int3 t = plan_step(a.M, SS, s_tab, P, a.dbg_urows != nullptr);
-    // the suffix units come first
-    run(0, nsuf + t.y, [&](int u) { return u < nsuf ? by_index(u) : plan_unit<T>(a, P, p, u - nsuf, t.x, t.y); },
-        false);
-    if (iw == 0 && threadIdx.x == 0) {
-        if (a.dbg_uteams) a.dbg_uteams[p] = t.x;
-        if (a.dbg_urows) a.dbg_urows[p] = t.z;
+    const int tid = threadIdx.x, M = a.M;
+    const size_t tb0 = static_cast<size_t>(p) * M;
+    int run_u = nsuf, run_teams = 0, run_rows = 0;
+    for (int base = 0; base < M; base += kThreads * PT) {
+        const int g0 = base + tid * PT;
+        int sz[PT], bg[PT], hm[PT];
+#pragma unroll
+        for (int k = 0; k < PT; ++k) {
+            const int g = min(g0 + k, M - 1);
+            if (base == 0) {
+                sz[k] = s_tab[2 * g];
+                bg[k] = s_tab[2 * g + 1];
+            } else {
+                sz[k] = a.team_size[tb0 + g];
+                bg[k] = a.team_begin[tb0 + g];
+            }
+            hm[k] = 0;
+        }
+        if (g0 < M) {
+#pragma unroll
+            for (int k = 0; k < PT; ++k) {
+                const int g = min(g0 + k, M - 1);
+                hm[k] = static_cast<int>((SS->hm[g >> 2] >> (8 * (g & 3))) & 0xffu);
+            }
+        }
+        const int3 t = plan_records<PT>(g0, M, hm, sz, bg, P, a.dbg_urows != nullptr);
+        // the suffix units come first in the first pass's run
+        const int lo = base == 0 ? 0 : run_u, first = run_u;
+        run(lo, run_u + t.y,
+            [&](int u) { return u < first ? by_index(u) : plan_unit<T>(a, P, p, u - first, t.x, t.y); }, false);
+        run_u += t.y;
+        run_teams += t.x;
+        run_rows += t.z;
+        if (base + kThreads * PT < M) __syncthreads();  // the records are rewritten by the next pass
+    }
+    if (iw == 0 && tid == 0) {
+        if (a.dbg_uteams) a.dbg_uteams[p] = run_teams;
+        if (a.dbg_urows) a.dbg_urows[p] = run_rows;
     }
     return SS->ok != 0;
 }
@@ -1556,7 +1546,7 @@ __device__ void attend_mfma(const DecodeArgs& a, const Views& v, int p, int iw, 
 
     bool ok;
     if constexpr (STEP)
-        ok = step_walk_units<bf16_t, DENSE>(a, p, iw, plan_lds, SS, s_tab, run);
+        ok = step_walk_units<bf16_t, DENSE, PT>(a, p, iw, plan_lds, SS, s_tab, run);
     else
         ok = walk_units<bf16_t, DENSE, FUSED, PT>(a, v, p, iw, plan_lds, run);
 
@@ -1919,50 +1909,6 @@ __device__ __forceinline__ StepViews step_views(const DecodeArgs& a) {
     return v;
 }
 
-// What the step's first loads address, passed as the kernel's leading scalar
-// arguments so that the dispatch can preload them into scalar registers (the
-// kernel's first loads then wait for no argument fetch): the queries, the
-// routing keys, the team table's block (log n [B Hkv M] doubles, then the
-// team begins and sizes), the pairs' epochs and exchange words, and the
-// shapes packed three to a word: M | G << 12 | workgroups << 16 and
-// Hkv | Hq << 9 | B Hkv << 21.
-struct StepHot {
-    const float* q;
-    const void* reps;
-    const double* log_n;
-    const int* tbegin;
-    const int* tsize;
-    uint32_t* epoch;
-    uint64_t* xk;
-    int M, G, Hkv, Hq, nwg, BH;
-};
-
-// The step kernel's parameter list as a struct: the kernel argument segment
-// lays the parameters out as this struct's members.
-struct StepKernelArgs {
-    const float* q;
-    const void* reps;
-    const double* tab;
-    uint32_t* epochs;
-    uint64_t* xk;
-    uint32_t s0, s1;
-    DecodeArgs a;
-};
-
-// The step kernel's DecodeArgs, read in place in the kernel argument segment
-// through a pointer the compiler cannot see through, so that no argument
-// load is hoisted above (and no wait for one is placed before) the loads
-// issued ahead of this point.  The parameter itself is never named in the
-// kernel: naming it would make a private copy.
-__device__ __forceinline__ const DecodeArgs& late_args() {
-    using ConstArgs = const __attribute__((address_space(4))) DecodeArgs;
-    const __attribute__((address_space(4))) char* const seg =
-        (const __attribute__((address_space(4))) char*)__builtin_amdgcn_kernarg_segment_ptr();
-    ConstArgs* p = (ConstArgs*)(seg + offsetof(StepKernelArgs, a));
-    asm volatile("" : "+s"(p));
-    return *(const DecodeArgs*)(p);
-}
-
 // Publish Y (as its order key, high and low 32 bits) and phi of (head h,
 // team g) to the pair's exchange words (rx covers the pair's G * 3 * M words).
 __device__ __forceinline__ void publish_item(__amdgpu_buffer_rsrc_t rx, int M, int h, int g, double phi, double y,
@@ -2073,19 +2019,18 @@ __device__ __forceinline__ double readlane_f64(double v, int l) {
 // Both land in s_pg (phi [8][8], then the variates [8][8]); route_publish
 // forms Y after the workgroup barrier that follows.
 template <int D>
-__device__ __forceinline__ void route_split(const DecodeArgs& a, const StepHot& hot, int p, int c0, int nt,
-                                            double* s_pg) {
+__device__ __forceinline__ void route_split(const DecodeArgs& a, int p, int c0, int nt, double* s_pg) {
     constexpr int EPL = D / 32;  // 4 (d = 128) or 2 (d = 64)
     static_assert(EPL == 2 || EPL == 4, "two or four dims per lane");
     const int lane = lane_id(), w = wave_id();
-    const int G = hot.G, M = hot.M, b = p / hot.Hkv, kv = p - b * hot.Hkv;
+    const int G = a.G, M = a.M, b = p / a.Hkv, kv = p - b * a.Hkv;
     if (w < 4) {
         if (2 * w >= nt) return;  // uniform
         const int t = 2 * w + (lane >> 5), l = lane & 31;
         const int g = c0 + min(t, nt - 1);
         const size_t tg = static_cast<size_t>(p) * M + g;
         // every load first (heads beyond G read head G - 1's dims)
-        const bf16_t* row = static_cast<const bf16_t*>(hot.reps) + tg * D + l * EPL;
+        const bf16_t* row = static_cast<const bf16_t*>(a.reps) + tg * D + l * EPL;
         uint32_t kr[EPL / 2];
         if constexpr (EPL == 4) {
             const uint2 x = *reinterpret_cast<const uint2*>(row);
@@ -2094,8 +2039,8 @@ __device__ __forceinline__ void route_split(const DecodeArgs& a, const StepHot& 
         } else {
             kr[0] = *reinterpret_cast<const uint32_t*>(row);
         }
-        const double ln = hot.log_n[tg];
-        const float* qg = hot.q + (static_cast<size_t>(b) * hot.Hq + kv * G) * D + l * EPL;
+        const double ln = a.log_n[tg];
+        const float* qg = a.q + (static_cast<size_t>(b) * a.Hq + kv * G) * D + l * EPL;
         float qv[kMaxGroup][EPL];
 #pragma unroll
         for (int h = 0; h < kMaxGroup; ++h) {
@@ -2328,10 +2273,9 @@ __device__ uint32_t wave_rank32_exact(const uint32_t (&k)[KPL], int M, int want,
 // the count strictly above it: a 256-bin value histogram over [min, max] of
 // the keys' fp32 values, then a direct ranking of the keys in the bin that
 // holds rank `want`; the exact radix where that bin holds more than 64 keys
-// or the keys span no finite fp32 range.  `equal` is the count of keys equal
-// to the result (0 where the exact radix ran: not counted).
+// or the keys span no finite fp32 range.
 template <int KPL>
-__device__ uint32_t wave_rank32(const uint32_t (&k)[KPL], int M, int want, WaveSel& W, int& above, int& equal) {
+__device__ uint32_t wave_rank32(const uint32_t (&k)[KPL], int M, int want, WaveSel& W, int& above) {
     const int lane = lane_id();
     float y[KPL];
     float lo = __builtin_inff(), hi = -__builtin_inff();
@@ -2346,7 +2290,6 @@ __device__ uint32_t wave_rank32(const uint32_t (&k)[KPL], int M, int want, WaveS
     lo = wave_ext_f<true>(lo);
     hi = wave_ext_f<false>(hi);
     const float range = hi - lo;
-    equal = 0;
     if (!(range > 0.f) || !(range < 3.0e38f)) return wave_rank32_exact<KPL>(k, M, want, W, above);
     const float fs = 255.99f / range;
     reinterpret_cast<uint4*>(W.hist)[lane] = make_uint4(0, 0, 0, 0);
@@ -2383,7 +2326,6 @@ __device__ uint32_t wave_rank32(const uint32_t (&k)[KPL], int M, int want, WaveS
     const bool owner = lane < n && gt <= rest && rest < ge;
     const int src = __ffsll(static_cast<unsigned long long>(__ballot(owner))) - 1;
     above = hcnt + readlane(gt, src);
-    equal = readlane(ge - gt, src);  // keys equal to the result all fall in its bin
     return static_cast<uint32_t>(readlane(static_cast<int>(mine), src));
 }
 
@@ -2439,24 +2381,20 @@ __device__ bool step_select(const DecodeArgs& a, const StepViews& v, int p, int 
         if (64 * j + lane < M) valid |= 1u << j;
     }
     bool ok = poll_words<KPL>(rh, off, valid, tag, k);
-    int above, bcnt;
-    const uint32_t th = wave_rank32<KPL>(k, M, Kp, W, above, bcnt);
-    if (bcnt == 0) {  // uniform: the exact radix ran; count the keys equal to th
+    int above;
+    const uint32_t th = wave_rank32<KPL>(k, M, Kp, W, above);
+    int bcnt = 0;
 #pragma unroll
-        for (int j = 0; j < KPL; ++j) bcnt += static_cast<int>(__popcll(__ballot(((valid >> j) & 1u) && k[j] == th)));
-    }
+    for (int j = 0; j < KPL; ++j) bcnt += static_cast<int>(__popcll(__ballot(((valid >> j) & 1u) && k[j] == th)));
     uint64_t selw[KPL];
+    int tau_g = -1;
     uint32_t tau_lo = 0;
-    const bool fast = bcnt == 1;  // uniform
-    if (fast) {
-        // the sample is every key whose high half exceeds th: each lane sets
-        // the head's bit of its own sampled teams, and the lane that holds
-        // th names tau's team (its low half is read with the units' rows)
+    if (bcnt == 1) {  // uniform: the sample is every key whose high half exceeds th
 #pragma unroll
         for (int j = 0; j < KPL; ++j) {
-            const int g = 64 * j + lane;
-            if (((valid >> j) & 1u) && k[j] > th) atomicOr(&SS.hm[g >> 2], 1u << (h + 8 * (g & 3)));
-            if (((valid >> j) & 1u) && k[j] == th) SS.tau_g[h] = g;
+            selw[j] = __ballot(((valid >> j) & 1u) && k[j] > th);
+            const uint64_t t = __ballot(((valid >> j) & 1u) && k[j] == th);
+            if (t) tau_g = 64 * j + __ffsll(static_cast<unsigned long long>(t)) - 1;
         }
     } else {  // several keys share tau's high half: rank the exact keys
         uint32_t offl[KPL], lo[KPL];
@@ -2489,23 +2427,18 @@ __device__ bool step_select(const DecodeArgs& a, const StepViews& v, int p, int 
             selw[j] = sb;
         }
     }
-    // tau for the corrections: its high half (also the high half of the
-    // exact path's key: truncation keeps the order), and where its low half
-    // is
+    // tau for the corrections: its high half, and where its low half is
     if (lane == 0) {
-        SS.tau_hi[h] = th;
-        if (!fast) {
-            SS.tau_g[h] = -1;
-            SS.tau_lo[h] = tau_lo;
-        }
+        SS.tau_hi[h] = th;  // also the high half of the exact path's key (truncation keeps the order)
+        SS.tau_g[h] = tau_g;
+        SS.tau_lo[h] = tau_lo;
     }
-    if (!fast) {  // the head's bit in the masks of its sampled teams
+    // the head's bit in the masks of its sampled teams
 #pragma unroll
-        for (int j = 0; j < KPL; ++j) {
-            if ((selw[j] >> lane) & 1ull) {
-                const int g = 64 * j + lane;
-                atomicOr(&SS.hm[g >> 2], 1u << (h + 8 * (g & 3)));
-            }
+    for (int j = 0; j < KPL; ++j) {
+        if ((selw[j] >> lane) & 1ull) {
+            const int g = 64 * j + lane;
+            atomicOr(&SS.hm[g >> 2], 1u << (h + 8 * (g & 3)));
         }
     }
     // diagnostics (one workgroup of the pair): tau, the sample in ascending
@@ -2513,15 +2446,6 @@ __device__ bool step_select(const DecodeArgs& a, const StepViews& v, int p, int 
     const size_t bq = static_cast<size_t>(b) * a.Hq + kv * G + h;
     double tau = 0.0;
     if (iw == 0 && (a.dbg_tau || a.dbg_sel || a.dbg_logc)) {  // uniform
-        int tau_g = -1;
-        if (fast) {
-#pragma unroll
-            for (int j = 0; j < KPL; ++j) {
-                selw[j] = __ballot(((valid >> j) & 1u) && k[j] > th);
-                const uint64_t t = __ballot(((valid >> j) & 1u) && k[j] == th);
-                if (t) tau_g = 64 * j + __ffsll(static_cast<unsigned long long>(t)) - 1;
-            }
-        }
         uint32_t tl = tau_lo;
         if (tau_g >= 0) {
             uint32_t o1[1] = {row1 + static_cast<uint32_t>(tau_g) * 8u}, v1[1] = {0};
@@ -2698,69 +2622,59 @@ struct StepLds {
 };
 
 template <int D, int KPL, bool DENSE>
-__global__ __launch_bounds__(kThreads, 1) void k_step(const float* q, const void* reps, const double* tab,
-                                                      uint32_t* epochs, uint64_t* xk, uint32_t s0, uint32_t s1,
-                                                      DecodeArgs /* read through late_args() */) {
+__global__ __launch_bounds__(kThreads, 1) void k_step(DecodeArgs a) {
     using L = StepLds<D>;
     static_assert(L::t0 + L::t1 + L::misc <= 160 * 1024, "the step's LDS fits one compute unit");
     __shared__ __attribute__((aligned(16))) char s_t0[L::t0];
     __shared__ __attribute__((aligned(16))) char s_t1[L::t1];
     __shared__ __attribute__((aligned(16))) char s_misc[L::misc];
-    StepHot hot;
-    hot.q = q;
-    hot.reps = reps;
-    hot.M = static_cast<int>(s0 & 0xfffu);
-    hot.G = static_cast<int>((s0 >> 12) & 0xfu);
-    hot.nwg = static_cast<int>(s0 >> 16);
-    hot.Hkv = static_cast<int>(s1 & 0x1ffu);
-    hot.Hq = static_cast<int>((s1 >> 9) & 0xfffu);
-    hot.BH = static_cast<int>(s1 >> 21);
-    hot.log_n = tab;
-    hot.tbegin = reinterpret_cast<const int*>(tab + static_cast<size_t>(hot.BH) * hot.M);
-    hot.tsize = hot.tbegin + static_cast<size_t>(hot.BH) * hot.M;
-    hot.epoch = epochs;
-    hot.xk = xk;
-    const PairSlot sl = pair_slot(blockIdx.x, hot.nwg, hot.BH);
+    const StepViews v = step_views(a);
+    const PairSlot sl = pair_slot(blockIdx.x, gridDim.x, a.B * a.Hkv);
     const int p = sl.p, iw = sl.iw, nwp = sl.nwp;
     // the call's tag (epoch + 1) is formed where it is first needed, so that
     // the epoch load does not hold up the loads issued after it
-    const uint32_t epoch = load_u32_coherent(hot.epoch + p);
+    const uint32_t epoch = load_u32_coherent(v.epoch + p);
     StepSel* const SS = reinterpret_cast<StepSel*>(s_misc + L::sel_off);
     int* const s_tab = reinterpret_cast<int*>(s_t1);
     const int tid = threadIdx.x;
-    const int G = hot.G, M = hot.M;
-    const int b = p / hot.Hkv, kv = p - b * hot.Hkv;
-    const int S = step_slice(M, nwp);
-    const int t0 = iw * S, t1 = min(M, t0 + S);
-    // everything the routing needs is requested first: the plan's team table
-    // (M <= 512: a team per thread) and the pair's queries (widened for the
-    // octet routing, and the attention's fp32 copy; stored once the
-    // routing's own loads are out); the routing keys follow
-    static_assert(kStepMaxTeams <= kThreads, "the team table is one entry per thread");
-    constexpr int kQ = kMaxGroup * D / kThreads;
-    int tsz = 0, tbg = 0;
-    float qv[kQ];
+    // the plan passes take PT teams per thread when the heads' union fits one
+    // pass's records, else one
+    constexpr int PT = KPL >= 8 ? KPL / 8 : 1;
+    const bool wide = !DENSE && static_cast<long long>(a.G) * a.Kp <= kPlanRecs;
     if constexpr (!DENSE) {
-        const size_t tb0 = static_cast<size_t>(p) * M;
-        const int tg = min(tid, M - 1);
-        tsz = hot.tsize[tb0 + tg];
-        tbg = hot.tbegin[tb0 + tg];
-        const float* qg = hot.q + (static_cast<size_t>(b) * hot.Hq + kv * G) * D;
-#pragma unroll
-        for (int i = 0; i < kQ; ++i) qv[i] = tid + i * kThreads < G * D ? qg[tid + i * kThreads] : 0.f;
-    }
-    const DecodeArgs& a = late_args();
-    const StepViews v = step_views(a);
-    if constexpr (!DENSE) {
+        const int G = a.G, M = a.M;
+        const int b = p / a.Hkv, kv = p - b * a.Hkv;
         double* const s_qd = reinterpret_cast<double*>(s_t0);
         WaveSel* const s_ws = reinterpret_cast<WaveSel*>(s_t0 + L::qd);
-        const __amdgpu_buffer_rsrc_t rx = coherent_rsrc(hot.xk + 3 * static_cast<size_t>(p) * G * M,
+        const int S = step_slice(M, nwp);
+        const int t0 = iw * S, t1 = min(M, t0 + S);
+        const __amdgpu_buffer_rsrc_t rx = coherent_rsrc(v.xk + 3 * static_cast<size_t>(p) * G * M,
                                                         static_cast<uint32_t>(G) * M * 24u);
+        // everything the routing needs is requested at once: the slice's
+        // routing keys, the queries and the first plan pass's table
+        const size_t tb0 = static_cast<size_t>(p) * M;
+        const int first = min(M, kThreads * (wide ? PT : 1));
+        int tsz[PT], tbg[PT];
+#pragma unroll
+        for (int i = 0; i < PT; ++i) {
+            const int g = min(tid + i * kThreads, M - 1);
+            tsz[i] = a.team_size[tb0 + g];
+            tbg[i] = a.team_begin[tb0 + g];
+        }
+        // the pair's queries: widened for the octet routing, and the
+        // attention's fp32 copy; stored once the routing's loads are out
+        constexpr int kQ = kMaxGroup * D / kThreads;
+        float qv[kQ];
+        {
+            const float* qg = a.q + (static_cast<size_t>(b) * a.Hq + kv * G) * D;
+#pragma unroll
+            for (int i = 0; i < kQ; ++i) qv[i] = tid + i * kThreads < G * D ? qg[tid + i * kThreads] : 0.f;
+        }
         const bool by_wave = S <= kWaves;  // uniform: the split routing of at most eight teams
         RouteRegs<D> rr;
         double gum = 0.0;
         if (by_wave) {
-            route_split<D>(a, hot, p, t0, max(0, t1 - t0), s_qd);
+            route_split<D>(a, p, t0, max(0, t1 - t0), s_qd);
         } else {
             rr = route_issue<D>(a, p, t0, max(0, min(64, t1 - t0)));
             gum = route_gumbel(a, p, t0, min(64, t1 - t0));
@@ -2774,9 +2688,13 @@ __global__ __launch_bounds__(kThreads, 1) void k_step(const float* q, const void
             for (int i = 0; i < kQ; ++i)
                 if (tid + i * kThreads < G * D) s_q[tid + i * kThreads] = qv[i];
         }
-        if (tid < M) {
-            s_tab[2 * tid] = tsz;
-            s_tab[2 * tid + 1] = tbg;
+#pragma unroll
+        for (int i = 0; i < PT; ++i) {
+            const int g = tid + i * kThreads;
+            if (g < first) {
+                s_tab[2 * g] = tsz[i];
+                s_tab[2 * g + 1] = tbg[i];
+            }
         }
         for (int i = tid; i < (M + 3) / 4; i += kThreads) SS->hm[i] = 0;
         if (tid == 0) SS->ok = 1;
@@ -2802,9 +2720,12 @@ __global__ __launch_bounds__(kThreads, 1) void k_step(const float* q, const void
     }
     const uint32_t tag = epoch + 1u;
     const Views none{};
-    const StepCtx ctx{hot.xk + 3 * static_cast<size_t>(p) * G * M, tag,
+    const StepCtx ctx{v.xk + 3 * static_cast<size_t>(p) * a.G * a.M, tag,
                       DENSE ? nullptr : reinterpret_cast<const float*>(s_misc + L::q_off)};
-    attend_mfma<D, DENSE, false, 1, true>(a, none, p, iw, nwp, s_t0, s_t1, s_misc, SS, s_tab, &ctx);
+    if (wide)
+        attend_mfma<D, DENSE, false, PT, true>(a, none, p, iw, nwp, s_t0, s_t1, s_misc, SS, s_tab, &ctx);
+    else
+        attend_mfma<D, DENSE, false, 1, true>(a, none, p, iw, nwp, s_t0, s_t1, s_misc, SS, s_tab, &ctx);
     step_publish_merge<D>(a, v, p, iw, nwp, tag, s_t0);
 }
 
@@ -2939,36 +2860,12 @@ hipError_t decode_sampled(const DecodeArgs& a, hipStream_t s) {
 
 // The single-launch step (bf16): keys per lane of the selecting waves by the
 // team count.
-template <int D, int KPL, bool DENSE>
-hipError_t launch_step(const DecodeArgs& a, hipStream_t s) {
-    const int grid = a.lay.nwg, BH = a.B * a.Hkv;
-    // the packed shapes' fields (the step's own limits are narrower)
-    if (a.M > 0xfff || a.G > 0xf || grid > 0xffff || a.Hkv > 0x1ff || a.Hq > 0xfff || BH > 0x7ff)
-        return hipErrorInvalidValue;
-    const uint32_t s0 = static_cast<uint32_t>(a.M) | (static_cast<uint32_t>(a.G) << 12) |
-                        (static_cast<uint32_t>(grid) << 16);
-    const uint32_t s1 = static_cast<uint32_t>(a.Hkv) | (static_cast<uint32_t>(a.Hq) << 9) |
-                        (static_cast<uint32_t>(BH) << 21);
-    // the sampled step reads the team table through its block's base
-    if (!a.dense && (a.team_begin != reinterpret_cast<const int*>(a.log_n + static_cast<size_t>(BH) * a.M) ||
-                     a.team_size != a.team_begin + static_cast<size_t>(BH) * a.M))
-        return hipErrorInvalidValue;
-    uint32_t* const epochs = reinterpret_cast<uint32_t*>(a.ws + a.lay.epoch);
-    uint64_t* const xk = reinterpret_cast<uint64_t*>(a.ws + a.lay.xk);
-    auto* const kernel = k_step<D, KPL, DENSE>;
-    if (a.ev_start || a.ev_stop)
-        hipExtLaunchKernelGGL(kernel, dim3(grid), dim3(kThreads), 0, s, a.ev_start, a.ev_stop, 0, a.q, a.reps,
-                              a.log_n, epochs, xk, s0, s1, a);
-    else
-        hipLaunchKernelGGL(kernel, dim3(grid), dim3(kThreads), 0, s, a.q, a.reps, a.log_n, epochs, xk, s0, s1, a);
-    return hipGetLastError();
-}
-
 template <int D>
 hipError_t decode_step(const DecodeArgs& a, hipStream_t s) {
-    if (a.dense) return launch_step<D, 2, true>(a, s);
-    if (a.M <= 128) return launch_step<D, 2, false>(a, s);
-    if (a.M <= kStepMaxTeams) return launch_step<D, 8, false>(a, s);
+    const int grid = a.lay.nwg;
+    if (a.dense) return launch_one(a, k_step<D, 2, true>, grid, true, s);
+    if (a.M <= 128) return launch_one(a, k_step<D, 2, false>, grid, true, s);
+    if (a.M <= kStepMaxTeams) return launch_one(a, k_step<D, 8, false>, grid, true, s);
     return hipErrorInvalidValue;
 }
 
