@@ -2545,6 +2545,12 @@ __device__ void step_publish_merge(const DecodeArgs& a, const StepViews& v, int 
     // merge tasks: task t = 16 h + c (head h, dims [c D / 16, (c + 1) D / 16))
     // runs on workgroup t mod nwp, wave (t / nwp) mod 8, so that the merge of
     // a pair is spread over many compute units and each poll is small
+    // The merge waves hold off their first poll for about 0.8 us: the pair's
+    // last states land that long or more after this workgroup's, and polls
+    // issued meanwhile load the memory-side cache that the pair's last
+    // workgroups still read their rows through (measured: the step, sampled
+    // and dense, ends sooner with the pause than without it or with 2 us).
+    __builtin_amdgcn_s_sleep(30);
     for (int t = iw + wv * nwp; t < kParts * G; t += kWaves * nwp) {
         const int h = t / kParts, c = t % kParts;
         const bool live = lane < nwp;
@@ -2713,6 +2719,10 @@ __global__ __launch_bounds__(kThreads, 1) void k_step(DecodeArgs a) {
             }
         }
         if (wave_id() < G) {
+            // as for the merge: a pause of about 0.5 us before the first poll
+            // of the pair's keys, which the other workgroups are still
+            // publishing
+            __builtin_amdgcn_s_sleep(20);
             const bool ok = step_select<KPL>(a, v, p, iw, tag, s_ws[wave_id()], *SS);
             if (!ok && lane_id() == 0) SS->ok = 0;
         }
