@@ -18,7 +18,7 @@ constexpr int kLogcStride = 8;     // floats per union team in the read plan
 constexpr int kUnitRows = 32;      // rows per attention unit (one 32-row step of a wave)
 constexpr int kDecodeThreads = 512;  // threads of every decode workgroup (eight waves)
 constexpr int kStepMaxTeams = 512;   // teams per (b, kv) of the single-launch step
-constexpr int kStepMaxKp = 128;      // sampled teams per head of the single-launch step
+constexpr int kStepMaxKp = kStepMaxTeams;  // K + 1 of the single-launch step: any budget below M
 constexpr int kStepMaxWgs = 64;      // workgroups per (b, kv) pair of the single-launch step
 constexpr int kKmMaxCenters = 1024;  // k-means parents per (b, kv)
 constexpr int kKmMaxTrials = 8;      // seeding candidates per round: 2 + floor(ln 1024)
@@ -63,7 +63,7 @@ struct DecodeLayout {
 __host__ __device__ inline int step_state_bytes(int d) { return (d / 2 + 1) * 16; }
 
 // Whether a step takes the single-launch kernel: bf16 rows of 64 or 128 dims,
-// at most kStepMaxTeams teams and kStepMaxKp sampled teams (sampled steps), and
+// at most kStepMaxTeams teams (any budget below the team count), and
 // at most one (b, kv) pair per compute unit; unless SANTAPP_DECODE_LAUNCH asks
 // for the split or fused launches.
 bool step_mode(santapp_dtype dt, int d, long long BH, int M, int Kp, bool dense, int cus);

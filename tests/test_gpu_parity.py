@@ -154,6 +154,14 @@ def test_qwen8k():
     assert teams.M == 128
 
 
+def test_headline_32k_large_budget():
+    # K = 200 of 512 teams per head: the union is most of the teams, and the
+    # single-launch step's waves walk several units each
+    wl = datagen.WORKLOADS["qwen32k"]
+    _, res = _run(wl, K=200, steps=range(3), check_tables=False)
+    log(f"[gpu]   K=200: worst rel-L2 {max(c.rel_l2.max() for c, _, _ in res):.3e}")
+
+
 @pytest.mark.parametrize("K", [31, 32, 64])
 def test_headline_32k(K):
     # steps 0..99: 2800 (query, head) instances per budget
