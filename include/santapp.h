@@ -273,10 +273,14 @@ santapp_status santapp_workspace_zero(void* ws, size_t bytes, void* stream);
  * out:      [B,Hq,d] fp32 estimate U^ / Z^.
  * Routing logits, the perturbed scores, the selection and tau are computed in
  * fp64; attention scores and the online softmax in fp32.
- * A step runs as three launches (sampling, attention, merge); for bf16
- * tables, setting the environment variable SANTAPP_DECODE_LAUNCH=fused before
- * the first call of a process runs all three phases in one launch, in which
- * the phases hand work to each other through the workspace counters.
+ * A step on a bf16 table with d of 64 or 128, at most 512 teams per (b, kv)
+ * and at most one (b, kv) pair per compute unit runs as one launch, whose
+ * workgroups hand the perturbed scores and their partial results to each
+ * other through tagged words in the workspace; any other step runs as three
+ * launches (sampling, attention, merge).  santapp_decode_launch_info reports
+ * which.  The environment variable SANTAPP_DECODE_LAUNCH (read at the first
+ * call of a process) set to "split" forces the three launches, "fused" their
+ * one-launch form with counters in the workspace.
  * Never allocates and never synchronises.
  */
 santapp_status santapp_decode(const santapp_teams* teams, const float* q, const void* suffix_K,

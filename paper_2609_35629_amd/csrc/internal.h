@@ -18,7 +18,7 @@ constexpr int kLogcStride = 8;     // floats per union team in the read plan
 constexpr int kUnitRows = 32;      // rows per attention unit (one 32-row step of a wave)
 constexpr int kDecodeThreads = 512;  // threads of every decode workgroup (eight waves)
 constexpr int kStepMaxTeams = 512;   // teams per (b, kv) of the single-launch step
-constexpr int kStepMaxKp = kStepMaxTeams;  // K + 1 of the single-launch step: any budget below M
+constexpr int kStepMaxKp = kStepMaxTeams;  // budget of the single-launch step: any below M
 constexpr int kStepMaxWgs = 64;      // workgroups per (b, kv) pair of the single-launch step
 constexpr int kKmMaxCenters = 1024;  // k-means parents per (b, kv)
 constexpr int kKmMaxTrials = 8;      // seeding candidates per round: 2 + floor(ln 1024)
