@@ -155,7 +155,7 @@ def main():
 
     def run_dense(step, dbg=None):
         sp.dense_decode(db["q"], db["K"], db["V"], db["sK"], db["sV"], scale=wl.scale, out=dense_out,
-                        workspace=dense_ws)
+                        workspace=dense_ws, debug=dbg)
 
     hev = HipEvents(sp._lib.load())
 
@@ -196,6 +196,9 @@ def main():
     # second pass over the same steps with the library's stage markers on
     # (each marker adds a few microseconds, so the step time above has none)
     _, stages_us = timed(run_sparse, args.steps, 0, True)
+    dense_stages_us = None
+    if not args.no_dense:
+        _, dense_stages_us = timed(run_dense, args.steps, 0, True)
 
     # bytes each timed step read: the union rows of every (b, kv) (replayed
     # with the diagnostics on; same seed and step give the same selection)
@@ -320,6 +323,14 @@ def main():
         res["dense_us"] = round(d, 3)
         res["dense_gbs"] = round(dense_bytes / d / 1e3, 1)
         res["speedup_vs_dense"] = round(d / value, 3)
+        # the dense launch by its own start/end events: its rows' bytes over
+        # the kernel's execution time
+        dk = float(np.mean(dense_stages_us[:, 1]))
+        dense_kernel = (f"k_step<{wl.d}, 2, true>" if wl.dtype == datagen.BF16 and wl.B * wl.Hkv <= 256
+                        else "k_decode (dense)")
+        res["dense_roofline"] = {"kernel": dense_kernel, "kernel_us": round(dk, 3),
+                                 "achieved": round(dense_bytes / dk / 1e3, 1), "peak": 8000.0, "unit": "GB/s",
+                                 "frac": round(dense_bytes / dk / 1e3 / 8000.0, 4)}
     if check is not None:
         res.update(check)
     if loop is not None:

@@ -314,13 +314,16 @@ santapp_status santapp_dense_workspace_bytes(int B, int Hq, int Hkv, int N, int 
  * Dense softmax attention over K, V [B,Hkv,N,d] followed by the suffix rows
  * (eq. method-attention), with the same GQA mapping, suffix layout, dtypes
  * and scale convention as santapp_decode.  The workspace follows the same
- * rules (zeroed before first use; its counters are left zero).  Never
- * allocates or synchronises.
+ * rules (zeroed before first use; nothing between calls).  dbg may be NULL;
+ * only its events are used, as for santapp_decode (events[1] and events[2]
+ * stamped by the attention launch at its start and end).  Never allocates or
+ * synchronises.
  */
 santapp_status santapp_dense_decode(const float* q, const void* K, const void* V, int B, int Hkv,
                                     int N, int d, santapp_dtype dtype, const void* suffix_K,
                                     const void* suffix_V, int T, int suffix_stride, int Hq, double scale,
-                                    float* out, void* workspace, size_t ws_bytes, void* stream);
+                                    float* out, void* workspace, size_t ws_bytes,
+                                    const santapp_decode_debug* dbg, void* stream);
 
 /* Workspace for santapp_routing_kl (bytes, host-only query). */
 santapp_status santapp_routing_kl_workspace_bytes(const santapp_teams* teams, int Hq, size_t* bytes);

@@ -330,9 +330,10 @@ def dense_decode(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor,
                  suffix_K: Optional[torch.Tensor], suffix_V: Optional[torch.Tensor],
                  scale: float = 0.0, out: Optional[torch.Tensor] = None,
                  workspace: Optional[torch.Tensor] = None, stream=None,
-                 T: Optional[int] = None) -> torch.Tensor:
+                 T: Optional[int] = None, debug: Optional[DebugOut] = None) -> torch.Tensor:
     """Dense attention over K, V ``[B, Hkv, N, d]`` plus the first ``T`` suffix
-    rows of ``[B, Hkv, capacity, d]`` (default: all)."""
+    rows of ``[B, Hkv, capacity, d]`` (default: all).  ``debug``: only its
+    stage events are used."""
     B, Hq, d = q.shape
     _need(q, "q", dtype=torch.float32)
     _need(K, "K")
@@ -343,7 +344,8 @@ def dense_decode(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor,
         out = torch.empty((B, Hq, d), dtype=torch.float32, device=q.device)
     if workspace is None:
         workspace = dense_workspace(B, Hq, Hkv, N, T, d)
+    dbg = ctypes.byref(debug.struct()) if debug is not None else None
     check(_lib.load().santapp_dense_decode(
         _ptr(q), _ptr(K), _ptr(V), B, Hkv, N, d, _dtype_code(K), _ptr(suffix_K), _ptr(suffix_V),
-        T, stride, Hq, float(scale), _ptr(out), _ptr(workspace), workspace.numel(), _stream(stream)))
+        T, stride, Hq, float(scale), _ptr(out), _ptr(workspace), workspace.numel(), dbg, _stream(stream)))
     return out

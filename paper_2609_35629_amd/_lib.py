@@ -89,7 +89,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                                         ctypes.POINTER(DecodeDebug), vp]
     L.santapp_dense_workspace_bytes.argtypes = [i, i, i, i, i, i, ctypes.POINTER(sz)]
     L.santapp_dense_decode.argtypes = [vp, vp, vp, i, i, i, i, i, vp, vp, i, i, i, ctypes.c_double,
-                                       vp, vp, sz, vp]
+                                       vp, vp, sz, ctypes.POINTER(DecodeDebug), vp]
     L.santapp_teams_set_route_keys.argtypes = [vp, i, vp]
     L.santapp_routing_kl_workspace_bytes.argtypes = [vp, i, ctypes.POINTER(sz)]
     L.santapp_routing_kl.argtypes = [vp, vp, i, ctypes.c_double, vp, vp, sz, vp]

@@ -911,7 +911,8 @@ santapp_status santapp_decode_static(const santapp_teams* t, const float* q, con
 santapp_status santapp_dense_decode(const float* q, const void* K, const void* V, int B, int Hkv,
                                     int N, int d, santapp_dtype dtype, const void* suffix_K,
                                     const void* suffix_V, int T, int suffix_stride, int Hq, double scale,
-                                    float* out, void* workspace, size_t ws_bytes, void* stream) {
+                                    float* out, void* workspace, size_t ws_bytes,
+                                    const santapp_decode_debug* dbg, void* stream) {
     if (!q || !out) return fail(SANTAPP_EINVAL, "q and out must be device pointers");
     if (B < 1 || Hkv < 1 || N < 0 || T < 0 || N + T < 1)
         return fail(SANTAPP_EINVAL, "invalid sizes");
@@ -952,8 +953,20 @@ santapp_status santapp_dense_decode(const float* q, const void* K, const void* V
     A.lay = L;
     A.ws = static_cast<char*>(workspace);
     A.fused = dtype == SANTAPP_BF16 && fused_wanted() && L.nwg % 8 == 0;
-    const hipError_t e = launch_decode(A, static_cast<hipStream_t>(stream));
-    return e == hipSuccess ? ok() : hip_fail(e, "dense decode kernels");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (dbg) {  // the stage events only
+        A.ev_start = static_cast<hipEvent_t>(dbg->events[1]);
+        A.ev_stop = static_cast<hipEvent_t>(dbg->events[2]);
+    }
+    auto mark = [&](int i) -> hipError_t {
+        if (dbg && dbg->events[i]) return hipEventRecord(static_cast<hipEvent_t>(dbg->events[i]), s);
+        return hipSuccess;
+    };
+    hipError_t e;
+    if ((e = mark(0)) != hipSuccess) return hip_fail(e, "event record");
+    if ((e = launch_decode(A, s)) != hipSuccess) return hip_fail(e, "dense decode kernels");
+    if ((e = mark(3)) != hipSuccess) return hip_fail(e, "event record");
+    return ok();
 }
 
 }  // extern "C"

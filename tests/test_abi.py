@@ -70,9 +70,9 @@ def test_host_argument_checks():
     assert L.santapp_build_teams(odd, fake, 1, 1, 16, 64, 0, 4, 2, None, ctypes.byref(h)) == _lib.EINVAL
     assert b"aligned" in L.santapp_last_error()
     assert L.santapp_dense_decode(odd, fake, fake, 1, 4, 100, 128, 0, None, None, 0, 0, 28, 0.0,
-                                  fake, fake, 1 << 30, None) == _lib.EINVAL
+                                  fake, fake, 1 << 30, None, None) == _lib.EINVAL
     assert L.santapp_dense_decode(fake, fake, fake, 1, 4, 100, 128, 0, None, None, 0, 0, 28, 0.0,
-                                  fake, odd, 1 << 30, None) == _lib.EINVAL
+                                  fake, odd, 1 << 30, None, None) == _lib.EINVAL
     # decode without a table
     assert L.santapp_decode(None, fake, None, None, 0, 0, 1, 1, 0, 0, 0.0, fake, fake, 10, None, None) == _lib.EINVAL
     # dense workspace query is pure host arithmetic
@@ -82,20 +82,20 @@ def test_host_argument_checks():
     assert L.santapp_dense_workspace_bytes(1, 27, 4, 32768, 128, 128, ctypes.byref(n)) == _lib.EINVAL
     # dense decode: bad GQA grouping, too-small workspace, bad scale
     assert L.santapp_dense_decode(fake, fake, fake, 1, 4, 100, 128, 0, None, None, 0, 0, 27, 0.0,
-                                  fake, fake, 1 << 30, None) == _lib.EINVAL
+                                  fake, fake, 1 << 30, None, None) == _lib.EINVAL
     assert L.santapp_dense_decode(fake, fake, fake, 1, 4, 100, 128, 0, None, None, 0, 0, 28, 0.0,
-                                  fake, fake, 16, None) == _lib.EWORKSPACE
+                                  fake, fake, 16, None, None) == _lib.EWORKSPACE
     assert L.santapp_dense_decode(fake, fake, fake, 1, 4, 100, 128, 0, None, None, 0, 0, 28, -1.0,
-                                  fake, fake, 1 << 30, None) == _lib.EINVAL
+                                  fake, fake, 1 << 30, None, None) == _lib.EINVAL
     assert L.santapp_dense_decode(fake, fake, fake, 1, 4, 100, 128, 0, None, None, 5, 0, 28, 0.0,
-                                  fake, fake, 1 << 30, None) == _lib.EINVAL  # T > 0, no suffix
+                                  fake, fake, 1 << 30, None, None) == _lib.EINVAL  # T > 0, no suffix
     # suffix rows of a pair further apart than the buffer allows
     assert L.santapp_dense_decode(fake, fake, fake, 1, 4, 100, 128, 0, fake, fake, 5, 4, 28, 0.0,
-                                  fake, fake, 1 << 30, None) == _lib.EINVAL
+                                  fake, fake, 1 << 30, None, None) == _lib.EINVAL
     assert b"suffix_stride" in L.santapp_last_error()
     # a misaligned suffix buffer
     assert L.santapp_dense_decode(fake, fake, fake, 1, 4, 100, 128, 0, odd, fake, 5, 8, 28, 0.0,
-                                  fake, fake, 1 << 30, None) == _lib.EINVAL
+                                  fake, fake, 1 << 30, None, None) == _lib.EINVAL
 
 
 def test_kmeans_and_label_table_argument_checks():
