@@ -148,6 +148,29 @@ def test_tiny_no_suffix():
     _run(datagen.WORKLOADS["tiny"].with_(T=0), steps=(0, 5))
 
 
+def test_launch_shape():
+    """A bf16 step over at most 512 teams per (b, kv) is one launch at any
+    budget (a budget of every team runs the dense form of the same kernel);
+    fp32 rows and larger tables take the three launches (sampling, attention,
+    merge)."""
+    q8 = datagen.WORKLOADS["qwen8k"]
+    db = dev_batch(datagen.generate(q8))
+    t = sp.build_teams(db.K, db.V, q8.P, q8.R)
+    assert t.M == 128
+    for K in (1, 32, 100, 127, 128):
+        kernels, wgs = sp.decode_launch_info(t, q8.Hq, q8.T, K)
+        assert kernels == 1 and wgs >= q8.B * q8.Hkv, (K, kernels, wgs)
+    tiny = datagen.WORKLOADS["tiny"]
+    dbt = dev_batch(datagen.generate(tiny))
+    tt = sp.build_teams(dbt.K, dbt.V, tiny.P, tiny.R)
+    assert sp.decode_launch_info(tt, tiny.Hq, tiny.T, tiny.K)[0] == 3
+    lim = datagen.WORKLOADS["limit"]
+    dbl = dev_batch(datagen.generate(lim))
+    tl = sp.build_teams(dbl.K, dbl.V, lim.P, lim.R)
+    assert tl.M == lim.N
+    assert sp.decode_launch_info(tl, lim.Hq, lim.T, lim.K)[0] == 3
+
+
 def test_qwen8k():
     wl = datagen.WORKLOADS["qwen8k"]
     teams, res = _run(wl, steps=(0, 1, 2))
