@@ -28,6 +28,7 @@ struct santapp_teams {
     int* rep_token;
     int* perm;
     int* team_count;  // [B*Hkv] teams of each pair (M for contiguous parents)
+    void* block;      // the one device allocation every array above is carved from
     // cap[x]: the most attention chunks any x distinct teams of one (b, kv)
     // need (sum of their x largest chunk counts, maximum over (b, kv))
     std::vector<int> cap;
@@ -105,19 +106,11 @@ void release(void* p) {
 
 void free_teams(santapp_teams* t) {
     if (!t) return;
-    release(t->packed_K);
-    release(t->packed_V);
-    release(t->reps);
-    release(t->team_begin);
-    release(t->team_size);
-    release(t->log_n);
-    release(t->rep_token);
-    release(t->perm);
-    release(t->team_count);
+    release(t->block);
     delete t;
 }
 
-santapp_status finish_table(santapp_teams* t, santapp_teams** out);
+santapp_status finish_table(santapp_teams* t, hipStream_t s, santapp_teams** out);
 
 }  // namespace
 
@@ -142,6 +135,33 @@ struct Carver {
         return at;
     }
 };
+
+// Every device array of a table (t->B, Hkv, N, M, d and dtype set) from one
+// allocation, each 256-byte aligned.
+hipError_t alloc_table(santapp_teams* t) {
+    const size_t BH = static_cast<size_t>(t->B) * t->Hkv;
+    const size_t N = static_cast<size_t>(t->N), M = static_cast<size_t>(t->M);
+    const size_t row = static_cast<size_t>(t->d) * elem_size(t->dtype);
+    Carver c;
+    const size_t oK = c.take(BH * N * row), oV = c.take(BH * N * row), oR = c.take(BH * M * row);
+    const size_t ob = c.take(BH * M * sizeof(int)), os = c.take(BH * M * sizeof(int));
+    const size_t ol = c.take(BH * M * sizeof(double)), ot = c.take(BH * M * sizeof(int));
+    const size_t op = c.take(BH * N * sizeof(int)), oc = c.take(BH * sizeof(int));
+    char* b = nullptr;
+    const hipError_t e = hipMalloc(reinterpret_cast<void**>(&b), c.off);
+    if (e != hipSuccess) return e;
+    t->block = b;
+    t->packed_K = b + oK;
+    t->packed_V = b + oV;
+    t->reps = b + oR;
+    t->team_begin = reinterpret_cast<int*>(b + ob);
+    t->team_size = reinterpret_cast<int*>(b + os);
+    t->log_n = reinterpret_cast<double*>(b + ol);
+    t->rep_token = reinterpret_cast<int*>(b + ot);
+    t->perm = reinterpret_cast<int*>(b + op);
+    t->team_count = reinterpret_cast<int*>(b + oc);
+    return hipSuccess;
+}
 
 }  // namespace
 
@@ -297,19 +317,10 @@ santapp_status santapp_build_teams(const void* K, const void* V, int B, int Hkv,
     t->M = static_cast<int>(M);
     double* mind = nullptr;
     int* owner = nullptr;
-    hipError_t e = hipSuccess;
+    hipError_t e = alloc_table(t);
     auto alloc = [&](void** p, size_t bytes) {
         if (e == hipSuccess) e = hipMalloc(p, bytes);
     };
-    alloc(&t->packed_K, BH * N * row);
-    alloc(&t->packed_V, BH * N * row);
-    alloc(&t->reps, BH * M * row);
-    alloc(reinterpret_cast<void**>(&t->team_begin), BH * M * sizeof(int));
-    alloc(reinterpret_cast<void**>(&t->team_size), BH * M * sizeof(int));
-    alloc(reinterpret_cast<void**>(&t->log_n), BH * M * sizeof(double));
-    alloc(reinterpret_cast<void**>(&t->rep_token), BH * M * sizeof(int));
-    alloc(reinterpret_cast<void**>(&t->perm), BH * N * sizeof(int));
-    alloc(reinterpret_cast<void**>(&t->team_count), BH * sizeof(int));
     if (!build_packs_in_place(N, d, dtype, parent_size, reps_per_parent)) {
         // running minimum and owner per token, for the general build kernel
         alloc(reinterpret_cast<void**>(&mind), BH * N * sizeof(double));
@@ -326,7 +337,8 @@ santapp_status santapp_build_teams(const void* K, const void* V, int B, int Hkv,
     bool packed = false;
     e = launch_build_parents(K, V, dtype, static_cast<int>(BH), N, d, parent_size, reps_per_parent,
                              t->M, mind, owner, t->team_begin, t->team_size, t->log_n,
-                             t->rep_token, t->perm, t->packed_K, t->packed_V, t->reps, &packed, s);
+                             t->rep_token, t->perm, t->packed_K, t->packed_V, t->reps, t->team_count,
+                             &packed, s);
     if (e == hipSuccess && !packed) {
         what = "packing K";
         e = launch_gather_rows(K, t->packed_K, t->perm, static_cast<int>(BH), N, N, row, s);
@@ -339,35 +351,32 @@ santapp_status santapp_build_teams(const void* K, const void* V, int B, int Hkv,
         what = "gathering representatives";
         e = launch_gather_rows(K, t->reps, t->rep_token, static_cast<int>(BH), t->M, N, row, s);
     }
-    if (e == hipSuccess) {
-        what = "team build sync";
-        e = hipStreamSynchronize(s);
-    }
-    release(mind);
-    release(owner);
-    if (e == hipSuccess) {
-        what = "team counts";
-        const std::vector<int> counts(BH, t->M);
-        e = hipMemcpy(t->team_count, counts.data(), BH * sizeof(int), hipMemcpyHostToDevice);
-    }
     if (e != hipSuccess) {
+        // a launch failed: nothing of this call is left queued that uses the
+        // buffers (hipFree waits for the device)
+        release(mind);
+        release(owner);
         free_teams(t);
         return hip_fail(e, what);
     }
-    return finish_table(t, out);
+    const santapp_status st = finish_table(t, s, out);  // waits for the build
+    release(mind);
+    release(owner);
+    return st;
 }
 
 namespace {
 
-// Chunk capacities and the device's compute units of a built table; frees it
-// on failure.
-santapp_status finish_table(santapp_teams* t, santapp_teams** out) {
+// Waits for the build queued on s, then sets the chunk capacities and the
+// device's compute units of the table; frees it on failure.
+santapp_status finish_table(santapp_teams* t, hipStream_t s, santapp_teams** out) {
     const size_t BH = static_cast<size_t>(t->B) * t->Hkv;
     std::vector<int> sizes(BH * t->M);
-    const hipError_t e = hipMemcpy(sizes.data(), t->team_size, sizes.size() * sizeof(int), hipMemcpyDeviceToHost);
+    hipError_t e = hipMemcpyAsync(sizes.data(), t->team_size, sizes.size() * sizeof(int), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) {
         free_teams(t);
-        return hip_fail(e, "team size copy");
+        return hip_fail(e, "team build");
     }
     int dev = 0;
     t->cus = 0;
@@ -543,15 +552,7 @@ santapp_status santapp_build_teams_from_labels(const void* K, const void* V, int
     t->P = 0;
     t->R = reps_per_parent;
     t->M = M;
-    alloc(&t->packed_K, BH * N * row);
-    alloc(&t->packed_V, BH * N * row);
-    alloc(&t->reps, BH * M * row);
-    alloc(reinterpret_cast<void**>(&t->team_begin), BH * M * sizeof(int));
-    alloc(reinterpret_cast<void**>(&t->team_size), BH * M * sizeof(int));
-    alloc(reinterpret_cast<void**>(&t->log_n), BH * M * sizeof(double));
-    alloc(reinterpret_cast<void**>(&t->rep_token), BH * M * sizeof(int));
-    alloc(reinterpret_cast<void**>(&t->perm), BH * N * sizeof(int));
-    alloc(reinterpret_cast<void**>(&t->team_count), BH * sizeof(int));
+    e = alloc_table(t);
     if (e != hipSuccess) {
         cleanup();
         free_teams(t);
@@ -583,16 +584,14 @@ santapp_status santapp_build_teams_from_labels(const void* K, const void* V, int
         what = "gathering representatives";
         e = launch_gather_rows(K, t->reps, t->rep_token, static_cast<int>(BH), M, N, row, s);
     }
-    if (e == hipSuccess) {
-        what = "team build sync";
-        e = hipStreamSynchronize(s);
-    }
-    cleanup();
     if (e != hipSuccess) {
+        cleanup();
         free_teams(t);
         return hip_fail(e, what);
     }
-    return finish_table(t, out);
+    const santapp_status st = finish_table(t, s, out);  // waits for the build
+    cleanup();
+    return st;
 }
 
 santapp_status santapp_teams_info(const santapp_teams* t, santapp_teams_desc* d) {

@@ -96,8 +96,11 @@ __global__ __launch_bounds__(NT) void k_build_parent(
     const T* __restrict__ K, int N, int d, int P, int R, int M, double* __restrict__ mind_all,
     int* __restrict__ owner_all, int* __restrict__ team_begin, int* __restrict__ team_size,
     double* __restrict__ log_n, int* __restrict__ rep_token, int* __restrict__ perm,
-    const int* __restrict__ members, const int* __restrict__ pbeg, const int* __restrict__ toff, int Mp) {
+    const int* __restrict__ members, const int* __restrict__ pbeg, const int* __restrict__ toff, int Mp,
+    int* __restrict__ team_count) {
 #pragma clang fp contract(off)
+    // contiguous parents: every pair has M teams
+    if (!LIST && blockIdx.x == 0 && threadIdx.x == 0) team_count[blockIdx.y] = M;
     __shared__ double s_vec[kMaxHeadDim];
     __shared__ ArgVal s_red[(NT / kWave)];
     __shared__ int s_reps[kMaxReps];
@@ -284,6 +287,25 @@ struct RegRow<bf16_t, D> {
 #pragma unroll
         for (int k = 0; k < kWords / 4; ++k) p[k] = make_uint4(w[4 * k], w[4 * k + 1], w[4 * k + 2], w[4 * k + 3]);
     }
+    // the row as kWords / 4 chunks of 16 bytes, chunk c at position c ^ sw
+    __device__ __forceinline__ void store_swizzled(uint4* dst, int sw) const {
+#pragma unroll
+        for (int k = 0; k < kWords / 4; ++k) dst[k ^ sw] = make_uint4(w[4 * k], w[4 * k + 1], w[4 * k + 2], w[4 * k + 3]);
+    }
+    // element j of a row stored by store_swizzled
+    static __device__ __forceinline__ float swizzled_elem(const uint4* src, int j, int sw) {
+        const uint16_t* c = reinterpret_cast<const uint16_t*>(src + ((j >> 3) ^ sw));
+        return __uint_as_float(static_cast<uint32_t>(c[j & 7]) << 16);
+    }
+    // lane l < kWords widens the stored row's word l (dimensions 2l, 2l + 1)
+    // to fp64
+    static __device__ __forceinline__ void widen(const uint32_t* words, double* out, int lane) {
+        if (lane < kWords) {
+            const uint32_t x = words[lane];
+            *reinterpret_cast<double2*>(out + 2 * lane) =
+                make_double2(static_cast<double>(bf16lo(x)), static_cast<double>(bf16hi(x)));
+        }
+    }
 };
 
 template <int D>
@@ -315,6 +337,19 @@ struct RegRow<float, D> {
 #pragma unroll
         for (int k = 0; k < kWords / 4; ++k) p[k] = make_float4(w[4 * k], w[4 * k + 1], w[4 * k + 2], w[4 * k + 3]);
     }
+    __device__ __forceinline__ void store_swizzled(uint4* dst, int sw) const {
+#pragma unroll
+        for (int k = 0; k < kWords / 4; ++k)
+            dst[k ^ sw] = make_uint4(__float_as_uint(w[4 * k]), __float_as_uint(w[4 * k + 1]),
+                                     __float_as_uint(w[4 * k + 2]), __float_as_uint(w[4 * k + 3]));
+    }
+    static __device__ __forceinline__ float swizzled_elem(const uint4* src, int j, int sw) {
+        return reinterpret_cast<const float*>(src + ((j >> 2) ^ sw))[j & 3];
+    }
+    // lane l < kWords widens the stored row's dimension l to fp64
+    static __device__ __forceinline__ void widen(const uint32_t* words, double* out, int lane) {
+        if (lane < kWords) out[lane] = static_cast<double>(__uint_as_float(words[lane]));
+    }
 };
 
 // |k - c|^2 with c an fp64 vector in LDS (read as broadcasts), summed in
@@ -337,20 +372,45 @@ __device__ __forceinline__ double reg_sqdist(const RegRow<T, D>& r, const double
     return acc;
 }
 
+// (value, index) extremum over the wave (wave-uniform): DPP row rotations
+// within each 16-lane row, then the four rows' results.  The order is total
+// (value, then the smaller index; NaN never reaches it), so any reduction
+// order gives the same winner.
+template <bool kMax>
+__device__ __forceinline__ ArgVal wave_arg(ArgVal x) {
+#define SANTAPP_ARGSTEP(CTRL)                                                  \
+    {                                                                          \
+        ArgVal y;                                                              \
+        y.v = dpp_f64<CTRL>(x.v);                                              \
+        y.i = __builtin_amdgcn_update_dpp(0, x.i, CTRL, 0xF, 0xF, false);     \
+        x = kMax ? pick_max(x, y) : pick_min(x, y);                            \
+    }
+    SANTAPP_ARGSTEP(0x128)
+    SANTAPP_ARGSTEP(0x124)
+    SANTAPP_ARGSTEP(0x122)
+    SANTAPP_ARGSTEP(0x121)
+#undef SANTAPP_ARGSTEP
+    const uint64_t vb = static_cast<uint64_t>(__double_as_longlong(x.v));
+    ArgVal r{__longlong_as_double(static_cast<long long>(readlane(vb, 0))), readlane(x.i, 0)};
+#pragma unroll
+    for (int row = 1; row < 4; ++row) {
+        const ArgVal y{__longlong_as_double(static_cast<long long>(readlane(vb, 16 * row))), readlane(x.i, 16 * row)};
+        r = kMax ? pick_max(r, y) : pick_min(r, y);
+    }
+    return r;
+}
+
 // (value, index) reduction over the workgroup's waves; s_red holds one
 // entry per wave.  The caller separates reuses of s_red by a barrier.
 template <bool kMax>
 __device__ __forceinline__ ArgVal reg_block_arg(ArgVal x, ArgVal* s_red, int nw) {
-    for (int off = kWave / 2; off > 0; off >>= 1) {
-        ArgVal y;
-        y.v = __shfl_xor(x.v, off);
-        y.i = __shfl_xor(x.i, off);
-        x = kMax ? pick_max(x, y) : pick_min(x, y);
-    }
+    x = wave_arg<kMax>(x);
     if (lane_id() == 0) s_red[wave_id()] = x;
     __syncthreads();
     ArgVal r = s_red[0];
-    for (int w = 1; w < nw; ++w) r = kMax ? pick_max(r, s_red[w]) : pick_min(r, s_red[w]);
+#pragma unroll
+    for (int w = 1; w < kRegWaves; ++w)
+        if (w < nw) r = kMax ? pick_max(r, s_red[w]) : pick_min(r, s_red[w]);
     return r;
 }
 
@@ -365,10 +425,16 @@ __global__ __launch_bounds__(kRegThreads) void k_build_parent_regs(
     const T* __restrict__ K, const T* __restrict__ V, int N, int P, int R, int M,
     int* __restrict__ team_begin, int* __restrict__ team_size, double* __restrict__ log_n,
     int* __restrict__ rep_token, int* __restrict__ perm, T* __restrict__ packed_K,
-    T* __restrict__ packed_V, T* __restrict__ reps) {
+    T* __restrict__ packed_V, T* __restrict__ reps, int* __restrict__ team_count) {
 #pragma clang fp contract(off)
-    __shared__ __align__(16) double s_vec[2][D];  // the mean, then each new representative
-    __shared__ __align__(16) float s_tile[kWave][D];  // one wave's rows, for the mean
+    __shared__ __align__(16) double s_mean[D];
+    __shared__ __align__(16) uint32_t s_raw[RegRow<T, D>::kWords];  // the new representative's words
+    __shared__ __align__(16) double s_cw[kRegWaves][D];  // each wave's fp64 copy of it
+    // one slot's rows (member t + k nt in row t), for the mean; 16-byte
+    // chunk c of row t sits at position c ^ (t mod chunks) so that the
+    // lanes' row stores spread over the banks
+    constexpr int kChunks = RegRow<T, D>::kWords / 4;
+    __shared__ __align__(16) uint4 s_rows[kRegThreads][kChunks];
     __shared__ ArgVal s_red[2][kRegWaves];
     __shared__ int s_reps[kMaxReps];
     __shared__ int s_cnt[kMaxReps];
@@ -387,6 +453,7 @@ __global__ __launch_bounds__(kRegThreads) void k_build_parent_regs(
     const int r = min(R, n);
     const int team0 = p * min(R, P);  // every earlier parent is full-size
     const T* Kc = K + (static_cast<size_t>(bh) * N + start) * D;
+    if (p == 0 && tid == 0) team_count[bh] = M;  // every pair has M teams
 
     RegRow<T, D> row[MPT];
     bool member[MPT];
@@ -397,30 +464,35 @@ __global__ __launch_bounds__(kRegThreads) void k_build_parent_regs(
         if (member[k]) row[k].load(Kc + static_cast<size_t>(i) * D);
     }
 
-    // parent mean, summed over members in token order: the rows pass
-    // through LDS 64 members (one wave's slot) at a time, and thread j < D
-    // adds dimension j of each staged row in turn
+    // parent mean, summed over members in token order: each slot's rows
+    // pass through LDS at once, and thread j < D adds dimension j of each
+    // staged row in turn, the reads 16 rows ahead of their (serial)
+    // additions
     double msum = 0.0;
-    for (int g = 0; g * kWave < n; ++g) {
-        const int gk = g / nw, gw = g - gk * nw;  // slot and wave holding members 64g..
 #pragma unroll
-        for (int k = 0; k < MPT; ++k) {
-            row[k].opaque();
-            if (k == gk && w == gw && member[k]) {
-#pragma unroll
-                for (int j = 0; j < D; j += 4)
-                    *reinterpret_cast<float4*>(&s_tile[lane][j]) =
-                        make_float4(row[k].elem(j), row[k].elem(j + 1), row[k].elem(j + 2), row[k].elem(j + 3));
-            }
-        }
+    for (int k = 0; k < MPT; ++k) {
+        const int cnt = min(nt, n - k * nt);  // members of slot k
+        if (cnt <= 0) break;
+        if (k > 0) __syncthreads();  // the previous slot's reads are done
+        row[k].opaque();
+        if (member[k]) row[k].store_swizzled(s_rows[tid], tid & (kChunks - 1));
         __syncthreads();
         if (tid < D) {
-            const int cnt = min(kWave, n - g * kWave);
-            for (int i = 0; i < cnt; ++i) msum = msum + static_cast<double>(s_tile[i][tid]);
+            int i0 = 0;
+            for (; i0 + 16 <= cnt; i0 += 16) {
+                float x[16];
+#pragma unroll
+                for (int i = 0; i < 16; ++i)
+                    x[i] = RegRow<T, D>::swizzled_elem(s_rows[i0 + i], tid, (i0 + i) & (kChunks - 1));
+#pragma unroll
+                for (int i = 0; i < 16; ++i) msum = msum + static_cast<double>(x[i]);
+                asm volatile("" : "+v"(msum)::"memory");  // one batch of reads in flight at a time
+            }
+            for (; i0 < cnt; ++i0)
+                msum = msum + static_cast<double>(RegRow<T, D>::swizzled_elem(s_rows[i0], tid, i0 & (kChunks - 1)));
         }
-        __syncthreads();
     }
-    if (tid < D) s_vec[0][tid] = msum / static_cast<double>(n);
+    if (tid < D) s_mean[tid] = msum / static_cast<double>(n);
     __syncthreads();
 
     // distances of this thread's members to the vector c in LDS: |k - c|^2
@@ -457,7 +529,7 @@ __global__ __launch_bounds__(kRegThreads) void k_build_parent_regs(
 
     // first representative: the member nearest the mean
     double dd[MPT];
-    distances(s_vec[0], dd);
+    distances(s_mean, dd);
     ArgVal best{INFINITY, 0x7fffffff};
 #pragma unroll
     for (int k = 0; k < MPT; ++k)
@@ -467,9 +539,13 @@ __global__ __launch_bounds__(kRegThreads) void k_build_parent_regs(
 
     // farthest-first rounds with a running minimum; a chosen representative
     // gets -1 so that it is never chosen again.  Round u uses buffer
-    // (u + 1) & 1 of s_vec and s_red (the mean used buffer 0): a buffer is
-    // rewritten two rounds after it was read, past both barriers of the
-    // round between.
+    // (u + 1) & 1 of s_red (the mean used buffer 0): a buffer is rewritten
+    // two rounds after it was read, past both barriers of the round between.
+    // The new representative's owner stores its raw words to s_raw, and
+    // after the barrier every wave widens them into its own fp64 copy
+    // (wave-private, so no second barrier); s_raw is rewritten only after
+    // the round's reduction barrier, which every wave reaches after its
+    // widening.
     double m[MPT];
     int o[MPT];
 #pragma unroll
@@ -483,19 +559,13 @@ __global__ __launch_bounds__(kRegThreads) void k_build_parent_regs(
         if (tid == rep - rk * nt) {
             s_reps[u] = rep;
 #pragma unroll
-            for (int k = 0; k < MPT; ++k) {
-                if (k == rk) {
-#pragma unroll
-                    for (int j = 0; j < D; j += 2) {
-                        if (j % 8 == 0) row[k].opaque8(j);
-                        *reinterpret_cast<double2*>(&s_vec[b][j]) = make_double2(
-                            static_cast<double>(row[k].elem(j)), static_cast<double>(row[k].elem(j + 1)));
-                    }
-                }
-            }
+            for (int k = 0; k < MPT; ++k)
+                if (k == rk) row[k].store(reinterpret_cast<T*>(s_raw));
         }
         __syncthreads();
-        distances(s_vec[b], dd);
+        double* cw = s_cw[w];
+        RegRow<T, D>::widen(s_raw, cw, lane);
+        distances(cw, dd);
         ArgVal far{-INFINITY, 0x7fffffff};
 #pragma unroll
         for (int k = 0; k < MPT; ++k) {
@@ -586,7 +656,6 @@ __global__ __launch_bounds__(kRegThreads) void k_build_parent_regs(
 
     // packed copies: key rows from registers, value rows copied, and each
     // team's representative key (its member's row, re-read from memory)
-    constexpr int kChunks = D * static_cast<int>(sizeof(T)) / 16;  // 16-byte chunks per row
     const size_t prow0 = static_cast<size_t>(bh) * N + start;
 #pragma unroll
     for (int k = 0; k < MPT; ++k) {
@@ -635,8 +704,8 @@ bool build_packs_in_place(int N, int d, santapp_dtype dtype, int P, int R) {
 hipError_t launch_build_parents(const void* K, const void* V, santapp_dtype dtype, int BH, int N,
                                 int d, int P, int R, int M, double* mind, int* owner,
                                 int* team_begin, int* team_size, double* log_n, int* rep_token,
-                                int* perm, void* packed_K, void* packed_V, void* reps, bool* packed,
-                                hipStream_t s) {
+                                int* perm, void* packed_K, void* packed_V, void* reps, int* team_count,
+                                bool* packed, hipStream_t s) {
     *packed = false;
     const dim3 grid((N + P - 1) / P, BH);
     // register-resident kernel where a parent fits 2 kRegThreads members and
@@ -653,7 +722,7 @@ hipError_t launch_build_parents(const void* K, const void* V, santapp_dtype dtyp
         kern<<<grid, threads, 0, s>>>(static_cast<const TT*>(K), static_cast<const TT*>(V), N, P, R, \
                                       M, team_begin, team_size, log_n, rep_token, perm,           \
                                       static_cast<TT*>(packed_K), static_cast<TT*>(packed_V),    \
-                                      static_cast<TT*>(reps));                                    \
+                                      static_cast<TT*>(reps), team_count);                        \
         *packed = true;                                                                           \
         return hipGetLastError();                                                                 \
     } while (0)
@@ -665,11 +734,11 @@ hipError_t launch_build_parents(const void* K, const void* V, santapp_dtype dtyp
     if (dtype == SANTAPP_BF16)
         k_build_parent<bf16_t, false, kBuildThreads><<<grid, kBuildThreads, 0, s>>>(
             static_cast<const bf16_t*>(K), N, d, P, R, M, mind, owner, team_begin, team_size,
-            log_n, rep_token, perm, nullptr, nullptr, nullptr, 0);
+            log_n, rep_token, perm, nullptr, nullptr, nullptr, 0, team_count);
     else
         k_build_parent<float, false, kBuildThreads><<<grid, kBuildThreads, 0, s>>>(
             static_cast<const float*>(K), N, d, P, R, M, mind, owner, team_begin, team_size,
-            log_n, rep_token, perm, nullptr, nullptr, nullptr, 0);
+            log_n, rep_token, perm, nullptr, nullptr, nullptr, 0, team_count);
     return hipGetLastError();
 }
 
@@ -681,11 +750,11 @@ hipError_t launch_build_parent_lists(const void* K, santapp_dtype dtype, int BH,
     if (dtype == SANTAPP_BF16)
         k_build_parent<bf16_t, true, kListBuildThreads><<<grid, kListBuildThreads, 0, s>>>(
             static_cast<const bf16_t*>(K), N, d, 0, R, M, mind, owner, team_begin, team_size, log_n,
-            rep_token, perm, members, pbeg, toff, Mp);
+            rep_token, perm, members, pbeg, toff, Mp, nullptr);
     else
         k_build_parent<float, true, kListBuildThreads><<<grid, kListBuildThreads, 0, s>>>(
             static_cast<const float*>(K), N, d, 0, R, M, mind, owner, team_begin, team_size, log_n,
-            rep_token, perm, members, pbeg, toff, Mp);
+            rep_token, perm, members, pbeg, toff, Mp, nullptr);
     return hipGetLastError();
 }
 

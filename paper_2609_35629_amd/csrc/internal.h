@@ -120,14 +120,15 @@ __host__ __device__ inline int chunk_count(int rows) { return (rows + kUnitRows 
 // needs no per-token scratch and writes the packed copies itself).
 bool build_packs_in_place(int N, int d, santapp_dtype dtype, int P, int R);
 
-// Team table of every parent.  Where the register-resident kernel runs it
-// also writes the packed copies (packed_K, packed_V, reps) and sets *packed;
-// otherwise the caller gathers them from perm and rep_token.
+// Team table of every parent, and team_count[bh] = M.  Where the
+// register-resident kernel runs it also writes the packed copies (packed_K,
+// packed_V, reps) and sets *packed; otherwise the caller gathers them from
+// perm and rep_token.
 hipError_t launch_build_parents(const void* K, const void* V, santapp_dtype dtype, int BH, int N,
                                 int d, int P, int R, int M, double* mind, int* owner,
                                 int* team_begin, int* team_size, double* log_n, int* rep_token,
-                                int* perm, void* packed_K, void* packed_V, void* reps, bool* packed,
-                                hipStream_t s);
+                                int* perm, void* packed_K, void* packed_V, void* reps, int* team_count,
+                                bool* packed, hipStream_t s);
 
 hipError_t launch_gather_rows(const void* src, void* dst, const int* index, int BH, int rows_out,
                               int rows_in, size_t row_bytes, hipStream_t s);
