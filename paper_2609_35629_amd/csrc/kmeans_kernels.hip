@@ -139,15 +139,19 @@ __global__ __launch_bounds__(kKppThreads) void k_kpp_dist(
     const bool valid = j < s0;
     const T* x = X + static_cast<size_t>(valid ? samp[j] : 0) * D;
     const double dcur = (valid && c > 0) ? D2[static_cast<size_t>(bh) * s0 + j] : 0.0;
-    // one pass over the point's row; candidate t's sum runs in dimension order
+    // one pass over the point's row, all of it loaded up front; candidate
+    // t's sum runs in dimension order
     double acc[kKmMaxTrials];
 #pragma unroll
     for (int t = 0; t < kKmMaxTrials; ++t) acc[t] = 0.0;
     constexpr int kPer = 16 / static_cast<int>(sizeof(T));
-#pragma unroll 2
+    uint4 raw[D / kPer];
+#pragma unroll
+    for (int q = 0; q < D / kPer; ++q) raw[q] = reinterpret_cast<const uint4*>(x)[q];
+#pragma unroll
     for (int k0 = 0; k0 < D; k0 += kPer) {
         float xv[kPer];
-        load_row16(x + k0, xv);
+        load_row16(reinterpret_cast<const T*>(&raw[k0 / kPer]), xv);
 #pragma unroll
         for (int q = 0; q < kPer; ++q) {
 #pragma unroll
