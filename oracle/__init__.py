@@ -22,7 +22,9 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "santapp_oracle.c")
-_SO = os.path.join(_HERE, "liboracle.so")
+# SANTAPP_ORACLE_LIB names another build of the same source to load (the
+# sanitizer test's instrumented copy)
+_SO = os.environ.get("SANTAPP_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 _lib = None
 
 _d = ctypes.POINTER(ctypes.c_double)
@@ -30,14 +32,21 @@ _i = ctypes.POINTER(ctypes.c_int)
 _u64 = ctypes.POINTER(ctypes.c_uint64)
 
 
-def build() -> str:
-    """Compile the oracle into ``oracle/liboracle.so`` (always recompiles)."""
-    tmp = _SO + ".tmp"
+def build(out: Optional[str] = None, sanitize: bool = False) -> str:
+    """Compile the oracle into ``oracle/liboracle.so``, or ``out`` (always
+    recompiles).  ``sanitize``: a host build with AddressSanitizer and
+    UndefinedBehaviorSanitizer, every finding fatal, for the sanitizer test
+    (loaded with the ASan runtime preloaded)."""
+    out = out or _SO
+    tmp = out + ".tmp"
     cmd = ["gcc", "-O2", "-std=gnu11", "-fPIC", "-shared", "-ffp-contract=off",
            "-fno-fast-math", "-Wall", "-o", tmp, _SRC, "-lm"]
+    if sanitize:
+        cmd[1:2] = ["-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+                    "-fno-sanitize-recover=all"]
     subprocess.run(cmd, check=True)
-    os.replace(tmp, _SO)
-    return _SO
+    os.replace(tmp, out)
+    return out
 
 
 def lib():

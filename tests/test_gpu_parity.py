@@ -16,6 +16,7 @@ Bars (all through the C ABI):
 * read statistics: per (sequence, KV head), the union of the query heads'
   teams and its prompt rows equal the oracle's (eq. qwen-logical-access).
 """
+import ctypes
 from collections import Counter
 
 import numpy as np
@@ -413,3 +414,61 @@ def test_limiting_case_sampling_law():
 def test_head_dims_and_groups(name, kw):
     wl = datagen.WORKLOADS["qwen8k"].with_(name=name, **kw)
     _run(wl, steps=(0, 3))
+
+
+# Guard bands around the caller's buffers: every byte a launch may write
+# lies inside the workspace and the output, so canary bytes on both sides
+# of each stay as they were.
+GUARD = 1 << 16   # bytes on each side (a multiple of 256: the buffers keep their alignment)
+CANARY = 0xA5
+
+
+def _guarded(nbytes):
+    big = torch.full((nbytes + 2 * GUARD,), CANARY, dtype=torch.uint8, device="cuda")
+    return big, big[GUARD:GUARD + nbytes]
+
+
+def _bands_intact(big, nbytes):
+    torch.cuda.synchronize()
+    return bool((big[:GUARD] == CANARY).all().item()) and bool((big[GUARD + nbytes:] == CANARY).all().item())
+
+
+def _zero_workspace(ws):
+    from paper_2609_35629_amd import _lib
+    sp.check(_lib.load().santapp_workspace_zero(ctypes.c_void_p(ws.data_ptr()), ws.numel(),
+                                                ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)))
+
+
+@pytest.mark.parametrize("base,K,kw", [
+    ("tiny", 8, {}),                  # fp32 rows: three launches
+    ("qwen8k", 32, {}),               # the single launch, sampled
+    ("qwen8k", 128, {}),              # the single launch over every team
+    ("qwen8k", 100, dict(T=0)),       # no suffix
+])
+def test_canary_guarded_buffers(base, K, kw):
+    wl = datagen.WORKLOADS[base].with_(**kw)
+    log(f"[gpu] canary-guarded decode {base} K={K} {kw}")
+    db = dev_batch(datagen.generate(wl))
+    teams = sp.build_teams(db.K, db.V, wl.P, wl.R)
+    n_ws = sp.decode_workspace(teams, wl.Hq, wl.T, K).numel()
+    ws_big, ws = _guarded(n_ws)
+    _zero_workspace(ws)
+    n_out = wl.B * wl.Hq * wl.d * 4
+    out_big, out8 = _guarded(n_out)
+    out = out8.view(torch.float32).view(wl.B, wl.Hq, wl.d)
+    for step in range(3):
+        sp.decode(teams, db.q, db.sK, db.sV, K, seed=wl.seed, step=step, scale=wl.scale, out=out,
+                  workspace=ws)
+        ref = sp.decode(teams, db.q, db.sK, db.sV, K, seed=wl.seed, step=step, scale=wl.scale)
+        assert _bands_intact(ws_big, n_ws), f"workspace guard band overwritten at step {step}"
+        assert _bands_intact(out_big, n_out), f"output guard band overwritten at step {step}"
+        assert torch.equal(out, ref)
+    # the dense step over the same shape
+    n_dws = sp.dense_workspace(wl.B, wl.Hq, wl.Hkv, wl.N, wl.T, wl.d).numel()
+    dws_big, dws = _guarded(n_dws)
+    _zero_workspace(dws)
+    sp.dense_decode(db.q, db.K, db.V, db.sK, db.sV, scale=wl.scale, out=out, workspace=dws)
+    ref = sp.dense_decode(db.q, db.K, db.V, db.sK, db.sV, scale=wl.scale)
+    assert _bands_intact(dws_big, n_dws) and _bands_intact(out_big, n_out)
+    assert torch.equal(out, ref)
+    teams.close()
