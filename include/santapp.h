@@ -60,7 +60,16 @@ typedef enum {
     SANTAPP_ELIMIT = 6      /* valid but beyond this library's supported sizes      */
 } santapp_status;
 
-typedef enum { SANTAPP_BF16 = 0, SANTAPP_FP32 = 1 } santapp_dtype;
+/* The input enumerations below span the whole int range (their last two
+ * enumerators are never valid arguments), so that a caller may pass any int
+ * and an unknown value is answered with an error status instead of being
+ * undefined behaviour in the library. */
+typedef enum {
+    SANTAPP_BF16 = 0,
+    SANTAPP_FP32 = 1,
+    SANTAPP_DTYPE_INT_MIN_ = -2147483647 - 1,
+    SANTAPP_DTYPE_INT_MAX_ = 2147483647
+} santapp_dtype;
 
 /* Opaque team table of one layer: owns its device buffers. */
 typedef struct santapp_teams santapp_teams;
@@ -185,7 +194,12 @@ santapp_status santapp_build_teams_from_labels(const void* K, const void* V, int
  * uses whichever keys it holds; the team partition is unchanged.  Enqueued
  * on `stream`; never allocates.
  */
-typedef enum { SANTAPP_ROUTE_REPRESENTATIVE = 0, SANTAPP_ROUTE_CENTROID = 1 } santapp_route_key;
+typedef enum {
+    SANTAPP_ROUTE_REPRESENTATIVE = 0,
+    SANTAPP_ROUTE_CENTROID = 1,
+    SANTAPP_ROUTE_INT_MIN_ = -2147483647 - 1,
+    SANTAPP_ROUTE_INT_MAX_ = 2147483647
+} santapp_route_key;
 
 santapp_status santapp_teams_set_route_keys(santapp_teams* teams, santapp_route_key kind, void* stream);
 

@@ -51,6 +51,34 @@ def _link(objs, out):
     os.replace(tmp, out)
 
 
+# AddressSanitizer and UndefinedBehaviorSanitizer for host code only (each
+# option applies to the host pass; the device code is built as usual)
+HOST_SANITIZE = [
+    "-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+    "-Xarch_host", "-fno-sanitize-recover=all", "-Xarch_host", "-fno-omit-frame-pointer",
+]
+
+
+def build_host_sanitized(out: str) -> str:
+    """``out``: the library with the host code of ``api.hip`` (the entry
+    points and their argument checks) built under HOST_SANITIZE, linked with
+    the other files' regular objects (built first where missing).  For the
+    host sanitizer test, which loads it with the ASan runtime preloaded."""
+    os.makedirs(OBJDIR, exist_ok=True)
+    others = [s for s in SOURCES if s != "api.hip"]
+    objs = []
+    for src in others:
+        obj = os.path.join(OBJDIR, os.path.splitext(src)[0] + ".o")
+        objs.append(obj if os.path.exists(obj) else _compile(src))
+    san = os.path.splitext(out)[0] + "_api.o"
+    cmd = [hipcc(), *CFLAGS, *HOST_SANITIZE, "-c", os.path.join(CSRC, "api.hip"), "-o", san]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed on api.hip (sanitized):\n{r.stderr}")
+    _link([san, *objs], out)
+    return out
+
+
 def build(verbose: bool = False) -> str:
     """Compile every kernel file and link ``libsantapp.so`` (and the
     streaming-read probe ``libsantapp_probe.so``) next to this file."""
