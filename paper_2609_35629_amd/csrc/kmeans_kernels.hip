@@ -48,6 +48,7 @@ namespace {
 
 constexpr int kKppThreads = 256;
 constexpr int kPickThreads = 1024;
+constexpr int kPickCache = 16;  // sample values per thread k_kpp_pick keeps in registers
 constexpr int kAsgThreads = 256;
 constexpr int kAsgPts = 64;   // batch points per assignment workgroup
 constexpr int kAsgCen = 32;   // centers per LDS tile
@@ -222,8 +223,21 @@ __global__ __launch_bounds__(kPickThreads) void k_kpp_pick(
     // the contiguous range [tid per, (tid + 1) per)
     const int per = (s0 + kPickThreads - 1) / kPickThreads;
     const int j0 = min(s0, tid * per), j1 = min(s0, j0 + per);
+    // the range's first kPickCache values, loaded together (indices clamped
+    // into the sample, so no load is conditional) and kept for both passes;
+    // the sums still run in index order
+    double vals[kPickCache];
+#pragma unroll
+    for (int q = 0; q < kPickCache; ++q) vals[q] = src[min(j0 + q, s0 - 1)];
     double loc = 0.0;
-    for (int j = j0; j < j1; ++j) {
+#pragma unroll
+    for (int q = 0; q < kPickCache; ++q) {
+        if (j0 + q < j1) {
+            dst[j0 + q] = vals[q];
+            loc = loc + vals[q];
+        }
+    }
+    for (int j = j0 + kPickCache; j < j1; ++j) {
         const double v = src[j];
         dst[j] = v;
         loc = loc + v;
@@ -253,15 +267,30 @@ __global__ __launch_bounds__(kPickThreads) void k_kpp_pick(
 #pragma unroll
     for (int t = 0; t < kKmMaxTrials; ++t) found[t] = s0;
     double run = pre;
-    for (int j = j0; j < j1; ++j) {
+#pragma unroll
+    for (int q = 0; q < kPickCache; ++q) {
+        if (j0 + q < j1) {
+            run = run + vals[q];
+#pragma unroll
+            for (int t = 0; t < kKmMaxTrials; ++t)
+                if (t < L && found[t] == s0 && run > target[t]) found[t] = j0 + q;
+        }
+    }
+    for (int j = j0 + kPickCache; j < j1; ++j) {
         run = run + src[j];
 #pragma unroll
         for (int t = 0; t < kKmMaxTrials; ++t)
             if (t < L && found[t] == s0 && run > target[t]) found[t] = j;
     }
+    // the first crossing of each trial: every thread past it has found a
+    // position too, so the wave's minimum goes to LDS, one atomic per wave
 #pragma unroll
-    for (int t = 0; t < kKmMaxTrials; ++t)
-        if (t < L && found[t] < s0) atomicMin(&s_first[t], found[t]);
+    for (int t = 0; t < kKmMaxTrials; ++t) {
+        if (t < L) {  // uniform
+            const int f = static_cast<int>(wave_min64(static_cast<uint64_t>(found[t])));
+            if (lane_id() == 0 && f < s0) atomicMin(&s_first[t], f);
+        }
+    }
     __syncthreads();
     if (tid < L) cand[bh * L + tid] = s_first[tid];
 }
