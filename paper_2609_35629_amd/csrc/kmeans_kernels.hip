@@ -358,9 +358,22 @@ __global__ __launch_bounds__(kAsgThreads) void k_km_assign(
     for (int ct = 0; ct < M; ct += kAsgCen) {
         __syncthreads();  // the previous tile is no longer read
         const int nct = min(kAsgCen, M - ct);
-        for (int e = tid; e < kAsgCen * D; e += kAsgThreads) {
-            const int u = e / D, k = e % D;
-            s_c[u][k] = u < nct ? cb[static_cast<size_t>(ct + u) * D + k] : 0.0;
+        {
+            // the tile's values, all loads in flight before the LDS stores
+            // (rows past the last center read center 0 and store zero)
+            static_assert(kAsgCen * D % kAsgThreads == 0, "whole tile elements per thread");
+            constexpr int kPer = kAsgCen * D / kAsgThreads;
+            double v[kPer];
+#pragma unroll
+            for (int q = 0; q < kPer; ++q) {
+                const int e = q * kAsgThreads + tid, u = e / D, k = e % D;
+                v[q] = cb[static_cast<size_t>(u < nct ? ct + u : 0) * D + k];
+            }
+#pragma unroll
+            for (int q = 0; q < kPer; ++q) {
+                const int e = q * kAsgThreads + tid, u = e / D, k = e % D;
+                s_c[u][k] = u < nct ? v[q] : 0.0;
+            }
         }
         __syncthreads();
         double acc[4][2];
