@@ -457,19 +457,33 @@ __global__ __launch_bounds__(kAsgThreads) void k_km_assign(
         bcnt[blk * M + u] = n;
     }
     __syncthreads();
-    // each present center's sum, in point order, one thread per dimension
+    // each present center's sum, in point order, one thread per dimension;
+    // 16 sorted points' positions, labels and values are read ahead of
+    // their additions (indices clamped into the valid points)
     if (tid < D) {
         int cur = -1;
         double acc = 0.0;
-        for (int r = 0; r < nv; ++r) {
-            const int p = s_ord[r];
-            const int u = s_lab[p];
-            if (u != cur) {
-                if (cur >= 0) bpart[(blk * M + cur) * D + tid] = acc;
-                cur = u;
-                acc = 0.0;
+        for (int r0 = 0; r0 < nv; r0 += 16) {
+            int pp[16], uu[16];
+            float xx[16];
+#pragma unroll
+            for (int q = 0; q < 16; ++q) pp[q] = s_ord[min(r0 + q, nv - 1)];
+#pragma unroll
+            for (int q = 0; q < 16; ++q) {
+                uu[q] = s_lab[pp[q]];
+                xx[q] = s_x[pp[q]][tid];
             }
-            acc = acc + static_cast<double>(s_x[p][tid]);
+#pragma unroll
+            for (int q = 0; q < 16; ++q) {
+                if (r0 + q < nv) {
+                    if (uu[q] != cur) {
+                        if (cur >= 0) bpart[(blk * M + cur) * D + tid] = acc;
+                        cur = uu[q];
+                        acc = 0.0;
+                    }
+                    acc = acc + static_cast<double>(xx[q]);
+                }
+            }
         }
         if (cur >= 0) bpart[(blk * M + cur) * D + tid] = acc;
     }
