@@ -533,25 +533,30 @@ __global__ __launch_bounds__(256) void k_km_control(
     double* __restrict__ w, KmState* __restrict__ state) {
 #pragma clang fp contract(off)
     __shared__ int s_mark[kKmMaxCenters];
+    __shared__ double s_wb[kKmMaxCenters];
     __shared__ int s_count;
     __shared__ double s_wkeep;
     const int bh = blockIdx.x, tid = threadIdx.x;
     KmState* st = state + bh;
     if (st->stop) return;
     double* wb = w + static_cast<size_t>(bh) * M;
+    // the weights staged in LDS by every thread, then scanned in index order
+    // by one
+    for (int u = tid; u < M; u += 256) s_wb[u] = wb[u];
+    __syncthreads();
     if (tid == 0) {
         int count = 0;
         double wkeep = INFINITY;
         if (ratio > 0.0) {
-            double wmax = wb[0];
+            double wmax = s_wb[0];
             for (int u = 1; u < M; ++u)
-                if (wb[u] > wmax) wmax = wb[u];
+                if (s_wb[u] > wmax) wmax = s_wb[u];
             const double thr = ratio * wmax;
             for (int u = 0; u < M; ++u) {
-                if (wb[u] < thr && count < batch / 2)
+                if (s_wb[u] < thr && count < batch / 2)
                     s_mark[count++] = u;
-                else if (wb[u] < wkeep)
-                    wkeep = wb[u];
+                else if (s_wb[u] < wkeep)
+                    wkeep = s_wb[u];
             }
         }
         s_count = count;
