@@ -52,6 +52,7 @@ constexpr int kPickCache = 16;  // sample values per thread k_kpp_pick keeps in 
 constexpr int kAsgThreads = 256;
 constexpr int kAsgPts = 64;   // batch points per assignment workgroup
 constexpr int kAsgCen = 32;   // centers per LDS tile
+constexpr int kUpdBatch = 32; // workgroup partials the center update loads at once
 constexpr int kListThreads = 1024;
 constexpr int kListWaves = kListThreads / kWave;
 
@@ -496,22 +497,22 @@ __global__ __launch_bounds__(D) void k_km_update(int M, int nblk, const double* 
 #pragma clang fp contract(off)
     const int u = blockIdx.x, bh = blockIdx.y, k = threadIdx.x;
     if (state[bh].stop) return;
-    // eight workgroups' counts and partial sums loaded together (a partial
-    // of a center the workgroup did not see is stale and not added), then
-    // added in workgroup order
+    // kUpdBatch workgroups' counts and partial sums loaded together (a
+    // partial of a center the workgroup did not see is stale and not added),
+    // then added in workgroup order
     double S = 0.0;
     int n = 0;
-    for (int b0 = 0; b0 < nblk; b0 += 8) {
-        int c[8];
-        double v[8];
+    for (int b0 = 0; b0 < nblk; b0 += kUpdBatch) {
+        int c[kUpdBatch];
+        double v[kUpdBatch];
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
+        for (int q = 0; q < kUpdBatch; ++q) {
             const size_t blk = static_cast<size_t>(bh) * nblk + min(b0 + q, nblk - 1);
             c[q] = b0 + q < nblk ? bcnt[blk * M + u] : 0;
             v[q] = bpart[(blk * M + u) * D + k];
         }
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
+        for (int q = 0; q < kUpdBatch; ++q) {
             if (c[q]) {
                 S = S + v[q];
                 n += c[q];
