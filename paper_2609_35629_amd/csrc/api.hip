@@ -494,35 +494,27 @@ santapp_status santapp_build_teams_from_labels(const void* K, const void* V, int
     const size_t row = static_cast<size_t>(d) * esz;
     const int Mp = num_labels;
 
-    // parent lists, then the team counts that size the table
-    int *members = nullptr, *pbeg = nullptr, *toff = nullptr, *tcount = nullptr, *bad = nullptr;
-    double* mind = nullptr;
-    int* owner = nullptr;
-    hipError_t e = hipSuccess;
-    auto alloc = [&](void** p, size_t bytes) {
-        if (e == hipSuccess) e = hipMalloc(p, bytes);
-    };
-    auto cleanup = [&]() {
-        release(members);
-        release(pbeg);
-        release(toff);
-        release(tcount);
-        release(bad);
-        release(mind);
-        release(owner);
-    };
-    alloc(reinterpret_cast<void**>(&members), BH * N * sizeof(int));
-    alloc(reinterpret_cast<void**>(&pbeg), BH * (Mp + 1) * sizeof(int));
-    alloc(reinterpret_cast<void**>(&toff), BH * (Mp + 1) * sizeof(int));
-    alloc(reinterpret_cast<void**>(&tcount), BH * sizeof(int));
-    alloc(reinterpret_cast<void**>(&bad), sizeof(int));
-    alloc(reinterpret_cast<void**>(&mind), BH * N * sizeof(double));
-    alloc(reinterpret_cast<void**>(&owner), BH * N * sizeof(int));
+    // parent lists, then the team counts that size the table; the build's
+    // scratch arrays are carved from one allocation
+    Carver sc;
+    const size_t o_mem = sc.take(BH * N * sizeof(int)), o_pbeg = sc.take(BH * (Mp + 1) * sizeof(int));
+    const size_t o_toff = sc.take(BH * (Mp + 1) * sizeof(int)), o_tcount = sc.take(BH * sizeof(int));
+    const size_t o_bad = sc.take(sizeof(int)), o_mind = sc.take(BH * N * sizeof(double));
+    const size_t o_owner = sc.take(BH * N * sizeof(int));
+    char* scratch = nullptr;
+    hipError_t e = hipMalloc(reinterpret_cast<void**>(&scratch), sc.off);
     if (e != hipSuccess) {
-        cleanup();
         (void)hipGetLastError();
         return fail(SANTAPP_ENOMEM, "device allocation failed: %s", hipGetErrorString(e));
     }
+    auto cleanup = [&]() { release(scratch); };
+    int* members = reinterpret_cast<int*>(scratch + o_mem);
+    int* pbeg = reinterpret_cast<int*>(scratch + o_pbeg);
+    int* toff = reinterpret_cast<int*>(scratch + o_toff);
+    int* tcount = reinterpret_cast<int*>(scratch + o_tcount);
+    int* bad = reinterpret_cast<int*>(scratch + o_bad);
+    double* mind = reinterpret_cast<double*>(scratch + o_mind);
+    int* owner = reinterpret_cast<int*>(scratch + o_owner);
     const char* what = "parent lists";
     e = hipMemsetAsync(bad, 0, sizeof(int), s);
     if (e == hipSuccess)
